@@ -1,0 +1,156 @@
+/*
+ * curvadion.h — C ABI of the CurvaDion optimizer step on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * One call performs one step of the paper's Algorithm 2 (CurvaDion, Sec. 2.2)
+ * for one weight matrix ("layer") or for a group of layers:
+ *
+ *   B = M + G                                   buffer update
+ *   RMMC = |‖B‖_F - prev| / (prev + eps); prev = ‖B‖_F     (Eq. 1 as executed)
+ *   g = max over the layers of RMMC;  sync = g > tau      gate
+ *   sync:  P~ = B Q;  P = Orthogonalize(P~);  R = B^T P   power iteration
+ *          M = B - (1 - mu) P R^T                     error feedback
+ *          Q = ColumnNormalize(R)
+ *          X = X - eta sqrt(m/n) P Q^T                weight update
+ *   local: M = B;  X = X - eta_local G                (Q unchanged)
+ *
+ * The sync branch is the Dion step of Algorithm 1 (Sec. 1.1).  With one GPU
+ * the data-parallel all-reduces of both algorithms are identities.
+ *
+ * Memory: every matrix argument is a DEVICE pointer into the memory of the GPU
+ * that is current when the layer is created, row-major and contiguous
+ * (leading dimension = number of columns), 16-byte aligned.  The caller owns
+ * G (read only), M, X (m x n fp32, updated in place) and Q (n x r fp32,
+ * updated in place on sync steps).  The library owns its workspace (the
+ * P~/P/R panels, Gram and factor matrices, partial sums) and the per-layer
+ * prev_norm; both live until cd_destroy.
+ *
+ * Ordering: all work is enqueued on the HIP stream passed to a step call
+ * (NULL = the default stream).  A step blocks the calling host thread once,
+ * after the RMMC gate, to read the decision back (the single device-to-host
+ * crossing that stands in for the max all-reduce); it returns as soon as the
+ * chosen branch is enqueued.  Read M, X, Q only after synchronising the stream.
+ *
+ * Errors: arguments are checked before anything is enqueued; CD_EINVAL leaves
+ * every buffer and the layer state untouched.  No C++ exception crosses this
+ * interface.  cd_last_error() returns a thread-local message for the last
+ * failing call on the calling thread.
+ */
+#ifndef CURVADION_H
+#define CURVADION_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CD_ABI_VERSION 1
+
+typedef enum cd_status {
+  CD_OK = 0,
+  CD_EINVAL = -1,      /* invalid argument; nothing was enqueued */
+  CD_ENOMEM = -2,      /* device or host allocation failed */
+  CD_EHIP = -3,        /* a HIP runtime call failed; see cd_last_error() */
+  CD_ENONFINITE = -4,  /* some ‖B‖ was NaN/Inf; the step still ran (local branch) */
+  CD_ERANKDEF = -5     /* reserved: rank deficiency is reported by
+                          cd_layer_rank_deficient(), not by a step's status */
+} cd_status;
+
+typedef enum cd_dtype { CD_F32 = 0, CD_BF16 = 1 } cd_dtype;
+
+/* How the branch is chosen (Algorithm 2 gate, or a fixed policy). */
+typedef enum cd_policy {
+  CD_POLICY_RMMC = 0,         /* sync iff max_l RMMC_l > tau (Algorithm 2) */
+  CD_POLICY_ALWAYS_SYNC = 1,  /* every step syncs: Dion, Algorithm 1 */
+  CD_POLICY_NEVER_SYNC = 2,   /* every step takes the local branch */
+  CD_POLICY_EVERY_H = 3       /* sync on steps H, 2H, ...: Scheduled Sync Dion (Sec. 4.3) */
+} cd_policy;
+
+typedef struct cd_layer_desc {
+  int m;                    /* rows of the weight matrix (and of P) */
+  int n;                    /* columns (rows of Q and R) */
+  int r_max;                /* largest rank any step of this layer will use;
+                               1 <= r_max <= min(m, n); sizes the workspace */
+  cd_dtype grad_dtype;      /* element type of G: fp32 or bf16 */
+  double tau;               /* gate threshold (strict >) */
+  double eps;               /* RMMC denominator guard; the paper leaves it
+                               unstated, 1e-8 is the usual choice; >= 0 */
+  double eta_local_scale;   /* eta_local = eta_local_scale * eta; >= 0 */
+  cd_policy policy;
+  int H;                    /* period for CD_POLICY_EVERY_H (>= 1), else ignored */
+} cd_layer_desc;
+
+typedef struct cd_result {
+  double rmmc;       /* the gate statistic: max over the layers of RMMC */
+  int sync_flag;     /* 1 = the sync branch ran, 0 = the local branch ran */
+} cd_result;
+
+typedef struct cd_layer cd_layer;
+typedef struct cd_group cd_group;
+
+/* Create one layer on the current device: allocates the workspace for
+ * (m, n, r_max), sets prev_norm = 0 and the step counter to 0 (Algorithm 2
+ * initialisation).  CD_EINVAL for a NULL pointer, a non-positive size,
+ * r_max > min(m, n), an unknown dtype or policy, eps < 0, tau NaN, or H < 1
+ * under CD_POLICY_EVERY_H. */
+cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out);
+
+/* One step for one layer (Algorithm 2 with the max taken over this layer
+ * alone).  G: m x n of desc.grad_dtype; M, X: m x n fp32; Q: n x r fp32.
+ * mu in [0, 1], eta finite and >= 0, 1 <= r <= r_max.  `stream` is a
+ * hipStream_t (NULL = default stream).  `out` (host, may be NULL) receives
+ * the statistic and the branch taken.  Returns CD_OK or CD_ENONFINITE after a
+ * completed step, or an error before any work. */
+cd_status cd_step(cd_layer* layer, const void* G, float* M, float* X, float* Q,
+                  float mu, float eta, int r, void* stream, cd_result* out);
+
+/* Free the layer and its workspace.  Destroy any group that refers to the
+ * layer first.  NULL is accepted (no-op). */
+cd_status cd_destroy(cd_layer* layer);
+
+/* Group layers so that one step takes the max of RMMC over all of them before
+ * any layer branches (Algorithm 2).  All layers must share grad_dtype, tau,
+ * policy, H and device; the group refers to (does not own) the layers, and
+ * copies the pointer array.  n_layers >= 1. */
+cd_status cd_group_create(cd_layer* const* layers, int n_layers, cd_group** out);
+
+/* One step for every layer of the group.  G, M, X, Q are HOST arrays of
+ * n_layers DEVICE pointers, in the order the group was created with; shapes as
+ * for cd_step with each layer's (m, n) and the common rank r (1 <= r <= every
+ * layer's r_max).  `rmmc_per_layer` (host, may be NULL) receives n_layers
+ * values of RMMC_l.  Returns CD_OK or CD_ENONFINITE after a completed step, or
+ * an error before any work. */
+cd_status cd_group_step(cd_group* group, const void* const* G, float* const* M,
+                        float* const* X, float* const* Q, float mu, float eta, int r,
+                        void* stream, double* rmmc_per_layer, cd_result* out);
+
+cd_status cd_group_destroy(cd_group* group);
+
+/* Checkpoint support: the library-owned state of a layer is prev_norm (the
+ * last ‖B‖_F) and the step counter; M, X and Q belong to the caller.  These
+ * calls synchronise the device. */
+cd_status cd_layer_get_state(const cd_layer* layer, double* prev_norm, long long* step);
+cd_status cd_layer_set_state(cd_layer* layer, double prev_norm, long long step);
+
+/* Device pointers to the orthonormal P (m x r) and to R = B^T P (n x r) of
+ * the layer's last sync step, row-major, owned by the library and valid until
+ * its next step or cd_destroy.  For inspection and tests. */
+cd_status cd_layer_last_factors(const cd_layer* layer, const float** P, const float** R);
+
+/* Waits for the layer's last step to finish, then sets *flag = 1 if the last
+ * sync step found P~ numerically rank deficient (a Cholesky pivot at or below
+ * 1e-13 times the largest Gram diagonal): M, X and Q were still written, but
+ * columns of P beyond the numerical rank are not orthonormal and their values
+ * are not unique.  *flag = 0 otherwise. */
+cd_status cd_layer_rank_deficient(const cd_layer* layer, int* flag);
+
+/* Thread-local text of the last error on this thread ("" if none). */
+const char* cd_last_error(void);
+
+/* CD_ABI_VERSION of the built library. */
+int cd_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CURVADION_H */

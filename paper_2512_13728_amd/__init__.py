@@ -1,0 +1,208 @@
+"""CurvaDion optimizer step on AMD Instinct MI355X: Python binding.
+
+A thin ctypes layer over ``libcurvadion.so`` (the C ABI in
+``include/curvadion.h``).  It only marshals arguments: every step of the method
+runs in the library's HIP kernels.  PyTorch supplies device memory and the
+current HIP stream.  There is no fallback path: if the library is missing the
+import succeeds but every call raises ``LibraryNotBuilt``.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence, Tuple
+
+__all__ = [
+    "LibraryNotBuilt", "CurvaDionError", "Layer", "Group", "lib", "library_path",
+    "POLICY_RMMC", "POLICY_ALWAYS_SYNC", "POLICY_NEVER_SYNC", "POLICY_EVERY_H",
+    "F32", "BF16", "EXPORTED_SYMBOLS",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+library_path = os.path.join(_HERE, "libcurvadion.so")
+
+CD_OK, CD_EINVAL, CD_ENOMEM, CD_EHIP, CD_ENONFINITE, CD_ERANKDEF = 0, -1, -2, -3, -4, -5
+F32, BF16 = 0, 1
+POLICY_RMMC, POLICY_ALWAYS_SYNC, POLICY_NEVER_SYNC, POLICY_EVERY_H = 0, 1, 2, 3
+_STATUS = {0: "CD_OK", -1: "CD_EINVAL", -2: "CD_ENOMEM", -3: "CD_EHIP",
+           -4: "CD_ENONFINITE", -5: "CD_ERANKDEF"}
+
+#: every function the header declares
+EXPORTED_SYMBOLS = (
+    "cd_layer_create", "cd_step", "cd_destroy", "cd_group_create", "cd_group_step",
+    "cd_group_destroy", "cd_layer_get_state", "cd_layer_set_state",
+    "cd_layer_last_factors", "cd_layer_rank_deficient", "cd_last_error", "cd_abi_version",
+)
+
+
+class LibraryNotBuilt(RuntimeError):
+    pass
+
+
+class CurvaDionError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int), ("n", ctypes.c_int), ("r_max", ctypes.c_int),
+                ("grad_dtype", ctypes.c_int), ("tau", ctypes.c_double),
+                ("eps", ctypes.c_double), ("eta_local_scale", ctypes.c_double),
+                ("policy", ctypes.c_int), ("H", ctypes.c_int)]
+
+
+class Result(ctypes.Structure):
+    _fields_ = [("rmmc", ctypes.c_double), ("sync_flag", ctypes.c_int)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises LibraryNotBuilt if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(library_path):
+        raise LibraryNotBuilt(
+            f"{library_path} is missing; build it with `python -m paper_2512_13728_amd.build`")
+    L = ctypes.CDLL(library_path)
+    vp, i, f, d = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_double
+    L.cd_layer_create.argtypes = [ctypes.POINTER(LayerDesc), ctypes.POINTER(vp)]
+    L.cd_step.argtypes = [vp, vp, vp, vp, vp, f, f, i, vp, ctypes.POINTER(Result)]
+    L.cd_destroy.argtypes = [vp]
+    L.cd_group_create.argtypes = [ctypes.POINTER(vp), i, ctypes.POINTER(vp)]
+    L.cd_group_step.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                ctypes.POINTER(vp), f, f, i, vp, ctypes.POINTER(d),
+                                ctypes.POINTER(Result)]
+    L.cd_group_destroy.argtypes = [vp]
+    L.cd_layer_get_state.argtypes = [vp, ctypes.POINTER(d), ctypes.POINTER(ctypes.c_longlong)]
+    L.cd_layer_set_state.argtypes = [vp, d, ctypes.c_longlong]
+    L.cd_layer_last_factors.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp)]
+    L.cd_layer_rank_deficient.argtypes = [vp, ctypes.POINTER(i)]
+    L.cd_last_error.restype = ctypes.c_char_p
+    L.cd_last_error.argtypes = []
+    L.cd_abi_version.restype = i
+    for name in EXPORTED_SYMBOLS:
+        if name not in ("cd_last_error", "cd_abi_version"):
+            getattr(L, name).restype = i
+    _lib = L
+    return L
+
+
+def _check(st: int, allow=(CD_OK,)) -> int:
+    if st not in allow:
+        raise CurvaDionError(st, lib().cd_last_error().decode(errors="replace"))
+    return st
+
+
+def _ptr(t) -> int:
+    """Device address of a tensor (or an int address)."""
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+class Layer:
+    """One weight matrix under CurvaDion (m x n, rank up to r_max)."""
+
+    def __init__(self, m: int, n: int, r_max: int, *, grad_dtype: str = "f32",
+                 tau: float = 0.5, eps: float = 1e-8, eta_local_scale: float = 1.0,
+                 policy: int = POLICY_RMMC, H: int = 1):
+        self._h = None
+        desc = LayerDesc(m, n, r_max, BF16 if grad_dtype == "bf16" else F32, tau, eps,
+                         eta_local_scale, policy, H)
+        h = ctypes.c_void_p()
+        _check(lib().cd_layer_create(ctypes.byref(desc), ctypes.byref(h)))
+        self._h = h
+        self.m, self.n, self.r_max = m, n, r_max
+        self.grad_dtype = grad_dtype
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        return self._h
+
+    def step(self, G, M, X, Q, mu: float, eta: float, r: Optional[int] = None,
+             stream=None) -> Tuple[float, bool, int]:
+        """One CurvaDion step; returns (rmmc, sync_flag, status)."""
+        r = Q.shape[1] if r is None and hasattr(Q, "shape") else r
+        res = Result()
+        st = lib().cd_step(self._h, _ptr(G), _ptr(M), _ptr(X), _ptr(Q), mu, eta, r,
+                           _stream_handle(stream), ctypes.byref(res))
+        _check(st, allow=(CD_OK, CD_ENONFINITE))
+        return res.rmmc, bool(res.sync_flag), st
+
+    def get_state(self) -> Tuple[float, int]:
+        p, s = ctypes.c_double(), ctypes.c_longlong()
+        _check(lib().cd_layer_get_state(self._h, ctypes.byref(p), ctypes.byref(s)))
+        return p.value, s.value
+
+    def set_state(self, prev_norm: float, step: int) -> None:
+        _check(lib().cd_layer_set_state(self._h, prev_norm, step))
+
+    def last_factors(self) -> Tuple[int, int]:
+        """Device addresses of the last sync step's P (m x r) and R (n x r)."""
+        P, R = ctypes.c_void_p(), ctypes.c_void_p()
+        _check(lib().cd_layer_last_factors(self._h, ctypes.byref(P), ctypes.byref(R)))
+        return P.value, R.value
+
+    def rank_deficient(self) -> bool:
+        f = ctypes.c_int()
+        _check(lib().cd_layer_rank_deficient(self._h, ctypes.byref(f)))
+        return bool(f.value)
+
+    def close(self) -> None:
+        if self._h is not None and _lib is not None:
+            lib().cd_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Group:
+    """Layers stepped together: the gate takes the max of RMMC over all of them."""
+
+    def __init__(self, layers: Sequence[Layer]):
+        self._h = None
+        self.layers = list(layers)
+        arr = (ctypes.c_void_p * len(layers))(*[L.handle.value for L in layers])
+        h = ctypes.c_void_p()
+        _check(lib().cd_group_create(arr, len(layers), ctypes.byref(h)))
+        self._h = h
+
+    def step(self, G, M, X, Q, mu: float, eta: float, r: int, stream=None):
+        """One step over every layer; returns (rmmc_max, sync_flag, rmmc_per_layer, status)."""
+        n = len(self.layers)
+        mk = lambda ts: (ctypes.c_void_p * n)(*[_ptr(t) for t in ts])
+        per = (ctypes.c_double * n)()
+        res = Result()
+        st = lib().cd_group_step(self._h, mk(G), mk(M), mk(X), mk(Q), mu, eta, r,
+                                 _stream_handle(stream), per, ctypes.byref(res))
+        _check(st, allow=(CD_OK, CD_ENONFINITE))
+        return res.rmmc, bool(res.sync_flag), list(per), st
+
+    def close(self) -> None:
+        if self._h is not None and _lib is not None:
+            lib().cd_group_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,546 @@
+// C ABI of the CurvaDion step (include/curvadion.h): argument checks, layer and
+// group lifetimes, workspace, launch planning and the per-step schedule.
+//
+// One group step (Algorithm 2 of the paper):
+//   1. per shape class: B = M + G with per-block partial sums of B^2
+//   2. gate kernel: fixed-order norms, RMMC_l, prev_norm update, max, flag
+//   3. one device-to-host copy of {max, flag, RMMC_l}: the decision point that
+//      stands in for the max all-reduce at one worker
+//   4. sync branch, per shape class: P~ = B Q; CholQR twice (fp64 Gram,
+//      Cholesky + inverse, apply); R = B^T P; ColumnNormalize; M/X update.
+//      local branch: X -= eta_local G (M already holds B).
+// Layers of equal (m, n) share every launch (up to MAXB per launch).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/curvadion.h"
+#include "common.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+cd_status fail(cd_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define CD_HIP(call)                                                                         \
+  do {                                                                                       \
+    hipError_t e_ = (call);                                                                  \
+    if (e_ != hipSuccess)                                                                    \
+      return fail(CD_EHIP, "%s failed: %s (%s:%d)", #call, hipGetErrorString(e_), __FILE__, \
+                  __LINE__);                                                                 \
+  } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) { ok = false; return; }
+    if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+// K-splitting so that one launch has >= ~1024 blocks, each slice >= 256 deep.
+int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk) {
+  const long long bm = cd::gemm_bm(N, fp64), bn = cd::gemm_bn(N, fp64);
+  const long long tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn) * nl;
+  int s = 1;
+  while (tiles * s < 1024 && K / (2 * s) >= 256 && s < 32) s *= 2;
+  int kc = (K + s - 1) / s;
+  kc = (kc + cd::GBK - 1) / cd::GBK * cd::GBK;
+  *kchunk = kc;
+  return (K + kc - 1) / kc;
+}
+
+template <typename T>
+hipError_t dalloc(T** p, size_t count) {
+  *p = nullptr;
+  if (count == 0) count = 1;
+  return hipMalloc(reinterpret_cast<void**>(p), count * sizeof(T));
+}
+
+}  // namespace
+
+struct cd_layer {
+  cd_layer_desc d{};
+  int device = 0;
+  long long step = 0;
+  double* prev = nullptr;       // device, 1 double
+  int* rankdef = nullptr;       // device, 1 int
+  double* pa = nullptr;         // m x r_max fp64: P~
+  double* pb = nullptr;         // m x r_max fp64: P~ after the first CholQR pass
+  float* P = nullptr;           // m x r_max fp32: the orthonormal P
+  float* R = nullptr;           // n x r_max
+  double* W = nullptr;          // r_max^2 Gram / Cholesky factor
+  double* U = nullptr;          // r_max^2 inverse factor
+  double* gram_part = nullptr;  // split-K partials of the Gram matrix
+  void* split_part = nullptr;   // split-K partials of the skinny GEMMs (fp32 or fp64)
+  double* colsq = nullptr;      // column sum-of-squares partials
+  float* colnrm = nullptr;      // r_max column norms
+  cd_group* self = nullptr;     // one-layer group used by cd_step
+  hipStream_t last_stream = nullptr;
+  int last_r = 0;
+};
+
+struct ShapeClass {
+  int m, n;
+  std::vector<int> idx;  // positions in the group
+};
+
+struct cd_group {
+  std::vector<cd_layer*> layers;
+  std::vector<ShapeClass> shapes;
+  int device = 0;
+  int L = 0;
+  bool g_bf16 = false;
+  double tau = 0, eps = 0;
+  cd_policy policy = CD_POLICY_RMMC;
+  int H = 1;
+  int nparts_stride = 0;
+  double* parts = nullptr;      // [L][nparts_stride]
+  int* nparts = nullptr;        // [L]
+  double** prev = nullptr;      // [L] device pointers to each layer's prev_norm
+  cd::GateOut* out_dev = nullptr;
+  void* out_host = nullptr;     // pinned
+  hipEvent_t ev = nullptr;
+};
+
+namespace {
+
+void free_layer(cd_layer* L) {
+  if (!L) return;
+  void* ptrs[] = {L->prev, L->rankdef, L->pa, L->pb, L->P, L->R, L->W, L->U,
+                  L->gram_part, L->split_part, L->colsq, L->colnrm};
+  for (void* p : ptrs)
+    if (p) (void)hipFree(p);
+  delete L;
+}
+
+void free_group(cd_group* g) {
+  if (!g) return;
+  if (g->parts) (void)hipFree(g->parts);
+  if (g->nparts) (void)hipFree(g->nparts);
+  if (g->prev) (void)hipFree(g->prev);
+  if (g->out_dev) (void)hipFree(g->out_dev);
+  if (g->out_host) (void)hipHostFree(g->out_host);
+  if (g->ev) (void)hipEventDestroy(g->ev);
+  delete g;
+}
+
+long long blocks_for(long long numel) { return (numel + cd::FORM_CHUNK - 1) / cd::FORM_CHUNK; }
+
+cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
+  cd_group* g = new (std::nothrow) cd_group();
+  if (!g) return fail(CD_ENOMEM, "host allocation failed");
+  g->layers.assign(layers, layers + n);
+  g->L = n;
+  g->device = layers[0]->device;
+  g->g_bf16 = layers[0]->d.grad_dtype == CD_BF16;
+  g->tau = layers[0]->d.tau;
+  g->eps = layers[0]->d.eps;
+  g->policy = layers[0]->d.policy;
+  g->H = layers[0]->d.H;
+  for (int i = 0; i < n; ++i) {
+    const cd_layer* L = layers[i];
+    auto it = std::find_if(g->shapes.begin(), g->shapes.end(), [&](const ShapeClass& s) {
+      return s.m == L->d.m && s.n == L->d.n;
+    });
+    if (it == g->shapes.end()) g->shapes.push_back(ShapeClass{L->d.m, L->d.n, {i}});
+    else it->idx.push_back(i);
+    g->nparts_stride = std::max<int>(g->nparts_stride,
+                                     static_cast<int>(blocks_for(1LL * L->d.m * L->d.n)));
+  }
+  DeviceGuard dg(g->device);
+  if (!dg.ok) { free_group(g); return fail(CD_EHIP, "cannot select device %d", g->device); }
+  std::vector<int> np(n);
+  std::vector<double*> pv(n);
+  for (int i = 0; i < n; ++i) {
+    np[i] = static_cast<int>(blocks_for(1LL * layers[i]->d.m * layers[i]->d.n));
+    pv[i] = layers[i]->prev;
+  }
+  hipError_t e = hipSuccess;
+  if (e == hipSuccess) e = dalloc(&g->parts, static_cast<size_t>(n) * g->nparts_stride);
+  if (e == hipSuccess) e = dalloc(&g->nparts, n);
+  if (e == hipSuccess) e = dalloc(&g->prev, n);
+  if (e == hipSuccess)
+    e = hipMalloc(reinterpret_cast<void**>(&g->out_dev), sizeof(cd::GateOut) + sizeof(double) * n);
+  if (e == hipSuccess) e = hipHostMalloc(&g->out_host, sizeof(cd::GateOut) + sizeof(double) * n);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&g->ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipMemcpy(g->nparts, np.data(), sizeof(int) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(g->prev, pv.data(), sizeof(double*) * n, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    free_group(g);
+    return fail(e == hipErrorOutOfMemory ? CD_ENOMEM : CD_EHIP, "group setup: %s",
+                hipGetErrorString(e));
+  }
+  *out = g;
+  return CD_OK;
+}
+
+cd_status check_desc(const cd_layer_desc* d) {
+  if (!d) return fail(CD_EINVAL, "desc is NULL");
+  if (d->m < 1 || d->n < 1) return fail(CD_EINVAL, "m and n must be >= 1 (got %d, %d)", d->m, d->n);
+  if (d->r_max < 1 || d->r_max > std::min(d->m, d->n))
+    return fail(CD_EINVAL, "r_max must be in [1, min(m, n)] (got %d)", d->r_max);
+  if (d->r_max > 1024) return fail(CD_EINVAL, "r_max above 1024 is not supported (got %d)", d->r_max);
+  if (d->grad_dtype != CD_F32 && d->grad_dtype != CD_BF16) return fail(CD_EINVAL, "unknown grad dtype");
+  if (d->policy < CD_POLICY_RMMC || d->policy > CD_POLICY_EVERY_H) return fail(CD_EINVAL, "unknown policy");
+  if (std::isnan(d->tau)) return fail(CD_EINVAL, "tau is NaN");
+  if (!(d->eps >= 0.0) || !std::isfinite(d->eps)) return fail(CD_EINVAL, "eps must be finite and >= 0");
+  if (!(d->eta_local_scale >= 0.0) || !std::isfinite(d->eta_local_scale))
+    return fail(CD_EINVAL, "eta_local_scale must be finite and >= 0");
+  if (d->policy == CD_POLICY_EVERY_H && d->H < 1) return fail(CD_EINVAL, "H must be >= 1");
+  return CD_OK;
+}
+
+// Enqueue the sync branch for the layers `sel` (all of one shape) of group g.
+cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>& sel,
+                       float* const* M, float* const* X, float* const* Q, float mu, float eta,
+                       int r, hipStream_t s) {
+  const int m = sc.m, n = sc.n, nl = static_cast<int>(sel.size());
+  auto lay = [&](int j) { return g->layers[sel[j]]; };
+
+  // skinny GEMM C = A.B with optional split-K and fixed-order reduction
+  auto gemm = [&](cd::GemmKind kind, int Mr, int Nr, int K, bool a_kc, int lda, bool b_kc, int ldb,
+                  bool upper, auto Aof, auto Bof, auto Cof, auto Pof) -> cd_status {
+    const bool acc64 = cd::gemm_acc64(kind);
+    cd::GemmArgs ga{};
+    ga.M = Mr; ga.N = Nr; ga.K = K; ga.lda = lda; ga.ldb = ldb; ga.ldc = Nr;
+    ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper;
+    ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk);
+    ga.split_stride = 1LL * Mr * Nr;
+    for (int j = 0; j < nl; ++j) {
+      ga.A[j] = Aof(j);
+      ga.B[j] = Bof(j);
+      ga.C[j] = ga.splits > 1 ? Pof(j) : Cof(j);
+    }
+    CD_HIP(cd::launch_gemm(ga, nl, kind, s));
+    if (ga.splits > 1) {
+      cd::ReduceArgs ra{};
+      ra.count = 1LL * Mr * Nr; ra.stride = ga.split_stride; ra.splits = ga.splits;
+      for (int j = 0; j < nl; ++j) { ra.part[j] = Pof(j); ra.out[j] = Cof(j); }
+      const bool out64 = kind == cd::GemmKind::F64 || kind == cd::GemmKind::F64_FROM_F32;
+      CD_HIP(cd::launch_reduce_splits(ra, nl, acc64, out64, s));
+    }
+    return CD_OK;
+  };
+  auto part = [&](int j) { return lay(j)->split_part; };
+  cd_status st;
+  // P~ = B Q in fp64 (B lives in M)
+  st = gemm(cd::GemmKind::F64_FROM_F32, m, r, n, true, n, false, r, false,
+            [&](int j) { return static_cast<const void*>(M[sel[j]]); },
+            [&](int j) { return static_cast<const void*>(Q[sel[j]]); },
+            [&](int j) { return static_cast<void*>(lay(j)->pa); }, part);
+  if (st != CD_OK) return st;
+  // Orthogonalize: two CholQR passes in fp64, pa -> pb -> P (rounded to fp32)
+  for (int pass = 0; pass < 2; ++pass) {
+    auto In = [&](int j) { return static_cast<const void*>(pass == 0 ? lay(j)->pa : lay(j)->pb); };
+    st = gemm(cd::GemmKind::F64, r, r, m, false, r, false, r, true, In, In,
+              [&](int j) { return static_cast<void*>(lay(j)->W); },
+              [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
+    if (st != CD_OK) return st;
+    cd::CholArgs ca{};
+    ca.r = r;
+    ca.accumulate = pass;
+    for (int j = 0; j < nl; ++j) {
+      ca.W[j] = lay(j)->W; ca.U[j] = lay(j)->U; ca.rankdef[j] = lay(j)->rankdef;
+    }
+    CD_HIP(cd::launch_chol_inv(ca, nl, s));
+    st = gemm(pass == 0 ? cd::GemmKind::F64 : cd::GemmKind::F64_TO_F32, m, r, r, true, r, false, r,
+              false, In, [&](int j) { return static_cast<const void*>(lay(j)->U); },
+              [&](int j) {
+                return pass == 0 ? static_cast<void*>(lay(j)->pb) : static_cast<void*>(lay(j)->P);
+              },
+              part);
+    if (st != CD_OK) return st;
+  }
+  // R = B^T P
+  st = gemm(cd::GemmKind::F32, n, r, m, false, n, false, r, false,
+            [&](int j) { return static_cast<const void*>(M[sel[j]]); },
+            [&](int j) { return static_cast<const void*>(lay(j)->P); },
+            [&](int j) { return static_cast<void*>(lay(j)->R); }, part);
+  if (st != CD_OK) return st;
+  // Q = ColumnNormalize(R)
+  cd::ColnormArgs cn{};
+  cn.n = n; cn.r = r; cn.nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
+  for (int j = 0; j < nl; ++j) {
+    cn.R[j] = lay(j)->R; cn.part[j] = lay(j)->colsq; cn.nrm[j] = lay(j)->colnrm; cn.Q[j] = Q[sel[j]];
+  }
+  CD_HIP(cd::launch_colnorm(cn, nl, s));
+  // M = B - (1 - mu) P R^T;  X -= eta sqrt(m/n) P Q^T
+  cd::UpdateArgs ua{};
+  ua.m = m; ua.n = n; ua.r = r;
+  ua.one_minus_mu = static_cast<float>(1.0 - static_cast<double>(mu));
+  ua.c = static_cast<float>(static_cast<double>(eta) * std::sqrt(static_cast<double>(m) / n));
+  for (int j = 0; j < nl; ++j) {
+    ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]]; ua.P[j] = lay(j)->P; ua.R[j] = lay(j)->R; ua.Q[j] = Q[sel[j]];
+  }
+  CD_HIP(cd::launch_update(ua, nl, s));
+  return CD_OK;
+}
+
+cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, float* const* X,
+                          float* const* Q, float mu, float eta, int r, void* stream,
+                          double* rmmc_per_layer, cd_result* out) {
+  if (!g) return fail(CD_EINVAL, "group is NULL");
+  if (!G || !M || !X || !Q) return fail(CD_EINVAL, "pointer array is NULL");
+  if (!(mu >= 0.0f && mu <= 1.0f)) return fail(CD_EINVAL, "mu must be in [0, 1] (got %g)", mu);
+  if (!std::isfinite(eta) || eta < 0.0f) return fail(CD_EINVAL, "eta must be finite and >= 0 (got %g)", eta);
+  if (r < 1) return fail(CD_EINVAL, "r must be >= 1 (got %d)", r);
+  for (int i = 0; i < g->L; ++i) {
+    const cd_layer* L = g->layers[i];
+    if (r > L->d.r_max) return fail(CD_EINVAL, "r = %d exceeds r_max = %d of layer %d", r, L->d.r_max, i);
+    if (!G[i] || !M[i] || !X[i] || !Q[i]) return fail(CD_EINVAL, "NULL matrix pointer for layer %d", i);
+    if (!aligned16(G[i]) || !aligned16(M[i]) || !aligned16(X[i]) || !aligned16(Q[i]))
+      return fail(CD_EINVAL, "matrix pointers of layer %d must be 16-byte aligned", i);
+  }
+  DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CD_EHIP, "cannot select device %d", g->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  // 1. B = M + G, partial sums of B^2
+  for (const ShapeClass& sc : g->shapes) {
+    const long long numel = 1LL * sc.m * sc.n;
+    for (size_t c0 = 0; c0 < sc.idx.size(); c0 += cd::MAXB) {
+      const int nl = static_cast<int>(std::min<size_t>(cd::MAXB, sc.idx.size() - c0));
+      cd::FormArgs fa{};
+      fa.numel = numel;
+      fa.blocks_per_layer = static_cast<int>(blocks_for(numel));
+      for (int j = 0; j < nl; ++j) {
+        const int li = sc.idx[c0 + j];
+        fa.M[j] = M[li]; fa.G[j] = G[li]; fa.part[j] = g->parts + 1LL * li * g->nparts_stride;
+      }
+      CD_HIP(cd::launch_form_buffer(fa, nl, g->g_bf16, s));
+    }
+  }
+  // 2. gate
+  cd::GateArgs ga{};
+  ga.L = g->L; ga.nparts_stride = g->nparts_stride; ga.parts = g->parts; ga.nparts = g->nparts;
+  ga.prev = g->prev; ga.eps = g->eps; ga.tau = g->tau; ga.out = g->out_dev;
+  CD_HIP(cd::launch_gate(ga, s));
+  // 3. decision point
+  const size_t out_bytes = sizeof(cd::GateOut) + sizeof(double) * g->L;
+  CD_HIP(hipMemcpyAsync(g->out_host, g->out_dev, out_bytes, hipMemcpyDeviceToHost, s));
+  CD_HIP(hipEventRecord(g->ev, s));
+  CD_HIP(hipEventSynchronize(g->ev));
+  const cd::GateOut* go = static_cast<const cd::GateOut*>(g->out_host);
+  const double* rm = reinterpret_cast<const double*>(go + 1);
+  for (cd_layer* L : g->layers) { L->step += 1; L->last_stream = s; }
+  const long long step = g->layers[0]->step;
+  bool sync = false;
+  switch (g->policy) {
+    case CD_POLICY_RMMC: sync = go->flag != 0; break;
+    case CD_POLICY_ALWAYS_SYNC: sync = true; break;
+    case CD_POLICY_NEVER_SYNC: sync = false; break;
+    case CD_POLICY_EVERY_H: sync = (step % g->H) == 0; break;
+  }
+  const double gmax = go->g;
+  const bool nonfinite = go->nonfinite != 0;
+  if (rmmc_per_layer) std::memcpy(rmmc_per_layer, rm, sizeof(double) * g->L);
+
+  // 4. branch
+  for (const ShapeClass& sc : g->shapes) {
+    for (size_t c0 = 0; c0 < sc.idx.size(); c0 += cd::MAXB) {
+      const int nl = static_cast<int>(std::min<size_t>(cd::MAXB, sc.idx.size() - c0));
+      std::vector<int> sel(sc.idx.begin() + c0, sc.idx.begin() + c0 + nl);
+      if (sync) {
+        cd_status st = enqueue_sync(g, sc, sel, M, X, Q, mu, eta, r, s);
+        if (st != CD_OK) return st;
+        for (int li : sel) g->layers[li]->last_r = r;
+      } else {
+        cd::LocalArgs la{};
+        la.numel = 1LL * sc.m * sc.n;
+        la.blocks_per_layer = static_cast<int>(blocks_for(la.numel));
+        for (int j = 0; j < nl; ++j) {
+          const int li = sel[j];
+          la.X[j] = X[li]; la.G[j] = G[li];
+          la.coef[j] = static_cast<float>(g->layers[li]->d.eta_local_scale * static_cast<double>(eta));
+        }
+        CD_HIP(cd::launch_local_update(la, nl, g->g_bf16, s));
+      }
+    }
+  }
+  if (out) { out->rmmc = gmax; out->sync_flag = sync ? 1 : 0; }
+  if (nonfinite) return fail(CD_ENONFINITE, "a layer norm ||B|| was not finite");
+  return CD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
+  try {
+    if (!out) return fail(CD_EINVAL, "out is NULL");
+    *out = nullptr;
+    cd_status st = check_desc(desc);
+    if (st != CD_OK) return st;
+    cd_layer* L = new (std::nothrow) cd_layer();
+    if (!L) return fail(CD_ENOMEM, "host allocation failed");
+    L->d = *desc;
+    if (hipGetDevice(&L->device) != hipSuccess) { delete L; return fail(CD_EHIP, "hipGetDevice failed"); }
+    const int m = desc->m, n = desc->n, rm = desc->r_max;
+    // split-K capacity: the largest partial product any rank r <= r_max needs
+    size_t split_bytes = 8, gram_cap = 1;
+    for (int r = 1; r <= rm; ++r) {
+      int kc;
+      const size_t mr = static_cast<size_t>(m) * r, nr = static_cast<size_t>(n) * r;
+      split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, true, &kc) * mr * sizeof(double));
+      split_bytes = std::max(split_bytes, plan_splits(m, r, r, 1, true, &kc) * mr * sizeof(double));
+      split_bytes = std::max(split_bytes, plan_splits(n, r, m, 1, false, &kc) * nr * sizeof(float));
+      gram_cap = std::max(gram_cap, static_cast<size_t>(plan_splits(r, r, m, 1, true, &kc)) * r * r);
+    }
+    const size_t nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
+    hipError_t e = hipSuccess;
+    if (e == hipSuccess) e = dalloc(&L->prev, 1);
+    if (e == hipSuccess) e = dalloc(&L->rankdef, 1);
+    if (e == hipSuccess) e = dalloc(&L->pa, 1ULL * m * rm);
+    if (e == hipSuccess) e = dalloc(&L->pb, 1ULL * m * rm);
+    if (e == hipSuccess) e = dalloc(&L->P, 1ULL * m * rm);
+    if (e == hipSuccess) e = dalloc(&L->R, 1ULL * n * rm);
+    if (e == hipSuccess) e = dalloc(&L->W, 1ULL * rm * rm);
+    if (e == hipSuccess) e = dalloc(&L->U, 1ULL * rm * rm);
+    if (e == hipSuccess) e = dalloc(&L->gram_part, gram_cap);
+    if (e == hipSuccess) e = hipMalloc(&L->split_part, split_bytes);
+    if (e == hipSuccess) e = dalloc(&L->colsq, nchunks * rm);
+    if (e == hipSuccess) e = dalloc(&L->colnrm, static_cast<size_t>(rm));
+    if (e == hipSuccess) e = hipMemset(L->prev, 0, sizeof(double));
+    if (e == hipSuccess) e = hipMemset(L->rankdef, 0, sizeof(int));
+    if (e != hipSuccess) {
+      free_layer(L);
+      return fail(e == hipErrorOutOfMemory ? CD_ENOMEM : CD_EHIP, "layer allocation: %s",
+                  hipGetErrorString(e));
+    }
+    cd_layer* arr[1] = {L};
+    st = build_group(arr, 1, &L->self);
+    if (st != CD_OK) { free_layer(L); return st; }
+    *out = L;
+    return CD_OK;
+  } catch (...) {
+    return fail(CD_ENOMEM, "exception in cd_layer_create");
+  }
+}
+
+cd_status cd_step(cd_layer* layer, const void* G, float* M, float* X, float* Q, float mu, float eta,
+                  int r, void* stream, cd_result* out) {
+  try {
+    if (!layer) return fail(CD_EINVAL, "layer is NULL");
+    const void* Ga[1] = {G};
+    float* Ma[1] = {M};
+    float* Xa[1] = {X};
+    float* Qa[1] = {Q};
+    return group_step_impl(layer->self, Ga, Ma, Xa, Qa, mu, eta, r, stream, nullptr, out);
+  } catch (...) {
+    return fail(CD_ENOMEM, "exception in cd_step");
+  }
+}
+
+cd_status cd_destroy(cd_layer* layer) {
+  if (!layer) return CD_OK;
+  DeviceGuard dg(layer->device);
+  free_group(layer->self);
+  free_layer(layer);
+  return CD_OK;
+}
+
+cd_status cd_group_create(cd_layer* const* layers, int n_layers, cd_group** out) {
+  try {
+    if (!out) return fail(CD_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!layers || n_layers < 1) return fail(CD_EINVAL, "need at least one layer");
+    if (n_layers > 4096) return fail(CD_EINVAL, "at most 4096 layers per group");
+    for (int i = 0; i < n_layers; ++i) {
+      if (!layers[i]) return fail(CD_EINVAL, "layer %d is NULL", i);
+      const cd_layer_desc& a = layers[0]->d;
+      const cd_layer_desc& b = layers[i]->d;
+      if (a.grad_dtype != b.grad_dtype || a.tau != b.tau || a.policy != b.policy ||
+          (a.policy == CD_POLICY_EVERY_H && a.H != b.H) || a.eps != b.eps ||
+          layers[i]->device != layers[0]->device)
+        return fail(CD_EINVAL, "layer %d differs from layer 0 in dtype, tau, eps, policy, H or device", i);
+      for (int j = 0; j < i; ++j)
+        if (layers[j] == layers[i]) return fail(CD_EINVAL, "layer %d appears twice", i);
+    }
+    return build_group(layers, n_layers, out);
+  } catch (...) {
+    return fail(CD_ENOMEM, "exception in cd_group_create");
+  }
+}
+
+cd_status cd_group_step(cd_group* group, const void* const* G, float* const* M, float* const* X,
+                        float* const* Q, float mu, float eta, int r, void* stream,
+                        double* rmmc_per_layer, cd_result* out) {
+  try {
+    return group_step_impl(group, G, M, X, Q, mu, eta, r, stream, rmmc_per_layer, out);
+  } catch (...) {
+    return fail(CD_ENOMEM, "exception in cd_group_step");
+  }
+}
+
+cd_status cd_group_destroy(cd_group* group) {
+  if (!group) return CD_OK;
+  DeviceGuard dg(group->device);
+  free_group(group);
+  return CD_OK;
+}
+
+cd_status cd_layer_get_state(const cd_layer* layer, double* prev_norm, long long* step) {
+  if (!layer || !prev_norm || !step) return fail(CD_EINVAL, "NULL argument");
+  DeviceGuard dg(layer->device);
+  CD_HIP(hipDeviceSynchronize());
+  CD_HIP(hipMemcpy(prev_norm, layer->prev, sizeof(double), hipMemcpyDeviceToHost));
+  *step = layer->step;
+  return CD_OK;
+}
+
+cd_status cd_layer_set_state(cd_layer* layer, double prev_norm, long long step) {
+  if (!layer) return fail(CD_EINVAL, "layer is NULL");
+  if (step < 0) return fail(CD_EINVAL, "step must be >= 0");
+  DeviceGuard dg(layer->device);
+  CD_HIP(hipDeviceSynchronize());
+  CD_HIP(hipMemcpy(layer->prev, &prev_norm, sizeof(double), hipMemcpyHostToDevice));
+  layer->step = step;
+  return CD_OK;
+}
+
+cd_status cd_layer_last_factors(const cd_layer* layer, const float** P, const float** R) {
+  if (!layer || !P || !R) return fail(CD_EINVAL, "NULL argument");
+  *P = layer->P;
+  *R = layer->R;
+  return CD_OK;
+}
+
+cd_status cd_layer_rank_deficient(const cd_layer* layer, int* flag) {
+  if (!layer || !flag) return fail(CD_EINVAL, "NULL argument");
+  DeviceGuard dg(layer->device);
+  CD_HIP(hipStreamSynchronize(layer->last_stream));
+  CD_HIP(hipMemcpy(flag, layer->rankdef, sizeof(int), hipMemcpyDeviceToHost));
+  return CD_OK;
+}
+
+const char* cd_last_error(void) { return g_err.c_str(); }
+
+int cd_abi_version(void) { return CD_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,139 @@
+// Shared declarations of the CurvaDion HIP kernels (gfx950, wave64).
+//
+// Kernels take small by-value argument structs that carry one pointer per
+// layer for up to CD_MAXB layers of identical shape ("batch"); blockIdx.z (or
+// .y) selects the layer.  Host launchers live next to their kernels and are
+// declared here for the C-ABI layer in api.cpp.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cd {
+
+constexpr int MAXB = 32;          // layers per batched launch
+constexpr int NTHREADS = 256;     // threads per block for the streaming kernels
+constexpr int GBK = 32;           // GEMM k per LDS stage; split-K slices are multiples
+
+// ---- a1: B = M + G and per-block sum of B^2 -------------------------------
+// Every block covers FORM_CHUNK consecutive elements of one layer.
+constexpr int FORM_CHUNK = NTHREADS * 4 * 8;   // 8192 elements
+struct FormArgs {
+  long long numel;                 // elements per layer (m*n)
+  int blocks_per_layer;            // ceil(numel / FORM_CHUNK)
+  float* M[MAXB];                  // in: M_{t-1}; out: B_t
+  const void* G[MAXB];             // fp32 or bf16
+  double* part[MAXB];              // out: blocks_per_layer partial sums of B^2
+};
+hipError_t launch_form_buffer(const FormArgs& a, int nl, bool g_bf16, hipStream_t s);
+
+// ---- local branch: X = X - eta_local G --------------------------------------
+struct LocalArgs {
+  long long numel;
+  int blocks_per_layer;
+  float* X[MAXB];
+  const void* G[MAXB];
+  float coef[MAXB];                // eta_local per layer
+};
+hipError_t launch_local_update(const LocalArgs& a, int nl, bool g_bf16, hipStream_t s);
+
+// ---- gate: fixed-order reduction of the partials, RMMC, prev update, max ----
+struct GateOut {                   // device-side result, copied to the host
+  double g;                        // max over layers of RMMC (NaN if any is NaN)
+  int flag;                        // g > tau
+  int nonfinite;                   // some ‖B‖ was NaN/Inf
+  // followed by L doubles: RMMC per layer
+};
+struct GateArgs {
+  int L;                           // layers in the group
+  int nparts_stride;               // leading dimension of parts (per layer)
+  const double* parts;             // [L][nparts_stride]
+  const int* nparts;               // [L] partials per layer
+  double* const* prev;             // [L] pointers to each layer's prev_norm
+  double eps;
+  double tau;
+  GateOut* out;                    // + L doubles after the header
+};
+hipError_t launch_gate(const GateArgs& a, hipStream_t s);
+
+// ---- skinny GEMM on MFMA ----------------------------------------------------
+// C[M x N] = A[M x K] * B[K x N] for a batch of layers with identical sizes.
+// A(i,k) is at A[i*lda + k] when a_kc (k contiguous) else A[k*lda + i];
+// B(k,j) is at B[j*ldb + k] when b_kc else B[k*ldb + j].  With splits > 1 the
+// K range is cut in `splits` slices and slice s writes its partial product (in
+// the accumulation type) to part + s*split_stride; launch_reduce_splits adds
+// them in order s = 0, 1, ... into C.
+enum class GemmKind {
+  F32,          // fp32 operands, fp32 MFMA, fp32 result
+  F64_FROM_F32, // fp32 operands, fp64 MFMA, fp64 result
+  F64,          // fp64 operands, fp64 MFMA, fp64 result
+  F64_TO_F32    // fp64 operands, fp64 MFMA, result rounded to fp32
+};
+struct GemmArgs {
+  int M, N, K;
+  int lda, ldb, ldc;
+  int splits;
+  int kchunk;                      // K per split (multiple of GBK)
+  long long split_stride;          // elements between split partials
+  bool a_kc, b_kc;
+  bool upper_only;                 // skip tiles strictly below the diagonal
+  const void* A[MAXB];
+  const void* B[MAXB];
+  void* C[MAXB];                   // result (splits == 1) or partials (splits > 1)
+};
+hipError_t launch_gemm(const GemmArgs& a, int nl, GemmKind kind, hipStream_t s);
+int gemm_bm(int N, bool fp64);     // tile rows the launcher uses for this N
+int gemm_bn(int N, bool fp64);     // tile columns
+inline bool gemm_acc64(GemmKind k) { return k != GemmKind::F32; }
+
+// out[i] = sum_{s < splits} part[s*stride + i] in order s = 0, 1, ...
+// Partials are fp64 when part64, and the output is fp64 when out64.
+struct ReduceArgs {
+  long long count;
+  long long stride;
+  int splits;
+  const void* part[MAXB];
+  void* out[MAXB];
+};
+hipError_t launch_reduce_splits(const ReduceArgs& a, int nl, bool part64, bool out64, hipStream_t s);
+
+// ---- Cholesky of the Gram matrix and inverse of the factor -----------------
+// W (r x r fp64, upper triangle read) = T^T T, T upper; writes U = T^{-1}
+// (r x r fp64, zero below the diagonal).  rankdef[l] is set to 1 when a pivot
+// had to be raised to the floor.
+struct CholArgs {
+  int r;
+  int accumulate;                  // 0: rankdef = this factorisation's flag; 1: OR into it
+  double* W[MAXB];
+  double* U[MAXB];
+  int* rankdef[MAXB];
+};
+hipError_t launch_chol_inv(const CholArgs& a, int nl, hipStream_t s);
+
+// ---- ColumnNormalize --------------------------------------------------------
+constexpr int COLNORM_ROWS = 256;  // rows per partial
+struct ColnormArgs {
+  int n, r;
+  int nchunks;                     // ceil(n / COLNORM_ROWS)
+  const float* R[MAXB];
+  double* part[MAXB];              // [nchunks][r]
+  float* nrm[MAXB];                // [r] max(‖R_j‖, floor) as fp32
+  float* Q[MAXB];                  // out: n x r
+};
+hipError_t launch_colnorm(const ColnormArgs& a, int nl, hipStream_t s);
+
+// ---- error-feedback momentum and weight update ------------------------------
+// M = M - (1-mu) P R^T (M holds B on entry); X = X - c P Q^T, c = eta sqrt(m/n)
+struct UpdateArgs {
+  int m, n, r;
+  float one_minus_mu;
+  float c;
+  float* M[MAXB];
+  float* X[MAXB];
+  const float* P[MAXB];
+  const float* R[MAXB];
+  const float* Q[MAXB];
+};
+hipError_t launch_update(const UpdateArgs& a, int nl, hipStream_t s);
+
+}  // namespace cd

@@ -1,0 +1,140 @@
+// Skinny GEMMs of the Dion power iteration (Algorithm 1 / Algorithm 2, sync
+// branch) on MFMA:
+//   P~ = B Q            (m x n . n x r; A = B row-major, k contiguous)
+//   W  = P~^T P~        (Gram matrix, upper tiles only)
+//   P1 = P~ T^{-1}      (apply the inverse Cholesky factor, K = r)
+//   R  = B^T P          (n x m . m x r; A = B^T, i contiguous)
+// The first three run in fp64 (v_mfma_f64_16x16x4_f64 on fp32 or fp64
+// operands): P~ is the ill-conditioned panel, and keeping it, its Gram matrix
+// and the CholQR passes in fp64 makes the orthonormal P accurate to fp32
+// rounding whatever kappa(P~) is.  R = B^T P runs on v_mfma_f32_16x16x4_f32.
+// K can be split over blockIdx.y into partial products that
+// launch_reduce_splits adds in a fixed order (deterministic).
+#include "common.hpp"
+#include "mfma_tile.hpp"
+
+namespace cd {
+namespace {
+
+template <typename T, typename TIn, typename TOut, int BM, int BN>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
+  constexpr int WN_WAVES = (BN >= 64) ? 2 : 1;
+  constexpr int WM_WAVES = 4 / WN_WAVES;
+  constexpr int WM = BM / WM_WAVES, WN = BN / WN_WAVES;
+  constexpr int TM = WM / 16, TN = WN / 16;
+  static_assert(TM >= 1 && TN >= 1, "tile too small");
+  __shared__ __attribute__((aligned(16))) T As[BM * GLDK];
+  __shared__ __attribute__((aligned(16))) T Bs[BN * GLDK];
+
+  const int layer = blockIdx.z;
+  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  const int t = xcd_tile(blockIdx.x, tiles_m * tiles_n);
+  if (t >= tiles_m * tiles_n) return;
+  const int tm = t / tiles_n, tn = t - tm * tiles_n;
+  if (g.upper_only && tm > tn) return;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kb = blockIdx.y * g.kchunk;
+  const int ke = min(g.K, kb + g.kchunk);
+  const TIn* A = static_cast<const TIn*>(g.A[layer]);
+  const TIn* Bm = static_cast<const TIn*>(g.B[layer]);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave / WN_WAVES) * WM, wn0 = (wave % WN_WAVES) * WN;
+
+  typename Mfma<T>::acc_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = typename Mfma<T>::acc_t{};
+
+  for (int k0 = kb; k0 < ke; k0 += GBK) {
+    stage_tile<T, TIn, BM, 256>(As, A, g.lda, g.a_kc, m0, g.M, k0, ke, tid);
+    stage_tile<T, TIn, BN, 256>(Bs, Bm, g.ldb, g.b_kc, n0, g.N, k0, ke, tid);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < GBK; kk += 16) {
+      typename Mfma<T>::vec4_t a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) a[i] = frag<T>(As, wm0 + i * 16, kk, lane);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) b[j] = frag<T>(Bs, wn0 + j * 16, kk, lane);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::mma(a[i][q], b[j][q], acc[i][j]);
+    }
+    __syncthreads();
+  }
+
+  // split partials keep the accumulation type; a single slice writes TOut
+  const bool partial = g.splits > 1;
+  T* Cp = static_cast<T*>(g.C[layer]) + static_cast<long long>(blockIdx.y) * g.split_stride;
+  TOut* Co = static_cast<TOut*>(g.C[layer]);
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = m0 + wm0 + i * 16 + Mfma<T>::out_row(lane, v);
+        const int col = n0 + wn0 + j * 16 + (lane & 15);
+        if (row < g.M && col < g.N) {
+          const long long o = static_cast<long long>(row) * g.ldc + col;
+          if (partial) Cp[o] = acc[i][j][v];
+          else Co[o] = static_cast<TOut>(acc[i][j][v]);
+        }
+      }
+}
+
+template <typename TP, typename TO>
+__global__ __launch_bounds__(256) void k_reduce(ReduceArgs a) {
+  const int l = blockIdx.y;
+  const TP* p = static_cast<const TP*>(a.part[l]);
+  TO* o = static_cast<TO*>(a.out[l]);
+  for (long long i = blockIdx.x * 256LL + threadIdx.x; i < a.count; i += 256LL * gridDim.x) {
+    TP s = p[i];
+    for (int k = 1; k < a.splits; ++k) s += p[k * a.stride + i];
+    o[i] = static_cast<TO>(s);
+  }
+}
+
+template <typename T, typename TIn, typename TOut, int BM, int BN>
+hipError_t launch_t(const GemmArgs& g, int nl, hipStream_t s) {
+  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  const dim3 grid(xcd_grid(tiles), g.splits, nl);
+  hipLaunchKernelGGL((k_gemm<T, TIn, TOut, BM, BN>), grid, dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Tile shape by N (the rank side): 64x64 for N > 32, 128x32, or 256x16.
+int gemm_bm(int N, bool fp64) { return (fp64 || N > 32) ? 64 : (N > 16 ? 128 : 256); }
+int gemm_bn(int N, bool fp64) { return (fp64 || N > 32) ? 64 : (N > 16 ? 32 : 16); }
+
+hipError_t launch_gemm(const GemmArgs& g, int nl, GemmKind kind, hipStream_t s) {
+  if (nl <= 0) return hipSuccess;
+  switch (kind) {
+    case GemmKind::F64_FROM_F32: return launch_t<double, float, double, 64, 64>(g, nl, s);
+    case GemmKind::F64: return launch_t<double, double, double, 64, 64>(g, nl, s);
+    case GemmKind::F64_TO_F32: return launch_t<double, double, float, 64, 64>(g, nl, s);
+    case GemmKind::F32: break;
+  }
+  if (g.N > 32) return launch_t<float, float, float, 64, 64>(g, nl, s);
+  if (g.N > 16) return launch_t<float, float, float, 128, 32>(g, nl, s);
+  return launch_t<float, float, float, 256, 16>(g, nl, s);
+}
+
+hipError_t launch_reduce_splits(const ReduceArgs& a, int nl, bool part64, bool out64, hipStream_t s) {
+  if (nl <= 0 || a.count <= 0) return hipSuccess;
+  long long blocks = (a.count + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  const dim3 grid(static_cast<unsigned>(blocks), nl);
+  if (part64 && out64) hipLaunchKernelGGL((k_reduce<double, double>), grid, dim3(256), 0, s, a);
+  else if (part64) hipLaunchKernelGGL((k_reduce<double, float>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((k_reduce<float, float>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace cd

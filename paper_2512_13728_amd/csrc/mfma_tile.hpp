@@ -1,0 +1,128 @@
+// Building blocks for the MFMA GEMM kernels (gfx950, wave64).
+//
+// Tiles are staged in LDS as [rows][LDK] with k contiguous, whatever the
+// layout in global memory, so that every lane reads its MFMA operands with
+// one 16-byte LDS load: for a 16-wide k slice, lane l of a 16x16x4 MFMA group
+// owns row (l % 16) and k = 4 * (l / 16) + q for the q-th of four MFMAs.  A
+// and B operands use the same k permutation, so the contraction is unchanged.
+// With LDK = 36 (BK = 32 plus 4 pad) the 16 rows read by one b128 load fall on
+// distinct bank groups.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "common.hpp"
+
+namespace cd {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+constexpr int GLDK = GBK + 4;    // padded LDS row
+
+template <typename T> struct Mfma;
+// Output layout: lane l, accumulator register v holds D[out_row(l, v)][l % 16].
+// (Measured on gfx950: fp32 16x16x4 packs four consecutive rows per lane
+// group, fp64 16x16x4 interleaves them with stride 4.)
+template <> struct Mfma<float> {
+  typedef f32x4 acc_t;
+  typedef f32x4 vec4_t;
+  static __device__ __forceinline__ int out_row(int lane, int v) { return 4 * (lane >> 4) + v; }
+  static __device__ __forceinline__ acc_t mma(float a, float b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mfma<double> {
+  typedef f64x4 acc_t;
+  typedef f64x4 vec4_t;
+  static __device__ __forceinline__ int out_row(int lane, int v) { return (lane >> 4) + 4 * v; }
+  static __device__ __forceinline__ acc_t mma(double a, double b, acc_t c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+  }
+};
+
+// Four consecutive elements of an fp32 or fp64 operand (16- or 32-byte load).
+__device__ __forceinline__ void load4(const float* p, float& a, float& b, float& c, float& d) {
+  const float4 f = *reinterpret_cast<const float4*>(p);
+  a = f.x; b = f.y; c = f.z; d = f.w;
+}
+__device__ __forceinline__ void load4(const double* p, double& a, double& b, double& c, double& d) {
+  const double2 f = *reinterpret_cast<const double2*>(p);
+  const double2 g = *reinterpret_cast<const double2*>(p + 2);
+  a = f.x; b = f.y; c = g.x; d = g.y;
+}
+
+// Stage rows [r0, r0 + ROWS) x k in [k0, k0 + GBK) of an operand of element
+// type TIn into S[ROWS][GLDK] (type T), zero-filling rows >= nrows and
+// k >= kend.  kc: element (row, k) at src[row * ld + k]; otherwise at
+// src[k * ld + row].  Vector loads need ld % 4 == 0 (and an aligned base).
+template <typename T, typename TIn, int ROWS, int NT>
+__device__ __forceinline__ void stage_tile(T* __restrict__ S, const TIn* __restrict__ src, int ld,
+                                           bool kc, int r0, int nrows, int k0, int kend, int tid) {
+  const bool vec = (ld & 3) == 0;
+  if (kc) {
+    constexpr int SLOTS = ROWS * (GBK / 4);
+#pragma unroll
+    for (int slot = tid; slot < SLOTS; slot += NT) {
+      const int row = slot / (GBK / 4);
+      const int kq = (slot % (GBK / 4)) * 4;
+      const int gr = r0 + row, gk = k0 + kq;
+      TIn v0 = 0, v1 = 0, v2 = 0, v3 = 0;
+      if (gr < nrows) {
+        const TIn* p = src + static_cast<long long>(gr) * ld + gk;
+        if (vec && gk + 3 < kend) {
+          load4(p, v0, v1, v2, v3);
+        } else {
+          if (gk + 0 < kend) v0 = p[0];
+          if (gk + 1 < kend) v1 = p[1];
+          if (gk + 2 < kend) v2 = p[2];
+          if (gk + 3 < kend) v3 = p[3];
+        }
+      }
+      T* d = S + row * GLDK + kq;
+      d[0] = v0; d[1] = v1; d[2] = v2; d[3] = v3;
+    }
+  } else {
+    constexpr int SLOTS = GBK * (ROWS / 4);
+#pragma unroll
+    for (int slot = tid; slot < SLOTS; slot += NT) {
+      const int kk = slot / (ROWS / 4);
+      const int rq = (slot % (ROWS / 4)) * 4;
+      const int gr = r0 + rq, gk = k0 + kk;
+      TIn v0 = 0, v1 = 0, v2 = 0, v3 = 0;
+      if (gk < kend) {
+        const TIn* p = src + static_cast<long long>(gk) * ld + gr;
+        if (vec && gr + 3 < nrows) {
+          load4(p, v0, v1, v2, v3);
+        } else {
+          if (gr + 0 < nrows) v0 = p[0];
+          if (gr + 1 < nrows) v1 = p[1];
+          if (gr + 2 < nrows) v2 = p[2];
+          if (gr + 3 < nrows) v3 = p[3];
+        }
+      }
+      S[(rq + 0) * GLDK + kk] = v0;
+      S[(rq + 1) * GLDK + kk] = v1;
+      S[(rq + 2) * GLDK + kk] = v2;
+      S[(rq + 3) * GLDK + kk] = v3;
+    }
+  }
+}
+
+// Operand fragment for one 16-row group at k slice kk: four consecutive k.
+template <typename T>
+__device__ __forceinline__ typename Mfma<T>::vec4_t frag(const T* S, int row0, int kk, int lane) {
+  return *reinterpret_cast<const typename Mfma<T>::vec4_t*>(S + (row0 + (lane & 15)) * GLDK + kk +
+                                                            4 * (lane >> 4));
+}
+
+// Block index -> tile index so that consecutive tiles land on the same XCD
+// (workgroups are dispatched round-robin over the 8 XCDs).  The grid must be
+// padded to 8 * per; indices >= ntiles are idle.
+__device__ __forceinline__ int xcd_tile(int b, int ntiles) {
+  const int per = (ntiles + 7) >> 3;
+  return (b & 7) * per + (b >> 3);
+}
+__host__ __device__ inline int xcd_grid(int ntiles) { return ((ntiles + 7) >> 3) * 8; }
+
+}  // namespace cd

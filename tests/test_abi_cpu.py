@@ -1,0 +1,110 @@
+"""CPU checks of the C-ABI library: it loads, exports every function that
+include/curvadion.h declares, and rejects invalid arguments before touching
+the GPU (no compute call is made here)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2512_13728_amd as cdl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "curvadion.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(cdl.library_path):
+        from paper_2512_13728_amd import build
+        build.build()
+    return cdl.lib()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cd_[a-z_]+)\s*\(", text)))
+
+
+def test_header_matches_binding_list():
+    assert header_functions() == sorted(cdl.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol(L):
+    out = subprocess.run(["nm", "-D", "--defined-only", cdl.library_path],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s(cd_[a-z_]+)$", out, flags=re.M))
+    for name in header_functions():
+        assert name in exported, name
+        assert hasattr(L, name)
+    assert L.cd_abi_version() == 1
+
+
+def _desc(**kw):
+    d = dict(m=64, n=32, r_max=8, grad_dtype=cdl.F32, tau=0.5, eps=1e-8, eta_local_scale=1.0,
+             policy=cdl.POLICY_RMMC, H=1)
+    d.update(kw)
+    return cdl.LayerDesc(**d)
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(m=0), "m and n"), (dict(n=-3), "m and n"), (dict(r_max=0), "r_max"),
+    (dict(r_max=33), "r_max"), (dict(m=4000, n=4000, r_max=2000), "1024"),
+    (dict(grad_dtype=7), "dtype"), (dict(policy=9), "policy"),
+    (dict(tau=float("nan")), "tau"), (dict(eps=-1.0), "eps"), (dict(eps=float("inf")), "eps"),
+    (dict(eta_local_scale=-0.5), "eta_local_scale"), (dict(policy=cdl.POLICY_EVERY_H, H=0), "H"),
+])
+def test_layer_create_rejects_bad_descriptors(L, kw, msg):
+    h = ctypes.c_void_p(123)
+    d = _desc(**kw)
+    assert L.cd_layer_create(ctypes.byref(d), ctypes.byref(h)) == cdl.CD_EINVAL
+    assert h.value is None
+    assert msg in L.cd_last_error().decode()
+
+
+def test_null_arguments_are_einval(L):
+    h = ctypes.c_void_p()
+    assert L.cd_layer_create(None, ctypes.byref(h)) == cdl.CD_EINVAL
+    d = _desc()
+    assert L.cd_layer_create(ctypes.byref(d), None) == cdl.CD_EINVAL
+    res = cdl.Result()
+    assert L.cd_step(None, 1, 2, 3, 4, 0.9, 0.01, 4, None, ctypes.byref(res)) == cdl.CD_EINVAL
+    assert L.cd_group_create(None, 1, ctypes.byref(h)) == cdl.CD_EINVAL
+    arr = (ctypes.c_void_p * 1)(None)
+    assert L.cd_group_create(arr, 0, ctypes.byref(h)) == cdl.CD_EINVAL
+    assert L.cd_group_create(arr, 1, ctypes.byref(h)) == cdl.CD_EINVAL
+    assert L.cd_group_step(None, None, None, None, None, 0.9, 0.01, 4, None, None, None) == cdl.CD_EINVAL
+    p, s = ctypes.c_double(), ctypes.c_longlong()
+    assert L.cd_layer_get_state(None, ctypes.byref(p), ctypes.byref(s)) == cdl.CD_EINVAL
+    assert L.cd_layer_set_state(None, 1.0, 0) == cdl.CD_EINVAL
+    P, R = ctypes.c_void_p(), ctypes.c_void_p()
+    assert L.cd_layer_last_factors(None, ctypes.byref(P), ctypes.byref(R)) == cdl.CD_EINVAL
+    f = ctypes.c_int()
+    assert L.cd_layer_rank_deficient(None, ctypes.byref(f)) == cdl.CD_EINVAL
+    assert L.cd_destroy(None) == cdl.CD_OK
+    assert L.cd_group_destroy(None) == cdl.CD_OK
+
+
+def test_product_path_has_no_fallback():
+    """The binding refuses to run without the library: no CPU path exists."""
+    import importlib
+    import paper_2512_13728_amd as mod
+    saved_path, saved_lib = mod.library_path, mod._lib
+    try:
+        mod.library_path = os.path.join(ROOT, "does_not_exist.so")
+        mod._lib = None
+        with pytest.raises(mod.LibraryNotBuilt):
+            mod.Layer(8, 8, 2)
+    finally:
+        mod.library_path, mod._lib = saved_path, saved_lib
+
+
+def test_package_does_not_import_oracle():
+    src_dir = os.path.join(ROOT, "paper_2512_13728_amd")
+    for dirpath, _, files in os.walk(src_dir):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".hpp", ".h")):
+                text = open(os.path.join(dirpath, f), errors="replace").read()
+                assert "oracle" not in text.lower().replace("oracles", ""), f

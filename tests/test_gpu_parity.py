@@ -1,0 +1,249 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on
+the same seeded inputs.  Tolerances (rel-Frobenius, per step, teacher-forced
+unless stated):
+
+* M, X:     1e-5 (fp32 storage and arithmetic of B and of the rank-r update)
+* RMMC:     relative 1e-5 (norms of fp32-rounded B; fp64 accumulation)
+* sync flag: identical; every case asserts its decision margin is > 1e-4
+* P, Q:     max(1e-5, 8 kappa_2(P~) 2^-24): B is rounded to fp32 before the
+            power iteration and the QR factor moves by about kappa u under such
+            a perturbation (Higham, ch. 19); kappa is printed per step
+* dX = X_t - X_{t-1}: that bound plus 2 u ‖X_t‖ / ‖dX‖ (X_t is stored in fp32)
+* P^T P - I and |‖Q_j‖ - 1|: 1e-5 (absolute, Frobenius / max)
+* local branch: M bit-exact against fp32 M + G, X within 1 ulp of fp32 FMA
+Free-running trajectories check every decision against the free-running
+oracle and every step teacher-forced (the oracle restarted from the GPU
+state) with the bounds above; the drift between the two free-running states
+is bounded only loosely (it is a property of the dynamics, not of the kernels).
+"""
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+
+import oracle as O  # noqa: E402
+import paper_2512_13728_amd as cdl  # noqa: E402
+import synthetic as S  # noqa: E402
+from gpu_util import (assert_rmmc_close, f32, f64, qr_tol, rel,  # noqa: E402
+                      step_and_compare)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    cdl.lib()  # fail loudly if the library is missing
+    yield
+
+
+def _state(w, li, r=None, device=DEV):
+    M0, X0, Q0 = S.initial_state(w, li, device="cpu", r=r)
+    return M0.to(device), X0.to(device), Q0.to(device).contiguous()
+
+
+def _print(tag, d):
+    keys = ["flag_gpu", "rmmc_gpu", "err_M", "err_X", "err_dX", "err_Q", "err_P", "orth_P", "kappa"]
+    print(tag, {k: (f"{d[k]:.3g}" if isinstance(d.get(k), float) else d.get(k)) for k in keys if k in d},
+          flush=True)
+
+
+def _check_step(d, tau, policy):
+    assert d["flag_gpu"] == d["flag_oracle"], d
+    assert_rmmc_close(d["rmmc_gpu"], d["rmmc_oracle"])
+    if policy == O.POLICY_RMMC and math.isfinite(d["rmmc_oracle"]):
+        assert abs(d["rmmc_oracle"] - tau) / tau > 1e-4, "decision too close to tau"
+    assert d["err_M"] <= 1e-5, d
+    assert d["err_X"] <= 1e-5, d
+    if d["flag_oracle"]:
+        tol = qr_tol(d["kappa"])
+        assert d["orth_P"] <= 1e-5, d
+        assert d["colnorm_dev"] <= 1e-5, d
+        assert d["err_P"] <= tol, (d, tol)
+        assert d["err_Q"] <= tol, (d, tol)
+        assert d["err_dX"] <= tol + d["dx_floor"], (d, tol)
+    else:
+        assert d["err_Q"] == 0.0
+        assert d["err_dX"] <= 1e-6 + d["dx_floor"], d
+
+
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("m,n,gd", [(13, 7, "f32"), (256, 256, "f32"), (300, 1000, "bf16"),
+                                    (1000, 333, "f32"), (8192 + 5, 3, "bf16")])
+def test_local_branch_exact(m, n, gd):
+    """Local branch: M = M + G bit-exact in fp32; X = X - eta_l G within 1 ulp."""
+    w = S.small_workload(m, n, 1, grad_dtype=gd)
+    M, X, Q = _state(w, 0)
+    L = cdl.Layer(m, n, 1, grad_dtype=gd, policy=cdl.POLICY_NEVER_SYNC, eta_local_scale=0.5)
+    stream = S.GradientStream(w, 0, device="cpu")
+    for t in range(3):
+        G = stream.next().to(DEV)
+        M32, X32, G32 = M.cpu().numpy().copy(), X.cpu().numpy().copy(), G.float().cpu().numpy()
+        rm, flag, _ = L.step(G, M, X, Q, 0.95, 0.01, 1)
+        torch.cuda.synchronize()
+        assert flag is False
+        assert np.array_equal(M.cpu().numpy(), M32 + G32)
+        c = np.float32(np.float32(0.01) * 0.5)
+        Xref = (X32.astype(np.float64) - np.float64(c) * G32.astype(np.float64)).astype(np.float32)
+        ulp = np.abs(X.cpu().numpy().view(np.int32).astype(np.int64) - Xref.view(np.int32).astype(np.int64))
+        assert ulp.max() <= 1
+        assert np.array_equal(Q.cpu().numpy(), _state(w, 0)[2].cpu().numpy())
+
+
+def test_rmmc_exactly_zero_and_deterministic():
+    """After a local step, G = 0 leaves ‖B‖ unchanged: RMMC is exactly 0.
+    Re-running the same inputs gives bit-identical RMMC and state."""
+    w = S.small_workload(777, 1234, 8)
+    results = []
+    for rep in range(2):
+        M, X, Q = _state(w, 0)
+        L = cdl.Layer(777, 1234, 8, policy=cdl.POLICY_RMMC, tau=0.5)
+        stream = S.GradientStream(w, 0, device="cpu")
+        rms = []
+        for t in range(3):
+            G = stream.next().to(DEV)
+            rms.append(L.step(G, M, X, Q, 0.95, 0.01, 8)[0])
+        rm0, flag0, _ = L.step(torch.zeros_like(G), M, X, Q, 0.95, 0.01, 8)
+        torch.cuda.synchronize()
+        results.append((rms, M.cpu().numpy(), X.cpu().numpy(), Q.cpu().numpy()))
+        assert rm0 == 0.0 and flag0 is False
+    assert results[0][0] == results[1][0]
+    for a, b in zip(results[0][1:], results[1][1:]):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("m,n,r", [(256, 256, 16), (300, 1000, 37), (1000, 300, 64), (64, 64, 64),
+                                   (97, 513, 1), (2048, 768, 192), (513, 640, 130)])
+def test_sync_step_teacher_forced(m, n, r):
+    w = S.small_workload(m, n, r, k=max(2, r // 2))
+    M, X, Q = _state(w, 0)
+    L = cdl.Layer(m, n, r, policy=cdl.POLICY_ALWAYS_SYNC)
+    stream = S.GradientStream(w, 0, device="cpu")
+    for t in range(3):
+        G = stream.next().to(DEV)
+        d = step_and_compare(L, G, M, X, Q, 0.95, 0.01, r, 0.5, O.POLICY_ALWAYS_SYNC)
+        _print(f"sync {m}x{n} r={r} t={t + 1}", d)
+        _check_step(d, 0.5, O.POLICY_ALWAYS_SYNC)
+    assert not L.rank_deficient()
+
+
+def test_full_rank_gives_mu_B():
+    """r = m <= n: the sync update leaves M = mu B."""
+    m, n = 48, 80
+    w = S.small_workload(m, n, m)
+    M, X, Q = _state(w, 0)
+    L = cdl.Layer(m, n, m, policy=cdl.POLICY_ALWAYS_SYNC)
+    G = S.GradientStream(w, 0, device="cpu").next().to(DEV)
+    B = f64(M) + f64(G)
+    L.step(G, M, X, Q, 0.9, 0.01, m)
+    torch.cuda.synchronize()
+    assert rel(f64(M), f32(0.9) * B) <= 1e-5
+
+
+def test_zero_buffer_sync_is_defined():
+    """B = 0 on a sync step: P~ = 0 (rank deficient), yet M = 0, Q = 0 and X
+    unchanged, as in the oracle; the layer reports the rank deficiency."""
+    m, n, r = 64, 96, 8
+    L = cdl.Layer(m, n, r, policy=cdl.POLICY_ALWAYS_SYNC)
+    M = torch.zeros(m, n, device=DEV)
+    X = torch.randn(m, n, device=DEV)
+    X0 = X.clone()
+    Q = torch.zeros(n, r, device=DEV)
+    Q[:r, :r] = torch.eye(r, device=DEV)
+    G = torch.zeros(m, n, device=DEV)
+    L.step(G, M, X, Q, 0.95, 0.01, r)
+    torch.cuda.synchronize()
+    assert torch.all(M == 0) and torch.all(Q == 0) and torch.equal(X, X0)
+    assert L.rank_deficient()
+
+
+@pytest.mark.parametrize("tau,policy", [(0.5, O.POLICY_RMMC), (0.1, O.POLICY_RMMC),
+                                        (0.5, O.POLICY_ALWAYS_SYNC)])
+def test_single256_trajectory(tau, policy):
+    """The 256 x 256, r = 16 workload for 20 steps.  Decisions match the
+    free-running oracle at every step; each step also matches a teacher-forced
+    oracle step (started from the GPU's state) within the strict bounds."""
+    w = S.WORKLOADS["single256"]
+    M, X, Q = _state(w, 0)
+    L = cdl.Layer(256, 256, 16, policy=policy, tau=tau)
+    free = O.OracleLayer.from_arrays(f64(M), f64(X), f64(Q))
+    stream = S.GradientStream(w, 0, device="cpu")
+    drift = {"M": 0.0, "Q": 0.0}
+    syncs = []
+    for t in range(w.steps):
+        G = stream.next()
+        d = step_and_compare(L, G.to(DEV), M, X, Q, w.mu, w.eta, 16, tau, policy)
+        _check_step(d, tau, policy)
+        res = O.group_step([free], [f64(G)], f32(w.mu), f32(w.eta), tau, policy=policy)
+        assert d["flag_gpu"] == res["flag"], (t + 1, d["rmmc_gpu"], res["g"])
+        if res["flag"]:
+            syncs.append(t + 1)
+        drift["M"] = max(drift["M"], rel(f64(M), free.M))
+        drift["Q"] = max(drift["Q"], rel(f64(Q), free.Q))
+    print(f"tau={tau} policy={policy} syncs={syncs} free-running drift {drift}", flush=True)
+    assert drift["M"] <= 1e-4 and drift["Q"] <= 1e-2
+
+
+def test_group_mixed_shapes_rmmc_gate():
+    """A group of layers of different (and ragged) shapes: per-layer RMMC, one
+    decision from the max, sync and local steps, against the oracle."""
+    shapes = [(256, 384), (384, 256), (100, 300), (256, 384), (640, 64)]
+    r = 32
+    tau = 0.3
+    w = S.Workload("grp", tuple(shapes), r=r, grad_dtype="f32", steps=6, k=8, tau=tau, stream_id=91)
+    Ls = [cdl.Layer(m, n, r, tau=tau) for m, n in shapes]
+    Gp = cdl.Group(Ls)
+    st = [_state(w, i) for i in range(len(shapes))]
+    OLs = [O.OracleLayer.from_arrays(f64(s[0]), f64(s[1]), f64(s[2])) for s in st]
+    streams = [S.GradientStream(w, i, device="cpu") for i in range(len(shapes))]
+    flags = []
+    for t in range(w.steps):
+        Gs = [s.next() for s in streams]
+        g, flag, per, _ = Gp.step([G.to(DEV) for G in Gs], [s[0] for s in st], [s[1] for s in st],
+                                  [s[2] for s in st], w.mu, w.eta, r)
+        torch.cuda.synchronize()
+        res = O.group_step(OLs, [f64(G) for G in Gs], f32(w.mu), f32(w.eta), tau, with_kappa=True)
+        flags.append(flag)
+        assert flag == res["flag"]
+        assert abs(res["g"] - tau) / tau > 1e-4
+        for a, b in zip(per, res["rmmc"]):
+            assert_rmmc_close(a, b)
+        for s, OL in zip(st, OLs):
+            assert rel(f64(s[0]), OL.M) <= 1e-5 * (t + 1)
+    assert any(flags) and not all(flags)
+
+
+@pytest.mark.parametrize("gd", ["bf16"])
+def test_bf16_gradient_steps(gd):
+    m, n, r = 512, 1536, 64
+    w = S.small_workload(m, n, r, grad_dtype=gd, k=16)
+    M, X, Q = _state(w, 0)
+    L = cdl.Layer(m, n, r, grad_dtype=gd, policy=cdl.POLICY_RMMC, tau=0.5)
+    stream = S.GradientStream(w, 0, device="cpu")
+    for t in range(3):
+        G = stream.next().to(DEV)
+        d = step_and_compare(L, G, M, X, Q, 0.95, 0.01, r, 0.5, O.POLICY_RMMC)
+        _print(f"bf16 t={t + 1}", d)
+        _check_step(d, 0.5, O.POLICY_RMMC)
+
+
+def test_state_roundtrip_and_every_h_policy():
+    m, n, r = 64, 64, 4
+    L = cdl.Layer(m, n, r, policy=cdl.POLICY_EVERY_H, H=3)
+    w = S.small_workload(m, n, r)
+    M, X, Q = _state(w, 0)
+    stream = S.GradientStream(w, 0, device="cpu")
+    flags = [L.step(stream.next().to(DEV), M, X, Q, 0.95, 0.01, r)[1] for _ in range(6)]
+    assert flags == [False, False, True, False, False, True]
+    p, s = L.get_state()
+    assert s == 6 and p > 0
+    L.set_state(123.0, 41)
+    assert L.get_state() == (123.0, 41)
