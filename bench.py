@@ -1,0 +1,270 @@
+#!/usr/bin/env python3
+"""Benchmark of the CurvaDion optimizer step (Dion + RMMC gate) on one MI355X.
+
+Workload (default): the 1.3B-shaped layer set -- the 96 weight matrices of a
+GPT with d_model 2048 and 24 blocks (2048x6144, 2048x2048, 2048x8192,
+8192x2048 per block; 1.208e9 parameters), rank r = 512, bf16 gradients, fp32
+momentum / weights / Q, seeded low-rank(64) + noise gradients, tau = 0.5.
+A "step" is one Algorithm-2 step over the whole set: buffer update and RMMC
+for every layer, the gate, then the branch the gate picks.  The timed region
+replays the workload's trajectory from step 1 (its first step always syncs:
+prev_norm starts at 0), so both branches are timed.
+
+Prints ONE JSON line: params updated per second (whole job), per-branch step
+times, the roofline of the kernel with the largest share of the timed region
+(measured with HIP events around every launch, inside the library), and the
+float64 oracle timed on this host's cores on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--policy rmmc|always|never]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Dion+RMMC optimizer step: params updated/sec/GPU + achieved HBM GB/s"
+PEAK_HBM_GBPS = 8000.0
+PEAK_TFLOPS = {"f64": 78.6, "f32": 157.3}
+# bound and peak per kernel kind reported by the library
+KIND_BOUND = {
+    "form_buffer": ("hbm", None), "local_update": ("hbm", None), "gate": ("hbm", None),
+    "reduce_splits": ("hbm", None), "colnorm": ("hbm", None),
+    "power_bq_f64": ("mfma", "f64"), "gram_f64": ("mfma", "f64"), "trsm_f64": ("mfma", "f64"),
+    "power_btp_f32": ("mfma", "f32"), "update_mx": ("mfma", "f32"), "cholesky_f64": ("mfma", "f64"),
+}
+POLICIES = {"rmmc": 0, "always": 1, "never": 2}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="gpt1p3b")
+    p.add_argument("--policy", default="rmmc", choices=sorted(POLICIES))
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--pool", type=int, default=20, help="distinct gradient sets kept resident")
+    return p.parse_args()
+
+
+def cpu_baseline(w, n_sync: int, n_local: int, steps: int):
+    """Time the float64 oracle on one layer of each distinct shape: one sync
+    step and one local step each, repeated until ~10 s have passed; scale to
+    the full set and to the timed region's mix of branches."""
+    import numpy as np
+    import oracle as O
+    import synthetic as S
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:  # pragma: no cover
+        threadpool_limits = None
+    cores = min(len(os.sched_getaffinity(0)), 16)
+    shapes = sorted(set(w.shapes), key=w.shapes.index)
+    idx = [w.shapes.index(s) for s in shapes]
+    sample_params = sum(m * n for m, n in shapes)
+    data = []
+    for li in idx:
+        M0, X0, Q0 = S.initial_state(w, li, device="cpu")
+        st = S.GradientStream(w, li, device="cpu")
+        G1, G2 = st.next().double().numpy(), st.next().double().numpy()
+        data.append((M0.double().numpy(), X0.double().numpy(), Q0.double().numpy(), G1, G2))
+    ctx = threadpool_limits(cores) if threadpool_limits else None
+    t_sync = t_local = 0.0
+    reps = 0
+    t_start = time.perf_counter()
+    try:
+        while reps == 0 or (time.perf_counter() - t_start < 10.0 and reps < 5):
+            Ls = [O.OracleLayer.from_arrays(M, X, Q) for (M, X, Q, _, _) in data]
+            t0 = time.perf_counter()
+            O.group_step(Ls, [d[3] for d in data], w.mu, w.eta, w.tau, policy=O.POLICY_ALWAYS_SYNC)
+            t1 = time.perf_counter()
+            O.group_step(Ls, [d[4] for d in data], w.mu, w.eta, w.tau, policy=O.POLICY_NEVER_SYNC)
+            t2 = time.perf_counter()
+            t_sync += t1 - t0
+            t_local += t2 - t1
+            reps += 1
+    finally:
+        if ctx is not None:
+            ctx.__exit__(None, None, None)
+    per_param_sync = t_sync / reps / sample_params
+    per_param_local = t_local / reps / sample_params
+    t_job = w.params * (n_sync * per_param_sync + n_local * per_param_local)
+    return {
+        "value": w.params * steps / t_job,
+        "unit": "params/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"float64 oracle, {len(shapes)} layers (one per shape, {sample_params} params), "
+                   f"1 sync + 1 local step x {reps} reps; scaled to {w.params} params and the timed "
+                   f"mix of {n_sync} sync + {n_local} local steps"),
+        "sync_step_s": per_param_sync * w.params,
+        "local_step_s": per_param_local * w.params,
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(the data-parallel all-reduces are identities at one worker). "
+              "Run without --gpus or with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2512_13728_amd as cdl
+    import synthetic as S
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = S.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    policy = POLICIES[args.policy]
+    K, W = args.steps, args.warmup
+    L = len(w.shapes)
+    log(f"[bench] workload {w.name}: {L} matrices, {w.params} params, r={w.r}, G {w.grad_dtype}")
+
+    layers = [cdl.Layer(m, n, w.r, grad_dtype=w.grad_dtype, tau=w.tau, eps=w.eps, policy=policy)
+              for (m, n) in w.shapes]
+    group = cdl.Group(layers)
+    t0 = time.perf_counter()
+    init = [S.initial_state(w, i, device=dev) for i in range(L)]
+    M = [s[0].clone() for s in init]
+    X = [s[1].clone() for s in init]
+    Q = [s[2].clone() for s in init]
+    pool = max(1, min(args.pool, max(K, W)))
+    streams = [S.GradientStream(w, i, device=dev) for i in range(L)]
+    grads = [[st.next() for st in streams] for _ in range(pool)]
+    torch.cuda.synchronize()
+    log(f"[bench] inputs resident in HBM ({pool} gradient sets) in {time.perf_counter() - t0:.1f}s")
+
+    def reset():
+        for i in range(L):
+            M[i].copy_(init[i][0]); X[i].copy_(init[i][1]); Q[i].copy_(init[i][2])
+        torch.cuda.synchronize()
+        for lay in layers:
+            lay.set_state(0.0, 0)
+
+    for t in range(W):
+        group.step(grads[t % pool], M, X, Q, w.mu, w.eta, w.r)
+    torch.cuda.synchronize()
+    reset()
+    log(f"[bench] {W} warmup steps done; timing {K} steps from step 1")
+
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    flags, rmmcs = [], []
+    group.set_timing(True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    ev[0].record(stream)
+    for t in range(K):
+        g, flag, _, _ = group.step(grads[t % pool], M, X, Q, w.mu, w.eta, w.r)
+        ev[t + 1].record(stream)
+        flags.append(flag)
+        rmmcs.append(g)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    kt = group.kernel_times()
+    group.set_timing(False)
+    step_ms = [ev[t].elapsed_time(ev[t + 1]) for t in range(K)]
+    log(f"[bench] timed {K} steps in {elapsed * 1e3:.2f} ms; syncs at "
+        f"{[t + 1 for t, f in enumerate(flags) if f]}")
+
+    n_sync = sum(flags)
+    n_local = K - n_sync
+    sync_ms = [x for x, f in zip(step_ms, flags) if f]
+    local_ms = [x for x, f in zip(step_ms, flags) if not f]
+    total_bytes = sum(v["bytes"] for v in kt.values())
+    total_flops = sum(v["flops"] for v in kt.values())
+    for name, v in sorted(kt.items(), key=lambda kv: -kv[1]["total_ms"]):
+        log(f"[bench]   {name:16s} launches {v['launches']:5d}  {v['total_ms']:9.3f} ms  "
+            f"{v['bytes'] / max(v['total_ms'], 1e-9) / 1e6:8.1f} GB/s  "
+            f"{v['flops'] / max(v['total_ms'], 1e-9) / 1e9:8.2f} TFLOP/s")
+
+    dom, dv = max(kt.items(), key=lambda kv: kv[1]["total_ms"])
+    bound, prec = KIND_BOUND.get(dom, ("hbm", None))
+    avg_ms = dv["total_ms"] / dv["launches"]
+    if bound == "hbm":
+        achieved = dv["bytes"] / dv["launches"] / (avg_ms * 1e-3) / 1e9
+        peak, unit = PEAK_HBM_GBPS, "GB/s"
+    else:
+        achieved = dv["flops"] / dv["launches"] / (avg_ms * 1e-3) / 1e12
+        peak, unit = PEAK_TFLOPS[prec], "TFLOP/s"
+    roofline = {"bound": bound, "kernel": dom, "achieved": round(achieved, 3), "peak": peak,
+                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                "avg_launch_ms": round(avg_ms, 4), "launches": dv["launches"],
+                "algorithmic_bytes_per_launch": dv["bytes"] / dv["launches"],
+                "algorithmic_flops_per_launch": dv["flops"] / dv["launches"]}
+
+    def branch(ms_list, count):
+        if not ms_list:
+            return {"count": 0}
+        med = float(np.median(ms_list))
+        return {"count": count, "median_ms": round(med, 4), "min_ms": round(min(ms_list), 4),
+                "max_ms": round(max(ms_list), 4), "params_per_s": w.params / (med * 1e-3)}
+
+    branches = {"sync": branch(sync_ms, n_sync), "local": branch(local_ms, n_local)}
+    if local_ms:
+        # per local step: one form_buffer launch per shape class + gate + one local_update per class
+        per_step_bytes = (kt["form_buffer"]["bytes"] / (n_sync + n_local)
+                          + kt["local_update"]["bytes"] / max(n_local, 1))
+        branches["local"]["algorithmic_GBps"] = per_step_bytes / (branches["local"]["median_ms"] * 1e-3) / 1e9
+        branches["local"]["frac_of_hbm_peak"] = branches["local"]["algorithmic_GBps"] / PEAK_HBM_GBPS
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the float64 oracle on a bounded sample ...")
+        cpu = cpu_baseline(w, n_sync, n_local, K)
+        log(f"[bench] oracle: {cpu['value']:.3e} params/s on {cpu['cores']} cores")
+
+    value = w.params * K / elapsed
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": elapsed * 1e3 / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{w.name}: {L} matrices of the 1.3B-shaped GPT set (d_model 2048, 24 blocks)"
+                         if w.name == "gpt1p3b" else w.name),
+            "params": w.params, "rank": w.r, "grad_dtype": w.grad_dtype, "state_dtype": "f32",
+            "power_iteration_dtype": "f64 (P~, Gram, CholQR), f32 (R = B^T P, M/X update)",
+            "policy": args.policy, "tau": w.tau, "trajectory_steps": K,
+            "sync_steps": n_sync, "local_steps": n_local, "parallelism": "none (1 GPU)",
+        },
+        "hbm_GBps": total_bytes / elapsed / 1e9,
+        "achieved_TFLOPs": total_flops / elapsed / 1e12,
+        "branches": branches,
+        "roofline": roofline,
+        "kernels": {k: {"launches": v["launches"], "total_ms": round(v["total_ms"], 4)}
+                    for k, v in kt.items()},
+        "rmmc_trace": [None if (isinstance(x, float) and math.isnan(x)) else x for x in rmmcs],
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

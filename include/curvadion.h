@@ -143,6 +143,26 @@ cd_status cd_layer_last_factors(const cd_layer* layer, const float** P, const fl
  * are not unique.  *flag = 0 otherwise. */
 cd_status cd_layer_rank_deficient(const cd_layer* layer, int* flag);
 
+/* Kernel timing, for measurement.  While timing is on, every kernel launch of
+ * the group's steps is bracketed by two HIP events recorded on the launch
+ * stream.  cd_group_kernel_times() waits for the last recorded event, then
+ * returns one entry per kernel kind that ran since timing was switched on (or
+ * since the previous query): launch count, summed event time, and the
+ * algorithmic bytes and flops of those launches (compulsory traffic of the
+ * inputs and outputs each kernel must touch, and the flops of its arithmetic
+ * as written in the method; neither counts re-reads or padding).  Records are
+ * cleared by each query.  *count receives the number of kinds available even
+ * when it exceeds max_kinds. */
+typedef struct cd_kernel_time {
+  char name[32];
+  int launches;
+  double total_ms;
+  double bytes;
+  double flops;
+} cd_kernel_time;
+cd_status cd_group_set_timing(cd_group* group, int enable);
+cd_status cd_group_kernel_times(cd_group* group, cd_kernel_time* out, int max_kinds, int* count);
+
 /* Thread-local text of the last error on this thread ("" if none). */
 const char* cd_last_error(void);
 

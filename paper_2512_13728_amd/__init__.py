@@ -32,7 +32,8 @@ _STATUS = {0: "CD_OK", -1: "CD_EINVAL", -2: "CD_ENOMEM", -3: "CD_EHIP",
 EXPORTED_SYMBOLS = (
     "cd_layer_create", "cd_step", "cd_destroy", "cd_group_create", "cd_group_step",
     "cd_group_destroy", "cd_layer_get_state", "cd_layer_set_state",
-    "cd_layer_last_factors", "cd_layer_rank_deficient", "cd_last_error", "cd_abi_version",
+    "cd_layer_last_factors", "cd_layer_rank_deficient", "cd_group_set_timing",
+    "cd_group_kernel_times", "cd_last_error", "cd_abi_version",
 )
 
 
@@ -55,6 +56,12 @@ class LayerDesc(ctypes.Structure):
 
 class Result(ctypes.Structure):
     _fields_ = [("rmmc", ctypes.c_double), ("sync_flag", ctypes.c_int)]
+
+
+class KernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int),
+                ("total_ms", ctypes.c_double), ("bytes", ctypes.c_double),
+                ("flops", ctypes.c_double)]
 
 
 _lib = None
@@ -82,6 +89,8 @@ def lib() -> ctypes.CDLL:
     L.cd_layer_set_state.argtypes = [vp, d, ctypes.c_longlong]
     L.cd_layer_last_factors.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp)]
     L.cd_layer_rank_deficient.argtypes = [vp, ctypes.POINTER(i)]
+    L.cd_group_set_timing.argtypes = [vp, i]
+    L.cd_group_kernel_times.argtypes = [vp, ctypes.POINTER(KernelTime), i, ctypes.POINTER(i)]
     L.cd_last_error.restype = ctypes.c_char_p
     L.cd_last_error.argtypes = []
     L.cd_abi_version.restype = i
@@ -195,6 +204,20 @@ class Group:
                                  _stream_handle(stream), per, ctypes.byref(res))
         _check(st, allow=(CD_OK, CD_ENONFINITE))
         return res.rmmc, bool(res.sync_flag), list(per), st
+
+    def set_timing(self, enable: bool) -> None:
+        """Bracket every kernel launch with HIP events (see kernel_times)."""
+        _check(lib().cd_group_set_timing(self._h, 1 if enable else 0))
+
+    def kernel_times(self) -> dict:
+        """{kind: dict(launches, total_ms, bytes, flops)} since timing was
+        switched on or since the previous call (which clears the records)."""
+        buf = (KernelTime * 32)()
+        n = ctypes.c_int()
+        _check(lib().cd_group_kernel_times(self._h, buf, 32, ctypes.byref(n)))
+        return {buf[k].name.decode(): dict(launches=buf[k].launches, total_ms=buf[k].total_ms,
+                                           bytes=buf[k].bytes, flops=buf[k].flops)
+                for k in range(min(n.value, 32))}
 
     def close(self) -> None:
         if self._h is not None and _lib is not None:

@@ -81,6 +81,34 @@ hipError_t dalloc(T** p, size_t count) {
   return hipMalloc(reinterpret_cast<void**>(p), count * sizeof(T));
 }
 
+// ---- optional per-kernel timing (HIP events on the launch stream) ----------
+enum Kind { K_FORM, K_GATE, K_LOCAL, K_PBQ, K_GRAM, K_CHOL, K_APPLY, K_PBTP, K_REDUCE, K_COLNORM,
+            K_UPDATE, K_NKINDS };
+const char* const kKindName[K_NKINDS] = {
+    "form_buffer", "gate", "local_update", "power_bq_f64", "gram_f64", "cholesky_f64",
+    "trsm_f64", "power_btp_f32", "reduce_splits", "colnorm", "update_mx"};
+
+struct Timer {
+  struct Rec { int kind; hipEvent_t a, b; double bytes, flops; };
+  bool on = false;
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t get() {
+    hipEvent_t e = nullptr;
+    if (!pool.empty()) { e = pool.back(); pool.pop_back(); return e; }
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+  void release() {
+    for (auto& r : recs) { pool.push_back(r.a); pool.push_back(r.b); }
+    recs.clear();
+  }
+  ~Timer() {
+    release();
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+  }
+};
+
 }  // namespace
 
 struct cd_layer {
@@ -93,8 +121,9 @@ struct cd_layer {
   double* pb = nullptr;         // m x r_max fp64: P~ after the first CholQR pass
   float* P = nullptr;           // m x r_max fp32: the orthonormal P
   float* R = nullptr;           // n x r_max
-  double* W = nullptr;          // r_max^2 Gram / Cholesky factor
-  double* U = nullptr;          // r_max^2 inverse factor
+  double* W = nullptr;          // r_max^2 Gram matrix, then its Cholesky factor
+  double* Dinv = nullptr;       // inverses of the 64 x 64 diagonal blocks of the factor
+  double* floor_ = nullptr;     // pivot floor of the current factorisation
   double* gram_part = nullptr;  // split-K partials of the Gram matrix
   void* split_part = nullptr;   // split-K partials of the skinny GEMMs (fp32 or fp64)
   double* colsq = nullptr;      // column sum-of-squares partials
@@ -125,13 +154,18 @@ struct cd_group {
   cd::GateOut* out_dev = nullptr;
   void* out_host = nullptr;     // pinned
   hipEvent_t ev = nullptr;
+  cd::CholTab* chol_tab = nullptr;      // [L] static workspace pointers
+  cd::TrsmTab* trsm_tab[2] = {nullptr, nullptr};  // CholQR pass 0 / 1
+  int2* trsm_tiles = nullptr;           // (layer, 64-row tile) pairs
+  int ntiles = 0;
+  Timer timer;
 };
 
 namespace {
 
 void free_layer(cd_layer* L) {
   if (!L) return;
-  void* ptrs[] = {L->prev, L->rankdef, L->pa, L->pb, L->P, L->R, L->W, L->U,
+  void* ptrs[] = {L->prev, L->rankdef, L->pa, L->pb, L->P, L->R, L->W, L->Dinv, L->floor_,
                   L->gram_part, L->split_part, L->colsq, L->colnrm};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
@@ -146,6 +180,10 @@ void free_group(cd_group* g) {
   if (g->out_dev) (void)hipFree(g->out_dev);
   if (g->out_host) (void)hipHostFree(g->out_host);
   if (g->ev) (void)hipEventDestroy(g->ev);
+  if (g->chol_tab) (void)hipFree(g->chol_tab);
+  if (g->trsm_tab[0]) (void)hipFree(g->trsm_tab[0]);
+  if (g->trsm_tab[1]) (void)hipFree(g->trsm_tab[1]);
+  if (g->trsm_tiles) (void)hipFree(g->trsm_tiles);
   delete g;
 }
 
@@ -176,10 +214,19 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   if (!dg.ok) { free_group(g); return fail(CD_EHIP, "cannot select device %d", g->device); }
   std::vector<int> np(n);
   std::vector<double*> pv(n);
+  std::vector<cd::CholTab> ct(n);
+  std::vector<cd::TrsmTab> t0(n), t1(n);
+  std::vector<int2> tiles;
   for (int i = 0; i < n; ++i) {
-    np[i] = static_cast<int>(blocks_for(1LL * layers[i]->d.m * layers[i]->d.n));
-    pv[i] = layers[i]->prev;
+    cd_layer* L = layers[i];
+    np[i] = static_cast<int>(blocks_for(1LL * L->d.m * L->d.n));
+    pv[i] = L->prev;
+    ct[i] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef};
+    t0[i] = cd::TrsmTab{L->pa, L->pb, L->W, L->Dinv, L->d.m};
+    t1[i] = cd::TrsmTab{L->pb, L->P, L->W, L->Dinv, L->d.m};
+    for (int rt = 0; rt < (L->d.m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) tiles.push_back(int2{i, rt});
   }
+  g->ntiles = static_cast<int>(tiles.size());
   hipError_t e = hipSuccess;
   if (e == hipSuccess) e = dalloc(&g->parts, static_cast<size_t>(n) * g->nparts_stride);
   if (e == hipSuccess) e = dalloc(&g->nparts, n);
@@ -190,6 +237,15 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   if (e == hipSuccess) e = hipEventCreateWithFlags(&g->ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipMemcpy(g->nparts, np.data(), sizeof(int) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->prev, pv.data(), sizeof(double*) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = dalloc(&g->chol_tab, n);
+  if (e == hipSuccess) e = dalloc(&g->trsm_tab[0], n);
+  if (e == hipSuccess) e = dalloc(&g->trsm_tab[1], n);
+  if (e == hipSuccess) e = dalloc(&g->trsm_tiles, tiles.size());
+  if (e == hipSuccess) e = hipMemcpy(g->chol_tab, ct.data(), sizeof(cd::CholTab) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[0], t0.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[1], t1.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(g->trsm_tiles, tiles.data(), sizeof(int2) * tiles.size(), hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     free_group(g);
     return fail(e == hipErrorOutOfMemory ? CD_ENOMEM : CD_EHIP, "group setup: %s",
@@ -215,16 +271,37 @@ cd_status check_desc(const cd_layer_desc* d) {
   return CD_OK;
 }
 
-// Enqueue the sync branch for the layers `sel` (all of one shape) of group g.
+// Launch through `launch`, bracketed by timing events when timing is on.
+template <typename F>
+cd_status run(cd_group* g, int kind, double bytes, double flops, hipStream_t s, F&& launch) {
+  if (!g->timer.on) {
+    CD_HIP(launch());
+    return CD_OK;
+  }
+  hipEvent_t a = g->timer.get(), b = g->timer.get();
+  if (!a || !b) return fail(CD_EHIP, "hipEventCreate failed");
+  CD_HIP(hipEventRecord(a, s));
+  CD_HIP(launch());
+  CD_HIP(hipEventRecord(b, s));
+  g->timer.recs.push_back(Timer::Rec{kind, a, b, bytes, flops});
+  return CD_OK;
+}
+
+// One stage of the sync branch for the layers `sel` (all of one shape):
+//   0: P~ = B Q (fp64)            1, 2: Gram matrix of CholQR pass 0 / 1
+//   3: R = B^T P, ColumnNormalize, the M / X update
+// The Cholesky factorisations and triangular solves run between the stages
+// over all layers at once (enqueue_orthogonalize).
 cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>& sel,
                        float* const* M, float* const* X, float* const* Q, float mu, float eta,
-                       int r, hipStream_t s) {
+                       int r, int stage, hipStream_t s) {
   const int m = sc.m, n = sc.n, nl = static_cast<int>(sel.size());
   auto lay = [&](int j) { return g->layers[sel[j]]; };
 
   // skinny GEMM C = A.B with optional split-K and fixed-order reduction
-  auto gemm = [&](cd::GemmKind kind, int Mr, int Nr, int K, bool a_kc, int lda, bool b_kc, int ldb,
-                  bool upper, auto Aof, auto Bof, auto Cof, auto Pof) -> cd_status {
+  auto gemm = [&](int tkind, double flops, double bytes, cd::GemmKind kind, int Mr, int Nr, int K,
+                  bool a_kc, int lda, bool b_kc, int ldb, bool upper, auto Aof, auto Bof, auto Cof,
+                  auto Pof) -> cd_status {
     const bool acc64 = cd::gemm_acc64(kind);
     cd::GemmArgs ga{};
     ga.M = Mr; ga.N = Nr; ga.K = K; ga.lda = lda; ga.ldb = ldb; ga.ldc = Nr;
@@ -236,48 +313,39 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
       ga.B[j] = Bof(j);
       ga.C[j] = ga.splits > 1 ? Pof(j) : Cof(j);
     }
-    CD_HIP(cd::launch_gemm(ga, nl, kind, s));
+    cd_status st2 = run(g, tkind, bytes * nl, flops * nl, s, [&] { return cd::launch_gemm(ga, nl, kind, s); });
+    if (st2 != CD_OK) return st2;
     if (ga.splits > 1) {
       cd::ReduceArgs ra{};
       ra.count = 1LL * Mr * Nr; ra.stride = ga.split_stride; ra.splits = ga.splits;
       for (int j = 0; j < nl; ++j) { ra.part[j] = Pof(j); ra.out[j] = Cof(j); }
       const bool out64 = kind == cd::GemmKind::F64 || kind == cd::GemmKind::F64_FROM_F32;
-      CD_HIP(cd::launch_reduce_splits(ra, nl, acc64, out64, s));
+      const double rb = static_cast<double>(ra.count) * nl * (acc64 ? 8.0 : 4.0) * (ga.splits + 1);
+      st2 = run(g, K_REDUCE, rb, 0.0, s, [&] { return cd::launch_reduce_splits(ra, nl, acc64, out64, s); });
+      if (st2 != CD_OK) return st2;
     }
     return CD_OK;
   };
   auto part = [&](int j) { return lay(j)->split_part; };
-  cd_status st;
-  // P~ = B Q in fp64 (B lives in M)
-  st = gemm(cd::GemmKind::F64_FROM_F32, m, r, n, true, n, false, r, false,
-            [&](int j) { return static_cast<const void*>(M[sel[j]]); },
-            [&](int j) { return static_cast<const void*>(Q[sel[j]]); },
-            [&](int j) { return static_cast<void*>(lay(j)->pa); }, part);
-  if (st != CD_OK) return st;
-  // Orthogonalize: two CholQR passes in fp64, pa -> pb -> P (rounded to fp32)
-  for (int pass = 0; pass < 2; ++pass) {
+  const double mn = 1.0 * m * n, mr = 1.0 * m * r, nr = 1.0 * n * r, rr = 1.0 * r * r;
+  if (stage == 0) {
+    // P~ = B Q in fp64 (B lives in M)
+    return gemm(K_PBQ, 2.0 * mn * r, 4.0 * mn + 4.0 * nr + 8.0 * mr, cd::GemmKind::F64_FROM_F32, m, r,
+                n, true, n, false, r, false,
+                [&](int j) { return static_cast<const void*>(M[sel[j]]); },
+                [&](int j) { return static_cast<const void*>(Q[sel[j]]); },
+                [&](int j) { return static_cast<void*>(lay(j)->pa); }, part);
+  }
+  if (stage == 1 || stage == 2) {
+    const int pass = stage - 1;
     auto In = [&](int j) { return static_cast<const void*>(pass == 0 ? lay(j)->pa : lay(j)->pb); };
-    st = gemm(cd::GemmKind::F64, r, r, m, false, r, false, r, true, In, In,
-              [&](int j) { return static_cast<void*>(lay(j)->W); },
-              [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
-    if (st != CD_OK) return st;
-    cd::CholArgs ca{};
-    ca.r = r;
-    ca.accumulate = pass;
-    for (int j = 0; j < nl; ++j) {
-      ca.W[j] = lay(j)->W; ca.U[j] = lay(j)->U; ca.rankdef[j] = lay(j)->rankdef;
-    }
-    CD_HIP(cd::launch_chol_inv(ca, nl, s));
-    st = gemm(pass == 0 ? cd::GemmKind::F64 : cd::GemmKind::F64_TO_F32, m, r, r, true, r, false, r,
-              false, In, [&](int j) { return static_cast<const void*>(lay(j)->U); },
-              [&](int j) {
-                return pass == 0 ? static_cast<void*>(lay(j)->pb) : static_cast<void*>(lay(j)->P);
-              },
-              part);
-    if (st != CD_OK) return st;
+    return gemm(K_GRAM, mr * (r + 1), 8.0 * mr + 8.0 * rr, cd::GemmKind::F64, r, r, m, false, r, false,
+                r, true, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); },
+                [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
   }
   // R = B^T P
-  st = gemm(cd::GemmKind::F32, n, r, m, false, n, false, r, false,
+  cd_status st = gemm(K_PBTP, 2.0 * mn * r, 4.0 * mn + 4.0 * mr + 4.0 * nr, cd::GemmKind::F32, n, r, m, false,
+            n, false, r, false,
             [&](int j) { return static_cast<const void*>(M[sel[j]]); },
             [&](int j) { return static_cast<const void*>(lay(j)->P); },
             [&](int j) { return static_cast<void*>(lay(j)->R); }, part);
@@ -288,7 +356,8 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   for (int j = 0; j < nl; ++j) {
     cn.R[j] = lay(j)->R; cn.part[j] = lay(j)->colsq; cn.nrm[j] = lay(j)->colnrm; cn.Q[j] = Q[sel[j]];
   }
-  CD_HIP(cd::launch_colnorm(cn, nl, s));
+  st = run(g, K_COLNORM, 12.0 * nr * nl, 3.0 * nr * nl, s, [&] { return cd::launch_colnorm(cn, nl, s); });
+  if (st != CD_OK) return st;
   // M = B - (1 - mu) P R^T;  X -= eta sqrt(m/n) P Q^T
   cd::UpdateArgs ua{};
   ua.m = m; ua.n = n; ua.r = r;
@@ -297,8 +366,25 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   for (int j = 0; j < nl; ++j) {
     ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]]; ua.P[j] = lay(j)->P; ua.R[j] = lay(j)->R; ua.Q[j] = Q[sel[j]];
   }
-  CD_HIP(cd::launch_update(ua, nl, s));
-  return CD_OK;
+  return run(g, K_UPDATE, 16.0 * mn * nl, 4.0 * mn * r * nl, s, [&] { return cd::launch_update(ua, nl, s); });
+}
+
+// CholQR pass `pass` over every layer: Cholesky of each W, then P = P~ T^{-1}
+// (pass 0: pa -> pb in fp64; pass 1: pb -> P rounded to fp32).
+cd_status enqueue_orthogonalize(cd_group* g, int r, int pass, hipStream_t s) {
+  const double L = g->L, rr = 1.0 * r * r;
+  cd_status st = run(g, K_CHOL, 16.0 * rr * L, (1.0 / 3.0) * rr * r * L, s,
+                     [&] { return cd::launch_cholesky(g->chol_tab, g->L, r, pass, s); });
+  if (st != CD_OK) return st;
+  double flops = 0, bytes = 0;
+  for (const cd_layer* Ly : g->layers) {
+    const double mr = 1.0 * Ly->d.m * r;
+    flops += mr * r;
+    bytes += 8.0 * mr + (pass == 0 ? 8.0 : 4.0) * mr + 8.0 * rr / 2;
+  }
+  return run(g, K_APPLY, bytes, flops, s, [&] {
+    return cd::launch_trsm(g->trsm_tab[pass], g->trsm_tiles, g->ntiles, r, true, pass == 0, s);
+  });
 }
 
 cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, float* const* X,
@@ -332,14 +418,20 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
         const int li = sc.idx[c0 + j];
         fa.M[j] = M[li]; fa.G[j] = G[li]; fa.part[j] = g->parts + 1LL * li * g->nparts_stride;
       }
-      CD_HIP(cd::launch_form_buffer(fa, nl, g->g_bf16, s));
+      const double fb = static_cast<double>(numel) * nl * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
+      cd_status st = run(g, K_FORM, fb, 3.0 * numel * nl, s,
+                         [&] { return cd::launch_form_buffer(fa, nl, g->g_bf16, s); });
+      if (st != CD_OK) return st;
     }
   }
   // 2. gate
   cd::GateArgs ga{};
   ga.L = g->L; ga.nparts_stride = g->nparts_stride; ga.parts = g->parts; ga.nparts = g->nparts;
   ga.prev = g->prev; ga.eps = g->eps; ga.tau = g->tau; ga.out = g->out_dev;
-  CD_HIP(cd::launch_gate(ga, s));
+  {
+    cd_status st = run(g, K_GATE, 8.0 * g->L * g->nparts_stride, 0.0, s, [&] { return cd::launch_gate(ga, s); });
+    if (st != CD_OK) return st;
+  }
   // 3. decision point
   const size_t out_bytes = sizeof(cd::GateOut) + sizeof(double) * g->L;
   CD_HIP(hipMemcpyAsync(g->out_host, g->out_dev, out_bytes, hipMemcpyDeviceToHost, s));
@@ -361,26 +453,45 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   if (rmmc_per_layer) std::memcpy(rmmc_per_layer, rm, sizeof(double) * g->L);
 
   // 4. branch
-  for (const ShapeClass& sc : g->shapes) {
-    for (size_t c0 = 0; c0 < sc.idx.size(); c0 += cd::MAXB) {
-      const int nl = static_cast<int>(std::min<size_t>(cd::MAXB, sc.idx.size() - c0));
-      std::vector<int> sel(sc.idx.begin() + c0, sc.idx.begin() + c0 + nl);
-      if (sync) {
-        cd_status st = enqueue_sync(g, sc, sel, M, X, Q, mu, eta, r, s);
+  auto for_chunks = [&](auto&& fn) -> cd_status {
+    for (const ShapeClass& sc : g->shapes) {
+      for (size_t c0 = 0; c0 < sc.idx.size(); c0 += cd::MAXB) {
+        const int nl = static_cast<int>(std::min<size_t>(cd::MAXB, sc.idx.size() - c0));
+        std::vector<int> sel(sc.idx.begin() + c0, sc.idx.begin() + c0 + nl);
+        cd_status st = fn(sc, sel);
         if (st != CD_OK) return st;
-        for (int li : sel) g->layers[li]->last_r = r;
-      } else {
-        cd::LocalArgs la{};
-        la.numel = 1LL * sc.m * sc.n;
-        la.blocks_per_layer = static_cast<int>(blocks_for(la.numel));
-        for (int j = 0; j < nl; ++j) {
-          const int li = sel[j];
-          la.X[j] = X[li]; la.G[j] = G[li];
-          la.coef[j] = static_cast<float>(g->layers[li]->d.eta_local_scale * static_cast<double>(eta));
-        }
-        CD_HIP(cd::launch_local_update(la, nl, g->g_bf16, s));
       }
     }
+    return CD_OK;
+  };
+  if (sync) {
+    for (int stage = 0; stage < 4; ++stage) {
+      cd_status st = for_chunks([&](const ShapeClass& sc, const std::vector<int>& sel) {
+        return enqueue_sync(g, sc, sel, M, X, Q, mu, eta, r, stage, s);
+      });
+      if (st != CD_OK) return st;
+      if (stage == 1 || stage == 2) {
+        st = enqueue_orthogonalize(g, r, stage - 1, s);
+        if (st != CD_OK) return st;
+      }
+    }
+    for (cd_layer* Ly : g->layers) Ly->last_r = r;
+  } else {
+    cd_status st = for_chunks([&](const ShapeClass& sc, const std::vector<int>& sel) -> cd_status {
+      const int nl = static_cast<int>(sel.size());
+      cd::LocalArgs la{};
+      la.numel = 1LL * sc.m * sc.n;
+      la.blocks_per_layer = static_cast<int>(blocks_for(la.numel));
+      for (int j = 0; j < nl; ++j) {
+        const int li = sel[j];
+        la.X[j] = X[li]; la.G[j] = G[li];
+        la.coef[j] = static_cast<float>(g->layers[li]->d.eta_local_scale * static_cast<double>(eta));
+      }
+      const double lb = static_cast<double>(la.numel) * nl * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
+      return run(g, K_LOCAL, lb, 2.0 * la.numel * nl, s,
+                 [&] { return cd::launch_local_update(la, nl, g->g_bf16, s); });
+    });
+    if (st != CD_OK) return st;
   }
   if (out) { out->rmmc = gmax; out->sync_flag = sync ? 1 : 0; }
   if (nonfinite) return fail(CD_ENONFINITE, "a layer norm ||B|| was not finite");
@@ -421,7 +532,9 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
     if (e == hipSuccess) e = dalloc(&L->P, 1ULL * m * rm);
     if (e == hipSuccess) e = dalloc(&L->R, 1ULL * n * rm);
     if (e == hipSuccess) e = dalloc(&L->W, 1ULL * rm * rm);
-    if (e == hipSuccess) e = dalloc(&L->U, 1ULL * rm * rm);
+    const size_t nblk = (rm + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK;
+    if (e == hipSuccess) e = dalloc(&L->Dinv, nblk * cd::CHOL_BLOCK * cd::CHOL_BLOCK);
+    if (e == hipSuccess) e = dalloc(&L->floor_, 1);
     if (e == hipSuccess) e = dalloc(&L->gram_part, gram_cap);
     if (e == hipSuccess) e = hipMalloc(&L->split_part, split_bytes);
     if (e == hipSuccess) e = dalloc(&L->colsq, nchunks * rm);
@@ -502,6 +615,46 @@ cd_status cd_group_destroy(cd_group* group) {
   if (!group) return CD_OK;
   DeviceGuard dg(group->device);
   free_group(group);
+  return CD_OK;
+}
+
+cd_status cd_group_set_timing(cd_group* group, int enable) {
+  if (!group) return fail(CD_EINVAL, "group is NULL");
+  DeviceGuard dg(group->device);
+  if (!group->timer.recs.empty()) {
+    CD_HIP(hipEventSynchronize(group->timer.recs.back().b));
+    group->timer.release();
+  }
+  group->timer.on = enable != 0;
+  return CD_OK;
+}
+
+cd_status cd_group_kernel_times(cd_group* group, cd_kernel_time* out, int max_kinds, int* count) {
+  if (!group || !count || (max_kinds > 0 && !out)) return fail(CD_EINVAL, "NULL argument");
+  DeviceGuard dg(group->device);
+  Timer& t = group->timer;
+  cd_kernel_time agg[K_NKINDS];
+  for (int k = 0; k < K_NKINDS; ++k) {
+    std::memset(&agg[k], 0, sizeof(agg[k]));
+    std::snprintf(agg[k].name, sizeof(agg[k].name), "%s", kKindName[k]);
+  }
+  if (!t.recs.empty()) CD_HIP(hipEventSynchronize(t.recs.back().b));
+  for (const auto& r : t.recs) {
+    float ms = 0.f;
+    CD_HIP(hipEventElapsedTime(&ms, r.a, r.b));
+    agg[r.kind].launches += 1;
+    agg[r.kind].total_ms += ms;
+    agg[r.kind].bytes += r.bytes;
+    agg[r.kind].flops += r.flops;
+  }
+  t.release();
+  int n = 0;
+  for (int k = 0; k < K_NKINDS; ++k) {
+    if (agg[k].launches == 0) continue;
+    if (n < max_kinds) out[n] = agg[k];
+    ++n;
+  }
+  *count = n;
   return CD_OK;
 }
 

@@ -97,18 +97,31 @@ struct ReduceArgs {
 };
 hipError_t launch_reduce_splits(const ReduceArgs& a, int nl, bool part64, bool out64, hipStream_t s);
 
-// ---- Cholesky of the Gram matrix and inverse of the factor -----------------
-// W (r x r fp64, upper triangle read) = T^T T, T upper; writes U = T^{-1}
-// (r x r fp64, zero below the diagonal).  rankdef[l] is set to 1 when a pivot
-// had to be raised to the floor.
-struct CholArgs {
-  int r;
-  int accumulate;                  // 0: rankdef = this factorisation's flag; 1: OR into it
-  double* W[MAXB];
-  double* U[MAXB];
-  int* rankdef[MAXB];
+// ---- Cholesky of the Gram matrix and triangular solve ------------------------
+// Per-layer workspace pointers (static for the life of a group) for the
+// blocked fp64 Cholesky W = T^T T (T overwrites the upper triangle of W, r x r,
+// ld = r) and the inverses D_k of its CHOL_BLOCK x CHOL_BLOCK diagonal blocks.
+constexpr int CHOL_BLOCK = 64;
+struct CholTab {
+  double* W;
+  double* Dinv;                    // ceil(r / CHOL_BLOCK) blocks of 64 x 64
+  double* floor_;                  // pivot floor of the current factorisation
+  int* rankdef;                    // set to 1 when a pivot was raised to the floor
 };
-hipError_t launch_chol_inv(const CholArgs& a, int nl, hipStream_t s);
+// All CHOL_BLOCK steps for `nlayers` layers of rank r; `pass` 0 clears rankdef.
+hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s);
+
+// P = P~ T^{-1} by block columns (in place is not allowed: Pin != Pout).
+struct TrsmTab {
+  const void* Pin;                 // m x r, fp64 or fp32
+  void* Pout;                      // m x r, fp64 or fp32
+  const double* W;                 // T in the upper triangle
+  const double* Dinv;
+  int m;
+};
+// tiles: one (layer, 64-row tile) pair per workgroup.
+hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r, bool in64, bool out64,
+                       hipStream_t s);
 
 // ---- ColumnNormalize --------------------------------------------------------
 constexpr int COLNORM_ROWS = 256;  // rows per partial

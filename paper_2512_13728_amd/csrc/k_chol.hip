@@ -1,200 +1,297 @@
-// Cholesky factor of the Gram matrix and its inverse, for the CholQR
-// orthonormalisation of P~ (the paper's Orthogonalize step is unspecified; the
-// thin-QR factor with positive-diagonal R is what it computes here).
+// Orthogonalize (the paper leaves the method open; here: the thin-QR factor
+// with positive-diagonal R, by CholQR): given the Gram matrix W = P~^T P~,
+// factor W = T^T T (T upper triangular) and form P = P~ T^{-1}.
 //
-// W = P~^T P~ = T^T T with T upper triangular, then U = T^{-1}; P~ U has
-// orthonormal columns and P~ = (P~ U) T is the thin QR factorisation.
-// One 1024-thread workgroup factors one layer's r x r matrix (r <= 1024) in
-// fp64: right-looking blocked Cholesky with 16-row panels staged in LDS, then
-// a blocked back-substitution for the inverse, bottom row-block first.  A
-// pivot that is not above floor = 1e-13 * max_k W_kk (or is NaN) is raised to
-// the floor and the layer is flagged rank deficient.
+// Blocked in CB = 64 columns, fp64 throughout, every launch batched over all
+// layers of the group (they share r):
+//   chol_diag  (one workgroup per layer)  T_kk = chol(W_kk) in LDS and its
+//              inverse D_k = T_kk^{-1}; the first block also sets the pivot
+//              floor 1e-13 * max_i W_ii (smaller or NaN pivots are raised to
+//              it and the layer is flagged rank deficient)
+//   chol_panel X = D_k^T W[k, k+1:]: the k-th block row of T       (fp64 MFMA)
+//   chol_trail W[k+1:, k+1:] -= X^T X, upper tiles only            (fp64 MFMA)
+// and the triangular solve, one launch per block column c:
+//   P[:, c] = (P~[:, c] - P[:, :c] T[:c, c]) D_c                   (fp64 MFMA)
 #include "common.hpp"
+#include "mfma_tile.hpp"
 
 namespace cd {
 namespace {
 
-constexpr int CNB = 16;
-constexpr int CT = 1024;
-constexpr int NW = CT / 64;
+constexpr int CB = CHOL_BLOCK;
+constexpr int DLD = CB + 1;   // padded LDS row of the diagonal block
 
-__global__ __launch_bounds__(CT) void k_chol_inv(CholArgs a) {
-  extern __shared__ double Pn[];              // CNB x r panel
-  __shared__ double D[CNB][CNB + 1];
-  __shared__ double E[CNB][CNB + 1];
-  __shared__ double red[NW];
+__global__ __launch_bounds__(256) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
+                                                   int pass) {
+  __shared__ double A[CB][DLD];
+  __shared__ double E[CB][DLD];
+  __shared__ double red[4];
   __shared__ double s_floor;
-  __shared__ int s_rankdef;
-  const int l = blockIdx.x, r = a.r, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  double* __restrict__ W = a.W[l];
-  double* __restrict__ U = a.U[l];
+  __shared__ int s_def;
+  const CholTab t = tab[blockIdx.x];
+  const int tid = threadIdx.x;
   const long long ld = r;
-
-  double md = 0.0;
-  for (int k = tid; k < r; k += CT) {
-    const double d = W[k * ld + k];
-    if (d > md) md = d;
-  }
+  const int k0 = kb * CB, nb = min(CB, r - k0);
+  if (kb == 0) {
+    double md = 0.0;
+    for (int k = tid; k < r; k += 256) md = fmax(md, t.W[k * ld + k]);
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) md = fmax(md, __shfl_xor(md, o, 64));
-  if (lane == 0) red[wave] = md;
+    for (int o = 32; o > 0; o >>= 1) md = fmax(md, __shfl_xor(md, o, 64));
+    if ((tid & 63) == 0) red[tid >> 6] = md;
+    __syncthreads();
+    if (tid == 0) {
+      const double m = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+      *t.floor_ = fmax(1e-13 * m, 1e-300);
+      if (pass == 0) *t.rankdef = 0;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) { s_floor = *t.floor_; s_def = 0; }
+  for (int idx = tid; idx < CB * CB; idx += 256) {
+    const int i = idx / CB, j = idx % CB;
+    A[i][j] = (i < nb && j < nb && j >= i) ? t.W[(k0 + i) * ld + k0 + j] : 0.0;
+  }
   __syncthreads();
-  if (tid == 0) {
-    double m = 0.0;
-    for (int i = 0; i < NW; ++i) m = fmax(m, red[i]);
-    s_floor = fmax(1e-13 * m, 1e-300);
-    s_rankdef = 0;
+  const double fl = s_floor;
+  for (int p = 0; p < nb; ++p) {
+    if (tid == 0) {
+      double d = A[p][p];
+      if (!(d > fl)) { d = fl; s_def = 1; }
+      A[p][p] = sqrt(d);
+    }
+    __syncthreads();
+    if (tid > p && tid < nb) A[p][tid] /= A[p][p];
+    __syncthreads();
+    for (int idx = tid; idx < CB * CB; idx += 256) {
+      const int i = idx / CB, j = idx % CB;
+      if (i > p && i < nb && j >= i && j < nb) A[i][j] -= A[p][i] * A[p][j];
+    }
+    __syncthreads();
+  }
+  // D = T_kk^{-1}: column c by back substitution (T D = I)
+  if (tid < CB) {
+    const int c = tid;
+    for (int i = CB - 1; i >= 0; --i) {
+      double v = 0.0;
+      if (i < nb && c < nb && i <= c) {
+        double s = (i == c) ? 1.0 : 0.0;
+        for (int p = i + 1; p <= c; ++p) s -= A[i][p] * E[p][c];
+        v = s / A[i][i];
+      }
+      E[i][c] = v;
+    }
   }
   __syncthreads();
-  const double floor_ = s_floor;
+  for (int idx = tid; idx < CB * CB; idx += 256) {
+    const int i = idx / CB, j = idx % CB;
+    if (i < nb && j < nb && j >= i) t.W[(k0 + i) * ld + k0 + j] = A[i][j];
+    t.Dinv[static_cast<long long>(kb) * CB * CB + idx] = E[i][j];
+  }
+  if (tid == 0 && s_def) *t.rankdef = 1;
+}
 
-  // ---- Cholesky: T overwrites the upper triangle of W --------------------
-  for (int k0 = 0; k0 < r; k0 += CNB) {
-    const int nb = min(CNB, r - k0), k1 = k0 + nb;
-    if (tid < CNB * CNB) {
-      const int i = tid / CNB, j = tid % CNB;
-      D[i][j] = (i < nb && j < nb && j >= i) ? W[(k0 + i) * ld + k0 + j] : 0.0;
-    }
-    __syncthreads();
-    for (int p = 0; p < nb; ++p) {
-      if (tid == 0) {
-        double d = D[p][p];
-        if (!(d > floor_)) { d = floor_; s_rankdef = 1; }
-        D[p][p] = sqrt(d);
-      }
-      __syncthreads();
-      if (tid > p && tid < nb) D[p][tid] /= D[p][p];
-      __syncthreads();
-      if (tid < CNB * CNB) {
-        const int i = tid / CNB, j = tid % CNB;
-        if (i > p && i < nb && j >= i && j < nb) D[i][j] -= D[p][i] * D[p][j];
-      }
-      __syncthreads();
-    }
-    if (tid < CNB * CNB) {
-      const int i = tid / CNB, j = tid % CNB;
-      if (i < nb && j < nb && j >= i) W[(k0 + i) * ld + k0 + j] = D[i][j];
-    }
-    // panel row block: T_kk^T X = W[k0:k1, k1:r].  The empty asm with a memory
-    // clobber keeps the compiler from hoisting all of D into registers.
-#pragma unroll 1
-    for (int c = k1 + tid; c < r; c += CT) {
-      __asm__ volatile("" ::: "memory");
-      double x[CNB];
+// 64 x 64 fp64 MFMA tile: acc += A(64 x K) B(K x 64) with both operands staged
+// through LDS ([row][k] layout).  4 waves as 2 x 2, each 32 x 32.
+struct Tile64 {
+  f64x4 acc[2][2];
+  __device__ void zero() {
 #pragma unroll
-      for (int p = 0; p < CNB; ++p) {
-        x[p] = 0.0;
-        if (p < nb) {
-          double v = W[(k0 + p) * ld + c];
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int q = 0; q < p; ++q) v -= D[q][p] * x[q];
-          x[p] = v / D[p][p];
-        }
-      }
-#pragma unroll
-      for (int p = 0; p < CNB; ++p)
-        if (p < nb) {
-          W[(k0 + p) * ld + c] = x[p];
-          Pn[p * r + c] = x[p];
-        }
-    }
-    __syncthreads();
-    // trailing update of the upper triangle: W[i][j] -= sum_p X[p][i] X[p][j]
-    for (int i = k1 + wave; i < r; i += NW) {
-      double pi[CNB];
-#pragma unroll
-      for (int p = 0; p < CNB; ++p) pi[p] = (p < nb) ? Pn[p * r + i] : 0.0;
-#pragma unroll 1
-      for (int j = i + lane; j < r; j += 64) {
-        double s = 0.0;
-#pragma unroll
-        for (int p = 0; p < CNB; ++p)
-          if (p < nb) s += pi[p] * Pn[p * r + j];
-        W[i * ld + j] -= s;
-      }
-    }
-    __syncthreads();
+      for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{};
   }
+  __device__ void mma_stage(const double* As, const double* Bs, int wm0, int wn0, int lane) {
+#pragma unroll
+    for (int kk = 0; kk < GBK; kk += 16) {
+      f64x4 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = frag<double>(As, wm0 + i * 16, kk, lane);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = frag<double>(Bs, wn0 + j * 16, kk, lane);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+    }
+  }
+};
 
-  // ---- U = T^{-1}, row blocks from the bottom ------------------------------
-  const int nblk = (r + CNB - 1) / CNB;
-  for (int bi = nblk - 1; bi >= 0; --bi) {
-    const int k0 = bi * CNB, nb = min(CNB, r - k0), k1 = k0 + nb;
-    if (tid < CNB * CNB) {
-      const int i = tid / CNB, j = tid % CNB;
-      D[i][j] = (i < nb && j < nb && j >= i) ? W[(k0 + i) * ld + k0 + j] : 0.0;
-    }
+__global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ tab, int r, int kb) {
+  __shared__ __attribute__((aligned(16))) double As[CB * GLDK];
+  __shared__ __attribute__((aligned(16))) double Bs[CB * GLDK];
+  const CholTab t = tab[blockIdx.y];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
+  const int k0 = kb * CB, nb = min(CB, r - k0), k1 = k0 + nb;
+  const int j0 = k1 + blockIdx.x * CB;
+  const double* D = t.Dinv + static_cast<long long>(kb) * CB * CB;
+  const double* Wp = t.W + static_cast<long long>(k0) * r;  // block row k
+  Tile64 T;
+  T.zero();
+  for (int kk0 = 0; kk0 < nb; kk0 += GBK) {
+    // A(i, k) = D[k][i];  B(k, j) = W[k0 + k][j0 + j]
+    stage_tile<double, double, CB, 256>(As, D, CB, false, 0, nb, kk0, nb, tid);
+    stage_tile<double, double, CB, 256>(Bs, Wp + j0, r, false, 0, r - j0, kk0, nb, tid);
     __syncthreads();
-    if (tid < nb) {
-      const int c = tid;
-      E[c][c] = 1.0 / D[c][c];
-      for (int i = c - 1; i >= 0; --i) {
-        double s = 0.0;
-        for (int p = i + 1; p <= c; ++p) s += D[i][p] * E[p][c];
-        E[i][c] = -s / D[i][i];
-      }
-      for (int i = c + 1; i < CNB; ++i) E[i][c] = 0.0;
-    }
-    const int w = r - k1;
-    for (int idx = tid; idx < nb * w; idx += CT) {
-      const int p = idx / w, c = k1 + idx % w;
-      Pn[p * r + c] = W[(k0 + p) * ld + c];
-    }
-    __syncthreads();
-    // U[k0+i][c] = -sum_p E[i][p] * sum_{q=k1..c} T[k0+p][q] U[q][c]
-#pragma unroll 1
-    for (int c = k1 + tid; c < r; c += CT) {
-      double S[CNB];
-#pragma unroll
-      for (int p = 0; p < CNB; ++p) S[p] = 0.0;
-#pragma unroll 2
-      for (int q = k1; q <= c; ++q) {
-        const double u = U[q * ld + c];
-#pragma unroll
-        for (int p = 0; p < CNB; ++p)
-          if (p < nb) S[p] += Pn[p * r + q] * u;
-      }
-      __asm__ volatile("" ::: "memory");
-#pragma unroll
-      for (int i = 0; i < CNB; ++i)
-        if (i < nb) {
-          double v = 0.0;
-#pragma unroll
-          for (int p = 0; p < CNB; ++p)
-            if (p >= i && p < nb) v += E[i][p] * S[p];
-          U[(k0 + i) * ld + c] = -v;
-        }
-    }
-    if (tid < CNB * CNB) {
-      const int i = tid / CNB, j = tid % CNB;
-      if (i < nb && j < nb) U[(k0 + i) * ld + k0 + j] = (j >= i) ? E[i][j] : 0.0;
-    }
+    T.mma_stage(As, Bs, wm0, wn0, lane);
     __syncthreads();
   }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = wm0 + i * 16 + Mfma<double>::out_row(lane, v);
+        const int col = j0 + wn0 + j * 16 + (lane & 15);
+        if (row < nb && col < r) t.W[static_cast<long long>(k0 + row) * r + col] = T.acc[i][j][v];
+      }
+}
 
-  // zero the strictly lower triangle so U can be used as a full r x r operand
-  for (long long idx = tid; idx < ld * ld; idx += CT) {
-    const long long i = idx / ld, j = idx - i * ld;
-    if (j < i) U[idx] = 0.0;
+__global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ tab, int r, int kb) {
+  __shared__ __attribute__((aligned(16))) double As[CB * GLDK];
+  __shared__ __attribute__((aligned(16))) double Bs[CB * GLDK];
+  const CholTab t = tab[blockIdx.y];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
+  const int k0 = kb * CB, nb = min(CB, r - k0), k1 = k0 + nb;
+  const int nt = (r - k1 + CB - 1) / CB;
+  int u = blockIdx.x, ti = 0;
+  while (u >= nt - ti) { u -= nt - ti; ++ti; }
+  const int tj = ti + u;
+  const int i0 = k1 + ti * CB, j0 = k1 + tj * CB;
+  const double* X = t.W + static_cast<long long>(k0) * r;   // rows k0..k1 of T
+  Tile64 T;
+  T.zero();
+  for (int kk0 = 0; kk0 < nb; kk0 += GBK) {
+    // A(i, p) = X[p][i0 + i];  B(p, j) = X[p][j0 + j]
+    stage_tile<double, double, CB, 256>(As, X + i0, r, false, 0, r - i0, kk0, nb, tid);
+    stage_tile<double, double, CB, 256>(Bs, X + j0, r, false, 0, r - j0, kk0, nb, tid);
+    __syncthreads();
+    T.mma_stage(As, Bs, wm0, wn0, lane);
+    __syncthreads();
   }
-  if (tid == 0) {
-    if (a.accumulate) {
-      if (s_rankdef) *a.rankdef[l] = 1;
-    } else {
-      *a.rankdef[l] = s_rankdef;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = i0 + wm0 + i * 16 + Mfma<double>::out_row(lane, v);
+        const int col = j0 + wn0 + j * 16 + (lane & 15);
+        if (row < r && col < r) t.W[static_cast<long long>(row) * r + col] -= T.acc[i][j][v];
+      }
+}
+
+// Block column c of P = P~ T^{-1}; one 64-row tile of one layer per workgroup.
+template <typename TIn, typename TOut>
+__global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, const int2* __restrict__ tiles,
+                                              int r, int cb) {
+  constexpr int YLD = CB + 4;
+  __shared__ __attribute__((aligned(16))) double As[CB * GLDK];
+  __shared__ __attribute__((aligned(16))) double Bs[CB * GLDK];
+  __shared__ __attribute__((aligned(16))) double Ys[CB * YLD];
+  const int2 lt = tiles[blockIdx.x];
+  const TrsmTab t = tab[lt.x];
+  const int m = t.m;
+  const int i0 = lt.y * CB;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
+  const int c0 = cb * CB, nbc = min(CB, r - c0);
+  const TIn* Pin = static_cast<const TIn*>(t.Pin);
+  TOut* Pout = static_cast<TOut*>(t.Pout);
+  Tile64 T;
+  T.zero();
+  // acc = P[:, :c0] T[:c0, c0:c0+64]   (P is the output: earlier block columns)
+  for (int k0 = 0; k0 < c0; k0 += GBK) {
+    stage_tile<double, TOut, CB, 256>(As, Pout + static_cast<long long>(i0) * r, r, true, 0, m - i0,
+                                      k0, c0, tid);
+    stage_tile<double, double, CB, 256>(Bs, t.W + c0, r, false, 0, nbc, k0, c0, tid);
+    __syncthreads();
+    T.mma_stage(As, Bs, wm0, wn0, lane);
+    __syncthreads();
+  }
+  // Y = P~[:, c-block] - acc, into LDS as the next A operand ([row][k], k = column)
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = wm0 + i * 16 + Mfma<double>::out_row(lane, v);
+        const int col = wn0 + j * 16 + (lane & 15);
+        double y = 0.0;
+        if (i0 + row < m && col < nbc)
+          y = static_cast<double>(Pin[static_cast<long long>(i0 + row) * r + c0 + col]) - T.acc[i][j][v];
+        Ys[row * YLD + col] = y;
+      }
+  const double* D = t.Dinv + static_cast<long long>(cb) * CB * CB;
+  T.zero();
+  for (int k0 = 0; k0 < nbc; k0 += GBK) {
+    stage_tile<double, double, CB, 256>(Bs, D, CB, false, 0, nbc, k0, nbc, tid);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < GBK; kk += 16) {
+      f64x4 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        a[i] = *reinterpret_cast<const f64x4*>(Ys + (wm0 + i * 16 + (lane & 15)) * YLD + k0 + kk +
+                                               4 * (lane >> 4));
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = frag<double>(Bs, wn0 + j * 16, kk, lane);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            T.acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i][q], b[j][q], T.acc[i][j], 0, 0, 0);
     }
+    __syncthreads();
   }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = wm0 + i * 16 + Mfma<double>::out_row(lane, v);
+        const int col = wn0 + j * 16 + (lane & 15);
+        if (i0 + row < m && col < nbc)
+          Pout[static_cast<long long>(i0 + row) * r + c0 + col] = static_cast<TOut>(T.acc[i][j][v]);
+      }
 }
 
 }  // namespace
 
-hipError_t launch_chol_inv(const CholArgs& a, int nl, hipStream_t s) {
-  if (nl <= 0) return hipSuccess;
-  if (a.r < 1 || a.r > 1024) return hipErrorInvalidValue;
-  const size_t lds = static_cast<size_t>(CNB) * a.r * sizeof(double);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_chol_inv),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, CNB * 1024 * 8);
-  hipLaunchKernelGGL(k_chol_inv, dim3(nl), dim3(CT), lds, s, a);
+hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s) {
+  if (nlayers <= 0) return hipSuccess;
+  if (r < 1) return hipErrorInvalidValue;
+  const int nblk = (r + CB - 1) / CB;
+  for (int kb = 0; kb < nblk; ++kb) {
+    hipLaunchKernelGGL(k_chol_diag, dim3(nlayers), dim3(256), 0, s, tab, r, kb, pass);
+    const int k1 = min(r, (kb + 1) * CB);
+    if (k1 >= r) break;
+    const int nt = (r - k1 + CB - 1) / CB;
+    hipLaunchKernelGGL(k_chol_panel, dim3(nt, nlayers), dim3(256), 0, s, tab, r, kb);
+    hipLaunchKernelGGL(k_chol_trail, dim3(nt * (nt + 1) / 2, nlayers), dim3(256), 0, s, tab, r, kb);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r, bool in64, bool out64,
+                       hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  const int nblk = (r + CB - 1) / CB;
+  for (int cb = 0; cb < nblk; ++cb) {
+    if (in64 && out64) hipLaunchKernelGGL((k_trsm<double, double>), dim3(ntiles), dim3(256), 0, s, tab, tiles, r, cb);
+    else if (in64) hipLaunchKernelGGL((k_trsm<double, float>), dim3(ntiles), dim3(256), 0, s, tab, tiles, r, cb);
+    else if (out64) hipLaunchKernelGGL((k_trsm<float, double>), dim3(ntiles), dim3(256), 0, s, tab, tiles, r, cb);
+    else hipLaunchKernelGGL((k_trsm<float, float>), dim3(ntiles), dim3(256), 0, s, tab, tiles, r, cb);
+  }
   return hipGetLastError();
 }
 
