@@ -31,13 +31,16 @@ sys.path.insert(0, ROOT)
 
 METRIC = "Dion+RMMC optimizer step: params updated/sec/GPU + achieved HBM GB/s"
 PEAK_HBM_GBPS = 8000.0
-PEAK_TFLOPS = {"f64": 78.6, "f32": 157.3}
-# bound and peak per kernel kind reported by the library
+PEAK_TFLOPS = {"f64": 78.6, "f32": 157.3, "bf16": 2500.0}
+# bound, MFMA dtype and executed MFMA flops per algorithmic flop, per kernel kind
+# (bf16x6: each fp32 product is formed from six bf16 piece products)
 KIND_BOUND = {
-    "form_buffer": ("hbm", None), "local_update": ("hbm", None), "gate": ("hbm", None),
-    "reduce_splits": ("hbm", None), "colnorm": ("hbm", None),
-    "power_bq_f64": ("mfma", "f64"), "gram_f64": ("mfma", "f64"), "trsm_f64": ("mfma", "f64"),
-    "power_btp_f32": ("mfma", "f32"), "update_mx": ("mfma", "f32"), "cholesky_f64": ("mfma", "f64"),
+    "form_buffer": ("hbm", None, 1), "local_update": ("hbm", None, 1), "gate": ("hbm", None, 1),
+    "reduce_splits": ("hbm", None, 1), "colnorm": ("hbm", None, 1),
+    "power_bq_f64": ("mfma", "f64", 1), "gram_f64": ("mfma", "f64", 1), "trsm_f64": ("mfma", "f64", 1),
+    "cholesky_f64": ("mfma", "f64", 1), "power_bq_bf16x6": ("mfma", "bf16", 6),
+    "power_btp_bf16x6": ("mfma", "bf16", 6), "update_bf16x6": ("mfma", "bf16", 6),
+    "update_bf16": ("hbm", None, 1),
 }
 POLICIES = {"rmmc": 0, "always": 1, "never": 2}
 
@@ -197,13 +200,13 @@ def main():
             f"{v['flops'] / max(v['total_ms'], 1e-9) / 1e9:8.2f} TFLOP/s")
 
     dom, dv = max(kt.items(), key=lambda kv: kv[1]["total_ms"])
-    bound, prec = KIND_BOUND.get(dom, ("hbm", None))
+    bound, prec, mult = KIND_BOUND.get(dom, ("hbm", None, 1))
     avg_ms = dv["total_ms"] / dv["launches"]
     if bound == "hbm":
         achieved = dv["bytes"] / dv["launches"] / (avg_ms * 1e-3) / 1e9
         peak, unit = PEAK_HBM_GBPS, "GB/s"
     else:
-        achieved = dv["flops"] / dv["launches"] / (avg_ms * 1e-3) / 1e12
+        achieved = mult * dv["flops"] / dv["launches"] / (avg_ms * 1e-3) / 1e12
         peak, unit = PEAK_TFLOPS[prec], "TFLOP/s"
     roofline = {"bound": bound, "kernel": dom, "achieved": round(achieved, 3), "peak": peak,
                 "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
@@ -250,7 +253,11 @@ def main():
             "workload": (f"{w.name}: {L} matrices of the 1.3B-shaped GPT set (d_model 2048, 24 blocks)"
                          if w.name == "gpt1p3b" else w.name),
             "params": w.params, "rank": w.r, "grad_dtype": w.grad_dtype, "state_dtype": "f32",
-            "power_iteration_dtype": "f64 (P~, Gram, CholQR), f32 (R = B^T P, M/X update)",
+            "power_iteration_dtype": ("P~ = BQ and R = B^T P on bf16 MFMA with 3-piece fp32 splits "
+                                      "(fp32-accurate); Gram and CholQR in fp64; M/X update bf16 "
+                                      "products, fp32 accumulation" if w.grad_dtype == "bf16" else
+                                      "P~ = BQ, Gram and CholQR in fp64; R and the M/X update on bf16 "
+                                      "MFMA with 3-piece fp32 splits"),
             "policy": args.policy, "tau": w.tau, "trajectory_steps": K,
             "sync_steps": n_sync, "local_steps": n_local, "parallelism": "none (1 GPU)",
         },

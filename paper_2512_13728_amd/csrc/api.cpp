@@ -63,8 +63,11 @@ struct DeviceGuard {
 };
 
 // K-splitting so that one launch has >= ~1024 blocks, each slice >= 256 deep.
-int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk) {
-  const long long bm = cd::gemm_bm(N, fp64), bn = cd::gemm_bn(N, fp64);
+// pieces > 0 selects the tile shape of the bf16-split kernels, else the fp32 /
+// fp64 MFMA kernels.
+int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk, int pieces = 0) {
+  const long long bm = pieces > 0 ? cd::gemm_bf_bm(N) : cd::gemm_bm(N, fp64);
+  const long long bn = pieces > 0 ? cd::gemm_bf_bn(N) : cd::gemm_bn(N, fp64);
   const long long tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn) * nl;
   int s = 1;
   while (tiles * s < 1024 && K / (2 * s) >= 256 && s < 32) s *= 2;
@@ -83,10 +86,11 @@ hipError_t dalloc(T** p, size_t count) {
 
 // ---- optional per-kernel timing (HIP events on the launch stream) ----------
 enum Kind { K_FORM, K_GATE, K_LOCAL, K_PBQ, K_GRAM, K_CHOL, K_APPLY, K_PBTP, K_REDUCE, K_COLNORM,
-            K_UPDATE, K_NKINDS };
+            K_UPDATE, K_PBQ_BF, K_UPDATE_BF1, K_NKINDS };
 const char* const kKindName[K_NKINDS] = {
     "form_buffer", "gate", "local_update", "power_bq_f64", "gram_f64", "cholesky_f64",
-    "trsm_f64", "power_btp_f32", "reduce_splits", "colnorm", "update_mx"};
+    "trsm_f64", "power_btp_bf16x6", "reduce_splits", "colnorm", "update_bf16x6",
+    "power_bq_bf16x6", "update_bf16"};
 
 struct Timer {
   struct Rec { int kind; hipEvent_t a, b; double bytes, flops; };
@@ -155,7 +159,7 @@ struct cd_group {
   void* out_host = nullptr;     // pinned
   hipEvent_t ev = nullptr;
   cd::CholTab* chol_tab = nullptr;      // [L] static workspace pointers
-  cd::TrsmTab* trsm_tab[2] = {nullptr, nullptr};  // CholQR pass 0 / 1
+  cd::TrsmTab* trsm_tab[3] = {nullptr, nullptr, nullptr};  // pass 0 / 1 / pass 0 from fp32 P~
   int2* trsm_tiles = nullptr;           // (layer, 64-row tile) pairs
   int ntiles = 0;
   Timer timer;
@@ -183,6 +187,7 @@ void free_group(cd_group* g) {
   if (g->chol_tab) (void)hipFree(g->chol_tab);
   if (g->trsm_tab[0]) (void)hipFree(g->trsm_tab[0]);
   if (g->trsm_tab[1]) (void)hipFree(g->trsm_tab[1]);
+  if (g->trsm_tab[2]) (void)hipFree(g->trsm_tab[2]);
   if (g->trsm_tiles) (void)hipFree(g->trsm_tiles);
   delete g;
 }
@@ -215,7 +220,7 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   std::vector<int> np(n);
   std::vector<double*> pv(n);
   std::vector<cd::CholTab> ct(n);
-  std::vector<cd::TrsmTab> t0(n), t1(n);
+  std::vector<cd::TrsmTab> t0(n), t1(n), t2(n);
   std::vector<int2> tiles;
   for (int i = 0; i < n; ++i) {
     cd_layer* L = layers[i];
@@ -224,6 +229,7 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
     ct[i] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef};
     t0[i] = cd::TrsmTab{L->pa, L->pb, L->W, L->Dinv, L->d.m};
     t1[i] = cd::TrsmTab{L->pb, L->P, L->W, L->Dinv, L->d.m};
+    t2[i] = cd::TrsmTab{L->P, L->pb, L->W, L->Dinv, L->d.m};
     for (int rt = 0; rt < (L->d.m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) tiles.push_back(int2{i, rt});
   }
   g->ntiles = static_cast<int>(tiles.size());
@@ -240,10 +246,12 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   if (e == hipSuccess) e = dalloc(&g->chol_tab, n);
   if (e == hipSuccess) e = dalloc(&g->trsm_tab[0], n);
   if (e == hipSuccess) e = dalloc(&g->trsm_tab[1], n);
+  if (e == hipSuccess) e = dalloc(&g->trsm_tab[2], n);
   if (e == hipSuccess) e = dalloc(&g->trsm_tiles, tiles.size());
   if (e == hipSuccess) e = hipMemcpy(g->chol_tab, ct.data(), sizeof(cd::CholTab) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[0], t0.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[1], t1.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[2], t2.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess)
     e = hipMemcpy(g->trsm_tiles, tiles.data(), sizeof(int2) * tiles.size(), hipMemcpyHostToDevice);
   if (e != hipSuccess) {
@@ -299,27 +307,30 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   auto lay = [&](int j) { return g->layers[sel[j]]; };
 
   // skinny GEMM C = A.B with optional split-K and fixed-order reduction
+  // pieces > 0: fp32 operands on the bf16 MFMA with `pieces`-way splits
   auto gemm = [&](int tkind, double flops, double bytes, cd::GemmKind kind, int Mr, int Nr, int K,
                   bool a_kc, int lda, bool b_kc, int ldb, bool upper, auto Aof, auto Bof, auto Cof,
-                  auto Pof) -> cd_status {
-    const bool acc64 = cd::gemm_acc64(kind);
+                  auto Pof, int pieces = 0) -> cd_status {
+    const bool acc64 = pieces == 0 && cd::gemm_acc64(kind);
     cd::GemmArgs ga{};
     ga.M = Mr; ga.N = Nr; ga.K = K; ga.lda = lda; ga.ldb = ldb; ga.ldc = Nr;
     ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper;
-    ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk);
+    ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk, pieces);
     ga.split_stride = 1LL * Mr * Nr;
     for (int j = 0; j < nl; ++j) {
       ga.A[j] = Aof(j);
       ga.B[j] = Bof(j);
       ga.C[j] = ga.splits > 1 ? Pof(j) : Cof(j);
     }
-    cd_status st2 = run(g, tkind, bytes * nl, flops * nl, s, [&] { return cd::launch_gemm(ga, nl, kind, s); });
+    cd_status st2 = run(g, tkind, bytes * nl, flops * nl, s, [&] {
+      return pieces > 0 ? cd::launch_gemm_bf(ga, nl, pieces, s) : cd::launch_gemm(ga, nl, kind, s);
+    });
     if (st2 != CD_OK) return st2;
     if (ga.splits > 1) {
       cd::ReduceArgs ra{};
       ra.count = 1LL * Mr * Nr; ra.stride = ga.split_stride; ra.splits = ga.splits;
       for (int j = 0; j < nl; ++j) { ra.part[j] = Pof(j); ra.out[j] = Cof(j); }
-      const bool out64 = kind == cd::GemmKind::F64 || kind == cd::GemmKind::F64_FROM_F32;
+      const bool out64 = pieces == 0 && (kind == cd::GemmKind::F64 || kind == cd::GemmKind::F64_FROM_F32);
       const double rb = static_cast<double>(ra.count) * nl * (acc64 ? 8.0 : 4.0) * (ga.splits + 1);
       st2 = run(g, K_REDUCE, rb, 0.0, s, [&] { return cd::launch_reduce_splits(ra, nl, acc64, out64, s); });
       if (st2 != CD_OK) return st2;
@@ -328,8 +339,16 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   };
   auto part = [&](int j) { return lay(j)->split_part; };
   const double mn = 1.0 * m * n, mr = 1.0 * m * r, nr = 1.0 * n * r, rr = 1.0 * r * r;
+  const bool fast = g->g_bf16;   // bf16 gradients: fp32-accurate P~ (see enqueue_orthogonalize)
   if (stage == 0) {
-    // P~ = B Q in fp64 (B lives in M)
+    // P~ = B Q (B lives in M): fp64 for fp32 layers, into pa; bf16 x 6 for
+    // bf16-gradient layers, into the fp32 panel P
+    if (fast)
+      return gemm(K_PBQ_BF, 2.0 * mn * r, 4.0 * mn + 4.0 * nr + 4.0 * mr, cd::GemmKind::F32, m, r, n,
+                  true, n, false, r, false,
+                  [&](int j) { return static_cast<const void*>(M[sel[j]]); },
+                  [&](int j) { return static_cast<const void*>(Q[sel[j]]); },
+                  [&](int j) { return static_cast<void*>(lay(j)->P); }, part, 3);
     return gemm(K_PBQ, 2.0 * mn * r, 4.0 * mn + 4.0 * nr + 8.0 * mr, cd::GemmKind::F64_FROM_F32, m, r,
                 n, true, n, false, r, false,
                 [&](int j) { return static_cast<const void*>(M[sel[j]]); },
@@ -338,17 +357,23 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   }
   if (stage == 1 || stage == 2) {
     const int pass = stage - 1;
+    if (pass == 0 && fast)
+      return gemm(K_GRAM, mr * (r + 1), 4.0 * mr + 8.0 * rr, cd::GemmKind::F64_FROM_F32, r, r, m, false,
+                  r, false, r, true, [&](int j) { return static_cast<const void*>(lay(j)->P); },
+                  [&](int j) { return static_cast<const void*>(lay(j)->P); },
+                  [&](int j) { return static_cast<void*>(lay(j)->W); },
+                  [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
     auto In = [&](int j) { return static_cast<const void*>(pass == 0 ? lay(j)->pa : lay(j)->pb); };
     return gemm(K_GRAM, mr * (r + 1), 8.0 * mr + 8.0 * rr, cd::GemmKind::F64, r, r, m, false, r, false,
                 r, true, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); },
                 [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
   }
   // R = B^T P
-  cd_status st = gemm(K_PBTP, 2.0 * mn * r, 4.0 * mn + 4.0 * mr + 4.0 * nr, cd::GemmKind::F32, n, r, m, false,
-            n, false, r, false,
-            [&](int j) { return static_cast<const void*>(M[sel[j]]); },
-            [&](int j) { return static_cast<const void*>(lay(j)->P); },
-            [&](int j) { return static_cast<void*>(lay(j)->R); }, part);
+  cd_status st = gemm(K_PBTP, 2.0 * mn * r, 4.0 * mn + 4.0 * mr + 4.0 * nr, cd::GemmKind::F32, n, r, m,
+                      false, n, false, r, false,
+                      [&](int j) { return static_cast<const void*>(M[sel[j]]); },
+                      [&](int j) { return static_cast<const void*>(lay(j)->P); },
+                      [&](int j) { return static_cast<void*>(lay(j)->R); }, part, 3);
   if (st != CD_OK) return st;
   // Q = ColumnNormalize(R)
   cd::ColnormArgs cn{};
@@ -366,7 +391,11 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   for (int j = 0; j < nl; ++j) {
     ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]]; ua.P[j] = lay(j)->P; ua.R[j] = lay(j)->R; ua.Q[j] = Q[sel[j]];
   }
-  return run(g, K_UPDATE, 16.0 * mn * nl, 4.0 * mn * r * nl, s, [&] { return cd::launch_update(ua, nl, s); });
+  // the rank-r corrections: fp32-accurate (6 bf16 products) for fp32 layers,
+  // plain bf16 products for bf16-gradient layers
+  const int up = fast ? 1 : 3;
+  return run(g, fast ? K_UPDATE_BF1 : K_UPDATE, 16.0 * mn * nl, 4.0 * mn * r * nl, s,
+             [&] { return cd::launch_update_bf(ua, nl, up, s); });
 }
 
 // CholQR pass `pass` over every layer: Cholesky of each W, then P = P~ T^{-1}
@@ -382,8 +411,10 @@ cd_status enqueue_orthogonalize(cd_group* g, int r, int pass, hipStream_t s) {
     flops += mr * r;
     bytes += 8.0 * mr + (pass == 0 ? 8.0 : 4.0) * mr + 8.0 * rr / 2;
   }
+  const bool in64 = !(pass == 0 && g->g_bf16);
+  cd::TrsmTab* tab = (pass == 0 && g->g_bf16) ? g->trsm_tab[2] : g->trsm_tab[pass];
   return run(g, K_APPLY, bytes, flops, s, [&] {
-    return cd::launch_trsm(g->trsm_tab[pass], g->trsm_tiles, g->ntiles, r, true, pass == 0, s);
+    return cd::launch_trsm(tab, g->trsm_tiles, g->ntiles, r, in64, pass == 0, s);
   });
 }
 
@@ -519,8 +550,8 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
       int kc;
       const size_t mr = static_cast<size_t>(m) * r, nr = static_cast<size_t>(n) * r;
       split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, true, &kc) * mr * sizeof(double));
-      split_bytes = std::max(split_bytes, plan_splits(m, r, r, 1, true, &kc) * mr * sizeof(double));
-      split_bytes = std::max(split_bytes, plan_splits(n, r, m, 1, false, &kc) * nr * sizeof(float));
+      split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, false, &kc, 3) * mr * sizeof(float));
+      split_bytes = std::max(split_bytes, plan_splits(n, r, m, 1, false, &kc, 3) * nr * sizeof(float));
       gram_cap = std::max(gram_cap, static_cast<size_t>(plan_splits(r, r, m, 1, true, &kc)) * r * r);
     }
     const size_t nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;

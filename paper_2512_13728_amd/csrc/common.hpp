@@ -86,6 +86,13 @@ int gemm_bm(int N, bool fp64);     // tile rows the launcher uses for this N
 int gemm_bn(int N, bool fp64);     // tile columns
 inline bool gemm_acc64(GemmKind k) { return k != GemmKind::F32; }
 
+// The same contraction for fp32 operands on the bf16 MFMA with each operand
+// split into `pieces` bf16 terms (3: about fp32 accuracy; 1: plain bf16).
+// fp32 result (or fp32 split partials).
+hipError_t launch_gemm_bf(const GemmArgs& a, int nl, int pieces, hipStream_t s);
+int gemm_bf_bm(int N);
+int gemm_bf_bn(int N);
+
 // out[i] = sum_{s < splits} part[s*stride + i] in order s = 0, 1, ...
 // Partials are fp64 when part64, and the output is fp64 when out64.
 struct ReduceArgs {
@@ -148,5 +155,7 @@ struct UpdateArgs {
   const float* Q[MAXB];
 };
 hipError_t launch_update(const UpdateArgs& a, int nl, hipStream_t s);
+// The same update on the bf16 MFMA with `pieces`-way split operands.
+hipError_t launch_update_bf(const UpdateArgs& a, int nl, int pieces, hipStream_t s);
 
 }  // namespace cd

@@ -11,6 +11,8 @@ unless stated):
 * dX = X_t - X_{t-1}: that bound plus 2 u ‖X_t‖ / ‖dX‖ (X_t is stored in fp32)
 * P^T P - I and |‖Q_j‖ - 1|: 1e-5 (absolute, Frobenius / max)
 * local branch: M bit-exact against fp32 M + G, X within 1 ulp of fp32 FMA
+* bf16 gradients (the path may use bf16 products for the rank-r update):
+            M, X, P, Q, dX within 2e-2; decisions identical
 Free-running trajectories check every decision against the free-running
 oracle and every step teacher-forced (the oracle restarted from the GPU
 state) with the bounds above; the drift between the two free-running states
@@ -56,11 +58,18 @@ def _print(tag, d):
           flush=True)
 
 
-def _check_step(d, tau, policy):
+def _check_step(d, tau, policy, bf16=False):
     assert d["flag_gpu"] == d["flag_oracle"], d
     assert_rmmc_close(d["rmmc_gpu"], d["rmmc_oracle"])
     if policy == O.POLICY_RMMC and math.isfinite(d["rmmc_oracle"]):
-        assert abs(d["rmmc_oracle"] - tau) / tau > 1e-4, "decision too close to tau"
+        assert abs(d["rmmc_oracle"] - tau) / tau > (1e-2 if bf16 else 1e-4), "decision too close to tau"
+    if bf16:
+        for k in ("err_M", "err_X", "err_P", "err_Q", "err_dX"):
+            if k in d:
+                assert d[k] <= 2e-2, (k, d)
+        if d["flag_oracle"]:
+            assert d["orth_P"] <= 1e-5 and d["colnorm_dev"] <= 1e-5, d
+        return
     assert d["err_M"] <= 1e-5, d
     assert d["err_X"] <= 1e-5, d
     if d["flag_oracle"]:
@@ -221,18 +230,19 @@ def test_group_mixed_shapes_rmmc_gate():
     assert any(flags) and not all(flags)
 
 
-@pytest.mark.parametrize("gd", ["bf16"])
-def test_bf16_gradient_steps(gd):
-    m, n, r = 512, 1536, 64
+@pytest.mark.parametrize("policy", [O.POLICY_RMMC, O.POLICY_ALWAYS_SYNC])
+@pytest.mark.parametrize("m,n,r", [(512, 1536, 64), (2048, 512, 256), (300, 700, 37)])
+def test_bf16_gradient_steps(m, n, r, policy):
+    gd = "bf16"
     w = S.small_workload(m, n, r, grad_dtype=gd, k=16)
     M, X, Q = _state(w, 0)
-    L = cdl.Layer(m, n, r, grad_dtype=gd, policy=cdl.POLICY_RMMC, tau=0.5)
+    L = cdl.Layer(m, n, r, grad_dtype=gd, policy=policy, tau=0.5)
     stream = S.GradientStream(w, 0, device="cpu")
     for t in range(3):
         G = stream.next().to(DEV)
-        d = step_and_compare(L, G, M, X, Q, 0.95, 0.01, r, 0.5, O.POLICY_RMMC)
-        _print(f"bf16 t={t + 1}", d)
-        _check_step(d, 0.5, O.POLICY_RMMC)
+        d = step_and_compare(L, G, M, X, Q, 0.95, 0.01, r, 0.5, policy)
+        _print(f"bf16 {policy} t={t + 1}", d)
+        _check_step(d, 0.5, policy, bf16=True)
 
 
 def test_state_roundtrip_and_every_h_policy():
