@@ -131,6 +131,7 @@ struct cd_layer {
   double* gram_part = nullptr;  // split-K partials of the Gram matrix
   void* split_part = nullptr;   // split-K partials of the skinny GEMMs (fp32 or fp64)
   double* colsq = nullptr;      // column sum-of-squares partials
+  __bf16* planes = nullptr;     // bf16 split planes of P, R, Q for the update
   float* colnrm = nullptr;      // r_max column norms
   cd_group* self = nullptr;     // one-layer group used by cd_step
   hipStream_t last_stream = nullptr;
@@ -170,7 +171,7 @@ namespace {
 void free_layer(cd_layer* L) {
   if (!L) return;
   void* ptrs[] = {L->prev, L->rankdef, L->pa, L->pb, L->P, L->R, L->W, L->Dinv, L->floor_,
-                  L->gram_part, L->split_part, L->colsq, L->colnrm};
+                  L->gram_part, L->split_part, L->colsq, L->colnrm, L->planes};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   delete L;
@@ -383,19 +384,43 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   }
   st = run(g, K_COLNORM, 12.0 * nr * nl, 3.0 * nr * nl, s, [&] { return cd::launch_colnorm(cn, nl, s); });
   if (st != CD_OK) return st;
-  // M = B - (1 - mu) P R^T;  X -= eta sqrt(m/n) P Q^T
-  cd::UpdateArgs ua{};
-  ua.m = m; ua.n = n; ua.r = r;
+  // M = B - (1 - mu) P R^T;  X -= eta sqrt(m/n) P Q^T.  The rank-r
+  // corrections are fp32-accurate (6 bf16 piece products) for fp32 layers and
+  // plain bf16 products for bf16-gradient layers; P, R, Q are split into bf16
+  // planes once, then streamed by the update.
+  const int up = fast ? 1 : 3;
+  const int rp = (r + 31) / 32 * 32;
+  {
+    cd::PlaneArgs pa{};
+    pa.r = r; pa.rp = rp; pa.S = up;
+    const double pb = (4.0 + 2.0 * up);
+    pa.rows = m;
+    for (int j = 0; j < nl; ++j) { pa.src[j] = lay(j)->P; pa.dst[j] = lay(j)->planes; }
+    st = run(g, K_COLNORM, pb * mr * nl, 0.0, s, [&] { return cd::launch_split_planes(pa, nl, s); });
+    if (st != CD_OK) return st;
+    pa.rows = n;
+    for (int j = 0; j < nl; ++j) { pa.src[j] = lay(j)->R; pa.dst[j] = lay(j)->planes + 3LL * m * rp; }
+    st = run(g, K_COLNORM, pb * nr * nl, 0.0, s, [&] { return cd::launch_split_planes(pa, nl, s); });
+    if (st != CD_OK) return st;
+    for (int j = 0; j < nl; ++j) {
+      pa.src[j] = Q[sel[j]];
+      pa.dst[j] = lay(j)->planes + 3LL * m * rp + 3LL * n * rp;
+    }
+    st = run(g, K_COLNORM, pb * nr * nl, 0.0, s, [&] { return cd::launch_split_planes(pa, nl, s); });
+    if (st != CD_OK) return st;
+  }
+  cd::UpdatePlArgs ua{};
+  ua.m = m; ua.n = n; ua.r = r; ua.rp = rp;
   ua.one_minus_mu = static_cast<float>(1.0 - static_cast<double>(mu));
   ua.c = static_cast<float>(static_cast<double>(eta) * std::sqrt(static_cast<double>(m) / n));
   for (int j = 0; j < nl; ++j) {
-    ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]]; ua.P[j] = lay(j)->P; ua.R[j] = lay(j)->R; ua.Q[j] = Q[sel[j]];
+    ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]];
+    ua.P[j] = lay(j)->planes;
+    ua.R[j] = lay(j)->planes + 3LL * m * rp;
+    ua.Q[j] = lay(j)->planes + 3LL * m * rp + 3LL * n * rp;
   }
-  // the rank-r corrections: fp32-accurate (6 bf16 products) for fp32 layers,
-  // plain bf16 products for bf16-gradient layers
-  const int up = fast ? 1 : 3;
   return run(g, fast ? K_UPDATE_BF1 : K_UPDATE, 16.0 * mn * nl, 4.0 * mn * r * nl, s,
-             [&] { return cd::launch_update_bf(ua, nl, up, s); });
+             [&] { return cd::launch_update_planes(ua, nl, up, s); });
 }
 
 // CholQR pass `pass` over every layer: Cholesky of each W, then P = P~ T^{-1}
@@ -569,6 +594,8 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
     if (e == hipSuccess) e = dalloc(&L->gram_part, gram_cap);
     if (e == hipSuccess) e = hipMalloc(&L->split_part, split_bytes);
     if (e == hipSuccess) e = dalloc(&L->colsq, nchunks * rm);
+    const size_t rpm = (rm + 31) / 32 * 32;
+    if (e == hipSuccess) e = dalloc(&L->planes, 3ULL * (m + 2ULL * n) * rpm);
     if (e == hipSuccess) e = dalloc(&L->colnrm, static_cast<size_t>(rm));
     if (e == hipSuccess) e = hipMemset(L->prev, 0, sizeof(double));
     if (e == hipSuccess) e = hipMemset(L->rankdef, 0, sizeof(int));

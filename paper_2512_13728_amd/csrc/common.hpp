@@ -154,8 +154,27 @@ struct UpdateArgs {
   const float* R[MAXB];
   const float* Q[MAXB];
 };
-hipError_t launch_update(const UpdateArgs& a, int nl, hipStream_t s);
-// The same update on the bf16 MFMA with `pieces`-way split operands.
-hipError_t launch_update_bf(const UpdateArgs& a, int nl, int pieces, hipStream_t s);
+// bf16 planes of fp32 matrices (rows x r): plane s (s < S <= 3) holds the
+// s-th bf16 piece of each value, rows padded to rp (multiple of 32) with zeros.
+struct PlaneArgs {
+  int rows, r, rp, S;
+  const float* src[MAXB];
+  __bf16* dst[MAXB];               // S * rows * rp elements
+};
+hipError_t launch_split_planes(const PlaneArgs& a, int nl, hipStream_t s);
+
+// The update from bf16 planes of P (m x rp), R and Q (n x rp) on the bf16
+// MFMA; pieces = 3 forms fp32-accurate products, pieces = 1 plain bf16 ones.
+struct UpdatePlArgs {
+  int m, n, r, rp;
+  float one_minus_mu;
+  float c;
+  float* M[MAXB];
+  float* X[MAXB];
+  const __bf16* P[MAXB];
+  const __bf16* R[MAXB];
+  const __bf16* Q[MAXB];
+};
+hipError_t launch_update_planes(const UpdatePlArgs& a, int nl, int pieces, hipStream_t s);
 
 }  // namespace cd

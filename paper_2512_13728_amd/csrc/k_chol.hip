@@ -91,7 +91,7 @@ __global__ __launch_bounds__(256) void k_chol_diag(const CholTab* __restrict__ t
 }
 
 // 64 x 64 fp64 MFMA tile: acc += A(64 x K) B(K x 64) with both operands staged
-// through LDS ([row][k] layout).  4 waves as 2 x 2, each 32 x 32.
+// through LDS.  4 waves as 2 x 2, each 32 x 32.
 struct Tile64 {
   f64x4 acc[2][2];
   __device__ void zero() {
@@ -100,14 +100,16 @@ struct Tile64 {
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{};
   }
+  // B is always staged k-major; A as A_KC says
+  template <bool A_KC>
   __device__ void mma_stage(const double* As, const double* Bs, int wm0, int wn0, int lane) {
 #pragma unroll
     for (int kk = 0; kk < GBK; kk += 16) {
       f64x4 a[2], b[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = frag<double>(As, wm0 + i * 16, kk, lane);
+      for (int i = 0; i < 2; ++i) a[i] = frag<double, CB, A_KC>(As, wm0 + i * 16, kk, lane);
 #pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = frag<double>(Bs, wn0 + j * 16, kk, lane);
+      for (int j = 0; j < 2; ++j) b[j] = frag<double, CB, false>(Bs, wn0 + j * 16, kk, lane);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -120,8 +122,8 @@ struct Tile64 {
 };
 
 __global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ tab, int r, int kb) {
-  __shared__ __attribute__((aligned(16))) double As[CB * GLDK];
-  __shared__ __attribute__((aligned(16))) double Bs[CB * GLDK];
+  __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
+  __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
   const CholTab t = tab[blockIdx.y];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
@@ -133,10 +135,10 @@ __global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ 
   T.zero();
   for (int kk0 = 0; kk0 < nb; kk0 += GBK) {
     // A(i, k) = D[k][i];  B(k, j) = W[k0 + k][j0 + j]
-    stage_tile<double, double, CB, 256>(As, D, CB, false, 0, nb, kk0, nb, tid);
-    stage_tile<double, double, CB, 256>(Bs, Wp + j0, r, false, 0, r - j0, kk0, nb, tid);
+    stage_tile<double, double, CB, 256, false>(As, D, CB, 0, nb, kk0, nb, tid);
+    stage_tile<double, double, CB, 256, false>(Bs, Wp + j0, r, 0, r - j0, kk0, nb, tid);
     __syncthreads();
-    T.mma_stage(As, Bs, wm0, wn0, lane);
+    T.mma_stage<false>(As, Bs, wm0, wn0, lane);
     __syncthreads();
   }
 #pragma unroll
@@ -152,8 +154,8 @@ __global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ 
 }
 
 __global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ tab, int r, int kb) {
-  __shared__ __attribute__((aligned(16))) double As[CB * GLDK];
-  __shared__ __attribute__((aligned(16))) double Bs[CB * GLDK];
+  __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
+  __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
   const CholTab t = tab[blockIdx.y];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
@@ -168,10 +170,10 @@ __global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ 
   T.zero();
   for (int kk0 = 0; kk0 < nb; kk0 += GBK) {
     // A(i, p) = X[p][i0 + i];  B(p, j) = X[p][j0 + j]
-    stage_tile<double, double, CB, 256>(As, X + i0, r, false, 0, r - i0, kk0, nb, tid);
-    stage_tile<double, double, CB, 256>(Bs, X + j0, r, false, 0, r - j0, kk0, nb, tid);
+    stage_tile<double, double, CB, 256, false>(As, X + i0, r, 0, r - i0, kk0, nb, tid);
+    stage_tile<double, double, CB, 256, false>(Bs, X + j0, r, 0, r - j0, kk0, nb, tid);
     __syncthreads();
-    T.mma_stage(As, Bs, wm0, wn0, lane);
+    T.mma_stage<false>(As, Bs, wm0, wn0, lane);
     __syncthreads();
   }
 #pragma unroll
@@ -191,8 +193,8 @@ template <typename TIn, typename TOut>
 __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, const int2* __restrict__ tiles,
                                               int r, int cb) {
   constexpr int YLD = CB + 4;
-  __shared__ __attribute__((aligned(16))) double As[CB * GLDK];
-  __shared__ __attribute__((aligned(16))) double Bs[CB * GLDK];
+  __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
+  __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
   __shared__ __attribute__((aligned(16))) double Ys[CB * YLD];
   const int2 lt = tiles[blockIdx.x];
   const TrsmTab t = tab[lt.x];
@@ -207,11 +209,11 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
   T.zero();
   // acc = P[:, :c0] T[:c0, c0:c0+64]   (P is the output: earlier block columns)
   for (int k0 = 0; k0 < c0; k0 += GBK) {
-    stage_tile<double, TOut, CB, 256>(As, Pout + static_cast<long long>(i0) * r, r, true, 0, m - i0,
-                                      k0, c0, tid);
-    stage_tile<double, double, CB, 256>(Bs, t.W + c0, r, false, 0, nbc, k0, c0, tid);
+    stage_tile<double, TOut, CB, 256, true>(As, Pout + static_cast<long long>(i0) * r, r, 0, m - i0,
+                                            k0, c0, tid);
+    stage_tile<double, double, CB, 256, false>(Bs, t.W + c0, r, 0, nbc, k0, c0, tid);
     __syncthreads();
-    T.mma_stage(As, Bs, wm0, wn0, lane);
+    T.mma_stage<true>(As, Bs, wm0, wn0, lane);
     __syncthreads();
   }
   // Y = P~[:, c-block] - acc, into LDS as the next A operand ([row][k], k = column)
@@ -231,7 +233,7 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
   const double* D = t.Dinv + static_cast<long long>(cb) * CB * CB;
   T.zero();
   for (int k0 = 0; k0 < nbc; k0 += GBK) {
-    stage_tile<double, double, CB, 256>(Bs, D, CB, false, 0, nbc, k0, nbc, tid);
+    stage_tile<double, double, CB, 256, false>(Bs, D, CB, 0, nbc, k0, nbc, tid);
     __syncthreads();
 #pragma unroll
     for (int kk = 0; kk < GBK; kk += 16) {
@@ -241,7 +243,7 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
         a[i] = *reinterpret_cast<const f64x4*>(Ys + (wm0 + i * 16 + (lane & 15)) * YLD + k0 + kk +
                                                4 * (lane >> 4));
 #pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = frag<double>(Bs, wn0 + j * 16, kk, lane);
+      for (int j = 0; j < 2; ++j) b[j] = frag<double, CB, false>(Bs, wn0 + j * 16, kk, lane);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll

@@ -2,12 +2,11 @@
 // branch) on MFMA:
 //   P~ = B Q            (m x n . n x r; A = B row-major, k contiguous)
 //   W  = P~^T P~        (Gram matrix, upper tiles only)
-//   P1 = P~ T^{-1}      (apply the inverse Cholesky factor, K = r)
-//   R  = B^T P          (n x m . m x r; A = B^T, i contiguous)
-// The first three run in fp64 (v_mfma_f64_16x16x4_f64 on fp32 or fp64
-// operands): P~ is the ill-conditioned panel, and keeping it, its Gram matrix
-// and the CholQR passes in fp64 makes the orthonormal P accurate to fp32
-// rounding whatever kappa(P~) is.  R = B^T P runs on v_mfma_f32_16x16x4_f32.
+// These run in fp64 (v_mfma_f64_16x16x4_f64 on fp32 or fp64 operands): P~
+// is the ill-conditioned panel, and keeping it, its Gram matrix and the CholQR
+// passes in fp64 makes the orthonormal P accurate to fp32 rounding whatever
+// kappa(P~) is.  (R = B^T P and the fp32-accurate variants run on the
+// bf16-split kernels.)
 // K can be split over blockIdx.y into partial products that
 // launch_reduce_splits adds in a fixed order (deterministic).
 #include "common.hpp"
@@ -16,15 +15,15 @@
 namespace cd {
 namespace {
 
-template <typename T, typename TIn, typename TOut, int BM, int BN>
+template <typename T, typename TIn, typename TOut, int BM, int BN, bool A_KC, bool B_KC>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   constexpr int WN_WAVES = (BN >= 64) ? 2 : 1;
   constexpr int WM_WAVES = 4 / WN_WAVES;
   constexpr int WM = BM / WM_WAVES, WN = BN / WN_WAVES;
   constexpr int TM = WM / 16, TN = WN / 16;
   static_assert(TM >= 1 && TN >= 1, "tile too small");
-  __shared__ __attribute__((aligned(16))) T As[BM * GLDK];
-  __shared__ __attribute__((aligned(16))) T Bs[BN * GLDK];
+  __shared__ __attribute__((aligned(16))) T As[tile_elems<BM>()];
+  __shared__ __attribute__((aligned(16))) T Bs[tile_elems<BN>()];
 
   const int layer = blockIdx.z;
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
@@ -47,16 +46,16 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     for (int j = 0; j < TN; ++j) acc[i][j] = typename Mfma<T>::acc_t{};
 
   for (int k0 = kb; k0 < ke; k0 += GBK) {
-    stage_tile<T, TIn, BM, 256>(As, A, g.lda, g.a_kc, m0, g.M, k0, ke, tid);
-    stage_tile<T, TIn, BN, 256>(Bs, Bm, g.ldb, g.b_kc, n0, g.N, k0, ke, tid);
+    stage_tile<T, TIn, BM, 256, A_KC>(As, A, g.lda, m0, g.M, k0, ke, tid);
+    stage_tile<T, TIn, BN, 256, B_KC>(Bs, Bm, g.ldb, n0, g.N, k0, ke, tid);
     __syncthreads();
 #pragma unroll
     for (int kk = 0; kk < GBK; kk += 16) {
       typename Mfma<T>::vec4_t a[TM], b[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i) a[i] = frag<T>(As, wm0 + i * 16, kk, lane);
+      for (int i = 0; i < TM; ++i) a[i] = frag<T, BM, A_KC>(As, wm0 + i * 16, kk, lane);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) b[j] = frag<T>(Bs, wn0 + j * 16, kk, lane);
+      for (int j = 0; j < TN; ++j) b[j] = frag<T, BN, B_KC>(Bs, wn0 + j * 16, kk, lane);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -103,15 +102,20 @@ template <typename T, typename TIn, typename TOut, int BM, int BN>
 hipError_t launch_t(const GemmArgs& g, int nl, hipStream_t s) {
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   const dim3 grid(xcd_grid(tiles), g.splits, nl);
-  hipLaunchKernelGGL((k_gemm<T, TIn, TOut, BM, BN>), grid, dim3(256), 0, s, g);
+  if (g.a_kc && !g.b_kc)
+    hipLaunchKernelGGL((k_gemm<T, TIn, TOut, BM, BN, true, false>), grid, dim3(256), 0, s, g);
+  else if (!g.a_kc && !g.b_kc)
+    hipLaunchKernelGGL((k_gemm<T, TIn, TOut, BM, BN, false, false>), grid, dim3(256), 0, s, g);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
 }  // namespace
 
-// Tile shape by N (the rank side): 64x64 for N > 32, 128x32, or 256x16.
-int gemm_bm(int N, bool fp64) { return (fp64 || N > 32) ? 64 : (N > 16 ? 128 : 256); }
-int gemm_bn(int N, bool fp64) { return (fp64 || N > 32) ? 64 : (N > 16 ? 32 : 16); }
+// Tile shape of the fp64 kernels (64 x 64).
+int gemm_bm(int N, bool fp64) { (void)N; (void)fp64; return 64; }
+int gemm_bn(int N, bool fp64) { (void)N; (void)fp64; return 64; }
 
 hipError_t launch_gemm(const GemmArgs& g, int nl, GemmKind kind, hipStream_t s) {
   if (nl <= 0) return hipSuccess;
@@ -119,11 +123,9 @@ hipError_t launch_gemm(const GemmArgs& g, int nl, GemmKind kind, hipStream_t s) 
     case GemmKind::F64_FROM_F32: return launch_t<double, float, double, 64, 64>(g, nl, s);
     case GemmKind::F64: return launch_t<double, double, double, 64, 64>(g, nl, s);
     case GemmKind::F64_TO_F32: return launch_t<double, double, float, 64, 64>(g, nl, s);
-    case GemmKind::F32: break;
+    case GemmKind::F32: break;  // fp32 contractions run on the bf16-split kernels
   }
-  if (g.N > 32) return launch_t<float, float, float, 64, 64>(g, nl, s);
-  if (g.N > 16) return launch_t<float, float, float, 128, 32>(g, nl, s);
-  return launch_t<float, float, float, 256, 16>(g, nl, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_reduce_splits(const ReduceArgs& a, int nl, bool part64, bool out64, hipStream_t s) {

@@ -88,25 +88,108 @@ __global__ __launch_bounds__(256) void k_gemm_bf(GemmArgs g) {
       }
 }
 
-// M = B - (1 - mu) P R^T and X -= c P Q^T on a 128 x 64 tile of the m x n
-// matrices; K = r.  P (m x r), R and Q (n x r) are all k-contiguous.
-constexpr int UBM = 128, UBN = 64;
+// bf16 planes of an fp32 matrix (rows x r): plane s holds the s-th split piece,
+// row stride rp (r rounded up to 32, padding zero-filled).
+__global__ __launch_bounds__(256) void k_split_planes(PlaneArgs a) {
+  const int l = blockIdx.y;
+  const long long quads = static_cast<long long>(a.rows) * (a.rp / 4);
+  const long long plane = static_cast<long long>(a.rows) * a.rp;
+  const float* src = a.src[l];
+  __bf16* dst = a.dst[l];
+  for (long long q = blockIdx.x * 256LL + threadIdx.x; q < quads; q += 256LL * gridDim.x) {
+    const long long row = q / (a.rp / 4);
+    const int k = static_cast<int>(q - row * (a.rp / 4)) * 4;
+    float v[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = (k + c < a.r) ? src[row * a.r + k + c] : 0.0f;
+    __bf16 pc[4][3];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      float rest = v[c];
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        pc[c][s] = static_cast<__bf16>(rest);
+        rest -= static_cast<float>(pc[c][s]);
+      }
+    }
+    for (int s = 0; s < a.S; ++s) {
+      bf16x4 w = {pc[0][s], pc[1][s], pc[2][s], pc[3][s]};
+      *reinterpret_cast<bf16x4*>(dst + s * plane + row * a.rp + k) = w;
+    }
+  }
+}
 
-template <int S>
-__global__ __launch_bounds__(256) void k_update_bf(UpdateArgs u) {
-  constexpr int TM = 4, TN = 2;   // wave tile 64 x 32
-  __shared__ __attribute__((aligned(16))) __bf16 Ps[S * UBM * BLD];
-  __shared__ __attribute__((aligned(16))) __bf16 Rs[S * UBN * BLD];
-  __shared__ __attribute__((aligned(16))) __bf16 Qs[S * UBN * BLD];
+// M = B - (1 - mu) P R^T and X -= c P Q^T on a 128 x BN tile of the m x n
+// matrices; K = r.  P, R, Q come as bf16 planes (k_split_planes), so a stage
+// is plain 16-byte loads into LDS; the P planes of a 128-row panel are shared
+// by the BN-column tiles that the XCD-aware order keeps on one XCD.
+constexpr int UBM = 128;
+
+template <int S, int BN>
+__global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
+  constexpr int TM = 4, TN = BN / 32;   // wave tile 64 x BN/2
+  constexpr int PLANE_BYTES = S * (UBM + 2 * BN) * BLD * 2;
+  constexpr int SLD = BN + 4;           // padded row of the fp32 accumulator staging tile
+  constexpr int STAGE_BYTES = UBM * SLD * 4;
+  constexpr int SMEM = PLANE_BYTES > STAGE_BYTES ? PLANE_BYTES : STAGE_BYTES;
+  constexpr int ROWS = UBM + 2 * BN;    // LDS rows per plane: P, then R, then Q
+  constexpr int CHUNKS = S * ROWS * (BK16 / 8);   // 16-byte chunks per stage
+  constexpr int CPT = (CHUNKS + 255) / 256;
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  __bf16* Ls = reinterpret_cast<__bf16*>(smem);   // [S][ROWS][BLD]
   const int l = blockIdx.z;
-  const int tiles_n = (u.n + UBN - 1) / UBN;
-  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x - tm * tiles_n;
-  const int m0 = tm * UBM, n0 = tn * UBN;
+  const int tiles_n = (u.n + BN - 1) / BN;
+  const int ntiles = ((u.m + UBM - 1) / UBM) * tiles_n;
+  const int t = xcd_tile(blockIdx.x, ntiles);
+  if (t >= ntiles) return;
+  const int tm = t / tiles_n, tn = t - tm * tiles_n;
+  const int m0 = tm * UBM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 1) * 64, wn0 = (wave & 1) * 32;
-  const float* P = u.P[l];
-  const float* R = u.R[l];
-  const float* Q = u.Q[l];
+  const int wm0 = (wave >> 1) * 64, wn0 = (wave & 1) * (BN / 2);
+  const long long pP = static_cast<long long>(u.m) * u.rp, pN = static_cast<long long>(u.n) * u.rp;
+  // copy what the lambdas need out of the argument struct (taking the address
+  // of the by-value kernel argument would force it into scratch memory)
+  const __bf16* const gP = u.P[l];
+  const __bf16* const gR = u.R[l];
+  const __bf16* const gQ = u.Q[l];
+  const int um = u.m, un = u.n, urp = u.rp;
+
+  // chunk c -> (plane s, LDS row, 8-element k group)
+  auto chunk_src = [&](int c, int k0, bool& ok) -> const uint4* {
+    const int s = c / (ROWS * 4), rem = c - s * ROWS * 4;
+    const int row = rem >> 2, kg = (rem & 3) * 8;
+    const __bf16* base;
+    int grow, lim;
+    if (row < UBM) { base = gP + s * pP; grow = m0 + row; lim = um; }
+    else if (row < UBM + BN) { base = gR + s * pN; grow = n0 + row - UBM; lim = un; }
+    else { base = gQ + s * pN; grow = n0 + row - UBM - BN; lim = un; }
+    ok = grow < lim;
+    return reinterpret_cast<const uint4*>(base + static_cast<long long>(ok ? grow : 0) * urp + k0 + kg);
+  };
+  uint4 pre[CPT];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + i * 256;
+      uint4 v = {0u, 0u, 0u, 0u};
+      if (c < CHUNKS) {
+        bool ok;
+        const uint4* p = chunk_src(c, k0, ok);
+        if (ok) v = *p;
+      }
+      pre[i] = v;
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + i * 256;
+      if (c < CHUNKS) {
+        const int s = c / (ROWS * 4), rem = c - s * ROWS * 4;
+        *reinterpret_cast<uint4*>(Ls + (s * ROWS + (rem >> 2)) * BLD + (rem & 3) * 8) = pre[i];
+      }
+    }
+  };
 
   f32x4 am[TM][TN], ax[TM][TN];
 #pragma unroll
@@ -114,63 +197,72 @@ __global__ __launch_bounds__(256) void k_update_bf(UpdateArgs u) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) { am[i][j] = f32x4{}; ax[i][j] = f32x4{}; }
 
-  Stage<UBM, 256> sp;
-  Stage<UBN, 256> sr, sq;
-  sp.load(P, u.r, true, m0, u.m, 0, u.r, tid);
-  sr.load(R, u.r, true, n0, u.n, 0, u.r, tid);
-  sq.load(Q, u.r, true, n0, u.n, 0, u.r, tid);
-  for (int k0 = 0; k0 < u.r; k0 += BK16) {
-    sp.template store<S>(Ps, true, tid);
-    sr.template store<S>(Rs, true, tid);
-    sq.template store<S>(Qs, true, tid);
+  load(0);
+  for (int k0 = 0; k0 < u.rp; k0 += BK16) {
+    store();
     __syncthreads();
-    if (k0 + BK16 < u.r) {
-      sp.load(P, u.r, true, m0, u.m, k0 + BK16, u.r, tid);
-      sr.load(R, u.r, true, n0, u.n, k0 + BK16, u.r, tid);
-      sq.load(Q, u.r, true, n0, u.n, k0 + BK16, u.r, tid);
-    }
-    bf16x8 a[TM][S], rb[TN][S], qb[TN][S];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int s = 0; s < S; ++s) a[i][s] = bfrag(Ps + s * UBM * BLD, wm0 + i * 16, lane);
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int s = 0; s < S; ++s) {
-        rb[j][s] = bfrag(Rs + s * UBN * BLD, wn0 + j * 16, lane);
-        qb[j][s] = bfrag(Qs + s * UBN * BLD, wn0 + j * 16, lane);
-      }
+    if (k0 + BK16 < u.rp) load(k0 + BK16);
 #pragma unroll
     for (int sum = S - 1; sum >= 0; --sum)
 #pragma unroll
-      for (int p = 0; p <= sum; ++p)
+      for (int p = 0; p <= sum; ++p) {
+        const __bf16* Pp = Ls + p * ROWS * BLD;
+        const __bf16* Rq = Ls + ((sum - p) * ROWS + UBM) * BLD;
+        const __bf16* Qq = Rq + BN * BLD;
+        bf16x8 a[TM];
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i) a[i] = bfrag(Pp, wm0 + i * 16, lane);
 #pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            am[i][j] = mfma_bf16(a[i][p], rb[j][sum - p], am[i][j]);
-            ax[i][j] = mfma_bf16(a[i][p], qb[j][sum - p], ax[i][j]);
+        for (int j = 0; j < TN; ++j) {
+          const bf16x8 rb = bfrag(Rq, wn0 + j * 16, lane);
+          const bf16x8 qb = bfrag(Qq, wn0 + j * 16, lane);
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            am[i][j] = mfma_bf16(a[i], rb, am[i][j]);
+            ax[i][j] = mfma_bf16(a[i], qb, ax[i][j]);
           }
+        }
+      }
     __syncthreads();
   }
 
-  float* M = u.M[l];
-  float* X = u.X[l];
+  // Epilogue through LDS so that M and X are read and written as contiguous
+  // 16-byte row segments: M += -(1 - mu) (P R^T), then X += -c (P Q^T).
+  float* st = reinterpret_cast<float*>(smem);
+  const bool vec = (u.n & 3) == 0;
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int which = 0; which < 2; ++which) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = m0 + wm0 + i * 16 + 4 * (lane >> 4) + v;
-        const int col = n0 + wn0 + j * 16 + (lane & 15);
-        if (row < u.m && col < u.n) {
-          const long long o = static_cast<long long>(row) * u.n + col;
-          M[o] = fmaf(-u.one_minus_mu, am[i][j][v], M[o]);
-          X[o] = fmaf(-u.c, ax[i][j][v], X[o]);
-        }
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          st[(wm0 + i * 16 + 4 * (lane >> 4) + v) * SLD + wn0 + j * 16 + (lane & 15)] =
+              which == 0 ? am[i][j][v] : ax[i][j][v];
+    __syncthreads();
+    float* Y = which == 0 ? u.M[l] : u.X[l];
+    const float coef = which == 0 ? -u.one_minus_mu : -u.c;
+#pragma unroll 4
+    for (int e = tid; e < UBM * (BN / 4); e += 256) {
+      const int row = e / (BN / 4), c4 = (e % (BN / 4)) * 4;
+      const int grow = m0 + row, gcol = n0 + c4;
+      if (grow >= u.m) continue;
+      const float4 a = *reinterpret_cast<const float4*>(st + row * SLD + c4);
+      float* y = Y + static_cast<long long>(grow) * u.n + gcol;
+      if (vec && gcol + 3 < u.n) {
+        float4 w = *reinterpret_cast<const float4*>(y);
+        w.x = fmaf(coef, a.x, w.x); w.y = fmaf(coef, a.y, w.y);
+        w.z = fmaf(coef, a.z, w.z); w.w = fmaf(coef, a.w, w.w);
+        *reinterpret_cast<float4*>(y) = w;
+      } else {
+        const float av[4] = {a.x, a.y, a.z, a.w};
+        for (int c = 0; c < 4; ++c)
+          if (gcol + c < u.n) y[c] = fmaf(coef, av[c], y[c]);
       }
+    }
+    __syncthreads();
+  }
 }
 
 template <int S, int BM, int BN>
@@ -203,13 +295,24 @@ hipError_t launch_gemm_bf(const GemmArgs& g, int nl, int pieces, hipStream_t s) 
   return launch_s<1>(g, nl, s);
 }
 
-hipError_t launch_update_bf(const UpdateArgs& u, int nl, int pieces, hipStream_t s) {
+hipError_t launch_split_planes(const PlaneArgs& a, int nl, hipStream_t s) {
+  if (nl <= 0 || a.rows <= 0) return hipSuccess;
+  long long quads = static_cast<long long>(a.rows) * (a.rp / 4);
+  long long blocks = (quads + 255) / 256;
+  if (blocks > 2048) blocks = 2048;
+  hipLaunchKernelGGL(k_split_planes, dim3(static_cast<unsigned>(blocks), nl), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_update_planes(const UpdatePlArgs& u, int nl, int pieces, hipStream_t s) {
   if (nl <= 0) return hipSuccess;
-  const int tiles = ((u.m + UBM - 1) / UBM) * ((u.n + UBN - 1) / UBN);
-  const dim3 grid(tiles, 1, nl);
-  if (pieces == 3) hipLaunchKernelGGL(k_update_bf<3>, grid, dim3(256), 0, s, u);
-  else if (pieces == 2) hipLaunchKernelGGL(k_update_bf<2>, grid, dim3(256), 0, s, u);
-  else hipLaunchKernelGGL(k_update_bf<1>, grid, dim3(256), 0, s, u);
+  if (pieces == 3) {
+    const int tiles = ((u.m + UBM - 1) / UBM) * ((u.n + 63) / 64);
+    hipLaunchKernelGGL((k_update_pl<3, 64>), dim3(xcd_grid(tiles), 1, nl), dim3(256), 0, s, u);
+  } else {
+    const int tiles = ((u.m + UBM - 1) / UBM) * ((u.n + 127) / 128);
+    hipLaunchKernelGGL((k_update_pl<1, 128>), dim3(xcd_grid(tiles), 1, nl), dim3(256), 0, s, u);
+  }
   return hipGetLastError();
 }
 

@@ -52,15 +52,27 @@ __device__ __forceinline__ void load4(const double* p, double& a, double& b, dou
   a = f.x; b = f.y; c = g.x; d = g.y;
 }
 
+// LDS tiles.  A k-contiguous operand (element (row, k) at src[row * ld + k]) is
+// staged row-major, S[row][GLDK], and an operand of the other layout
+// (element (row, k) at src[k * ld + row]) is staged k-major, S[k][ROWS + KPAD];
+// either way the global loads and the LDS stores are 4-element vectors.
+constexpr int KPAD = 4;
+template <int ROWS>
+constexpr int tile_elems() { return ROWS * GLDK > GBK * (ROWS + KPAD) ? ROWS * GLDK : GBK * (ROWS + KPAD); }
+
+template <typename T>
+__device__ __forceinline__ void store4(T* d, T a, T b, T c, T e) {
+  d[0] = a; d[1] = b; d[2] = c; d[3] = e;
+}
+
 // Stage rows [r0, r0 + ROWS) x k in [k0, k0 + GBK) of an operand of element
-// type TIn into S[ROWS][GLDK] (type T), zero-filling rows >= nrows and
-// k >= kend.  kc: element (row, k) at src[row * ld + k]; otherwise at
-// src[k * ld + row].  Vector loads need ld % 4 == 0 (and an aligned base).
-template <typename T, typename TIn, int ROWS, int NT>
+// type TIn into S (type T), zero-filling rows >= nrows and k >= kend.  Vector
+// loads need ld % 4 == 0 (and an aligned base).
+template <typename T, typename TIn, int ROWS, int NT, bool KC>
 __device__ __forceinline__ void stage_tile(T* __restrict__ S, const TIn* __restrict__ src, int ld,
-                                           bool kc, int r0, int nrows, int k0, int kend, int tid) {
+                                           int r0, int nrows, int k0, int kend, int tid) {
   const bool vec = (ld & 3) == 0;
-  if (kc) {
+  if constexpr (KC) {
     constexpr int SLOTS = ROWS * (GBK / 4);
 #pragma unroll
     for (int slot = tid; slot < SLOTS; slot += NT) {
@@ -79,8 +91,7 @@ __device__ __forceinline__ void stage_tile(T* __restrict__ S, const TIn* __restr
           if (gk + 3 < kend) v3 = p[3];
         }
       }
-      T* d = S + row * GLDK + kq;
-      d[0] = v0; d[1] = v1; d[2] = v2; d[3] = v3;
+      store4<T>(S + row * GLDK + kq, v0, v1, v2, v3);
     }
   } else {
     constexpr int SLOTS = GBK * (ROWS / 4);
@@ -101,19 +112,27 @@ __device__ __forceinline__ void stage_tile(T* __restrict__ S, const TIn* __restr
           if (gr + 3 < nrows) v3 = p[3];
         }
       }
-      S[(rq + 0) * GLDK + kk] = v0;
-      S[(rq + 1) * GLDK + kk] = v1;
-      S[(rq + 2) * GLDK + kk] = v2;
-      S[(rq + 3) * GLDK + kk] = v3;
+      store4<T>(S + kk * (ROWS + KPAD) + rq, v0, v1, v2, v3);
     }
   }
 }
 
-// Operand fragment for one 16-row group at k slice kk: four consecutive k.
-template <typename T>
+// Operand fragment of a 16x16x4 MFMA for the 16 rows starting at row0 and the
+// k slice kk: lane l owns row (l % 16) and k = 4 (l / 16) + q, q = 0..3.
+template <typename T, int ROWS, bool KC>
 __device__ __forceinline__ typename Mfma<T>::vec4_t frag(const T* S, int row0, int kk, int lane) {
-  return *reinterpret_cast<const typename Mfma<T>::vec4_t*>(S + (row0 + (lane & 15)) * GLDK + kk +
-                                                            4 * (lane >> 4));
+  if constexpr (KC) {
+    return *reinterpret_cast<const typename Mfma<T>::vec4_t*>(S + (row0 + (lane & 15)) * GLDK + kk +
+                                                              4 * (lane >> 4));
+  } else {
+    const T* p = S + (kk + 4 * (lane >> 4)) * (ROWS + KPAD) + row0 + (lane & 15);
+    typename Mfma<T>::vec4_t v;
+    v[0] = p[0];
+    v[1] = p[ROWS + KPAD];
+    v[2] = p[2 * (ROWS + KPAD)];
+    v[3] = p[3 * (ROWS + KPAD)];
+    return v;
+  }
 }
 
 // Block index -> tile index so that consecutive tiles land on the same XCD
