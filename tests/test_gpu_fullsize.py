@@ -1,0 +1,154 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+benchmark uses (one group per workload).  Where the oracle cannot afford the
+whole set it checks what it can compute one layer at a time: every layer's
+RMMC and the common decision, and the full update of sampled layers (one of
+each shape), teacher-forced from the GPU state.  Tolerances as in
+test_gpu_parity.py."""
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+
+import oracle as O  # noqa: E402
+import paper_2512_13728_amd as cdl  # noqa: E402
+import synthetic as S  # noqa: E402
+from gpu_util import (assert_rmmc_close, device_to_numpy, f32, f64, qr_tol, rel)  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    cdl.lib()
+    yield
+
+
+def _sample_one_per_shape(w):
+    seen, idx = set(), []
+    for i, s in enumerate(w.shapes):
+        if s not in seen:
+            seen.add(s)
+            idx.append(i)
+    return idx
+
+
+def _group_case(w, policy, steps, tau=None, sample=None, bf16_tol=None, log=""):
+    """Run `steps` group steps of workload w on the GPU; per step compare every
+    layer's RMMC and the decision with the oracle (norms from the same inputs),
+    and the sampled layers' full update teacher-forced."""
+    tau = w.tau if tau is None else tau
+    L = len(w.shapes)
+    layers = [cdl.Layer(m, n, w.r, grad_dtype=w.grad_dtype, tau=tau, policy=policy) for m, n in w.shapes]
+    grp = cdl.Group(layers)
+    st = [S.initial_state(w, i, device=DEV) for i in range(L)]
+    M = [s[0] for s in st]
+    X = [s[1] for s in st]
+    Q = [s[2].contiguous() for s in st]
+    streams = [S.GradientStream(w, i, device=DEV) for i in range(L)]
+    prev = [0.0] * L
+    sample = _sample_one_per_shape(w) if sample is None else sample
+    bf16 = w.grad_dtype == "bf16"
+    flags = []
+    for t in range(steps):
+        G = [s.next() for s in streams]
+        snap = {i: (f64(M[i]), f64(X[i]), f64(Q[i])) for i in sample}
+        # oracle statistic for every layer, from the same inputs (one layer at a time)
+        rm_or = []
+        for i in range(L):
+            B = f64(M[i]) + f64(G[i])
+            nb = O.frobenius_norm(B)
+            rm_or.append(O.rmmc(nb, prev[i], w.eps))
+            prev[i] = nb
+            del B
+        g_or, flag_or = O.gate(rm_or, tau, policy, step=t + 1)
+        g, flag, per, _ = grp.step(G, M, X, Q, w.mu, w.eta, w.r)
+        torch.cuda.synchronize()
+        assert flag == flag_or, (t + 1, g, g_or)
+        if policy == O.POLICY_RMMC:
+            assert abs(g_or - tau) / tau > 1e-2
+        for a, b in zip(per, rm_or):
+            assert_rmmc_close(a, b)
+        flags.append(flag)
+        for i in sample:
+            M0, X0, Q0 = snap[i]
+            OL = O.OracleLayer.from_arrays(M0, X0, Q0, prev_norm=0.0)
+            Gi = f64(G[i])
+            if flag:
+                out = O.sync_update(M0 + Gi, X0, Q0, f32(w.mu), f32(w.eta))
+            else:
+                out = O.local_update(M0 + Gi, Gi, X0, f32(w.eta))
+                out["Q"] = Q0
+            e = {"M": rel(f64(M[i]), out["M"]), "X": rel(f64(X[i]), out["X"]),
+                 "Q": rel(f64(Q[i]), out["Q"])}
+            dX = out["X"] - X0
+            e["dX"] = rel(f64(X[i]) - X0, dX)
+            floor = 2 * 2.0 ** -24 * np.linalg.norm(out["X"]) / np.linalg.norm(dX)
+            if flag:
+                m, n = w.shapes[i]
+                P = device_to_numpy(layers[i].last_factors()[0], (m, w.r)).astype(np.float64)
+                e["P"] = rel(P, out["P"])
+                e["orth"] = float(np.linalg.norm(P.T @ P - np.eye(w.r)))
+                kappa = float(np.linalg.cond(out["P_tilde"]))
+            print(f"{log} step {t + 1} layer {i} {w.shapes[i]} flag={flag} "
+                  + " ".join(f"{k}={v:.2e}" for k, v in e.items())
+                  + (f" kappa={kappa:.3g}" if flag else ""), flush=True)
+            if bf16:
+                for k in ("M", "X", "Q", "dX", "P"):
+                    if k in e:
+                        assert e[k] <= 2e-2, (k, e)
+            else:
+                assert e["M"] <= 1e-5 and e["X"] <= 1e-5, e
+                if flag:
+                    tol = qr_tol(kappa)
+                    assert e["P"] <= tol and e["Q"] <= tol and e["dX"] <= tol + floor, (e, tol)
+            if flag:
+                assert e["orth"] <= 1e-5
+    return flags
+
+
+@pytest.mark.timeout(400)
+def test_gpt1p3b_full_set_two_steps():
+    """All 96 matrices of the 1.3B-shaped set, r = 512, bf16 gradients: step 1
+    (sync, prev_norm = 0) and step 2 (local under tau = 0.5)."""
+    w = S.WORKLOADS["gpt1p3b"]
+    flags = _group_case(w, O.POLICY_RMMC, 2, log="gpt1p3b")
+    assert flags == [True, False]
+
+
+@pytest.mark.timeout(300)
+def test_gpt1p3b_always_sync_second_step():
+    """Two always-sync steps on one layer of each shape of the 1.3B set: the
+    second has an ill-conditioned P~ (Q aligned with the previous signal)."""
+    w = S.WORKLOADS["gpt1p3b"]
+    w4 = S.Workload("gpt1p3b-4", tuple(w.shapes[:4]), r=w.r, grad_dtype="bf16", steps=2, k=w.k,
+                    sigma=w.sigma, tau=w.tau, stream_id=w.stream_id)
+    _group_case(w4, O.POLICY_ALWAYS_SYNC, 2, log="gpt1p3b-always")
+
+
+@pytest.mark.timeout(300)
+def test_gpt160m_full_set_spike():
+    """All 48 matrices of the 160M-shaped set (fp32, r = 192) through the first
+    spike (steps 1-10, tau = 0.3): decisions for every step, RMMC of every
+    layer, and the strict fp32 bounds on one layer per shape."""
+    w = S.WORKLOADS["gpt160m"]
+    flags = _group_case(w, O.POLICY_RMMC, 10, log="gpt160m")
+    assert flags[0] and flags[9]
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("r", [16, 64, 256, 1024])
+def test_sweep4096_ranks(r):
+    """One 4096 x 16384 fp32 matrix at each rank of the sweep: two always-sync
+    steps, strict fp32 bounds."""
+    w = S.WORKLOADS["sweep4096"]
+    w1 = S.Workload(f"sweep4096-r{r}", w.shapes, r=r, grad_dtype="f32", steps=2, k=w.k, sigma=w.sigma,
+                    tau=w.tau, stream_id=w.stream_id)
+    _group_case(w1, O.POLICY_ALWAYS_SYNC, 2, log=f"sweep r={r}")
