@@ -85,12 +85,12 @@ hipError_t dalloc(T** p, size_t count) {
 }
 
 // ---- optional per-kernel timing (HIP events on the launch stream) ----------
-enum Kind { K_FORM, K_GATE, K_LOCAL, K_PBQ, K_GRAM, K_CHOL, K_APPLY, K_PBTP, K_REDUCE, K_COLNORM,
-            K_UPDATE, K_PBQ_BF, K_UPDATE_BF1, K_NKINDS };
+enum Kind { K_FORM, K_GATE, K_LOCAL, K_PBQ, K_PBQ_BF, K_GRAM, K_GRAM_BF, K_CHOL, K_TRSM, K_TRTRI,
+            K_APPLY_BF, K_PBTP, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_NKINDS };
 const char* const kKindName[K_NKINDS] = {
-    "form_buffer", "gate", "local_update", "power_bq_f64", "gram_f64", "cholesky_f64",
-    "trsm_f64", "power_btp_bf16x6", "reduce_splits", "colnorm", "update_bf16x6",
-    "power_bq_bf16x6", "update_bf16"};
+    "form_buffer", "gate", "local_update", "power_bq_f64", "power_bq_bf16x6", "gram_f64",
+    "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_bf16x6",
+    "reduce_splits", "colnorm", "update_bf16x6", "update_bf16"};
 
 struct Timer {
   struct Rec { int kind; hipEvent_t a, b; double bytes, flops; };
@@ -122,7 +122,8 @@ struct cd_layer {
   double* prev = nullptr;       // device, 1 double
   int* rankdef = nullptr;       // device, 1 int
   double* pa = nullptr;         // m x r_max fp64: P~
-  double* pb = nullptr;         // m x r_max fp64: P~ after the first CholQR pass
+  float* pb = nullptr;          // m x r_max: P~ after the first CholQR pass
+  float* Uf = nullptr;          // r_max^2: inverse Cholesky factor (fp32) for the bf16 apply
   float* P = nullptr;           // m x r_max fp32: the orthonormal P
   float* R = nullptr;           // n x r_max
   double* W = nullptr;          // r_max^2 Gram matrix, then its Cholesky factor
@@ -160,9 +161,10 @@ struct cd_group {
   void* out_host = nullptr;     // pinned
   hipEvent_t ev = nullptr;
   cd::CholTab* chol_tab = nullptr;      // [L] static workspace pointers
-  cd::TrsmTab* trsm_tab[3] = {nullptr, nullptr, nullptr};  // pass 0 / 1 / pass 0 from fp32 P~
-  int2* trsm_tiles = nullptr;           // (layer, 64-row tile) pairs
-  int ntiles = 0;
+  cd::TrsmTab* trsm_tab[3] = {nullptr, nullptr, nullptr};  // P1 = P~ T^-1; U = T^-1; P = P1 T^-1
+  int2* trsm_tiles = nullptr;           // (layer, 64-row tile of m) pairs
+  int2* trtri_tiles = nullptr;          // (layer, 64-row tile of r_max) pairs
+  int ntiles = 0, ntiles_r = 0;
   Timer timer;
 };
 
@@ -170,7 +172,7 @@ namespace {
 
 void free_layer(cd_layer* L) {
   if (!L) return;
-  void* ptrs[] = {L->prev, L->rankdef, L->pa, L->pb, L->P, L->R, L->W, L->Dinv, L->floor_,
+  void* ptrs[] = {L->prev, L->rankdef, L->pa, L->pb, L->Uf, L->P, L->R, L->W, L->Dinv, L->floor_,
                   L->gram_part, L->split_part, L->colsq, L->colnrm, L->planes};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
@@ -190,6 +192,7 @@ void free_group(cd_group* g) {
   if (g->trsm_tab[1]) (void)hipFree(g->trsm_tab[1]);
   if (g->trsm_tab[2]) (void)hipFree(g->trsm_tab[2]);
   if (g->trsm_tiles) (void)hipFree(g->trsm_tiles);
+  if (g->trtri_tiles) (void)hipFree(g->trtri_tiles);
   delete g;
 }
 
@@ -222,18 +225,20 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   std::vector<double*> pv(n);
   std::vector<cd::CholTab> ct(n);
   std::vector<cd::TrsmTab> t0(n), t1(n), t2(n);
-  std::vector<int2> tiles;
+  std::vector<int2> tiles, rtiles;
   for (int i = 0; i < n; ++i) {
     cd_layer* L = layers[i];
     np[i] = static_cast<int>(blocks_for(1LL * L->d.m * L->d.n));
     pv[i] = L->prev;
     ct[i] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef};
     t0[i] = cd::TrsmTab{L->pa, L->pb, L->W, L->Dinv, L->d.m};
-    t1[i] = cd::TrsmTab{L->pb, L->P, L->W, L->Dinv, L->d.m};
-    t2[i] = cd::TrsmTab{L->P, L->pb, L->W, L->Dinv, L->d.m};
+    t1[i] = cd::TrsmTab{nullptr, L->Uf, L->W, L->Dinv, L->d.r_max};
+    t2[i] = cd::TrsmTab{L->pb, L->P, L->W, L->Dinv, L->d.m};
     for (int rt = 0; rt < (L->d.m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) tiles.push_back(int2{i, rt});
+    for (int rt = 0; rt < (L->d.r_max + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) rtiles.push_back(int2{i, rt});
   }
   g->ntiles = static_cast<int>(tiles.size());
+  g->ntiles_r = static_cast<int>(rtiles.size());
   hipError_t e = hipSuccess;
   if (e == hipSuccess) e = dalloc(&g->parts, static_cast<size_t>(n) * g->nparts_stride);
   if (e == hipSuccess) e = dalloc(&g->nparts, n);
@@ -249,10 +254,13 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   if (e == hipSuccess) e = dalloc(&g->trsm_tab[1], n);
   if (e == hipSuccess) e = dalloc(&g->trsm_tab[2], n);
   if (e == hipSuccess) e = dalloc(&g->trsm_tiles, tiles.size());
+  if (e == hipSuccess) e = dalloc(&g->trtri_tiles, rtiles.size());
   if (e == hipSuccess) e = hipMemcpy(g->chol_tab, ct.data(), sizeof(cd::CholTab) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[0], t0.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[1], t1.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[2], t2.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(g->trtri_tiles, rtiles.data(), sizeof(int2) * rtiles.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess)
     e = hipMemcpy(g->trsm_tiles, tiles.data(), sizeof(int2) * tiles.size(), hipMemcpyHostToDevice);
   if (e != hipSuccess) {
@@ -297,10 +305,15 @@ cd_status run(cd_group* g, int kind, double bytes, double flops, hipStream_t s, 
 }
 
 // One stage of the sync branch for the layers `sel` (all of one shape):
-//   0: P~ = B Q (fp64)            1, 2: Gram matrix of CholQR pass 0 / 1
-//   3: R = B^T P, ColumnNormalize, the M / X update
-// The Cholesky factorisations and triangular solves run between the stages
-// over all layers at once (enqueue_orthogonalize).
+//   0: P~ = B Q          1: Gram matrix of CholQR pass 0 (fp64)
+//   2: pass-0 apply, bf16-gradient layers: P1 = P~ U (bf16 x 6, U = T^-1 in fp32)
+//   3: Gram matrix of pass 1 (fp64 for fp32 layers; bf16 x 6 for bf16-gradient
+//      layers, whose P1 is well conditioned)
+//   4: pass-1 apply, bf16-gradient layers: P = P1 U
+//   5: R = B^T P, ColumnNormalize, the M / X update
+// Cholesky factorisations, triangular solves and inverses run between the
+// stages over all layers at once (enqueue_factor); fp32 layers apply T^-1 by
+// fp64 triangular solves there.
 cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>& sel,
                        float* const* M, float* const* X, float* const* Q, float mu, float eta,
                        int r, int stage, hipStream_t s) {
@@ -311,11 +324,11 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   // pieces > 0: fp32 operands on the bf16 MFMA with `pieces`-way splits
   auto gemm = [&](int tkind, double flops, double bytes, cd::GemmKind kind, int Mr, int Nr, int K,
                   bool a_kc, int lda, bool b_kc, int ldb, bool upper, auto Aof, auto Bof, auto Cof,
-                  auto Pof, int pieces = 0) -> cd_status {
+                  auto Pof, int pieces = 0, bool bf_out64 = false) -> cd_status {
     const bool acc64 = pieces == 0 && cd::gemm_acc64(kind);
     cd::GemmArgs ga{};
     ga.M = Mr; ga.N = Nr; ga.K = K; ga.lda = lda; ga.ldb = ldb; ga.ldc = Nr;
-    ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper;
+    ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper; ga.out64 = bf_out64;
     ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk, pieces);
     ga.split_stride = 1LL * Mr * Nr;
     for (int j = 0; j < nl; ++j) {
@@ -331,7 +344,8 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
       cd::ReduceArgs ra{};
       ra.count = 1LL * Mr * Nr; ra.stride = ga.split_stride; ra.splits = ga.splits;
       for (int j = 0; j < nl; ++j) { ra.part[j] = Pof(j); ra.out[j] = Cof(j); }
-      const bool out64 = pieces == 0 && (kind == cd::GemmKind::F64 || kind == cd::GemmKind::F64_FROM_F32);
+      const bool out64 = pieces == 0 ? (kind == cd::GemmKind::F64 || kind == cd::GemmKind::F64_FROM_F32)
+                                     : bf_out64;
       const double rb = static_cast<double>(ra.count) * nl * (acc64 ? 8.0 : 4.0) * (ga.splits + 1);
       st2 = run(g, K_REDUCE, rb, 0.0, s, [&] { return cd::launch_reduce_splits(ra, nl, acc64, out64, s); });
       if (st2 != CD_OK) return st2;
@@ -356,18 +370,39 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
                 [&](int j) { return static_cast<const void*>(Q[sel[j]]); },
                 [&](int j) { return static_cast<void*>(lay(j)->pa); }, part);
   }
-  if (stage == 1 || stage == 2) {
-    const int pass = stage - 1;
-    if (pass == 0 && fast)
+  if (stage == 1) {
+    // the pass-0 Gram matrix in fp64: kappa(P~) reaches 1e5-1e6 in these streams
+    if (fast)
       return gemm(K_GRAM, mr * (r + 1), 4.0 * mr + 8.0 * rr, cd::GemmKind::F64_FROM_F32, r, r, m, false,
                   r, false, r, true, [&](int j) { return static_cast<const void*>(lay(j)->P); },
                   [&](int j) { return static_cast<const void*>(lay(j)->P); },
                   [&](int j) { return static_cast<void*>(lay(j)->W); },
                   [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
-    auto In = [&](int j) { return static_cast<const void*>(pass == 0 ? lay(j)->pa : lay(j)->pb); };
     return gemm(K_GRAM, mr * (r + 1), 8.0 * mr + 8.0 * rr, cd::GemmKind::F64, r, r, m, false, r, false,
-                r, true, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); },
+                r, true, [&](int j) { return static_cast<const void*>(lay(j)->pa); },
+                [&](int j) { return static_cast<const void*>(lay(j)->pa); },
+                [&](int j) { return static_cast<void*>(lay(j)->W); },
                 [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
+  }
+  if (stage == 2 || stage == 4) {
+    // apply an inverse factor: out = in U, U upper triangular (fp32-accurate).
+    // Any error in U keeps span(out) and leaves the final Q-factor unchanged;
+    // it only changes how close to orthonormal `out` is.
+    if (!fast) return CD_OK;   // fp32 layers: fp64 triangular solves in enqueue_factor
+    auto In = [&](int j) { return static_cast<const void*>(stage == 2 ? lay(j)->P : lay(j)->pb); };
+    auto Out = [&](int j) { return static_cast<void*>(stage == 2 ? lay(j)->pb : lay(j)->P); };
+    return gemm(K_APPLY_BF, mr * r, 12.0 * mr + 4.0 * rr, cd::GemmKind::F32, m, r, r, true, r, false, r,
+                false, In, [&](int j) { return static_cast<const void*>(lay(j)->Uf); }, Out, part, 3);
+  }
+  if (stage == 3) {
+    auto In = [&](int j) { return static_cast<const void*>(lay(j)->pb); };
+    if (!fast)
+      return gemm(K_GRAM, mr * (r + 1), 4.0 * mr + 8.0 * rr, cd::GemmKind::F64_FROM_F32, r, r, m, false,
+                  r, false, r, true, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); },
+                  [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
+    // pass-1 Gram matrix of the nearly orthonormal P1, fp32-accurate, into fp64 W
+    return gemm(K_GRAM_BF, 2.0 * mr * r, 4.0 * mr + 8.0 * rr, cd::GemmKind::F32, r, r, m, false, r, false,
+                r, false, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); }, part, 3, true);
   }
   // R = B^T P
   cd_status st = gemm(K_PBTP, 2.0 * mn * r, 4.0 * mn + 4.0 * mr + 4.0 * nr, cd::GemmKind::F32, n, r, m,
@@ -423,23 +458,28 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
              [&] { return cd::launch_update_planes(ua, nl, up, s); });
 }
 
-// CholQR pass `pass` over every layer: Cholesky of each W, then P = P~ T^{-1}
-// (pass 0: pa -> pb in fp64; pass 1: pb -> P rounded to fp32).
-cd_status enqueue_orthogonalize(cd_group* g, int r, int pass, hipStream_t s) {
+// Between the stages of CholQR pass `pass`, over every layer: Cholesky of each
+// W, then either the fp64 triangular solve (fp32 layers: P1 = P~ T^-1, then
+// P = P1 T^-1) or the inverse U = T^-1 in fp32 for the bf16 x 6 apply.
+cd_status enqueue_factor(cd_group* g, int r, int pass, hipStream_t s) {
   const double L = g->L, rr = 1.0 * r * r;
   cd_status st = run(g, K_CHOL, 16.0 * rr * L, (1.0 / 3.0) * rr * r * L, s,
                      [&] { return cd::launch_cholesky(g->chol_tab, g->L, r, pass, s); });
   if (st != CD_OK) return st;
-  double flops = 0, bytes = 0;
-  for (const cd_layer* Ly : g->layers) {
-    const double mr = 1.0 * Ly->d.m * r;
-    flops += mr * r;
-    bytes += 8.0 * mr + (pass == 0 ? 8.0 : 4.0) * mr + 8.0 * rr / 2;
+  if (!g->g_bf16) {
+    double flops = 0, bytes = 0;
+    for (const cd_layer* Ly : g->layers) {
+      const double mr = 1.0 * Ly->d.m * r;
+      flops += mr * r;
+      bytes += (pass == 0 ? 8.0 : 4.0) * mr + 4.0 * mr + 4.0 * rr;
+    }
+    return run(g, K_TRSM, bytes, flops, s, [&] {
+      return cd::launch_trsm(g->trsm_tab[pass == 0 ? 0 : 2], g->trsm_tiles, g->ntiles, r, pass == 0,
+                             false, s);
+    });
   }
-  const bool in64 = !(pass == 0 && g->g_bf16);
-  cd::TrsmTab* tab = (pass == 0 && g->g_bf16) ? g->trsm_tab[2] : g->trsm_tab[pass];
-  return run(g, K_APPLY, bytes, flops, s, [&] {
-    return cd::launch_trsm(tab, g->trsm_tiles, g->ntiles, r, in64, pass == 0, s);
+  return run(g, K_TRTRI, 12.0 * rr * L, rr * r / 3.0 * L, s, [&] {
+    return cd::launch_trsm(g->trsm_tab[1], g->trtri_tiles, g->ntiles_r, r, true, false, s, true, r);
   });
 }
 
@@ -521,13 +561,13 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
     return CD_OK;
   };
   if (sync) {
-    for (int stage = 0; stage < 4; ++stage) {
+    for (int stage = 0; stage < 6; ++stage) {
       cd_status st = for_chunks([&](const ShapeClass& sc, const std::vector<int>& sel) {
         return enqueue_sync(g, sc, sel, M, X, Q, mu, eta, r, stage, s);
       });
       if (st != CD_OK) return st;
-      if (stage == 1 || stage == 2) {
-        st = enqueue_orthogonalize(g, r, stage - 1, s);
+      if (stage == 1 || stage == 3) {
+        st = enqueue_factor(g, r, stage == 1 ? 0 : 1, s);
         if (st != CD_OK) return st;
       }
     }
@@ -577,6 +617,8 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
       split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, true, &kc) * mr * sizeof(double));
       split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, false, &kc, 3) * mr * sizeof(float));
       split_bytes = std::max(split_bytes, plan_splits(n, r, m, 1, false, &kc, 3) * nr * sizeof(float));
+      split_bytes = std::max(split_bytes, plan_splits(m, r, r, 1, false, &kc, 3) * mr * sizeof(float));
+      split_bytes = std::max(split_bytes, plan_splits(r, r, m, 1, false, &kc, 3) * r * r * sizeof(float));
       gram_cap = std::max(gram_cap, static_cast<size_t>(plan_splits(r, r, m, 1, true, &kc)) * r * r);
     }
     const size_t nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
@@ -585,6 +627,7 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
     if (e == hipSuccess) e = dalloc(&L->rankdef, 1);
     if (e == hipSuccess) e = dalloc(&L->pa, 1ULL * m * rm);
     if (e == hipSuccess) e = dalloc(&L->pb, 1ULL * m * rm);
+    if (e == hipSuccess) e = dalloc(&L->Uf, 1ULL * rm * rm);
     if (e == hipSuccess) e = dalloc(&L->P, 1ULL * m * rm);
     if (e == hipSuccess) e = dalloc(&L->R, 1ULL * n * rm);
     if (e == hipSuccess) e = dalloc(&L->W, 1ULL * rm * rm);

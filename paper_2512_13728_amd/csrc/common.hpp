@@ -77,6 +77,7 @@ struct GemmArgs {
   long long split_stride;          // elements between split partials
   bool a_kc, b_kc;
   bool upper_only;                 // skip tiles strictly below the diagonal
+  bool out64;                      // bf16-split kernels: write the result as fp64
   const void* A[MAXB];
   const void* B[MAXB];
   void* C[MAXB];                   // result (splits == 1) or partials (splits > 1)
@@ -126,9 +127,10 @@ struct TrsmTab {
   const double* Dinv;
   int m;
 };
-// tiles: one (layer, 64-row tile) pair per workgroup.
+// tiles: one (layer, 64-row tile) pair per workgroup.  ident: Pin is the
+// identity (the result is T^{-1}); mlimit > 0 caps every layer's row count.
 hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r, bool in64, bool out64,
-                       hipStream_t s);
+                       hipStream_t s, bool ident = false, int mlimit = 0);
 
 // ---- ColumnNormalize --------------------------------------------------------
 constexpr int COLNORM_ROWS = 256;  // rows per partial

@@ -6,8 +6,9 @@
 // layers of the group (they share r):
 //   chol_diag  (one workgroup per layer)  T_kk = chol(W_kk) in LDS and its
 //              inverse D_k = T_kk^{-1}; the first block also sets the pivot
-//              floor 1e-13 * max_i W_ii (smaller or NaN pivots are raised to
-//              it and the layer is flagged rank deficient)
+//              floor max(1e-13 * max_i W_ii, 1e-60) (smaller or NaN pivots are raised to
+//              it and the layer is flagged rank deficient; the absolute floor
+//              keeps T^{-1} finite in fp32 when P~ is numerically zero)
 //   chol_panel X = D_k^T W[k, k+1:]: the k-th block row of T       (fp64 MFMA)
 //   chol_trail W[k+1:, k+1:] -= X^T X, upper tiles only            (fp64 MFMA)
 // and the triangular solve, one launch per block column c:
@@ -41,7 +42,7 @@ __global__ __launch_bounds__(256) void k_chol_diag(const CholTab* __restrict__ t
     __syncthreads();
     if (tid == 0) {
       const double m = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
-      *t.floor_ = fmax(1e-13 * m, 1e-300);
+      *t.floor_ = fmax(1e-13 * m, 1e-60);
       if (pass == 0) *t.rankdef = 0;
     }
     __syncthreads();
@@ -189,17 +190,20 @@ __global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ 
 }
 
 // Block column c of P = P~ T^{-1}; one 64-row tile of one layer per workgroup.
-template <typename TIn, typename TOut>
+// IDENT: P~ is the identity (P = T^{-1}, upper triangular, exact zeros below).
+// mlimit > 0 caps the row count (the identity has r rows).
+template <typename TIn, typename TOut, bool IDENT>
 __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, const int2* __restrict__ tiles,
-                                              int r, int cb) {
+                                              int r, int cb, int mlimit) {
   constexpr int YLD = CB + 4;
   __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
   __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
   __shared__ __attribute__((aligned(16))) double Ys[CB * YLD];
   const int2 lt = tiles[blockIdx.x];
   const TrsmTab t = tab[lt.x];
-  const int m = t.m;
+  const int m = mlimit > 0 ? min(t.m, mlimit) : t.m;
   const int i0 = lt.y * CB;
+  if (i0 >= m) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
   const int c0 = cb * CB, nbc = min(CB, r - c0);
@@ -226,8 +230,12 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
         const int row = wm0 + i * 16 + Mfma<double>::out_row(lane, v);
         const int col = wn0 + j * 16 + (lane & 15);
         double y = 0.0;
-        if (i0 + row < m && col < nbc)
-          y = static_cast<double>(Pin[static_cast<long long>(i0 + row) * r + c0 + col]) - T.acc[i][j][v];
+        if (i0 + row < m && col < nbc) {
+          double pin;
+          if constexpr (IDENT) pin = (i0 + row == c0 + col) ? 1.0 : 0.0;
+          else pin = static_cast<double>(Pin[static_cast<long long>(i0 + row) * r + c0 + col]);
+          y = pin - T.acc[i][j][v];
+        }
         Ys[row * YLD + col] = y;
       }
   const double* D = t.Dinv + static_cast<long long>(cb) * CB * CB;
@@ -285,14 +293,23 @@ hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hip
 }
 
 hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r, bool in64, bool out64,
-                       hipStream_t s) {
+                       hipStream_t s, bool ident, int mlimit) {
   if (ntiles <= 0) return hipSuccess;
   const int nblk = (r + CB - 1) / CB;
+  const dim3 grid(ntiles), block(256);
   for (int cb = 0; cb < nblk; ++cb) {
-    if (in64 && out64) hipLaunchKernelGGL((k_trsm<double, double>), dim3(ntiles), dim3(256), 0, s, tab, tiles, r, cb);
-    else if (in64) hipLaunchKernelGGL((k_trsm<double, float>), dim3(ntiles), dim3(256), 0, s, tab, tiles, r, cb);
-    else if (out64) hipLaunchKernelGGL((k_trsm<float, double>), dim3(ntiles), dim3(256), 0, s, tab, tiles, r, cb);
-    else hipLaunchKernelGGL((k_trsm<float, float>), dim3(ntiles), dim3(256), 0, s, tab, tiles, r, cb);
+    if (ident) {
+      if (out64) hipLaunchKernelGGL((k_trsm<double, double, true>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+      else hipLaunchKernelGGL((k_trsm<double, float, true>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+    } else if (in64 && out64) {
+      hipLaunchKernelGGL((k_trsm<double, double, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+    } else if (in64) {
+      hipLaunchKernelGGL((k_trsm<double, float, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+    } else if (out64) {
+      hipLaunchKernelGGL((k_trsm<float, double, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+    } else {
+      hipLaunchKernelGGL((k_trsm<float, float, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+    }
   }
   return hipGetLastError();
 }

@@ -135,6 +135,7 @@ hipError_t launch_reduce_splits(const ReduceArgs& a, int nl, bool part64, bool o
   const dim3 grid(static_cast<unsigned>(blocks), nl);
   if (part64 && out64) hipLaunchKernelGGL((k_reduce<double, double>), grid, dim3(256), 0, s, a);
   else if (part64) hipLaunchKernelGGL((k_reduce<double, float>), grid, dim3(256), 0, s, a);
+  else if (out64) hipLaunchKernelGGL((k_reduce<float, double>), grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL((k_reduce<float, float>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }

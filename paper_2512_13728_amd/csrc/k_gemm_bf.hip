@@ -75,7 +75,10 @@ __global__ __launch_bounds__(256) void k_gemm_bf(GemmArgs g) {
     __syncthreads();
   }
 
+  // fp32 split partials, or the result (fp32, or fp64 when out64)
   float* C = static_cast<float*>(g.C[layer]) + static_cast<long long>(blockIdx.y) * g.split_stride;
+  double* C64 = static_cast<double*>(g.C[layer]);
+  const bool wide = g.out64 && g.splits == 1;
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -84,7 +87,11 @@ __global__ __launch_bounds__(256) void k_gemm_bf(GemmArgs g) {
       for (int v = 0; v < 4; ++v) {
         const int row = m0 + wm0 + i * 16 + 4 * (lane >> 4) + v;
         const int col = n0 + wn0 + j * 16 + (lane & 15);
-        if (row < g.M && col < g.N) C[static_cast<long long>(row) * g.ldc + col] = acc[i][j][v];
+        if (row < g.M && col < g.N) {
+          const long long o = static_cast<long long>(row) * g.ldc + col;
+          if (wide) C64[o] = acc[i][j][v];
+          else C[o] = acc[i][j][v];
+        }
       }
 }
 

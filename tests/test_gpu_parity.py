@@ -11,8 +11,9 @@ unless stated):
 * dX = X_t - X_{t-1}: that bound plus 2 u ‖X_t‖ / ‖dX‖ (X_t is stored in fp32)
 * P^T P - I and |‖Q_j‖ - 1|: 1e-5 (absolute, Frobenius / max)
 * local branch: M bit-exact against fp32 M + G, X within 1 ulp of fp32 FMA
-* bf16 gradients (the path may use bf16 products for the rank-r update):
-            M, X, P, Q, dX within 2e-2; decisions identical
+* bf16 gradients (the path uses bf16 products for the rank-r update and
+            fp32-accurate arithmetic for the second CholQR pass): M, X, P, Q,
+            dX within 2e-2, ‖P^T P - I‖_F <= 1e-4; decisions identical
 Free-running trajectories check every decision against the free-running
 oracle and every step teacher-forced (the oracle restarted from the GPU
 state) with the bounds above; the drift between the two free-running states
@@ -68,7 +69,7 @@ def _check_step(d, tau, policy, bf16=False):
             if k in d:
                 assert d[k] <= 2e-2, (k, d)
         if d["flag_oracle"]:
-            assert d["orth_P"] <= 1e-5 and d["colnorm_dev"] <= 1e-5, d
+            assert d["orth_P"] <= 1e-4 and d["colnorm_dev"] <= 1e-5, d
         return
     assert d["err_M"] <= 1e-5, d
     assert d["err_X"] <= 1e-5, d
