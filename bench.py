@@ -35,7 +35,8 @@ PEAK_TFLOPS = {"f64": 78.6, "f32": 157.3, "bf16": 2500.0}
 # bound, MFMA dtype and executed MFMA flops per algorithmic flop, per kernel kind
 # (bf16x6: each fp32 product is formed from six bf16 piece products)
 KIND_BOUND = {
-    "form_buffer": ("hbm", None, 1), "local_update": ("hbm", None, 1), "gate": ("hbm", None, 1),
+    "form_buffer": ("hbm", None, 1), "form_buffer_local": ("hbm", None, 1),
+    "local_update": ("hbm", None, 1), "gate": ("hbm", None, 1),
     "reduce_splits": ("hbm", None, 1), "colnorm": ("hbm", None, 1),
     "power_bq_f64": ("mfma", "f64", 1), "gram_f64": ("mfma", "f64", 1), "trsm_f64": ("mfma", "f64", 1),
     "cholesky_f64": ("mfma", "f64", 1), "power_bq_bf16x6": ("mfma", "bf16", 6),

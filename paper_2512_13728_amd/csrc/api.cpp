@@ -85,10 +85,10 @@ hipError_t dalloc(T** p, size_t count) {
 }
 
 // ---- optional per-kernel timing (HIP events on the launch stream) ----------
-enum Kind { K_FORM, K_GATE, K_LOCAL, K_PBQ, K_PBQ_BF, K_GRAM, K_GRAM_BF, K_CHOL, K_TRSM, K_TRTRI,
+enum Kind { K_FORM, K_FORM_X, K_GATE, K_LOCAL, K_PBQ, K_PBQ_BF, K_GRAM, K_GRAM_BF, K_CHOL, K_TRSM, K_TRTRI,
             K_APPLY_BF, K_PBTP, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_NKINDS };
 const char* const kKindName[K_NKINDS] = {
-    "form_buffer", "gate", "local_update", "power_bq_f64", "power_bq_bf16x6", "gram_f64",
+    "form_buffer", "form_buffer_local", "gate", "local_update", "power_bq_f64", "power_bq_bf16x6", "gram_f64",
     "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_bf16x6",
     "reduce_splits", "colnorm", "update_bf16x6", "update_bf16"};
 
@@ -157,6 +157,9 @@ struct cd_group {
   double* parts = nullptr;      // [L][nparts_stride]
   int* nparts = nullptr;        // [L]
   double** prev = nullptr;      // [L] device pointers to each layer's prev_norm
+  double* norms = nullptr;      // [L] gate workspace
+  unsigned* counter = nullptr;  // gate completion counter (returns to zero)
+  bool predict_skip = false;    // RMMC policy: branch predicted for the next step
   cd::GateOut* out_dev = nullptr;
   void* out_host = nullptr;     // pinned
   hipEvent_t ev = nullptr;
@@ -184,6 +187,8 @@ void free_group(cd_group* g) {
   if (g->parts) (void)hipFree(g->parts);
   if (g->nparts) (void)hipFree(g->nparts);
   if (g->prev) (void)hipFree(g->prev);
+  if (g->norms) (void)hipFree(g->norms);
+  if (g->counter) (void)hipFree(g->counter);
   if (g->out_dev) (void)hipFree(g->out_dev);
   if (g->out_host) (void)hipHostFree(g->out_host);
   if (g->ev) (void)hipEventDestroy(g->ev);
@@ -243,6 +248,9 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   if (e == hipSuccess) e = dalloc(&g->parts, static_cast<size_t>(n) * g->nparts_stride);
   if (e == hipSuccess) e = dalloc(&g->nparts, n);
   if (e == hipSuccess) e = dalloc(&g->prev, n);
+  if (e == hipSuccess) e = dalloc(&g->norms, n);
+  if (e == hipSuccess) e = dalloc(&g->counter, 1);
+  if (e == hipSuccess) e = hipMemset(g->counter, 0, sizeof(unsigned));
   if (e == hipSuccess)
     e = hipMalloc(reinterpret_cast<void**>(&g->out_dev), sizeof(cd::GateOut) + sizeof(double) * n);
   if (e == hipSuccess) e = hipHostMalloc(&g->out_host, sizeof(cd::GateOut) + sizeof(double) * n);
@@ -315,6 +323,7 @@ cd_status run(cd_group* g, int kind, double bytes, double flops, hipStream_t s, 
 // stages over all layers at once (enqueue_factor); fp32 layers apply T^-1 by
 // fp64 triangular solves there.
 cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>& sel,
+                       const void* const* G, float eta_local_spec,
                        float* const* M, float* const* X, float* const* Q, float mu, float eta,
                        int r, int stage, hipStream_t s) {
   const int m = sc.m, n = sc.n, nl = static_cast<int>(sel.size());
@@ -448,13 +457,17 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   ua.m = m; ua.n = n; ua.r = r; ua.rp = rp;
   ua.one_minus_mu = static_cast<float>(1.0 - static_cast<double>(mu));
   ua.c = static_cast<float>(static_cast<double>(eta) * std::sqrt(static_cast<double>(m) / n));
+  ua.g_bf16 = g->g_bf16 ? 1 : 0;
   for (int j = 0; j < nl; ++j) {
+    ua.G[j] = G[sel[j]];
+    ua.gc[j] = static_cast<float>(lay(j)->d.eta_local_scale * static_cast<double>(eta_local_spec));
     ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]];
     ua.P[j] = lay(j)->planes;
     ua.R[j] = lay(j)->planes + 3LL * m * rp;
     ua.Q[j] = lay(j)->planes + 3LL * m * rp + 3LL * n * rp;
   }
-  return run(g, fast ? K_UPDATE_BF1 : K_UPDATE, 16.0 * mn * nl, 4.0 * mn * r * nl, s,
+  const double ub = (16.0 + (eta_local_spec != 0.0f ? (g->g_bf16 ? 2.0 : 4.0) : 0.0)) * mn * nl;
+  return run(g, fast ? K_UPDATE_BF1 : K_UPDATE, ub, 4.0 * mn * r * nl, s,
              [&] { return cd::launch_update_planes(ua, nl, up, s); });
 }
 
@@ -502,7 +515,21 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   if (!dg.ok) return fail(CD_EHIP, "cannot select device %d", g->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
-  // 1. B = M + G, partial sums of B^2
+  // Skip-branch speculation: when the coming decision is known or predicted
+  // to be "skip", X -= eta_local G rides along in the buffer pass, which saves
+  // the second read of G; should the step sync after all, the sync update
+  // first adds eta_local G back (in fp32, one rounding).  The RMMC policy
+  // predicts the previous step's branch.
+  const long long next_step = g->layers[0]->step + 1;
+  bool spec = false;
+  switch (g->policy) {
+    case CD_POLICY_RMMC: spec = g->predict_skip; break;
+    case CD_POLICY_ALWAYS_SYNC: spec = false; break;
+    case CD_POLICY_NEVER_SYNC: spec = true; break;
+    case CD_POLICY_EVERY_H: spec = (next_step % g->H) != 0; break;
+  }
+
+  // 1. B = M + G, partial sums of B^2 (and the speculative skip update)
   for (const ShapeClass& sc : g->shapes) {
     const long long numel = 1LL * sc.m * sc.n;
     for (size_t c0 = 0; c0 < sc.idx.size(); c0 += cd::MAXB) {
@@ -513,10 +540,12 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
       for (int j = 0; j < nl; ++j) {
         const int li = sc.idx[c0 + j];
         fa.M[j] = M[li]; fa.G[j] = G[li]; fa.part[j] = g->parts + 1LL * li * g->nparts_stride;
+        fa.X[j] = X[li];
+        fa.coef[j] = static_cast<float>(g->layers[li]->d.eta_local_scale * static_cast<double>(eta));
       }
-      const double fb = static_cast<double>(numel) * nl * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
-      cd_status st = run(g, K_FORM, fb, 3.0 * numel * nl, s,
-                         [&] { return cd::launch_form_buffer(fa, nl, g->g_bf16, s); });
+      const double fb = static_cast<double>(numel) * nl * ((spec ? 16.0 : 8.0) + (g->g_bf16 ? 2.0 : 4.0));
+      cd_status st = run(g, spec ? K_FORM_X : K_FORM, fb, (spec ? 5.0 : 3.0) * numel * nl, s,
+                         [&] { return cd::launch_form_buffer(fa, nl, g->g_bf16, spec, s); });
       if (st != CD_OK) return st;
     }
   }
@@ -524,6 +553,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   cd::GateArgs ga{};
   ga.L = g->L; ga.nparts_stride = g->nparts_stride; ga.parts = g->parts; ga.nparts = g->nparts;
   ga.prev = g->prev; ga.eps = g->eps; ga.tau = g->tau; ga.out = g->out_dev;
+  ga.norms = g->norms; ga.counter = g->counter;
   {
     cd_status st = run(g, K_GATE, 8.0 * g->L * g->nparts_stride, 0.0, s, [&] { return cd::launch_gate(ga, s); });
     if (st != CD_OK) return st;
@@ -563,7 +593,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   if (sync) {
     for (int stage = 0; stage < 6; ++stage) {
       cd_status st = for_chunks([&](const ShapeClass& sc, const std::vector<int>& sel) {
-        return enqueue_sync(g, sc, sel, M, X, Q, mu, eta, r, stage, s);
+        return enqueue_sync(g, sc, sel, G, spec ? eta : 0.0f, M, X, Q, mu, eta, r, stage, s);
       });
       if (st != CD_OK) return st;
       if (stage == 1 || stage == 3) {
@@ -572,7 +602,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
       }
     }
     for (cd_layer* Ly : g->layers) Ly->last_r = r;
-  } else {
+  } else if (!spec) {
     cd_status st = for_chunks([&](const ShapeClass& sc, const std::vector<int>& sel) -> cd_status {
       const int nl = static_cast<int>(sel.size());
       cd::LocalArgs la{};
@@ -589,6 +619,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
     });
     if (st != CD_OK) return st;
   }
+  g->predict_skip = !sync;
   if (out) { out->rmmc = gmax; out->sync_flag = sync ? 1 : 0; }
   if (nonfinite) return fail(CD_ENONFINITE, "a layer norm ||B|| was not finite");
   return CD_OK;

@@ -24,8 +24,10 @@ struct FormArgs {
   float* M[MAXB];                  // in: M_{t-1}; out: B_t
   const void* G[MAXB];             // fp32 or bf16
   double* part[MAXB];              // out: blocks_per_layer partial sums of B^2
+  float* X[MAXB];                  // with_x: the skip-branch update X -= coef G, fused
+  float coef[MAXB];                // eta_local per layer (with_x only)
 };
-hipError_t launch_form_buffer(const FormArgs& a, int nl, bool g_bf16, hipStream_t s);
+hipError_t launch_form_buffer(const FormArgs& a, int nl, bool g_bf16, bool with_x, hipStream_t s);
 
 // ---- local branch: X = X - eta_local G --------------------------------------
 struct LocalArgs {
@@ -53,6 +55,8 @@ struct GateArgs {
   double eps;
   double tau;
   GateOut* out;                    // + L doubles after the header
+  double* norms;                   // [L] workspace: ‖B‖ per layer
+  unsigned* counter;               // zero between launches (the last block resets it)
 };
 hipError_t launch_gate(const GateArgs& a, hipStream_t s);
 
@@ -176,6 +180,11 @@ struct UpdatePlArgs {
   const __bf16* P[MAXB];
   const __bf16* R[MAXB];
   const __bf16* Q[MAXB];
+  // reversal of a speculative skip-branch update: X += gc G before the rank-r
+  // correction (gc = 0: none)
+  const void* G[MAXB];
+  float gc[MAXB];
+  int g_bf16;
 };
 hipError_t launch_update_planes(const UpdatePlArgs& a, int nl, int pieces, hipStream_t s);
 

@@ -132,6 +132,22 @@ __global__ __launch_bounds__(256) void k_split_planes(PlaneArgs a) {
 // by the BN-column tiles that the XCD-aware order keeps on one XCD.
 constexpr int UBM = 128;
 
+// G elements for the reversal of a speculative skip update: fp32, or bf16
+// widened exactly.
+__device__ __forceinline__ float4 load_g4(const void* G, bool bf, long long i) {
+  if (bf) {
+    const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(G) + i);
+    return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                       __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+  }
+  return *reinterpret_cast<const float4*>(static_cast<const float*>(G) + i);
+}
+
+__device__ __forceinline__ float load_g1(const void* G, bool bf, long long i) {
+  if (bf) return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(G)[i]) << 16);
+  return static_cast<const float*>(G)[i];
+}
+
 template <int S, int BN>
 __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
   constexpr int TM = 4, TN = BN / 32;   // wave tile 64 x BN/2
@@ -250,22 +266,36 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
     __syncthreads();
     float* Y = which == 0 ? u.M[l] : u.X[l];
     const float coef = which == 0 ? -u.one_minus_mu : -u.c;
+    // X only: first undo a speculative skip-branch update (X += gc G)
+    const float gc = which == 0 ? 0.f : u.gc[l];
+    const void* const G = u.G[l];
+    const bool gbf = u.g_bf16 != 0;
 #pragma unroll 4
     for (int e = tid; e < UBM * (BN / 4); e += 256) {
       const int row = e / (BN / 4), c4 = (e % (BN / 4)) * 4;
       const int grow = m0 + row, gcol = n0 + c4;
       if (grow >= u.m) continue;
       const float4 a = *reinterpret_cast<const float4*>(st + row * SLD + c4);
-      float* y = Y + static_cast<long long>(grow) * u.n + gcol;
+      const long long off = static_cast<long long>(grow) * u.n + gcol;
+      float* y = Y + off;
       if (vec && gcol + 3 < u.n) {
         float4 w = *reinterpret_cast<const float4*>(y);
+        if (gc != 0.f) {
+          const float4 g = load_g4(G, gbf, off);
+          w.x = fmaf(gc, g.x, w.x); w.y = fmaf(gc, g.y, w.y);
+          w.z = fmaf(gc, g.z, w.z); w.w = fmaf(gc, g.w, w.w);
+        }
         w.x = fmaf(coef, a.x, w.x); w.y = fmaf(coef, a.y, w.y);
         w.z = fmaf(coef, a.z, w.z); w.w = fmaf(coef, a.w, w.w);
         *reinterpret_cast<float4*>(y) = w;
       } else {
         const float av[4] = {a.x, a.y, a.z, a.w};
-        for (int c = 0; c < 4; ++c)
-          if (gcol + c < u.n) y[c] = fmaf(coef, av[c], y[c]);
+        for (int c = 0; c < 4; ++c) {
+          if (gcol + c >= u.n) continue;
+          float w = y[c];
+          if (gc != 0.f) w = fmaf(gc, load_g1(G, gbf, off + c), w);
+          y[c] = fmaf(coef, av[c], w);
+        }
       }
     }
     __syncthreads();

@@ -1,7 +1,8 @@
 // Streaming kernels of the CurvaDion step: buffer formation with the fused
 // sum of squares (B = M + G; Algorithm 2, local buffer update, feeding the
-// norm of Eq. 1), the local-branch weight update (X -= eta_local G), and the
-// gate (fixed-order reduction, RMMC, prev_norm update, max over layers).
+// norm of Eq. 1), optionally with the skip branch's weight update fused into
+// the same pass, the stand-alone skip-branch update (X -= eta_local G), and
+// the gate (fixed-order reduction, RMMC, prev_norm update, max over layers).
 //
 // These passes are HBM-bound: each thread keeps eight 16-byte loads in flight,
 // blocks own fixed 8192-element chunks of one layer, and every reduction runs
@@ -53,21 +54,26 @@ __device__ double block_sum(double v) {
 
 constexpr int VPT = FORM_CHUNK / (NTHREADS * 4);   // float4 groups per thread (8)
 
-template <bool BF16>
+// B = M + G in place, the block's partial sum of B^2, and (WX) the skip
+// branch's X -= coef G in the same pass over G.
+template <bool BF16, bool WX>
 __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
   const int l = blockIdx.y;
   float* __restrict__ M = a.M[l];
   const void* __restrict__ G = a.G[l];
+  float* __restrict__ X = a.X[l];
+  const float c = a.coef[l];
   const long long base = static_cast<long long>(blockIdx.x) * FORM_CHUNK;
   const long long end = min(base + FORM_CHUNK, a.numel);
   double acc = 0.0;
   if (end - base == FORM_CHUNK) {
-    float4 m[VPT], g[VPT];
+    float4 m[VPT], g[VPT], x[VPT];
 #pragma unroll
     for (int v = 0; v < VPT; ++v) {
       const long long i = base + 4LL * (threadIdx.x + v * NTHREADS);
       m[v] = *reinterpret_cast<const float4*>(M + i);
       g[v] = load_g4<BF16>(G, i);
+      if constexpr (WX) x[v] = *reinterpret_cast<const float4*>(X + i);
     }
 #pragma unroll
     for (int v = 0; v < VPT; ++v) {
@@ -77,6 +83,12 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
       b.z = m[v].z + g[v].z; b.w = m[v].w + g[v].w;
       *reinterpret_cast<float4*>(M + i) = b;
       acc += sq(b.x); acc += sq(b.y); acc += sq(b.z); acc += sq(b.w);
+      if constexpr (WX) {
+        float4 y;
+        y.x = fmaf(-c, g[v].x, x[v].x); y.y = fmaf(-c, g[v].y, x[v].y);
+        y.z = fmaf(-c, g[v].z, x[v].z); y.w = fmaf(-c, g[v].w, x[v].w);
+        *reinterpret_cast<float4*>(X + i) = y;
+      }
     }
   } else {
     for (long long i = base + 4LL * threadIdx.x; i < end; i += 4LL * NTHREADS) {
@@ -87,11 +99,20 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
         b.x = mv.x + gv.x; b.y = mv.y + gv.y; b.z = mv.z + gv.z; b.w = mv.w + gv.w;
         *reinterpret_cast<float4*>(M + i) = b;
         acc += sq(b.x); acc += sq(b.y); acc += sq(b.z); acc += sq(b.w);
+        if constexpr (WX) {
+          const float4 xv = *reinterpret_cast<const float4*>(X + i);
+          float4 y;
+          y.x = fmaf(-c, gv.x, xv.x); y.y = fmaf(-c, gv.y, xv.y);
+          y.z = fmaf(-c, gv.z, xv.z); y.w = fmaf(-c, gv.w, xv.w);
+          *reinterpret_cast<float4*>(X + i) = y;
+        }
       } else {
         for (long long j = i; j < end; ++j) {
-          const float b = M[j] + load_g1<BF16>(G, j);
+          const float gj = load_g1<BF16>(G, j);
+          const float b = M[j] + gj;
           M[j] = b;
           acc += sq(b);
+          if constexpr (WX) X[j] = fmaf(-c, gj, X[j]);
         }
       }
     }
@@ -140,59 +161,79 @@ __global__ __launch_bounds__(NTHREADS) void k_local_update(LocalArgs a) {
   }
 }
 
-// One block of 16 waves; wave w reduces layers w, w+16, ... with lane-strided
-// partial sums and a fixed xor tree, then thread 0 takes the max in layer
-// order.  NaN propagates into the max (and NaN > tau is false).
-constexpr int GATE_THREADS = 1024;
-constexpr int GATE_MAX_LAYERS = 4096;
+// One block per layer reduces that layer's partials in a fixed order (strided
+// per thread, then the block tree), forms RMMC and replaces prev_norm.  The
+// last block to finish (device-scope counter, which wraps back to zero) takes
+// the max over layers; max is order-free, and any NaN makes the max NaN (and
+// NaN > tau is false).
+constexpr int GATE_THREADS = 256;
+
+__device__ __forceinline__ double load_coherent(const double* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 __global__ __launch_bounds__(GATE_THREADS) void k_gate(GateArgs a) {
-  __shared__ double rm[GATE_MAX_LAYERS];
-  __shared__ int nonfinite;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (threadIdx.x == 0) nonfinite = 0;
-  __syncthreads();
-  for (int l = w; l < a.L; l += GATE_THREADS / 64) {
-    const double* p = a.parts + static_cast<long long>(l) * a.nparts_stride;
-    const int np = a.nparts[l];
-    double s = 0.0;
-    for (int i = lane; i < np; i += 64) s += p[i];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-    if (lane == 0) {
-      const double nb = sqrt(s);
-      const double prev = *a.prev[l];
-      const double v = fabs(nb - prev) / (prev + a.eps);
-      *a.prev[l] = nb;
-      rm[l] = v;
-      if (!isfinite(nb)) atomicOr(&nonfinite, 1);
-    }
+  __shared__ int last;
+  __shared__ double wmax[GATE_THREADS / 64];
+  __shared__ int wflags[GATE_THREADS / 64];
+  const int l = blockIdx.x;
+  const double* p = a.parts + static_cast<long long>(l) * a.nparts_stride;
+  const int np = a.nparts[l];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < np; i += GATE_THREADS) s += p[i];
+  s = block_sum(s);
+  double* out_rm = reinterpret_cast<double*>(a.out + 1);
+  if (threadIdx.x == 0) {
+    const double nb = sqrt(s);
+    double* prev = a.prev[l];
+    const double pv = *prev;
+    out_rm[l] = fabs(nb - pv) / (pv + a.eps);
+    a.norms[l] = nb;
+    *prev = nb;
+    __threadfence();
+    last = atomicInc(a.counter, static_cast<unsigned>(a.L - 1)) == static_cast<unsigned>(a.L - 1);
   }
   __syncthreads();
-  double* out_rm = reinterpret_cast<double*>(a.out + 1);
-  for (int l = threadIdx.x; l < a.L; l += GATE_THREADS) out_rm[l] = rm[l];
+  if (!last) return;
+  __threadfence();
+  double g = -INFINITY;
+  int flags = 0;   // bit 0: a NaN RMMC; bit 1: a non-finite norm
+  for (int i = threadIdx.x; i < a.L; i += GATE_THREADS) {
+    const double v = load_coherent(out_rm + i);
+    if (isnan(v)) flags |= 1;
+    else g = fmax(g, v);
+    if (!isfinite(load_coherent(a.norms + i))) flags |= 2;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    g = fmax(g, __shfl_xor(g, o, 64));
+    flags |= __shfl_xor(flags, o, 64);
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) { wmax[w] = g; wflags[w] = flags; }
+  __syncthreads();
   if (threadIdx.x == 0) {
-    double g = -INFINITY;
-    bool has_nan = false;
-    for (int l = 0; l < a.L; ++l) {
-      const double v = rm[l];
-      if (isnan(v)) has_nan = true;
-      else if (v > g) g = v;
-    }
-    if (has_nan) g = NAN;
+#pragma unroll
+    for (int i = 0; i < GATE_THREADS / 64; ++i) { g = fmax(g, wmax[i]); flags |= wflags[i]; }
+    if (flags & 1) g = NAN;
     a.out->g = g;
     a.out->flag = (g > a.tau) ? 1 : 0;
-    a.out->nonfinite = nonfinite;
+    a.out->nonfinite = (flags & 2) ? 1 : 0;
   }
 }
 
 }  // namespace
 
-hipError_t launch_form_buffer(const FormArgs& a, int nl, bool g_bf16, hipStream_t s) {
+hipError_t launch_form_buffer(const FormArgs& a, int nl, bool g_bf16, bool with_x, hipStream_t s) {
   if (nl <= 0 || a.blocks_per_layer <= 0) return hipSuccess;
   const dim3 grid(a.blocks_per_layer, nl), block(NTHREADS);
-  if (g_bf16) hipLaunchKernelGGL(k_form_buffer<true>, grid, block, 0, s, a);
-  else hipLaunchKernelGGL(k_form_buffer<false>, grid, block, 0, s, a);
+  if (g_bf16) {
+    if (with_x) hipLaunchKernelGGL((k_form_buffer<true, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_form_buffer<true, false>), grid, block, 0, s, a);
+  } else {
+    if (with_x) hipLaunchKernelGGL((k_form_buffer<false, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_form_buffer<false, false>), grid, block, 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -205,8 +246,8 @@ hipError_t launch_local_update(const LocalArgs& a, int nl, bool g_bf16, hipStrea
 }
 
 hipError_t launch_gate(const GateArgs& a, hipStream_t s) {
-  if (a.L <= 0 || a.L > GATE_MAX_LAYERS) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_gate, dim3(1), dim3(GATE_THREADS), 0, s, a);
+  if (a.L <= 0 || !a.counter || !a.norms) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_gate, dim3(a.L), dim3(GATE_THREADS), 0, s, a);
   return hipGetLastError();
 }
 

@@ -74,8 +74,10 @@ def step_and_compare(layer: cdl.Layer, G, M, X, Q, mu, eta, r, tau, policy, eps=
     dX = OL.X - X0
     ndx = np.linalg.norm(dX)
     out["err_dX"] = rel(f64(X) - X0, dX) if ndx > 0 else float(np.max(np.abs(f64(X) - X0)))
-    # X is stored in fp32: rounding X_t alone moves dX by up to u |X_t| per entry
-    out["dx_floor"] = 2.0 * U32 * float(np.linalg.norm(OL.X)) / ndx if ndx > 0 else 0.0
+    # X is stored in fp32: each rounding of X moves dX by up to u |X| per entry;
+    # a sync step that follows a predicted skip rounds X three times (the
+    # speculative X -= eta_l G, its reversal, the rank-r update)
+    out["dx_floor"] = 4.0 * U32 * float(np.linalg.norm(OL.X)) / ndx if ndx > 0 else 0.0
     out["err_Q"] = rel(f64(Q), OL.Q)
     if res["flag"]:
         m, n = M.shape
