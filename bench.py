@@ -16,13 +16,29 @@ times, the roofline of the kernel with the largest share of the timed region
 float64 oracle timed on this host's cores on a bounded sample.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--policy rmmc|always|never]
+
+Profiling (rocprofv3 under the same command; the summaries go to profiles/):
+
+    rocprofv3 --kernel-trace --stats -f csv -d DIR -o bench -- python3 bench.py
+    python3 bench.py --summarize-trace DIR BENCH_JSON OUT
+    rocprofv3 --pmc FETCH_SIZE -f csv -d DIR_F -o pmc -- python3 bench.py --copy-calibration 1024 ...
+    rocprofv3 --pmc WRITE_SIZE -f csv -d DIR_W -o pmc -- python3 bench.py --copy-calibration 1024 ...
+    python3 bench.py --summarize-pmc DIR_F DIR_W OUT --copy-calibration 1024
+
+The counter summary records a digest of the kernels' sources; the bench line
+reports the dominant kernel's counted HBM traffic only while that digest still
+matches the sources.
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -46,6 +62,31 @@ KIND_BOUND = {
 }
 POLICIES = {"rmmc": 0, "always": 1, "never": 2}
 
+# kernel kind -> (kernel-name pattern in the profiler's output, source files);
+# kinds whose kernel template is shared with other kinds have no pattern
+CSRC = os.path.join(ROOT, "paper_2512_13728_amd", "csrc")
+_STREAM = ["k_stream.hip", "common.hpp"]
+_BF = ["k_gemm_bf.hip", "bf16_split.hpp", "mfma_tile.hpp", "common.hpp"]
+KIND_KERNEL = {
+    "form_buffer": (r"k_form_buffer<\w+, false>", _STREAM),
+    "form_buffer_local": (r"k_form_buffer<\w+, true>", _STREAM),
+    "local_update": (r"k_local_update<", _STREAM),
+    "gate": (r"k_gate\b", _STREAM),
+    "update_bf16": (r"k_update_pl<1,", _BF),
+    "update_bf16x6": (r"k_update_pl<3,", _BF),
+    "cholesky_f64": (None, ["k_chol.hip", "mfma_tile.hpp", "common.hpp"]),
+}
+COPY_PATTERN = r"neg_kernel"          # the calibration copy: b = -a, fp32, elementwise
+PMC_PROFILE = os.path.join(ROOT, "profiles", "{workload}_hbm_traffic_pmc.txt")
+
+
+def source_digest(files) -> str:
+    h = hashlib.sha256()
+    for f in sorted(files):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -60,7 +101,139 @@ def parse():
     p.add_argument("--policy", default="rmmc", choices=sorted(POLICIES))
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--pool", type=int, default=20, help="distinct gradient sets kept resident")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="first run a plain streaming copy of MIB MiB (fp32, b = -a) three times, "
+                        "the reference for the hardware byte counters")
+    p.add_argument("--summarize-trace", nargs=3, metavar=("DIR", "BENCH_JSON", "OUT"),
+                   help="write the kernel statistics of a rocprofv3 --kernel-trace --stats run")
+    p.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"),
+                   help="write the per-kernel HBM traffic of two rocprofv3 --pmc runs (give the "
+                        "same --copy-calibration size)")
     return p.parse_args()
+
+
+def _kernel_name(raw: str) -> str:
+    name = raw.replace("(anonymous namespace)::", "").replace("void ", "")
+    return name.split("(cd::")[0].strip()
+
+
+def summarize_trace(d: str, bench_json: str, out: str):
+    """Kernel statistics (rocprofv3 --kernel-trace --stats, csv) of one bench run."""
+    stats = glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True)
+    if not stats:
+        sys.exit(f"no *kernel_stats.csv under {d}")
+    rows = list(csv.DictReader(open(stats[0])))
+    ours = [r for r in rows if "cd::" in r["Name"]]
+    other_ns = sum(float(r["TotalDurationNs"]) for r in rows if "cd::" not in r["Name"])
+    b = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    lines = [f"# rocprofv3 kernel statistics: {b['config']['workload']}",
+             "# commands (from the repository root):",
+             f"#   rocprofv3 --kernel-trace --stats -f csv -d {d} -o bench -- python3 bench.py > {bench_json}",
+             f"#   python3 bench.py --summarize-trace {d} {bench_json} {out}",
+             "# calls include the warmup steps; torch kernels (input generation, state reset)",
+             f"# are left out below: {other_ns / 1e6:.1f} ms in total.", "",
+             f"{'kernel':64s} {'calls':>6s} {'avg_us':>10s} {'total_ms':>10s}"]
+    for r in sorted(ours, key=lambda r: -float(r["TotalDurationNs"])):
+        lines.append(f"{_kernel_name(r['Name'])[:64]:64s} {int(r['Calls']):6d} "
+                     f"{float(r['AverageNs']) / 1e3:10.1f} {float(r['TotalDurationNs']) / 1e6:10.3f}")
+    rf = b["roofline"]
+    lines += ["", "# the same run's bench line (timed region only; HIP events around every launch):",
+              f"#   value {b['value']:.4g} params/s, {b['ms_per_step']:.3f} ms/step, "
+              f"{b['config']['sync_steps']} sync + {b['config']['local_steps']} local steps",
+              f"#   dominant kernel {rf['kernel']}: avg launch {rf['avg_launch_ms'] * 1e3:.1f} us, "
+              f"{rf['achieved']} {rf['unit']} of {rf['peak']} ({rf['frac'] * 100:.1f}%)"]
+    for k, v in b["branches"].items():
+        lines.append(f"#   {k}: {json.dumps(v)}")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def _pmc_rows(d: str, counter: str):
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        sys.exit(f"no *counter_collection.csv under {d}")
+    per = {}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            key = (f, r["Dispatch_Id"])
+            per.setdefault(key, [r["Kernel_Name"], 0.0])[1] += float(r["Counter_Value"])
+    return list(per.values())
+
+
+def summarize_pmc(fdir: str, wdir: str, out: str, workload: str, cal_mib: int):
+    """HBM traffic per dispatch from FETCH_SIZE and WRITE_SIZE (KiB), each
+    scaled by what the counter reads for the calibration copy of known size."""
+    if cal_mib <= 0:
+        sys.exit("--summarize-pmc needs the --copy-calibration size the profiled runs used")
+    cal_bytes = cal_mib << 20
+    res = {}
+    for counter, d in (("FETCH_SIZE", fdir), ("WRITE_SIZE", wdir)):
+        rows = _pmc_rows(d, counter)
+        copy = [v for k, v in rows if re.search(COPY_PATTERN, k)]
+        if not copy:
+            sys.exit(f"{counter}: no calibration copy dispatch ({COPY_PATTERN}) in {d}")
+        res[counter] = (rows, copy)
+    factor = {}
+    for counter, (rows, copy) in res.items():
+        kib = sorted(copy)[len(copy) // 2]
+        factor[counter] = cal_bytes / (kib * 1024.0)
+    table = {}
+    for counter, (rows, _) in res.items():
+        for k, v in rows:
+            name = _kernel_name(k)
+            if "cd::" not in k:
+                continue
+            t = table.setdefault(name, {"FETCH_SIZE": [], "WRITE_SIZE": []})
+            t[counter].append(v * 1024.0 * factor[counter])
+    kinds = {}
+    for kind, (pat, files) in KIND_KERNEL.items():
+        if pat is None:
+            continue
+        f_all, w_all = [], []
+        for name, t in table.items():
+            if re.search(pat, name):
+                f_all += t["FETCH_SIZE"]
+                w_all += t["WRITE_SIZE"]
+        if f_all and w_all:
+            kinds[kind] = {"fetch_bytes_per_launch": sum(f_all) / len(f_all),
+                           "write_bytes_per_launch": sum(w_all) / len(w_all),
+                           "traffic_bytes_per_launch": sum(f_all) / len(f_all) + sum(w_all) / len(w_all),
+                           "dispatches": len(f_all), "source_digest": source_digest(files)}
+    lines = [f"# rocprofv3 hardware counters: HBM bytes per dispatch, workload {workload}",
+             "# commands (from the repository root):",
+             f"#   rocprofv3 --pmc FETCH_SIZE -f csv -d {fdir} -o pmc -- python3 bench.py "
+             f"--no-cpu-baseline --copy-calibration {cal_mib}",
+             f"#   rocprofv3 --pmc WRITE_SIZE -f csv -d {wdir} -o pmc -- python3 bench.py "
+             f"--no-cpu-baseline --copy-calibration {cal_mib}",
+             f"#   python3 bench.py --summarize-pmc {fdir} {wdir} {out} --copy-calibration {cal_mib}",
+             f"# calibration: a streaming copy (b = -a, fp32) of {cal_bytes} B read + {cal_bytes} B written;",
+             f"#   FETCH_SIZE x {factor['FETCH_SIZE']:.4f} and WRITE_SIZE x {factor['WRITE_SIZE']:.4f} give bytes",
+             "# all dispatches of the run (warmup and timed steps); bytes are scaled, per dispatch", "",
+             f"{'kernel':64s} {'disp':>5s} {'fetch_MB':>10s} {'write_MB':>10s}"]
+    for name, t in sorted(table.items(), key=lambda kv: -sum(kv[1]["FETCH_SIZE"]) - sum(kv[1]["WRITE_SIZE"])):
+        nf = max(len(t["FETCH_SIZE"]), 1)
+        nw = max(len(t["WRITE_SIZE"]), 1)
+        lines.append(f"{name[:64]:64s} {len(t['FETCH_SIZE']):5d} {sum(t['FETCH_SIZE']) / nf / 1e6:10.2f} "
+                     f"{sum(t['WRITE_SIZE']) / nw / 1e6:10.2f}")
+    lines += ["", "json " + json.dumps({"workload": workload, "factor": factor, "kinds": kinds})]
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def counted_traffic(workload: str, kind: str):
+    """Counted HBM bytes per launch of `kind` from the committed counter
+    summary, or None if there is none or the kernel's sources changed since."""
+    path = PMC_PROFILE.format(workload=workload)
+    if kind not in KIND_KERNEL or not os.path.exists(path):
+        return None
+    for line in open(path):
+        if line.startswith("json "):
+            info = json.loads(line[5:]).get("kinds", {}).get(kind)
+            if info and info["source_digest"] == source_digest(KIND_KERNEL[kind][1]):
+                return info["traffic_bytes_per_launch"]
+    return None
 
 
 def cpu_baseline(w, n_sync: int, n_local: int, steps: int):
@@ -120,6 +293,12 @@ def cpu_baseline(w, n_sync: int, n_local: int, steps: int):
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, workload=args.workload, cal_mib=args.copy_calibration)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -142,6 +321,14 @@ def main():
     K, W = args.steps, args.warmup
     L = len(w.shapes)
     log(f"[bench] workload {w.name}: {L} matrices, {w.params} params, r={w.r}, G {w.grad_dtype}")
+    if args.copy_calibration > 0:
+        a = torch.ones(args.copy_calibration * (1 << 18), dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            torch.neg(a, out=b)
+        torch.cuda.synchronize()
+        log(f"[bench] copy calibration: streaming copy b = -a, bytes={a.numel() * 4} read and written")
+        del a, b
 
     layers = [cdl.Layer(m, n, w.r, grad_dtype=w.grad_dtype, tau=w.tau, eps=w.eps, policy=policy)
               for (m, n) in w.shapes]
@@ -210,8 +397,9 @@ def main():
     else:
         achieved = mult * dv["flops"] / dv["launches"] / (avg_ms * 1e-3) / 1e12
         peak, unit = PEAK_TFLOPS[prec], "TFLOP/s"
+    traffic = counted_traffic(w.name, dom)
     roofline = {"bound": bound, "kernel": dom, "achieved": round(achieved, 3), "peak": peak,
-                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
                 "avg_launch_ms": round(avg_ms, 4), "launches": dv["launches"],
                 "algorithmic_bytes_per_launch": dv["bytes"] / dv["launches"],
                 "algorithmic_flops_per_launch": dv["flops"] / dv["launches"]}
@@ -224,12 +412,17 @@ def main():
                 "max_ms": round(max(ms_list), 4), "params_per_s": w.params / (med * 1e-3)}
 
     branches = {"sync": branch(sync_ms, n_sync), "local": branch(local_ms, n_local)}
-    if local_ms:
-        # per local step: one form_buffer launch per shape class + gate + one local_update per class
-        per_step_bytes = (kt["form_buffer"]["bytes"] / (n_sync + n_local)
-                          + kt["local_update"]["bytes"] / max(n_local, 1))
-        branches["local"]["algorithmic_GBps"] = per_step_bytes / (branches["local"]["median_ms"] * 1e-3) / 1e9
-        branches["local"]["frac_of_hbm_peak"] = branches["local"]["algorithmic_GBps"] / PEAK_HBM_GBPS
+    # compulsory bytes per step: read G, M, X and write M, X; a sync step also
+    # reads and writes Q (n x r per layer)
+    gb = 2 if w.grad_dtype == "bf16" else 4
+    skip_bytes = (16 + gb) * w.params
+    sync_bytes = skip_bytes + 8 * sum(n * w.r for _, n in w.shapes)
+    for name, nbytes in (("local", skip_bytes), ("sync", sync_bytes)):
+        if branches[name]["count"]:
+            gbps = nbytes / (branches[name]["median_ms"] * 1e-3) / 1e9
+            branches[name]["compulsory_bytes"] = nbytes
+            branches[name]["algorithmic_GBps"] = gbps
+            branches[name]["frac_of_hbm_peak"] = gbps / PEAK_HBM_GBPS
 
     cpu = None
     if not args.no_cpu_baseline:

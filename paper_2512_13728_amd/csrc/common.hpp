@@ -17,7 +17,7 @@ constexpr int GBK = 32;           // GEMM k per LDS stage; split-K slices are mu
 
 // ---- a1: B = M + G and per-block sum of B^2 -------------------------------
 // Every block covers FORM_CHUNK consecutive elements of one layer.
-constexpr int FORM_CHUNK = NTHREADS * 4 * 8;   // 8192 elements
+constexpr int FORM_CHUNK = NTHREADS * 4 * 4;   // 4096 elements
 struct FormArgs {
   long long numel;                 // elements per layer (m*n)
   int blocks_per_layer;            // ceil(numel / FORM_CHUNK)

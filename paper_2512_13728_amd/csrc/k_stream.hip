@@ -4,24 +4,40 @@
 // the same pass, the stand-alone skip-branch update (X -= eta_local G), and
 // the gate (fixed-order reduction, RMMC, prev_norm update, max over layers).
 //
-// These passes are HBM-bound: each thread keeps eight 16-byte loads in flight,
-// blocks own fixed 8192-element chunks of one layer, and every reduction runs
-// in a fixed order so that the statistic is bit-reproducible run to run.
+// These passes are HBM-bound: blocks own fixed 4096-element chunks of one
+// layer (four 16-byte segments per thread and stream), every operand is read
+// and written once with non-temporal hints (nothing is reused, so nothing
+// should displace other lines), and every reduction runs in a fixed order so
+// that the statistic is bit-reproducible run to run.
 #include "common.hpp"
 
 namespace cd {
 namespace {
+
+typedef float nt_f4 __attribute__((ext_vector_type(4)));
+typedef unsigned nt_u2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float4 ld_nt(const float* p) {
+  const nt_f4 v = __builtin_nontemporal_load(reinterpret_cast<const nt_f4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void st_nt(float* p, float4 v) {
+  const nt_f4 w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, reinterpret_cast<nt_f4*>(p));
+}
 
 // G element loads: fp32, or bf16 widened exactly (bf16 bits are the top half
 // of the fp32 bit pattern).
 template <bool BF16>
 __device__ __forceinline__ float4 load_g4(const void* G, long long i) {
   if constexpr (BF16) {
-    const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(G) + i);
+    const nt_u2 u = __builtin_nontemporal_load(
+        reinterpret_cast<const nt_u2*>(static_cast<const uint16_t*>(G) + i));
     return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
                        __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
   } else {
-    return *reinterpret_cast<const float4*>(static_cast<const float*>(G) + i);
+    return ld_nt(static_cast<const float*>(G) + i);
   }
 }
 
@@ -52,7 +68,7 @@ __device__ double block_sum(double v) {
   return s;
 }
 
-constexpr int VPT = FORM_CHUNK / (NTHREADS * 4);   // float4 groups per thread (8)
+constexpr int VPT = FORM_CHUNK / (NTHREADS * 4);   // float4 groups per thread (4)
 
 // B = M + G in place, the block's partial sum of B^2, and (WX) the skip
 // branch's X -= coef G in the same pass over G.
@@ -71,9 +87,9 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
 #pragma unroll
     for (int v = 0; v < VPT; ++v) {
       const long long i = base + 4LL * (threadIdx.x + v * NTHREADS);
-      m[v] = *reinterpret_cast<const float4*>(M + i);
+      m[v] = ld_nt(M + i);
       g[v] = load_g4<BF16>(G, i);
-      if constexpr (WX) x[v] = *reinterpret_cast<const float4*>(X + i);
+      if constexpr (WX) x[v] = ld_nt(X + i);
     }
 #pragma unroll
     for (int v = 0; v < VPT; ++v) {
@@ -81,13 +97,13 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
       float4 b;
       b.x = m[v].x + g[v].x; b.y = m[v].y + g[v].y;
       b.z = m[v].z + g[v].z; b.w = m[v].w + g[v].w;
-      *reinterpret_cast<float4*>(M + i) = b;
+      st_nt(M + i, b);
       acc += sq(b.x); acc += sq(b.y); acc += sq(b.z); acc += sq(b.w);
       if constexpr (WX) {
         float4 y;
         y.x = fmaf(-c, g[v].x, x[v].x); y.y = fmaf(-c, g[v].y, x[v].y);
         y.z = fmaf(-c, g[v].z, x[v].z); y.w = fmaf(-c, g[v].w, x[v].w);
-        *reinterpret_cast<float4*>(X + i) = y;
+        st_nt(X + i, y);
       }
     }
   } else {
@@ -134,7 +150,7 @@ __global__ __launch_bounds__(NTHREADS) void k_local_update(LocalArgs a) {
 #pragma unroll
     for (int v = 0; v < VPT; ++v) {
       const long long i = base + 4LL * (threadIdx.x + v * NTHREADS);
-      x[v] = *reinterpret_cast<const float4*>(X + i);
+      x[v] = ld_nt(X + i);
       g[v] = load_g4<BF16>(G, i);
     }
 #pragma unroll
@@ -143,7 +159,7 @@ __global__ __launch_bounds__(NTHREADS) void k_local_update(LocalArgs a) {
       float4 y;
       y.x = fmaf(-c, g[v].x, x[v].x); y.y = fmaf(-c, g[v].y, x[v].y);
       y.z = fmaf(-c, g[v].z, x[v].z); y.w = fmaf(-c, g[v].w, x[v].w);
-      *reinterpret_cast<float4*>(X + i) = y;
+      st_nt(X + i, y);
     }
   } else {
     for (long long i = base + 4LL * threadIdx.x; i < end; i += 4LL * NTHREADS) {

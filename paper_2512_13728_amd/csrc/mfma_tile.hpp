@@ -144,4 +144,17 @@ __device__ __forceinline__ int xcd_tile(int b, int ntiles) {
 }
 __host__ __device__ inline int xcd_grid(int ntiles) { return ((ntiles + 7) >> 3) * 8; }
 
+// Tile (tm, tn) of a tiles_m x tiles_n grid for linear index t, in bands of
+// G tile rows: inside a band the column advances only after all of its rows,
+// so consecutive tiles (one XCD's share under xcd_tile) touch at most G row
+// slices and a few column slices of the operands, which then stay in that
+// XCD's L2.  A bijection of [0, tiles_m * tiles_n).
+__device__ __forceinline__ void grouped_tile(int t, int tiles_m, int tiles_n, int G, int& tm, int& tn) {
+  const int span = G * tiles_n;
+  const int band = t / span, rem = t - band * span;
+  const int rows = min(G, tiles_m - band * G);
+  tn = rem / rows;
+  tm = band * G + (rem - tn * rows);
+}
+
 }  // namespace cd
