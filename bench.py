@@ -57,6 +57,7 @@ KIND_BOUND = {
     "power_bq_f64": ("mfma", "f64", 1), "gram_f64": ("mfma", "f64", 1), "trsm_f64": ("mfma", "f64", 1),
     "cholesky_f64": ("mfma", "f64", 1), "power_bq_bf16x6": ("mfma", "bf16", 6),
     "power_btp_bf16x6": ("mfma", "bf16", 6), "update_bf16x6": ("mfma", "bf16", 6),
+    "power_bq_bf16x3": ("mfma", "bf16", 3), "power_btp_bf16x3": ("mfma", "bf16", 3),
     "update_bf16": ("hbm", None, 1), "gram_bf16x6": ("mfma", "bf16", 6),
     "apply_bf16x6": ("mfma", "bf16", 6), "trtri_f64": ("mfma", "f64", 1),
 }
@@ -448,8 +449,8 @@ def main():
             "workload": (f"{w.name}: {L} matrices of the 1.3B-shaped GPT set (d_model 2048, 24 blocks)"
                          if w.name == "gpt1p3b" else w.name),
             "params": w.params, "rank": w.r, "grad_dtype": w.grad_dtype, "state_dtype": "f32",
-            "power_iteration_dtype": ("P~ = BQ and R = B^T P on bf16 MFMA with 3-piece fp32 splits "
-                                      "(fp32-accurate); CholQR2 pass 0 Gram + Cholesky in fp64, pass 1 "
+            "power_iteration_dtype": ("P~ = BQ and R = B^T P on bf16 MFMA with 2-piece fp32 splits "
+                                      "(3 products, ~2^-16 relative); CholQR2 pass 0 Gram + Cholesky in fp64, pass 1 "
                                       "fp32-accurate (bf16 x 6); M/X update bf16 products, fp32 "
                                       "accumulation" if w.grad_dtype == "bf16" else
                                       "P~ = BQ, Gram and CholQR in fp64; R and the M/X update on bf16 "

@@ -86,11 +86,11 @@ hipError_t dalloc(T** p, size_t count) {
 
 // ---- optional per-kernel timing (HIP events on the launch stream) ----------
 enum Kind { K_FORM, K_FORM_X, K_GATE, K_LOCAL, K_PBQ, K_PBQ_BF, K_GRAM, K_GRAM_BF, K_CHOL, K_TRSM, K_TRTRI,
-            K_APPLY_BF, K_PBTP, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_NKINDS };
+            K_APPLY_BF, K_PBTP, K_PBTP3, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_NKINDS };
 const char* const kKindName[K_NKINDS] = {
-    "form_buffer", "form_buffer_local", "gate", "local_update", "power_bq_f64", "power_bq_bf16x6", "gram_f64",
+    "form_buffer", "form_buffer_local", "gate", "local_update", "power_bq_f64", "power_bq_bf16x3", "gram_f64",
     "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_bf16x6",
-    "reduce_splits", "colnorm", "update_bf16x6", "update_bf16"};
+    "power_btp_bf16x3", "reduce_splits", "colnorm", "update_bf16x6", "update_bf16"};
 
 struct Timer {
   struct Rec { int kind; hipEvent_t a, b; double bytes, flops; };
@@ -363,16 +363,20 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   };
   auto part = [&](int j) { return lay(j)->split_part; };
   const double mn = 1.0 * m * n, mr = 1.0 * m * r, nr = 1.0 * n * r, rr = 1.0 * r * r;
-  const bool fast = g->g_bf16;   // bf16 gradients: fp32-accurate P~ (see enqueue_orthogonalize)
+  // bf16-gradient layers: the power-iteration products P~ = B Q and R = B^T P
+  // use two-piece splits (three bf16 products, relative error about 2^-16,
+  // an order below what the plain-bf16 rank-r update of M contributes);
+  // fp32 layers keep fp64 (P~) and six-product (R) arithmetic.
+  const bool fast = g->g_bf16;
   if (stage == 0) {
-    // P~ = B Q (B lives in M): fp64 for fp32 layers, into pa; bf16 x 6 for
+    // P~ = B Q (B lives in M): fp64 for fp32 layers, into pa; bf16 x 3 for
     // bf16-gradient layers, into the fp32 panel P
     if (fast)
       return gemm(K_PBQ_BF, 2.0 * mn * r, 4.0 * mn + 4.0 * nr + 4.0 * mr, cd::GemmKind::F32, m, r, n,
                   true, n, false, r, false,
                   [&](int j) { return static_cast<const void*>(M[sel[j]]); },
                   [&](int j) { return static_cast<const void*>(Q[sel[j]]); },
-                  [&](int j) { return static_cast<void*>(lay(j)->P); }, part, 3);
+                  [&](int j) { return static_cast<void*>(lay(j)->P); }, part, 2);
     return gemm(K_PBQ, 2.0 * mn * r, 4.0 * mn + 4.0 * nr + 8.0 * mr, cd::GemmKind::F64_FROM_F32, m, r,
                 n, true, n, false, r, false,
                 [&](int j) { return static_cast<const void*>(M[sel[j]]); },
@@ -414,11 +418,11 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
                 r, false, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); }, part, 3, true);
   }
   // R = B^T P
-  cd_status st = gemm(K_PBTP, 2.0 * mn * r, 4.0 * mn + 4.0 * mr + 4.0 * nr, cd::GemmKind::F32, n, r, m,
-                      false, n, false, r, false,
+  cd_status st = gemm(fast ? K_PBTP3 : K_PBTP, 2.0 * mn * r, 4.0 * mn + 4.0 * mr + 4.0 * nr,
+                      cd::GemmKind::F32, n, r, m, false, n, false, r, false,
                       [&](int j) { return static_cast<const void*>(M[sel[j]]); },
                       [&](int j) { return static_cast<const void*>(lay(j)->P); },
-                      [&](int j) { return static_cast<void*>(lay(j)->R); }, part, 3);
+                      [&](int j) { return static_cast<void*>(lay(j)->R); }, part, fast ? 2 : 3);
   if (st != CD_OK) return st;
   // Q = ColumnNormalize(R)
   cd::ColnormArgs cn{};

@@ -12,7 +12,8 @@ unless stated):
             up to three times per step)
 * P^T P - I and |‖Q_j‖ - 1|: 1e-5 (absolute, Frobenius / max)
 * local branch: M bit-exact against fp32 M + G, X within 1 ulp of fp32 FMA
-* bf16 gradients (the path uses bf16 products for the rank-r update and
+* bf16 gradients (the path uses two-piece bf16 products, about 2^-16, for
+            the power iteration, plain bf16 products for the rank-r update and
             fp32-accurate arithmetic for the second CholQR pass): M, X, P, Q,
             dX within 2e-2, ‖P^T P - I‖_F <= 1e-4; decisions identical
 Free-running trajectories check every decision against the free-running
