@@ -10,7 +10,11 @@
 // padded to 40 elements so the sixteen 16-byte fragment reads of a quarter-wave
 // hit distinct banks).  Operands whose global layout is not k-contiguous are
 // transposed in registers in 4 x 4 blocks before the LDS store, so every LDS
-// store is 8 contiguous bytes.
+// store is 8 contiguous bytes.  The four 16-byte k-granules of a row are
+// XOR-permuted by bits 4-5 of the row (lds_off): the transposed stores, where
+// the 16 lanes of a quarter-wave write rows 4 apart, then fall on distinct
+// banks too, and a fragment (16 consecutive rows from a multiple of 16) sees
+// one permutation for all its rows.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -25,6 +29,11 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BK16 = 32;          // k per stage (one MFMA depth)
 constexpr int BLD = BK16 + 8;     // padded LDS row (bf16 elements)
+
+// Element offset of (row, k), k < BK16, inside one LDS plane.
+__device__ __forceinline__ int lds_off(int row, int k) {
+  return row * BLD + ((((k >> 3) ^ (row >> 4)) & 3) << 3) + (k & 7);
+}
 
 template <int S>
 __device__ __forceinline__ void split_bf16(float v, __bf16 (&p)[S]) {
@@ -48,7 +57,7 @@ __device__ __forceinline__ void put4(__bf16* planes, int row, int kq, float v0, 
 #pragma unroll
   for (int s = 0; s < S; ++s) {
     bf16x4 w = {a[s], b[s], c[s], d[s]};
-    *reinterpret_cast<bf16x4*>(planes + (s * ROWS + row) * BLD + kq) = w;
+    *reinterpret_cast<bf16x4*>(planes + s * ROWS * BLD + lds_off(row, kq)) = w;
   }
 }
 
@@ -148,7 +157,7 @@ struct Stage {
 
 // bf16 fragment: lane l owns row (l % 16) and k = 8 (l / 16) .. + 7.
 __device__ __forceinline__ bf16x8 bfrag(const __bf16* plane, int row0, int lane) {
-  return *reinterpret_cast<const bf16x8*>(plane + (row0 + (lane & 15)) * BLD + 8 * (lane >> 4));
+  return *reinterpret_cast<const bf16x8*>(plane + lds_off(row0 + (lane & 15), 8 * (lane >> 4)));
 }
 
 __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {

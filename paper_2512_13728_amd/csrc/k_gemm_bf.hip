@@ -156,6 +156,9 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
   constexpr int STAGE_BYTES = UBM * SLD * 4;
   constexpr int SMEM = PLANE_BYTES > STAGE_BYTES ? PLANE_BYTES : STAGE_BYTES;
   constexpr int ROWS = UBM + 2 * BN;    // LDS rows per plane: P, then R, then Q
+  // the R and Q regions start at multiples of 64 rows, so the swizzle of
+  // lds_off agrees between plane rows (stores) and region rows (bfrag)
+  static_assert(UBM % 64 == 0 && BN % 64 == 0, "region offsets must be multiples of 64 rows");
   constexpr int CHUNKS = S * ROWS * (BK16 / 8);   // 16-byte chunks per stage
   constexpr int CPT = (CHUNKS + 255) / 256;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
@@ -209,7 +212,7 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
       const int c = tid + i * 256;
       if (c < CHUNKS) {
         const int s = c / (ROWS * 4), rem = c - s * ROWS * 4;
-        *reinterpret_cast<uint4*>(Ls + (s * ROWS + (rem >> 2)) * BLD + (rem & 3) * 8) = pre[i];
+        *reinterpret_cast<uint4*>(Ls + s * ROWS * BLD + lds_off(rem >> 2, (rem & 3) * 8)) = pre[i];
       }
     }
   };
