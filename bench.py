@@ -102,6 +102,11 @@ def parse():
     p.add_argument("--policy", default="rmmc", choices=sorted(POLICIES))
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--pool", type=int, default=20, help="distinct gradient sets kept resident")
+    p.add_argument("--rank", type=int, default=0, help="override the workload's rank r")
+    p.add_argument("--stream-inputs", action="store_true",
+                   help="draw every step's gradients on the GPU just before the step (outside its "
+                        "timed interval) instead of cycling a resident pool; the default for "
+                        "trajectories longer than the pool (the 200-step mixed workload)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="first run a plain streaming copy of MIB MiB (fp32, b = -a) three times, "
                         "the reference for the hardware byte counters")
@@ -316,6 +321,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     w = S.WORKLOADS[args.workload]
+    if args.rank > 0:
+        import dataclasses
+        w = dataclasses.replace(w, r=args.rank)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     policy = POLICIES[args.policy]
@@ -339,11 +347,13 @@ def main():
     M = [s[0].clone() for s in init]
     X = [s[1].clone() for s in init]
     Q = [s[2].clone() for s in init]
-    pool = max(1, min(args.pool, max(K, W)))
+    streamed = args.stream_inputs or K > args.pool
+    pool = 1 if streamed else max(1, min(args.pool, max(K, W)))
     streams = [S.GradientStream(w, i, device=dev) for i in range(L)]
     grads = [[st.next() for st in streams] for _ in range(pool)]
     torch.cuda.synchronize()
-    log(f"[bench] inputs resident in HBM ({pool} gradient sets) in {time.perf_counter() - t0:.1f}s")
+    log(f"[bench] inputs resident in HBM ({pool} gradient set{'s' if pool > 1 else ''}"
+        f"{', the rest drawn between steps' if streamed else ''}) in {time.perf_counter() - t0:.1f}s")
 
     def reset():
         for i in range(L):
@@ -359,22 +369,48 @@ def main():
     log(f"[bench] {W} warmup steps done; timing {K} steps from step 1")
 
     stream = torch.cuda.current_stream()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     flags, rmmcs = [], []
     group.set_timing(True)
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    ev[0].record(stream)
-    for t in range(K):
-        g, flag, _, _ = group.step(grads[t % pool], M, X, Q, w.mu, w.eta, w.r)
-        ev[t + 1].record(stream)
-        flags.append(flag)
-        rmmcs.append(g)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
+    if streamed:
+        # restart the streams so the timed trajectory is steps 1..K; each step's
+        # inputs are drawn before its interval, which brackets only the step
+        streams = [S.GradientStream(w, i, device=dev) for i in range(L)]
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K)]
+        wall = 0.0
+        for t in range(K):
+            G = grads[0] if t == 0 else [st.next() for st in streams]
+            if t == 0:
+                for st in streams:
+                    st.next()
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            ev[t][0].record(stream)
+            g, flag, _, _ = group.step(G, M, X, Q, w.mu, w.eta, w.r)
+            ev[t][1].record(stream)
+            torch.cuda.synchronize()
+            wall += time.perf_counter() - t1
+            flags.append(flag)
+            rmmcs.append(g)
+            if (t + 1) % 25 == 0:
+                log(f"[bench]   step {t + 1}: {sum(flags)} syncs so far")
+        elapsed = wall
+        step_ms = [a.elapsed_time(b) for a, b in ev]
+    else:
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+        torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        ev[0].record(stream)
+        for t in range(K):
+            g, flag, _, _ = group.step(grads[t % pool], M, X, Q, w.mu, w.eta, w.r)
+            ev[t + 1].record(stream)
+            flags.append(flag)
+            rmmcs.append(g)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t_start
+        step_ms = [ev[t].elapsed_time(ev[t + 1]) for t in range(K)]
     kt = group.kernel_times()
     group.set_timing(False)
-    step_ms = [ev[t].elapsed_time(ev[t + 1]) for t in range(K)]
     log(f"[bench] timed {K} steps in {elapsed * 1e3:.2f} ms; syncs at "
         f"{[t + 1 for t, f in enumerate(flags) if f]}")
 
@@ -457,6 +493,8 @@ def main():
                                       "MFMA with 3-piece fp32 splits"),
             "policy": args.policy, "tau": w.tau, "trajectory_steps": K,
             "sync_steps": n_sync, "local_steps": n_local, "parallelism": "none (1 GPU)",
+            "inputs": (f"gradients drawn on the GPU between steps, outside each step's timed interval"
+                       if streamed else f"{pool} gradient sets resident in HBM, cycled"),
         },
         "hbm_GBps": total_bytes / elapsed / 1e9,
         "achieved_TFLOPs": total_flops / elapsed / 1e12,

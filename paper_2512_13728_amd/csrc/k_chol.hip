@@ -4,7 +4,7 @@
 //
 // Blocked in CB = 64 columns, fp64 throughout, every launch batched over all
 // layers of the group (they share r):
-//   chol_diag  (one workgroup per layer)  T_kk = chol(W_kk) in LDS and its
+//   chol_diag  (one wave per layer)  T_kk = chol(W_kk) in registers and its
 //              inverse D_k = T_kk^{-1}; the first block also sets the pivot
 //              floor max(1e-13 * max_i W_ii, 1e-60) (smaller or NaN pivots are raised to
 //              it and the layer is flagged rank deficient; the absolute floor
@@ -20,75 +20,77 @@ namespace cd {
 namespace {
 
 constexpr int CB = CHOL_BLOCK;
-constexpr int DLD = CB + 1;   // padded LDS row of the diagonal block
 
-__global__ __launch_bounds__(256) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
-                                                   int pass) {
-  __shared__ double A[CB][DLD];
-  __shared__ double E[CB][DLD];
-  __shared__ double red[4];
-  __shared__ double s_floor;
-  __shared__ int s_def;
+// A double broadcast from one lane of the wave (two v_readlane).
+__device__ __forceinline__ double bcast(double v, int src) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(b), src);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), src);
+  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned>(lo));
+}
+
+// One wave per layer: lane j holds column j of the 64 x 64 diagonal block
+// (upper triangle; rows past the matrix padded with the identity) in
+// registers.  Right-looking Cholesky, then D = T^{-1} column by column by
+// back substitution (lane c solves T d = e_c); every row of T that a step
+// needs comes from the lane that owns it by v_readlane, so neither phase
+// touches LDS or waits at a barrier.  The loops are unrolled so that the
+// register arrays are indexed by constants.
+__global__ __launch_bounds__(64) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
+                                                  int pass) {
   const CholTab t = tab[blockIdx.x];
-  const int tid = threadIdx.x;
+  const int j = threadIdx.x;
   const long long ld = r;
   const int k0 = kb * CB, nb = min(CB, r - k0);
+  double fl;
   if (kb == 0) {
     double md = 0.0;
-    for (int k = tid; k < r; k += 256) md = fmax(md, t.W[k * ld + k]);
+    for (int k = j; k < r; k += 64) md = fmax(md, t.W[k * ld + k]);
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) md = fmax(md, __shfl_xor(md, o, 64));
-    if ((tid & 63) == 0) red[tid >> 6] = md;
-    __syncthreads();
-    if (tid == 0) {
-      const double m = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
-      *t.floor_ = fmax(1e-13 * m, 1e-60);
+    fl = fmax(1e-13 * md, 1e-60);
+    if (j == 0) {
+      *t.floor_ = fl;
       if (pass == 0) *t.rankdef = 0;
     }
-    __syncthreads();
+  } else {
+    fl = *t.floor_;
   }
-  if (tid == 0) { s_floor = *t.floor_; s_def = 0; }
-  for (int idx = tid; idx < CB * CB; idx += 256) {
-    const int i = idx / CB, j = idx % CB;
-    A[i][j] = (i < nb && j < nb && j >= i) ? t.W[(k0 + i) * ld + k0 + j] : 0.0;
+  double a[CB];
+#pragma unroll
+  for (int i = 0; i < CB; ++i) {
+    if (i < nb && j < nb) a[i] = i <= j ? t.W[(k0 + i) * ld + k0 + j] : 0.0;
+    else a[i] = i == j ? 1.0 : 0.0;
   }
-  __syncthreads();
-  const double fl = s_floor;
-  for (int p = 0; p < nb; ++p) {
-    if (tid == 0) {
-      double d = A[p][p];
-      if (!(d > fl)) { d = fl; s_def = 1; }
-      A[p][p] = sqrt(d);
-    }
-    __syncthreads();
-    if (tid > p && tid < nb) A[p][tid] /= A[p][p];
-    __syncthreads();
-    for (int idx = tid; idx < CB * CB; idx += 256) {
-      const int i = idx / CB, j = idx % CB;
-      if (i > p && i < nb && j >= i && j < nb) A[i][j] -= A[p][i] * A[p][j];
-    }
-    __syncthreads();
+  bool def = false;
+#pragma unroll
+  for (int p = 0; p < CB; ++p) {
+    double d = bcast(a[p], p);
+    if (p < nb && !(d > fl)) { d = fl; def = true; }
+    const double piv = sqrt(d);
+    a[p] = (j == p) ? piv : a[p] / piv;
+    // rows below p: A[i][j] -= T[p][i] T[p][j]; lanes j < i only touch the
+    // (unused) lower triangle
+#pragma unroll
+    for (int i = p + 1; i < CB; ++i) a[i] = fma(-bcast(a[p], i), a[p], a[i]);
   }
-  // D = T_kk^{-1}: column c by back substitution (T D = I)
-  if (tid < CB) {
-    const int c = tid;
-    for (int i = CB - 1; i >= 0; --i) {
-      double v = 0.0;
-      if (i < nb && c < nb && i <= c) {
-        double s = (i == c) ? 1.0 : 0.0;
-        for (int p = i + 1; p <= c; ++p) s -= A[i][p] * E[p][c];
-        v = s / A[i][i];
-      }
-      E[i][c] = v;
-    }
+  double e[CB];
+#pragma unroll
+  for (int i = 0; i < CB; ++i) e[i] = i == j ? 1.0 : 0.0;
+#pragma unroll
+  for (int p = CB - 1; p >= 0; --p) {
+    e[p] = e[p] / bcast(a[p], p);
+#pragma unroll
+    for (int i = 0; i < p; ++i) e[i] = fma(-bcast(a[i], p), e[p], e[i]);
   }
-  __syncthreads();
-  for (int idx = tid; idx < CB * CB; idx += 256) {
-    const int i = idx / CB, j = idx % CB;
-    if (i < nb && j < nb && j >= i) t.W[(k0 + i) * ld + k0 + j] = A[i][j];
-    t.Dinv[static_cast<long long>(kb) * CB * CB + idx] = E[i][j];
+  double* D = t.Dinv + static_cast<long long>(kb) * CB * CB;
+#pragma unroll
+  for (int i = 0; i < CB; ++i) {
+    const bool in = i < nb && j < nb;
+    if (in && i <= j) t.W[(k0 + i) * ld + k0 + j] = a[i];
+    D[i * CB + j] = in ? e[i] : 0.0;
   }
-  if (tid == 0 && s_def) *t.rankdef = 1;
+  if (j == 0 && def) *t.rankdef = 1;
 }
 
 // 64 x 64 fp64 MFMA tile: acc += A(64 x K) B(K x 64) with both operands staged
@@ -282,7 +284,7 @@ hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hip
   if (r < 1) return hipErrorInvalidValue;
   const int nblk = (r + CB - 1) / CB;
   for (int kb = 0; kb < nblk; ++kb) {
-    hipLaunchKernelGGL(k_chol_diag, dim3(nlayers), dim3(256), 0, s, tab, r, kb, pass);
+    hipLaunchKernelGGL(k_chol_diag, dim3(nlayers), dim3(64), 0, s, tab, r, kb, pass);
     const int k1 = min(r, (kb + 1) * CB);
     if (k1 >= r) break;
     const int nt = (r - k1 + CB - 1) / CB;

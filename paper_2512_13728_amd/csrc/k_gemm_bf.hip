@@ -350,8 +350,10 @@ hipError_t launch_update_planes(const UpdatePlArgs& u, int nl, int pieces, hipSt
     const int tiles = ((u.m + UBM - 1) / UBM) * ((u.n + 63) / 64);
     hipLaunchKernelGGL((k_update_pl<3, 64>), dim3(xcd_grid(tiles), 1, nl), dim3(256), 0, s, u);
   } else {
-    const int tiles = ((u.m + UBM - 1) / UBM) * ((u.n + 127) / 128);
-    hipLaunchKernelGGL((k_update_pl<1, 128>), dim3(xcd_grid(tiles), 1, nl), dim3(256), 0, s, u);
+    // 128 x 64 tiles: the LDS staging of the epilogue (35 KB) leaves room for
+    // more resident workgroups than 128 x 128 tiles
+    const int tiles = ((u.m + UBM - 1) / UBM) * ((u.n + 63) / 64);
+    hipLaunchKernelGGL((k_update_pl<1, 64>), dim3(xcd_grid(tiles), 1, nl), dim3(256), 0, s, u);
   }
   return hipGetLastError();
 }
