@@ -45,10 +45,20 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = typename Mfma<T>::acc_t{};
 
+  Prefetch<TIn, BM, 256, A_KC> pa;
+  Prefetch<TIn, BN, 256, B_KC> pb;
+  if (kb < ke) {
+    pa.load(A, g.lda, m0, g.M, kb, ke, tid);
+    pb.load(Bm, g.ldb, n0, g.N, kb, ke, tid);
+  }
   for (int k0 = kb; k0 < ke; k0 += GBK) {
-    stage_tile<T, TIn, BM, 256, A_KC>(As, A, g.lda, m0, g.M, k0, ke, tid);
-    stage_tile<T, TIn, BN, 256, B_KC>(Bs, Bm, g.ldb, n0, g.N, k0, ke, tid);
+    pa.template store<T>(As, tid);
+    pb.template store<T>(Bs, tid);
     __syncthreads();
+    if (k0 + GBK < ke) {
+      pa.load(A, g.lda, m0, g.M, k0 + GBK, ke, tid);
+      pb.load(Bm, g.ldb, n0, g.N, k0 + GBK, ke, tid);
+    }
 #pragma unroll
     for (int kk = 0; kk < GBK; kk += 16) {
       typename Mfma<T>::vec4_t a[TM], b[TN];

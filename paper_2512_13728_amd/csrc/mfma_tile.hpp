@@ -117,6 +117,73 @@ __device__ __forceinline__ void stage_tile(T* __restrict__ S, const TIn* __restr
   }
 }
 
+// The same staging split in two halves, so that the next stage's global loads
+// are in flight while the current stage is multiplied: load() fills registers
+// (same slot -> element mapping as stage_tile), store() writes them to LDS.
+template <typename TIn, int ROWS, int NT, bool KC>
+struct Prefetch {
+  static constexpr int SLOTS = KC ? ROWS * (GBK / 4) : GBK * (ROWS / 4);
+  static constexpr int PER = (SLOTS + NT - 1) / NT;
+  TIn v[PER][4];
+
+  __device__ __forceinline__ void load(const TIn* __restrict__ src, int ld, int r0, int nrows, int k0,
+                                       int kend, int tid) {
+    const bool vec = (ld & 3) == 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int slot = tid + i * NT;
+      TIn v0 = 0, v1 = 0, v2 = 0, v3 = 0;
+      if (slot < SLOTS) {
+        if constexpr (KC) {
+          const int row = slot / (GBK / 4), kq = (slot % (GBK / 4)) * 4;
+          const int gr = r0 + row, gk = k0 + kq;
+          if (gr < nrows) {
+            const TIn* p = src + static_cast<long long>(gr) * ld + gk;
+            if (vec && gk + 3 < kend) {
+              load4(p, v0, v1, v2, v3);
+            } else {
+              if (gk + 0 < kend) v0 = p[0];
+              if (gk + 1 < kend) v1 = p[1];
+              if (gk + 2 < kend) v2 = p[2];
+              if (gk + 3 < kend) v3 = p[3];
+            }
+          }
+        } else {
+          const int kk = slot / (ROWS / 4), rq = (slot % (ROWS / 4)) * 4;
+          const int gr = r0 + rq, gk = k0 + kk;
+          if (gk < kend) {
+            const TIn* p = src + static_cast<long long>(gk) * ld + gr;
+            if (vec && gr + 3 < nrows) {
+              load4(p, v0, v1, v2, v3);
+            } else {
+              if (gr + 0 < nrows) v0 = p[0];
+              if (gr + 1 < nrows) v1 = p[1];
+              if (gr + 2 < nrows) v2 = p[2];
+              if (gr + 3 < nrows) v3 = p[3];
+            }
+          }
+        }
+      }
+      v[i][0] = v0; v[i][1] = v1; v[i][2] = v2; v[i][3] = v3;
+    }
+  }
+
+  template <typename T>
+  __device__ __forceinline__ void store(T* __restrict__ S, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int slot = tid + i * NT;
+      if (slot < SLOTS) {
+        T* d;
+        if constexpr (KC) d = S + (slot / (GBK / 4)) * GLDK + (slot % (GBK / 4)) * 4;
+        else d = S + (slot / (ROWS / 4)) * (ROWS + KPAD) + (slot % (ROWS / 4)) * 4;
+        store4<T>(d, static_cast<T>(v[i][0]), static_cast<T>(v[i][1]), static_cast<T>(v[i][2]),
+                  static_cast<T>(v[i][3]));
+      }
+    }
+  }
+};
+
 // Operand fragment of a 16x16x4 MFMA for the 16 rows starting at row0 and the
 // k slice kk: lane l owns row (l % 16) and k = 4 (l / 16) + q, q = 0..3.
 template <typename T, int ROWS, bool KC>
