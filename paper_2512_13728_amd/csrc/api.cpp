@@ -67,7 +67,7 @@ struct DeviceGuard {
 // fp64 MFMA kernels.
 int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk, int pieces = 0) {
   const long long bm = pieces > 0 ? cd::gemm_bf_bm(N) : cd::gemm_bm(N, fp64);
-  const long long bn = pieces > 0 ? cd::gemm_bf_bn(N) : cd::gemm_bn(N, fp64);
+  const long long bn = pieces > 0 ? cd::gemm_bf_bn(N, pieces) : cd::gemm_bn(N, fp64);
   const long long tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn) * nl;
   int s = 1;
   while (tiles * s < 1024 && K / (2 * s) >= 256 && s < 32) s *= 2;
@@ -131,6 +131,8 @@ struct cd_layer {
   double* floor_ = nullptr;     // pivot floor of the current factorisation
   double* gram_part = nullptr;  // split-K partials of the Gram matrix
   void* split_part = nullptr;   // split-K partials of the skinny GEMMs (fp32 or fp64)
+  size_t split_cap = 0;         // bytes of split_part
+  size_t gram_cap = 0;          // doubles of gram_part
   double* colsq = nullptr;      // column sum-of-squares partials
   __bf16* planes = nullptr;     // bf16 split planes of P, R, Q for the update
   float* colnrm = nullptr;      // r_max column norms
@@ -340,6 +342,17 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
     ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper; ga.out64 = bf_out64;
     ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk, pieces);
     ga.split_stride = 1LL * Mr * Nr;
+    if (ga.splits > 1) {
+      // the partials must fit the workspace sized at create time
+      const size_t need = static_cast<size_t>(ga.splits) * Mr * Nr * (acc64 ? 8 : 4);
+      for (int j = 0; j < nl; ++j) {
+        const bool gram = Pof(j) == static_cast<void*>(lay(j)->gram_part);
+        const size_t cap = gram ? lay(j)->gram_cap * sizeof(double) : lay(j)->split_cap;
+        if (need > cap)
+          return fail(CD_ENOMEM, "split-K workspace too small (%zu > %zu bytes) for a %d x %d x %d product",
+                      need, cap, Mr, Nr, K);
+      }
+    }
     for (int j = 0; j < nl; ++j) {
       ga.A[j] = Aof(j);
       ga.B[j] = Bof(j);
@@ -644,16 +657,21 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
     L->d = *desc;
     if (hipGetDevice(&L->device) != hipSuccess) { delete L; return fail(CD_EHIP, "hipGetDevice failed"); }
     const int m = desc->m, n = desc->n, rm = desc->r_max;
-    // split-K capacity: the largest partial product any rank r <= r_max needs
+    // split-K capacity: the largest partial product any rank r <= r_max needs,
+    // for one layer per launch (the most splits) and every piece count (the
+    // tile width, hence the split count, depends on it)
     size_t split_bytes = 8, gram_cap = 1;
     for (int r = 1; r <= rm; ++r) {
       int kc;
       const size_t mr = static_cast<size_t>(m) * r, nr = static_cast<size_t>(n) * r;
       split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, true, &kc) * mr * sizeof(double));
-      split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, false, &kc, 3) * mr * sizeof(float));
-      split_bytes = std::max(split_bytes, plan_splits(n, r, m, 1, false, &kc, 3) * nr * sizeof(float));
-      split_bytes = std::max(split_bytes, plan_splits(m, r, r, 1, false, &kc, 3) * mr * sizeof(float));
-      split_bytes = std::max(split_bytes, plan_splits(r, r, m, 1, false, &kc, 3) * r * r * sizeof(float));
+      for (int pieces = 1; pieces <= 3; ++pieces) {
+        split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, false, &kc, pieces) * mr * sizeof(float));
+        split_bytes = std::max(split_bytes, plan_splits(n, r, m, 1, false, &kc, pieces) * nr * sizeof(float));
+        split_bytes = std::max(split_bytes, plan_splits(m, r, r, 1, false, &kc, pieces) * mr * sizeof(float));
+        split_bytes = std::max(split_bytes,
+                               plan_splits(r, r, m, 1, false, &kc, pieces) * r * r * sizeof(float));
+      }
       gram_cap = std::max(gram_cap, static_cast<size_t>(plan_splits(r, r, m, 1, true, &kc)) * r * r);
     }
     const size_t nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
@@ -671,6 +689,8 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
     if (e == hipSuccess) e = dalloc(&L->floor_, 1);
     if (e == hipSuccess) e = dalloc(&L->gram_part, gram_cap);
     if (e == hipSuccess) e = hipMalloc(&L->split_part, split_bytes);
+    L->split_cap = split_bytes;
+    L->gram_cap = gram_cap;
     if (e == hipSuccess) e = dalloc(&L->colsq, nchunks * rm);
     const size_t rpm = (rm + 31) / 32 * 32;
     if (e == hipSuccess) e = dalloc(&L->planes, 3ULL * (m + 2ULL * n) * rpm);

@@ -96,7 +96,7 @@ inline bool gemm_acc64(GemmKind k) { return k != GemmKind::F32; }
 // fp32 result (or fp32 split partials).
 hipError_t launch_gemm_bf(const GemmArgs& a, int nl, int pieces, hipStream_t s);
 int gemm_bf_bm(int N);
-int gemm_bf_bn(int N);
+int gemm_bf_bn(int N, int pieces);
 
 // out[i] = sum_{s < splits} part[s*stride + i] in order s = 0, 1, ...
 // Partials are fp64 when part64, and the output is fp64 when out64.

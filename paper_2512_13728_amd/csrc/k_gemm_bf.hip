@@ -12,7 +12,7 @@ namespace cd {
 namespace {
 
 template <int S, int BM, int BN, bool A_KC, bool B_KC>
-__global__ __launch_bounds__(256) void k_gemm_bf(GemmArgs g) {
+__global__ __launch_bounds__(256, 2) void k_gemm_bf(GemmArgs g) {
   constexpr int WN_WAVES = (BN >= 64) ? 2 : 1;
   constexpr int WM_WAVES = 4 / WN_WAVES;
   constexpr int WM = BM / WM_WAVES, WN = BN / WN_WAVES;
@@ -54,24 +54,27 @@ __global__ __launch_bounds__(256) void k_gemm_bf(GemmArgs g) {
       sa.load(A, g.lda, A_KC, m0, g.M, k0 + BK16, ke, tid);
       sb.load(Bm, g.ldb, B_KC, n0, g.N, k0 + BK16, ke, tid);
     }
-    bf16x8 a[TM][S], b[TN][S];
+    // A fragments stay in registers for the whole stage; B fragments are
+    // fetched one 16-column block at a time (wide wave tiles would not hold
+    // them all)
+    bf16x8 a[TM][S];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int s = 0; s < S; ++s) a[i][s] = bfrag(As + s * BM * BLD, wm0 + i * 16, lane);
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+    for (int j = 0; j < TN; ++j) {
+      bf16x8 b[S];
 #pragma unroll
-      for (int s = 0; s < S; ++s) b[j][s] = bfrag(Bs + s * BN * BLD, wn0 + j * 16, lane);
-    // piece products p + q <= S - 1 (0-based), smallest first
+      for (int s = 0; s < S; ++s) b[s] = bfrag(Bs + s * BN * BLD, wn0 + j * 16, lane);
+      // piece products p + q <= S - 1 (0-based), smallest first
 #pragma unroll
-    for (int sum = S - 1; sum >= 0; --sum)
+      for (int sum = S - 1; sum >= 0; --sum)
 #pragma unroll
-      for (int p = 0; p <= sum; ++p)
+        for (int p = 0; p <= sum; ++p)
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j) acc[i][j] = mfma_bf16(a[i][p], b[j][sum - p], acc[i][j]);
+          for (int i = 0; i < TM; ++i) acc[i][j] = mfma_bf16(a[i][p], b[sum - p], acc[i][j]);
+    }
     __syncthreads();
   }
 
@@ -318,6 +321,11 @@ hipError_t launch_bm(const GemmArgs& g, int nl, hipStream_t s) {
 
 template <int S>
 hipError_t launch_s(const GemmArgs& g, int nl, hipStream_t s) {
+  // 128 x 256 tiles (64 x 128 per wave) read a quarter less LDS per MFMA and
+  // half as many copies of the A operand; three-piece splits keep 128 x 128
+  if constexpr (S <= 2) {
+    if (g.N >= 256) return launch_bm<S, 128, 256>(g, nl, s);
+  }
   if (g.N > 64) return launch_bm<S, 128, 128>(g, nl, s);
   if (g.N > 32) return launch_bm<S, 128, 64>(g, nl, s);
   return launch_bm<S, 128, 32>(g, nl, s);
@@ -326,7 +334,10 @@ hipError_t launch_s(const GemmArgs& g, int nl, hipStream_t s) {
 }  // namespace
 
 int gemm_bf_bm(int N) { (void)N; return 128; }
-int gemm_bf_bn(int N) { return N > 64 ? 128 : (N > 32 ? 64 : 32); }
+int gemm_bf_bn(int N, int pieces) {
+  if (pieces <= 2 && N >= 256) return 256;
+  return N > 64 ? 128 : (N > 32 ? 64 : 32);
+}
 
 hipError_t launch_gemm_bf(const GemmArgs& g, int nl, int pieces, hipStream_t s) {
   if (nl <= 0) return hipSuccess;
