@@ -437,37 +437,30 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
                       [&](int j) { return static_cast<const void*>(lay(j)->P); },
                       [&](int j) { return static_cast<void*>(lay(j)->R); }, part, fast ? 2 : 3);
   if (st != CD_OK) return st;
-  // Q = ColumnNormalize(R)
-  cd::ColnormArgs cn{};
-  cn.n = n; cn.r = r; cn.nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
-  for (int j = 0; j < nl; ++j) {
-    cn.R[j] = lay(j)->R; cn.part[j] = lay(j)->colsq; cn.nrm[j] = lay(j)->colnrm; cn.Q[j] = Q[sel[j]];
-  }
-  st = run(g, K_COLNORM, 12.0 * nr * nl, 3.0 * nr * nl, s, [&] { return cd::launch_colnorm(cn, nl, s); });
-  if (st != CD_OK) return st;
   // M = B - (1 - mu) P R^T;  X -= eta sqrt(m/n) P Q^T.  The rank-r
   // corrections are fp32-accurate (6 bf16 piece products) for fp32 layers and
   // plain bf16 products for bf16-gradient layers; P, R, Q are split into bf16
   // planes once, then streamed by the update.
   const int up = fast ? 1 : 3;
   const int rp = (r + 31) / 32 * 32;
+  // Q = ColumnNormalize(R), with the planes of R and Q in the same pass
+  cd::ColnormArgs cn{};
+  cn.n = n; cn.r = r; cn.nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
+  cn.S = up; cn.rp = rp;
+  for (int j = 0; j < nl; ++j) {
+    cn.R[j] = lay(j)->R; cn.part[j] = lay(j)->colsq; cn.nrm[j] = lay(j)->colnrm; cn.Q[j] = Q[sel[j]];
+    cn.Rpl[j] = lay(j)->planes + 3LL * m * rp;
+    cn.Qpl[j] = lay(j)->planes + 3LL * m * rp + 3LL * n * rp;
+  }
+  st = run(g, K_COLNORM, (12.0 + 4.0 * up) * nr * nl, 3.0 * nr * nl, s,
+           [&] { return cd::launch_colnorm(cn, nl, s); });
+  if (st != CD_OK) return st;
   {
     cd::PlaneArgs pa{};
     pa.r = r; pa.rp = rp; pa.S = up;
-    const double pb = (4.0 + 2.0 * up);
     pa.rows = m;
     for (int j = 0; j < nl; ++j) { pa.src[j] = lay(j)->P; pa.dst[j] = lay(j)->planes; }
-    st = run(g, K_COLNORM, pb * mr * nl, 0.0, s, [&] { return cd::launch_split_planes(pa, nl, s); });
-    if (st != CD_OK) return st;
-    pa.rows = n;
-    for (int j = 0; j < nl; ++j) { pa.src[j] = lay(j)->R; pa.dst[j] = lay(j)->planes + 3LL * m * rp; }
-    st = run(g, K_COLNORM, pb * nr * nl, 0.0, s, [&] { return cd::launch_split_planes(pa, nl, s); });
-    if (st != CD_OK) return st;
-    for (int j = 0; j < nl; ++j) {
-      pa.src[j] = Q[sel[j]];
-      pa.dst[j] = lay(j)->planes + 3LL * m * rp + 3LL * n * rp;
-    }
-    st = run(g, K_COLNORM, pb * nr * nl, 0.0, s, [&] { return cd::launch_split_planes(pa, nl, s); });
+    st = run(g, K_COLNORM, (4.0 + 2.0 * up) * mr * nl, 0.0, s, [&] { return cd::launch_split_planes(pa, nl, s); });
     if (st != CD_OK) return st;
   }
   cd::UpdatePlArgs ua{};

@@ -137,7 +137,7 @@ hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r,
                        hipStream_t s, bool ident = false, int mlimit = 0);
 
 // ---- ColumnNormalize --------------------------------------------------------
-constexpr int COLNORM_ROWS = 256;  // rows per partial
+constexpr int COLNORM_ROWS = 64;   // rows per partial
 struct ColnormArgs {
   int n, r;
   int nchunks;                     // ceil(n / COLNORM_ROWS)
@@ -145,6 +145,10 @@ struct ColnormArgs {
   double* part[MAXB];              // [nchunks][r]
   float* nrm[MAXB];                // [r] max(‖R_j‖, floor) as fp32
   float* Q[MAXB];                  // out: n x r
+  // bf16 planes (pieces S, row stride rp) of R and of Q for the update
+  int S, rp;
+  __bf16* Rpl[MAXB];
+  __bf16* Qpl[MAXB];
 };
 hipError_t launch_colnorm(const ColnormArgs& a, int nl, hipStream_t s);
 

@@ -1,24 +1,35 @@
 // ColumnNormalize of the Dion sync branch (Algorithm 1 / Algorithm 2):
 //   Q_j = R_j / max(‖R_j‖, 1e-30)        (column 2-norms accumulated in fp64,
 //                                          partials in a fixed row order)
+// fused with the bf16 split planes of R and Q that the update streams.
 #include "common.hpp"
 
 namespace cd {
 namespace {
 
-// Partial column sums of squares over COLNORM_ROWS rows, in row order.
+// Partial column sums of squares over COLNORM_ROWS rows: thread j owns
+// column j; four interleaved accumulators (row i goes to i % 4) keep 16 loads
+// in flight and are combined in a fixed order.
 __global__ __launch_bounds__(256) void k_colsq(ColnormArgs a) {
   const int l = blockIdx.z, chunk = blockIdx.x;
+  const int j = blockIdx.y * 256 + threadIdx.x;
+  if (j >= a.r) return;
   const float* R = a.R[l];
   const int i0 = chunk * COLNORM_ROWS, i1 = min(a.n, i0 + COLNORM_ROWS);
-  for (int j = threadIdx.x; j < a.r; j += 256) {
-    double s = 0.0;
-    for (int i = i0; i < i1; ++i) {
-      const double v = R[static_cast<long long>(i) * a.r + j];
-      s += v * v;
-    }
-    a.part[l][static_cast<long long>(chunk) * a.r + j] = s;
+  double s[4] = {0.0, 0.0, 0.0, 0.0};
+  int i = i0;
+  for (; i + 16 <= i1; i += 16) {
+    float v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = R[static_cast<long long>(i + u) * a.r + j];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) s[u & 3] += static_cast<double>(v[u]) * v[u];
   }
+  for (; i < i1; ++i) {
+    const double v = R[static_cast<long long>(i) * a.r + j];
+    s[(i - i0) & 3] += v * v;
+  }
+  a.part[l][static_cast<long long>(chunk) * a.r + j] = (s[0] + s[1]) + (s[2] + s[3]);
 }
 
 __global__ __launch_bounds__(256) void k_colnorm_final(ColnormArgs a) {
@@ -30,14 +41,45 @@ __global__ __launch_bounds__(256) void k_colnorm_final(ColnormArgs a) {
   a.nrm[l][j] = static_cast<float>(fmax(sqrt(s), 1e-30));
 }
 
-__global__ __launch_bounds__(256) void k_colscale(ColnormArgs a) {
+// Q = R / norms, and the bf16 planes of R and Q (piece s of a value is
+// bf16(value - pieces < s), as for every split operand): one pass over R.
+// Four consecutive columns per thread; columns r..rp-1 of the planes are zero.
+__global__ __launch_bounds__(256) void k_colscale_planes(ColnormArgs a) {
   const int l = blockIdx.z;
-  const long long total = static_cast<long long>(a.n) * a.r;
+  const int qpr = a.rp / 4;   // quads per row
+  const long long quads = static_cast<long long>(a.n) * qpr;
+  const long long plane = static_cast<long long>(a.n) * a.rp;
   const float* R = a.R[l];
   const float* nrm = a.nrm[l];
   float* Q = a.Q[l];
-  for (long long i = blockIdx.x * 256LL + threadIdx.x; i < total; i += 256LL * gridDim.x) {
-    Q[i] = R[i] / nrm[i % a.r];
+  __bf16* Rp = a.Rpl[l];
+  __bf16* Qp = a.Qpl[l];
+  for (long long q = blockIdx.x * 256LL + threadIdx.x; q < quads; q += 256LL * gridDim.x) {
+    const long long row = q / qpr;
+    const int k = static_cast<int>(q - row * qpr) * 4;
+    float rv[4], qv[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const bool in = k + c < a.r;
+      rv[c] = in ? R[row * a.r + k + c] : 0.0f;
+      qv[c] = in ? rv[c] / nrm[k + c] : 0.0f;
+      if (in) Q[row * a.r + k + c] = qv[c];
+    }
+    float rr[4] = {rv[0], rv[1], rv[2], rv[3]}, qr[4] = {qv[0], qv[1], qv[2], qv[3]};
+    for (int s = 0; s < a.S; ++s) {
+      __bf16 pr[4], pq[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        pr[c] = static_cast<__bf16>(rr[c]);
+        rr[c] -= static_cast<float>(pr[c]);
+        pq[c] = static_cast<__bf16>(qr[c]);
+        qr[c] -= static_cast<float>(pq[c]);
+      }
+      typedef __bf16 b4 __attribute__((ext_vector_type(4)));
+      const b4 wr = {pr[0], pr[1], pr[2], pr[3]}, wq = {pq[0], pq[1], pq[2], pq[3]};
+      *reinterpret_cast<b4*>(Rp + s * plane + row * a.rp + k) = wr;
+      *reinterpret_cast<b4*>(Qp + s * plane + row * a.rp + k) = wq;
+    }
   }
 }
 
@@ -45,12 +87,13 @@ __global__ __launch_bounds__(256) void k_colscale(ColnormArgs a) {
 
 hipError_t launch_colnorm(const ColnormArgs& a, int nl, hipStream_t s) {
   if (nl <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_colsq, dim3(a.nchunks, 1, nl), dim3(256), 0, s, a);
+  if (a.rp % 32 != 0 || a.rp < a.r || a.S < 1 || a.S > 3) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_colsq, dim3(a.nchunks, (a.r + 255) / 256, nl), dim3(256), 0, s, a);
   hipLaunchKernelGGL(k_colnorm_final, dim3((a.r + 255) / 256, 1, nl), dim3(256), 0, s, a);
-  long long total = static_cast<long long>(a.n) * a.r;
-  long long blocks = (total + 255) / 256;
-  if (blocks > 2048) blocks = 2048;
-  hipLaunchKernelGGL(k_colscale, dim3(static_cast<unsigned>(blocks), 1, nl), dim3(256), 0, s, a);
+  long long quads = static_cast<long long>(a.n) * (a.rp / 4);
+  long long blocks = (quads + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_colscale_planes, dim3(static_cast<unsigned>(blocks), 1, nl), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
