@@ -62,13 +62,20 @@ struct DeviceGuard {
   }
 };
 
-// K-splitting so that one launch has >= ~1024 blocks, each slice >= 256 deep.
-// pieces > 0 selects the tile shape of the bf16-split kernels, else the fp32 /
-// fp64 MFMA kernels.
-int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk, int pieces = 0) {
+// K-splitting so that one launch has >= ~1024 working blocks, each slice >=
+// 256 deep.  pieces > 0 selects the tile shape of the bf16-split kernels, else
+// the fp32 / fp64 MFMA kernels; `upper` counts only the tiles an upper-only
+// product computes (the others exit at once).
+int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk, int pieces = 0, bool upper = false) {
   const long long bm = pieces > 0 ? cd::gemm_bf_bm(N) : cd::gemm_bm(N, fp64);
   const long long bn = pieces > 0 ? cd::gemm_bf_bn(N, pieces) : cd::gemm_bn(N, fp64);
-  const long long tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn) * nl;
+  const long long tiles_m = (M + bm - 1) / bm, tiles_n = (N + bn - 1) / bn;
+  long long per_layer = tiles_m * tiles_n;
+  if (upper) {
+    per_layer = 0;
+    for (long long i = 0; i < tiles_m; ++i) per_layer += std::max(0LL, tiles_n - i);
+  }
+  const long long tiles = per_layer * nl;
   int s = 1;
   while (tiles * s < 1024 && K / (2 * s) >= 256 && s < 32) s *= 2;
   int kc = (K + s - 1) / s;
@@ -340,7 +347,7 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
     cd::GemmArgs ga{};
     ga.M = Mr; ga.N = Nr; ga.K = K; ga.lda = lda; ga.ldb = ldb; ga.ldc = Nr;
     ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper; ga.out64 = bf_out64;
-    ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk, pieces);
+    ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk, pieces, upper);
     ga.split_stride = 1LL * Mr * Nr;
     if (ga.splits > 1) {
       // the partials must fit the workspace sized at create time
@@ -665,7 +672,7 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
         split_bytes = std::max(split_bytes,
                                plan_splits(r, r, m, 1, false, &kc, pieces) * r * r * sizeof(float));
       }
-      gram_cap = std::max(gram_cap, static_cast<size_t>(plan_splits(r, r, m, 1, true, &kc)) * r * r);
+      gram_cap = std::max(gram_cap, static_cast<size_t>(plan_splits(r, r, m, 1, true, &kc, 0, true)) * r * r);
     }
     const size_t nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
     hipError_t e = hipSuccess;

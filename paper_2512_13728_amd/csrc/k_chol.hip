@@ -211,10 +211,21 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
   const int c0 = cb * CB, nbc = min(CB, r - c0);
   const TIn* Pin = static_cast<const TIn*>(t.Pin);
   TOut* Pout = static_cast<TOut*>(t.Pout);
+  if constexpr (IDENT) {
+    // T^{-1} is upper triangular: a row tile below the diagonal block is zero
+    if (lt.y > cb) {
+      for (int idx = tid; idx < CB * CB; idx += 256) {
+        const int row = idx / CB, col = idx % CB;
+        if (i0 + row < m && col < nbc) Pout[static_cast<long long>(i0 + row) * r + c0 + col] = TOut(0);
+      }
+      return;
+    }
+  }
   Tile64 T;
   T.zero();
-  // acc = P[:, :c0] T[:c0, c0:c0+64]   (P is the output: earlier block columns)
-  for (int k0 = 0; k0 < c0; k0 += GBK) {
+  // acc = P[:, :c0] T[:c0, c0:c0+64]   (P is the output: earlier block columns;
+  // for T^{-1} its rows i0.. are zero left of column i0)
+  for (int k0 = IDENT ? i0 : 0; k0 < c0; k0 += GBK) {
     stage_tile<double, TOut, CB, 256, true>(As, Pout + static_cast<long long>(i0) * r, r, 0, m - i0,
                                             k0, c0, tid);
     stage_tile<double, double, CB, 256, false>(Bs, t.W + c0, r, 0, nbc, k0, c0, tid);

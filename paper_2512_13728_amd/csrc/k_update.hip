@@ -54,16 +54,25 @@ __global__ __launch_bounds__(256) void k_colscale_planes(ColnormArgs a) {
   float* Q = a.Q[l];
   __bf16* Rp = a.Rpl[l];
   __bf16* Qp = a.Qpl[l];
+  const bool vec = (a.r & 3) == 0;   // 16-byte rows segments of R and Q (and of the norms)
   for (long long q = blockIdx.x * 256LL + threadIdx.x; q < quads; q += 256LL * gridDim.x) {
     const long long row = q / qpr;
     const int k = static_cast<int>(q - row * qpr) * 4;
     float rv[4], qv[4];
+    if (vec && k + 3 < a.r) {
+      const float4 x = *reinterpret_cast<const float4*>(R + row * a.r + k);
+      const float4 d = *reinterpret_cast<const float4*>(nrm + k);
+      rv[0] = x.x; rv[1] = x.y; rv[2] = x.z; rv[3] = x.w;
+      qv[0] = x.x / d.x; qv[1] = x.y / d.y; qv[2] = x.z / d.z; qv[3] = x.w / d.w;
+      *reinterpret_cast<float4*>(Q + row * a.r + k) = make_float4(qv[0], qv[1], qv[2], qv[3]);
+    } else {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const bool in = k + c < a.r;
-      rv[c] = in ? R[row * a.r + k + c] : 0.0f;
-      qv[c] = in ? rv[c] / nrm[k + c] : 0.0f;
-      if (in) Q[row * a.r + k + c] = qv[c];
+      for (int c = 0; c < 4; ++c) {
+        const bool in = k + c < a.r;
+        rv[c] = in ? R[row * a.r + k + c] : 0.0f;
+        qv[c] = in ? rv[c] / nrm[k + c] : 0.0f;
+        if (in) Q[row * a.r + k + c] = qv[c];
+      }
     }
     float rr[4] = {rv[0], rv[1], rv[2], rv[3]}, qr[4] = {qv[0], qv[1], qv[2], qv[3]};
     for (int s = 0; s < a.S; ++s) {
