@@ -21,23 +21,19 @@ namespace {
 
 constexpr int CB = CHOL_BLOCK;
 
-// A double broadcast from one lane of the wave (two v_readlane).
-__device__ __forceinline__ double bcast(double v, int src) {
-  const long long b = __double_as_longlong(v);
-  const int lo = __builtin_amdgcn_readlane(static_cast<int>(b), src);
-  const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), src);
-  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned>(lo));
-}
-
 // One wave per layer: lane j holds column j of the 64 x 64 diagonal block
 // (upper triangle; rows past the matrix padded with the identity) in
-// registers.  Right-looking Cholesky, then D = T^{-1} column by column by
-// back substitution (lane c solves T d = e_c); every row of T that a step
-// needs comes from the lane that owns it by v_readlane, so neither phase
-// touches LDS or waits at a barrier.  The loops are unrolled so that the
-// register arrays are indexed by constants.
+// registers.  Right-looking Cholesky: at pivot p the lanes publish row p of
+// the updated block in LDS and every lane reads it back with uniform-address
+// loads (a broadcast), then updates its own column.  D = T^{-1} follows by
+// back substitution, lane c solving T d = e_c, with T read from LDS.  The
+// loops are unrolled so that the register arrays are indexed by constants.
+constexpr int TLD = CB + 1;   // padded row of T in LDS (column stores hit distinct banks)
+
 __global__ __launch_bounds__(64) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
                                                   int pass) {
+  __shared__ __attribute__((aligned(16))) double rowb[CB];
+  __shared__ double Ts[CB * TLD];   // Ts[j * TLD + i] = T[i][j]
   const CholTab t = tab[blockIdx.x];
   const int j = threadIdx.x;
   const long long ld = r;
@@ -65,23 +61,33 @@ __global__ __launch_bounds__(64) void k_chol_diag(const CholTab* __restrict__ ta
   bool def = false;
 #pragma unroll
   for (int p = 0; p < CB; ++p) {
-    double d = bcast(a[p], p);
+    rowb[j] = a[p];
+    __syncthreads();
+    double d = rowb[p];
     if (p < nb && !(d > fl)) { d = fl; def = true; }
     const double piv = sqrt(d);
-    a[p] = (j == p) ? piv : a[p] / piv;
+    a[p] = (j == p) ? piv : a[p] / piv;   // row p of T (lanes j > p)
+    __syncthreads();
+    rowb[j] = a[p];
+    __syncthreads();
     // rows below p: A[i][j] -= T[p][i] T[p][j]; lanes j < i only touch the
     // (unused) lower triangle
 #pragma unroll
-    for (int i = p + 1; i < CB; ++i) a[i] = fma(-bcast(a[p], i), a[p], a[i]);
+    for (int i = p + 1; i < CB; ++i) a[i] = fma(-rowb[i], a[p], a[i]);
+    __syncthreads();
   }
+#pragma unroll
+  for (int i = 0; i < CB; ++i) Ts[j * TLD + i] = a[i];
+  __syncthreads();
   double e[CB];
 #pragma unroll
   for (int i = 0; i < CB; ++i) e[i] = i == j ? 1.0 : 0.0;
 #pragma unroll
   for (int p = CB - 1; p >= 0; --p) {
-    e[p] = e[p] / bcast(a[p], p);
+    const double* col = Ts + p * TLD;   // column p of T: T[i][p] = col[i]
+    e[p] = e[p] / col[p];
 #pragma unroll
-    for (int i = 0; i < p; ++i) e[i] = fma(-bcast(a[i], p), e[p], e[i]);
+    for (int i = 0; i < p; ++i) e[i] = fma(-col[i], e[p], e[i]);
   }
   double* D = t.Dinv + static_cast<long long>(kb) * CB * CB;
 #pragma unroll
@@ -225,11 +231,23 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
   T.zero();
   // acc = P[:, :c0] T[:c0, c0:c0+64]   (P is the output: earlier block columns;
   // for T^{-1} its rows i0.. are zero left of column i0)
-  for (int k0 = IDENT ? i0 : 0; k0 < c0; k0 += GBK) {
-    stage_tile<double, TOut, CB, 256, true>(As, Pout + static_cast<long long>(i0) * r, r, 0, m - i0,
-                                            k0, c0, tid);
-    stage_tile<double, double, CB, 256, false>(Bs, t.W + c0, r, 0, nbc, k0, c0, tid);
+  // (the next stage's loads are in flight while this one is multiplied)
+  const int kbeg = IDENT ? i0 : 0;
+  const TOut* Prow = Pout + static_cast<long long>(i0) * r;
+  Prefetch<TOut, CB, 256, true> pa;
+  Prefetch<double, CB, 256, false> pb;
+  if (kbeg < c0) {
+    pa.load(Prow, r, 0, m - i0, kbeg, c0, tid);
+    pb.load(t.W + c0, r, 0, nbc, kbeg, c0, tid);
+  }
+  for (int k0 = kbeg; k0 < c0; k0 += GBK) {
+    pa.template store<double>(As, tid);
+    pb.template store<double>(Bs, tid);
     __syncthreads();
+    if (k0 + GBK < c0) {
+      pa.load(Prow, r, 0, m - i0, k0 + GBK, c0, tid);
+      pb.load(t.W + c0, r, 0, nbc, k0 + GBK, c0, tid);
+    }
     T.mma_stage<true>(As, Bs, wm0, wn0, lane);
     __syncthreads();
   }
