@@ -16,7 +16,7 @@ from typing import Optional, Sequence, Tuple
 __all__ = [
     "LibraryNotBuilt", "CurvaDionError", "Layer", "Group", "lib", "library_path",
     "POLICY_RMMC", "POLICY_ALWAYS_SYNC", "POLICY_NEVER_SYNC", "POLICY_EVERY_H",
-    "F32", "BF16", "EXPORTED_SYMBOLS",
+    "F32", "BF16", "EXPORTED_SYMBOLS", "PointerArray",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -183,6 +183,18 @@ class Layer:
             pass
 
 
+class PointerArray:
+    """One device address per layer, marshalled once (Group.pack); keeps the
+    tensors alive so the addresses stay valid."""
+
+    def __init__(self, array, keep):
+        self.array = array
+        self._keep = list(keep)
+
+    def __len__(self):
+        return len(self.array)
+
+
 class Group:
     """Layers stepped together: the gate takes the max of RMMC over all of them."""
 
@@ -194,10 +206,19 @@ class Group:
         _check(lib().cd_group_create(arr, len(layers), ctypes.byref(h)))
         self._h = h
 
-    def step(self, G, M, X, Q, mu: float, eta: float, r: int, stream=None):
-        """One step over every layer; returns (rmmc_max, sync_flag, rmmc_per_layer, status)."""
+    def pack(self, tensors) -> "PointerArray":
+        """The device addresses of one tensor per layer, marshalled once: pass
+        the result to step() in place of the list while those tensors live."""
         n = len(self.layers)
-        mk = lambda ts: (ctypes.c_void_p * n)(*[_ptr(t) for t in ts])
+        if len(tensors) != n:
+            raise ValueError(f"expected {n} tensors, got {len(tensors)}")
+        return PointerArray((ctypes.c_void_p * n)(*[_ptr(t) for t in tensors]), tensors)
+
+    def step(self, G, M, X, Q, mu: float, eta: float, r: int, stream=None):
+        """One step over every layer; returns (rmmc_max, sync_flag, rmmc_per_layer, status).
+        G, M, X, Q are lists with one tensor (or address) per layer, or pack() results."""
+        n = len(self.layers)
+        mk = lambda ts: ts.array if isinstance(ts, PointerArray) else (ctypes.c_void_p * n)(*[_ptr(t) for t in ts])
         per = (ctypes.c_double * n)()
         res = Result()
         st = lib().cd_group_step(self._h, mk(G), mk(M), mk(X), mk(Q), mu, eta, r,

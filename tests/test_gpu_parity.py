@@ -272,6 +272,33 @@ def test_sync_after_skip_reverses_speculation(m, n, r, gd):
     assert flags == [True, False, True, False]
 
 
+def test_packed_pointers_match_lists():
+    """Group.step with pointer arrays marshalled once (Group.pack) gives the
+    bit-identical result of passing the tensor lists."""
+    shapes = [(256, 384), (384, 256), (100, 300)]
+    r = 16
+    w = S.Workload("pack", tuple(shapes), r=r, grad_dtype="f32", steps=3, k=8, tau=0.3, stream_id=92)
+    outs = []
+    for packed in (False, True):
+        Ls = [cdl.Layer(m, n, r, tau=0.3) for m, n in shapes]
+        Gp = cdl.Group(Ls)
+        st = [_state(w, i) for i in range(len(shapes))]
+        M, X, Q = [s[0] for s in st], [s[1] for s in st], [s[2] for s in st]
+        args = (Gp.pack(M), Gp.pack(X), Gp.pack(Q)) if packed else (M, X, Q)
+        streams = [S.GradientStream(w, i, device="cpu") for i in range(len(shapes))]
+        res = []
+        for t in range(w.steps):
+            G = [s.next().to(DEV) for s in streams]
+            res.append(Gp.step(Gp.pack(G) if packed else G, *args, w.mu, w.eta, r)[:2])
+        torch.cuda.synchronize()
+        outs.append((res, [f64(t) for t in M + X + Q]))
+    assert outs[0][0] == outs[1][0]
+    for a, b in zip(outs[0][1], outs[1][1]):
+        assert np.array_equal(a, b)
+    with pytest.raises(ValueError):
+        Gp.pack(M[:1])
+
+
 def test_state_roundtrip_and_every_h_policy():
     m, n, r = 64, 64, 4
     L = cdl.Layer(m, n, r, policy=cdl.POLICY_EVERY_H, H=3)
