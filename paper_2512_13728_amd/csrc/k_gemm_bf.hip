@@ -134,6 +134,7 @@ __global__ __launch_bounds__(256) void k_split_planes(PlaneArgs a) {
 // is plain 16-byte loads into LDS; the P planes of a 128-row panel are shared
 // by the BN-column tiles that the XCD-aware order keeps on one XCD.
 constexpr int UBM = 128;
+typedef float nt4 __attribute__((ext_vector_type(4)));
 
 // G elements for the reversal of a speculative skip update: fp32, or bf16
 // widened exactly.
@@ -285,7 +286,9 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
       const long long off = static_cast<long long>(grow) * u.n + gcol;
       float* y = Y + off;
       if (vec && gcol + 3 < u.n) {
-        float4 w = *reinterpret_cast<const float4*>(y);
+        // non-temporal: M and X are touched once; the P/R/Q slices should keep L2
+        const nt4 wv = __builtin_nontemporal_load(reinterpret_cast<const nt4*>(y));
+        float4 w = make_float4(wv.x, wv.y, wv.z, wv.w);
         if (gc != 0.f) {
           const float4 g = load_g4(G, gbf, off);
           w.x = fmaf(gc, g.x, w.x); w.y = fmaf(gc, g.y, w.y);
@@ -293,7 +296,8 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
         }
         w.x = fmaf(coef, a.x, w.x); w.y = fmaf(coef, a.y, w.y);
         w.z = fmaf(coef, a.z, w.z); w.w = fmaf(coef, a.w, w.w);
-        *reinterpret_cast<float4*>(y) = w;
+        const nt4 ov = {w.x, w.y, w.z, w.w};
+        __builtin_nontemporal_store(ov, reinterpret_cast<nt4*>(y));
       } else {
         const float av[4] = {a.x, a.y, a.z, a.w};
         for (int c = 0; c < 4; ++c) {
