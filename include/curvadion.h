@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define CD_ABI_VERSION 1
+#define CD_ABI_VERSION 2
 
 typedef enum cd_status {
   CD_OK = 0,
@@ -77,6 +77,11 @@ typedef struct cd_layer_desc {
   double eta_local_scale;   /* eta_local = eta_local_scale * eta; >= 0 */
   cd_policy policy;
   int H;                    /* period for CD_POLICY_EVERY_H (>= 1), else ignored */
+  double weight_decay;      /* decoupled weight decay lambda >= 0: each step first
+                               scales X by (1 - eta * lambda), in either branch;
+                               M is untouched.  0 = Algorithm 2 exactly.  (The
+                               experiments of Sec. 4 use 0.01 without stating the
+                               form; this is the decoupled reading.) */
 } cd_layer_desc;
 
 typedef struct cd_result {
@@ -90,8 +95,8 @@ typedef struct cd_group cd_group;
 /* Create one layer on the current device: allocates the workspace for
  * (m, n, r_max), sets prev_norm = 0 and the step counter to 0 (Algorithm 2
  * initialisation).  CD_EINVAL for a NULL pointer, a non-positive size,
- * r_max > min(m, n), an unknown dtype or policy, eps < 0, tau NaN, or H < 1
- * under CD_POLICY_EVERY_H. */
+ * r_max > min(m, n), an unknown dtype or policy, eps < 0, tau NaN, a negative
+ * or non-finite weight_decay, or H < 1 under CD_POLICY_EVERY_H. */
 cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out);
 
 /* One step for one layer (Algorithm 2 with the max taken over this layer

@@ -26,6 +26,9 @@ notes of the repository):
 * Weight update scale sqrt(m/n) with m = rows, n = columns of the matrix.
 * Local (skip) branch: M = B, X -= eta_local * G, Q unchanged; eta_local = eta
   unless given.
+* Weight decay (the experiments of Sec. 4 use 0.01 and leave the form open):
+  decoupled, X <- (1 - eta * weight_decay) X before either branch's update; M
+  is untouched.  weight_decay = 0 (the default) is Algorithm 2 exactly.
 
 Parity pins for every function live in tests/test_oracle_pins.py.
 """
@@ -126,11 +129,11 @@ def power_iteration(B, Q_prev):
     return P_tilde, P, R
 
 
-def sync_update(B, X, Q_prev, mu: float, eta: float):
+def sync_update(B, X, Q_prev, mu: float, eta: float, x_decay: float = 1.0):
     """The full Dion update for one layer (Algorithm 2, sync branch).
 
     M_t = B_t - (1 - mu) P R^T;  Q_t = ColumnNormalize(R);
-    X_t = X_{t-1} - eta sqrt(m/n) P Q_t^T.
+    X_t = x_decay X_{t-1} - eta sqrt(m/n) P Q_t^T  (x_decay = 1 - eta * weight decay).
     Returns dict with M, X, Q, P, P_tilde, R.
     """
     B = _f64(B)
@@ -138,13 +141,13 @@ def sync_update(B, X, Q_prev, mu: float, eta: float):
     P_tilde, P, R = power_iteration(B, Q_prev)
     M = B - (1.0 - mu) * (P @ R.T)
     Q = column_normalize(R)
-    Xn = _f64(X) - eta * math.sqrt(m / n) * (P @ Q.T)
+    Xn = x_decay * _f64(X) - eta * math.sqrt(m / n) * (P @ Q.T)
     return dict(M=M, X=Xn, Q=Q, P=P, P_tilde=P_tilde, R=R)
 
 
-def local_update(B, G, X, eta_local: float):
-    """Local branch of Algorithm 2: M_t = B_t; X_t = X_{t-1} - eta_local G_t."""
-    return dict(M=_f64(B).copy(), X=_f64(X) - eta_local * _f64(G))
+def local_update(B, G, X, eta_local: float, x_decay: float = 1.0):
+    """Local branch of Algorithm 2: M_t = B_t; X_t = x_decay X_{t-1} - eta_local G_t."""
+    return dict(M=_f64(B).copy(), X=x_decay * _f64(X) - eta_local * _f64(G))
 
 
 # --- whole step over a set of layers -----------------------------------------
@@ -170,14 +173,17 @@ class OracleLayer:
 
 def group_step(layers: List[OracleLayer], grads, mu: float, eta: float, tau: float,
                eps: float = 1e-8, policy: int = POLICY_RMMC, H: int = 1,
-               eta_local: Optional[float] = None, with_kappa: bool = False):
+               eta_local: Optional[float] = None, with_kappa: bool = False,
+               weight_decay: float = 0.0):
     """One CurvaDion step over all layers (Algorithm 2), updating ``layers``.
+    weight_decay > 0 adds the decoupled decay X <- (1 - eta weight_decay) X.
 
     Every layer forms its buffer and RMMC first; the global max then decides one
     branch for all layers.  Returns dict(rmmc=[...], g=global max, flag=bool,
     kappa=[cond(P~) per layer] when requested and synced).
     """
     eta_local = eta if eta_local is None else eta_local
+    x_decay = 1.0 - eta * weight_decay
     Bs, vals = [], []
     for L, G in zip(layers, grads):
         B = buffer_update(L.M, G)
@@ -191,13 +197,13 @@ def group_step(layers: List[OracleLayer], grads, mu: float, eta: float, tau: flo
     kappa = []
     for L, G, B in zip(layers, grads, Bs):
         if flag:
-            out = sync_update(B, L.X, L.Q, mu, eta)
+            out = sync_update(B, L.X, L.Q, mu, eta, x_decay)
             L.M, L.X, L.Q = out["M"], out["X"], out["Q"]
             L.last = out
             if with_kappa:
                 kappa.append(float(np.linalg.cond(out["P_tilde"])))
         else:
-            out = local_update(B, G, L.X, eta_local)
+            out = local_update(B, G, L.X, eta_local, x_decay)
             L.M, L.X = out["M"], out["X"]
             L.last = out
     return dict(rmmc=vals, g=g, flag=flag, kappa=kappa)

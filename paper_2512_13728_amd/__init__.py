@@ -51,7 +51,7 @@ class LayerDesc(ctypes.Structure):
     _fields_ = [("m", ctypes.c_int), ("n", ctypes.c_int), ("r_max", ctypes.c_int),
                 ("grad_dtype", ctypes.c_int), ("tau", ctypes.c_double),
                 ("eps", ctypes.c_double), ("eta_local_scale", ctypes.c_double),
-                ("policy", ctypes.c_int), ("H", ctypes.c_int)]
+                ("policy", ctypes.c_int), ("H", ctypes.c_int), ("weight_decay", ctypes.c_double)]
 
 
 class Result(ctypes.Structure):
@@ -128,10 +128,10 @@ class Layer:
 
     def __init__(self, m: int, n: int, r_max: int, *, grad_dtype: str = "f32",
                  tau: float = 0.5, eps: float = 1e-8, eta_local_scale: float = 1.0,
-                 policy: int = POLICY_RMMC, H: int = 1):
+                 policy: int = POLICY_RMMC, H: int = 1, weight_decay: float = 0.0):
         self._h = None
         desc = LayerDesc(m, n, r_max, BF16 if grad_dtype == "bf16" else F32, tau, eps,
-                         eta_local_scale, policy, H)
+                         eta_local_scale, policy, H, weight_decay)
         h = ctypes.c_void_p()
         _check(lib().cd_layer_create(ctypes.byref(desc), ctypes.byref(h)))
         self._h = h

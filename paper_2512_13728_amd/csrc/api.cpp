@@ -302,6 +302,8 @@ cd_status check_desc(const cd_layer_desc* d) {
   if (!(d->eta_local_scale >= 0.0) || !std::isfinite(d->eta_local_scale))
     return fail(CD_EINVAL, "eta_local_scale must be finite and >= 0");
   if (d->policy == CD_POLICY_EVERY_H && d->H < 1) return fail(CD_EINVAL, "H must be >= 1");
+  if (!(d->weight_decay >= 0.0) || !std::isfinite(d->weight_decay))
+    return fail(CD_EINVAL, "weight_decay must be finite and >= 0");
   return CD_OK;
 }
 
@@ -478,6 +480,7 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   for (int j = 0; j < nl; ++j) {
     ua.G[j] = G[sel[j]];
     ua.gc[j] = static_cast<float>(lay(j)->d.eta_local_scale * static_cast<double>(eta_local_spec));
+    ua.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * lay(j)->d.weight_decay);
     ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]];
     ua.P[j] = lay(j)->planes;
     ua.R[j] = lay(j)->planes + 3LL * m * rp;
@@ -559,6 +562,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
         fa.M[j] = M[li]; fa.G[j] = G[li]; fa.part[j] = g->parts + 1LL * li * g->nparts_stride;
         fa.X[j] = X[li];
         fa.coef[j] = static_cast<float>(g->layers[li]->d.eta_local_scale * static_cast<double>(eta));
+        fa.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * g->layers[li]->d.weight_decay);
       }
       const double fb = static_cast<double>(numel) * nl * ((spec ? 16.0 : 8.0) + (g->g_bf16 ? 2.0 : 4.0));
       cd_status st = run(g, spec ? K_FORM_X : K_FORM, fb, (spec ? 5.0 : 3.0) * numel * nl, s,
@@ -629,6 +633,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
         const int li = sel[j];
         la.X[j] = X[li]; la.G[j] = G[li];
         la.coef[j] = static_cast<float>(g->layers[li]->d.eta_local_scale * static_cast<double>(eta));
+        la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * g->layers[li]->d.weight_decay);
       }
       const double lb = static_cast<double>(la.numel) * nl * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
       return run(g, K_LOCAL, lb, 2.0 * la.numel * nl, s,

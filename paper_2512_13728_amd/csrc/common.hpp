@@ -24,8 +24,9 @@ struct FormArgs {
   float* M[MAXB];                  // in: M_{t-1}; out: B_t
   const void* G[MAXB];             // fp32 or bf16
   double* part[MAXB];              // out: blocks_per_layer partial sums of B^2
-  float* X[MAXB];                  // with_x: the skip-branch update X -= coef G, fused
+  float* X[MAXB];                  // with_x: the skip-branch update X = xdecay X - coef G, fused
   float coef[MAXB];                // eta_local per layer (with_x only)
+  float xdecay[MAXB];              // 1 - eta * weight_decay per layer (with_x only)
 };
 hipError_t launch_form_buffer(const FormArgs& a, int nl, bool g_bf16, bool with_x, hipStream_t s);
 
@@ -36,6 +37,7 @@ struct LocalArgs {
   float* X[MAXB];
   const void* G[MAXB];
   float coef[MAXB];                // eta_local per layer
+  float xdecay[MAXB];              // 1 - eta * weight_decay per layer
 };
 hipError_t launch_local_update(const LocalArgs& a, int nl, bool g_bf16, hipStream_t s);
 
@@ -189,6 +191,9 @@ struct UpdatePlArgs {
   const void* G[MAXB];
   float gc[MAXB];
   int g_bf16;
+  // decoupled weight decay of X when no speculative update preceded (with one,
+  // X already carries it): X = xdecay X before the rank-r correction
+  float xdecay[MAXB];
 };
 hipError_t launch_update_planes(const UpdatePlArgs& a, int nl, int pieces, hipStream_t s);
 

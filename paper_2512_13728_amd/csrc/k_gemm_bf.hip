@@ -273,8 +273,10 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
     __syncthreads();
     float* Y = which == 0 ? u.M[l] : u.X[l];
     const float coef = which == 0 ? -u.one_minus_mu : -u.c;
-    // X only: first undo a speculative skip-branch update (X += gc G)
+    // X only: first undo a speculative skip-branch update (X += gc G; that
+    // update already applied the weight decay), else apply the decay
     const float gc = which == 0 ? 0.f : u.gc[l];
+    const float xd = which == 0 ? 1.f : u.xdecay[l];
     const void* const G = u.G[l];
     const bool gbf = u.g_bf16 != 0;
 #pragma unroll 4
@@ -293,6 +295,8 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
           const float4 g = load_g4(G, gbf, off);
           w.x = fmaf(gc, g.x, w.x); w.y = fmaf(gc, g.y, w.y);
           w.z = fmaf(gc, g.z, w.z); w.w = fmaf(gc, g.w, w.w);
+        } else {
+          w.x *= xd; w.y *= xd; w.z *= xd; w.w *= xd;
         }
         w.x = fmaf(coef, a.x, w.x); w.y = fmaf(coef, a.y, w.y);
         w.z = fmaf(coef, a.z, w.z); w.w = fmaf(coef, a.w, w.w);
@@ -304,6 +308,7 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
           if (gcol + c >= u.n) continue;
           float w = y[c];
           if (gc != 0.f) w = fmaf(gc, load_g1(G, gbf, off + c), w);
+          else w *= xd;
           y[c] = fmaf(coef, av[c], w);
         }
       }

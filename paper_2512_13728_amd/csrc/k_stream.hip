@@ -71,7 +71,8 @@ __device__ double block_sum(double v) {
 constexpr int VPT = FORM_CHUNK / (NTHREADS * 4);   // float4 groups per thread (4)
 
 // B = M + G in place, the block's partial sum of B^2, and (WX) the skip
-// branch's X -= coef G in the same pass over G.
+// branch's X = xdecay X - coef G in the same pass over G (xdecay = 1 - eta
+// weight_decay; 1 without weight decay, where the product is exact).
 template <bool BF16, bool WX>
 __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
   const int l = blockIdx.y;
@@ -79,6 +80,7 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
   const void* __restrict__ G = a.G[l];
   float* __restrict__ X = a.X[l];
   const float c = a.coef[l];
+  const float d = a.xdecay[l];
   const long long base = static_cast<long long>(blockIdx.x) * FORM_CHUNK;
   const long long end = min(base + FORM_CHUNK, a.numel);
   double acc = 0.0;
@@ -101,8 +103,8 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
       acc += sq(b.x); acc += sq(b.y); acc += sq(b.z); acc += sq(b.w);
       if constexpr (WX) {
         float4 y;
-        y.x = fmaf(-c, g[v].x, x[v].x); y.y = fmaf(-c, g[v].y, x[v].y);
-        y.z = fmaf(-c, g[v].z, x[v].z); y.w = fmaf(-c, g[v].w, x[v].w);
+        y.x = fmaf(-c, g[v].x, d * x[v].x); y.y = fmaf(-c, g[v].y, d * x[v].y);
+        y.z = fmaf(-c, g[v].z, d * x[v].z); y.w = fmaf(-c, g[v].w, d * x[v].w);
         st_nt(X + i, y);
       }
     }
@@ -118,8 +120,8 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
         if constexpr (WX) {
           const float4 xv = *reinterpret_cast<const float4*>(X + i);
           float4 y;
-          y.x = fmaf(-c, gv.x, xv.x); y.y = fmaf(-c, gv.y, xv.y);
-          y.z = fmaf(-c, gv.z, xv.z); y.w = fmaf(-c, gv.w, xv.w);
+          y.x = fmaf(-c, gv.x, d * xv.x); y.y = fmaf(-c, gv.y, d * xv.y);
+          y.z = fmaf(-c, gv.z, d * xv.z); y.w = fmaf(-c, gv.w, d * xv.w);
           *reinterpret_cast<float4*>(X + i) = y;
         }
       } else {
@@ -128,7 +130,7 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
           const float b = M[j] + gj;
           M[j] = b;
           acc += sq(b);
-          if constexpr (WX) X[j] = fmaf(-c, gj, X[j]);
+          if constexpr (WX) X[j] = fmaf(-c, gj, d * X[j]);
         }
       }
     }
@@ -143,6 +145,7 @@ __global__ __launch_bounds__(NTHREADS) void k_local_update(LocalArgs a) {
   float* __restrict__ X = a.X[l];
   const void* __restrict__ G = a.G[l];
   const float c = a.coef[l];
+  const float d = a.xdecay[l];
   const long long base = static_cast<long long>(blockIdx.x) * FORM_CHUNK;
   const long long end = min(base + FORM_CHUNK, a.numel);
   if (end - base == FORM_CHUNK) {
@@ -157,8 +160,8 @@ __global__ __launch_bounds__(NTHREADS) void k_local_update(LocalArgs a) {
     for (int v = 0; v < VPT; ++v) {
       const long long i = base + 4LL * (threadIdx.x + v * NTHREADS);
       float4 y;
-      y.x = fmaf(-c, g[v].x, x[v].x); y.y = fmaf(-c, g[v].y, x[v].y);
-      y.z = fmaf(-c, g[v].z, x[v].z); y.w = fmaf(-c, g[v].w, x[v].w);
+      y.x = fmaf(-c, g[v].x, d * x[v].x); y.y = fmaf(-c, g[v].y, d * x[v].y);
+      y.z = fmaf(-c, g[v].z, d * x[v].z); y.w = fmaf(-c, g[v].w, d * x[v].w);
       st_nt(X + i, y);
     }
   } else {
@@ -167,11 +170,11 @@ __global__ __launch_bounds__(NTHREADS) void k_local_update(LocalArgs a) {
         const float4 xv = *reinterpret_cast<const float4*>(X + i);
         const float4 gv = load_g4<BF16>(G, i);
         float4 y;
-        y.x = fmaf(-c, gv.x, xv.x); y.y = fmaf(-c, gv.y, xv.y);
-        y.z = fmaf(-c, gv.z, xv.z); y.w = fmaf(-c, gv.w, xv.w);
+        y.x = fmaf(-c, gv.x, d * xv.x); y.y = fmaf(-c, gv.y, d * xv.y);
+        y.z = fmaf(-c, gv.z, d * xv.z); y.w = fmaf(-c, gv.w, d * xv.w);
         *reinterpret_cast<float4*>(X + i) = y;
       } else {
-        for (long long j = i; j < end; ++j) X[j] = fmaf(-c, load_g1<BF16>(G, j), X[j]);
+        for (long long j = i; j < end; ++j) X[j] = fmaf(-c, load_g1<BF16>(G, j), d * X[j]);
       }
     }
   }

@@ -56,7 +56,7 @@ def qr_tol(kappa: float, c: float = 8.0) -> float:
 
 
 def step_and_compare(layer: cdl.Layer, G, M, X, Q, mu, eta, r, tau, policy, eps=1e-8,
-                     eta_local_scale=1.0):
+                     eta_local_scale=1.0, weight_decay=0.0):
     """Run one library step on (G, M, X, Q) and the oracle on the same inputs.
     Returns a dict of errors and both decisions.  M, X, Q are updated in place
     (the device state becomes the next step's input)."""
@@ -66,7 +66,8 @@ def step_and_compare(layer: cdl.Layer, G, M, X, Q, mu, eta, r, tau, policy, eps=
     torch.cuda.synchronize()
     OL = O.OracleLayer.from_arrays(M0, X0, Q0, prev_norm=prev0, step=step0)
     res = O.group_step([OL], [f64(G)], f32(mu), f32(eta), tau, eps=eps, policy=policy,
-                       eta_local=f32(eta) * eta_local_scale, with_kappa=True)
+                       eta_local=f32(eta) * eta_local_scale, with_kappa=True,
+                       weight_decay=weight_decay)
     out = dict(flag_gpu=flag, flag_oracle=res["flag"], rmmc_gpu=rm, rmmc_oracle=res["g"],
                status=st)
     out["err_M"] = rel(f64(M), OL.M)

@@ -39,7 +39,8 @@ def test_library_exports_every_declared_symbol(L):
     for name in header_functions():
         assert name in exported, name
         assert hasattr(L, name)
-    assert L.cd_abi_version() == 1
+    hdr = open(os.path.join(ROOT, "include", "curvadion.h")).read()
+    assert L.cd_abi_version() == int(re.search(r"#define CD_ABI_VERSION (\d+)", hdr).group(1))
 
 
 def _desc(**kw):
@@ -55,6 +56,7 @@ def _desc(**kw):
     (dict(grad_dtype=7), "dtype"), (dict(policy=9), "policy"),
     (dict(tau=float("nan")), "tau"), (dict(eps=-1.0), "eps"), (dict(eps=float("inf")), "eps"),
     (dict(eta_local_scale=-0.5), "eta_local_scale"), (dict(policy=cdl.POLICY_EVERY_H, H=0), "H"),
+    (dict(weight_decay=-0.01), "weight_decay"), (dict(weight_decay=float("nan")), "weight_decay"),
 ])
 def test_layer_create_rejects_bad_descriptors(L, kw, msg):
     h = ctypes.c_void_p(123)

@@ -272,6 +272,30 @@ def test_sync_after_skip_reverses_speculation(m, n, r, gd):
     assert flags == [True, False, True, False]
 
 
+@pytest.mark.parametrize("m,n,r,gd", [(256, 384, 32, "f32"), (300, 1000, 37, "bf16")])
+def test_weight_decay_every_branch(m, n, r, gd):
+    """Decoupled weight decay (lambda = 0.1) through every X-writing path:
+    a sync step, the stand-alone skip update, the fused speculative skip
+    update, and its reversal inside a sync step.  Decisions [sync, skip,
+    sync, skip], every step against the oracle with the same decay."""
+    w = S.small_workload(m, n, r, grad_dtype=gd, k=8)
+    M, X, Q = _state(w, 0)
+    tau, lam = 0.5, 0.1
+    L = cdl.Layer(m, n, r, grad_dtype=gd, policy=cdl.POLICY_RMMC, tau=tau, weight_decay=lam)
+    stream = S.GradientStream(w, 0, device="cpu")
+    flags = []
+    for t in range(4):
+        G = stream.next()
+        if t == 2:
+            G = (G.float() * 40.0).to(G.dtype)
+        d = step_and_compare(L, G.to(DEV), M, X, Q, 0.95, 0.01, r, tau, O.POLICY_RMMC,
+                             weight_decay=lam)
+        _print(f"decay {gd} t={t + 1}", d)
+        _check_step(d, tau, O.POLICY_RMMC, bf16=gd == "bf16")
+        flags.append(d["flag_gpu"])
+    assert flags == [True, False, True, False]
+
+
 def test_packed_pointers_match_lists():
     """Group.step with pointer arrays marshalled once (Group.pack) gives the
     bit-identical result of passing the tensor lists."""

@@ -290,13 +290,39 @@ def check_policies_match_algorithms(o):
     np.testing.assert_allclose(L.X, X0 - 0.05 * sum(grads), atol=1e-13)
 
 
+def check_weight_decay_decoupled(o):
+    """Decoupled weight decay: X <- (1 - eta lambda) X before either branch's
+    update, M and Q untouched.  A local step with G = 0 and a sync step with
+    B = 0 only scale X; with any input, turning the decay on moves X by exactly
+    (d - 1) X_{t-1} and nothing else."""
+    m, n, r, mu, eta, lam = 7, 5, 2, 0.9, 0.05, 0.3
+    d = 1.0 - eta * lam
+    rng = _rng(15)
+    M0, X0 = rng.standard_normal((m, n)), rng.standard_normal((m, n))
+    Q0 = o.orthogonalize(rng.standard_normal((n, r)))
+    L = o.OracleLayer.from_arrays(M0, X0, Q0, prev_norm=np.linalg.norm(M0))
+    res = o.group_step([L], [np.zeros((m, n))], mu, eta, 0.5, weight_decay=lam)
+    assert res["flag"] is False and np.array_equal(L.M, M0) and np.array_equal(L.X, d * X0)
+    L = o.OracleLayer.from_arrays(np.zeros((m, n)), X0, Q0)
+    o.group_step([L], [np.zeros((m, n))], mu, eta, 0.5, policy=o.POLICY_ALWAYS_SYNC, weight_decay=lam)
+    assert np.array_equal(L.X, d * X0) and not np.any(L.M)
+    G = rng.standard_normal((m, n))
+    for policy in (o.POLICY_ALWAYS_SYNC, o.POLICY_NEVER_SYNC):
+        A, Bl = o.OracleLayer.from_arrays(M0, X0, Q0), o.OracleLayer.from_arrays(M0, X0, Q0)
+        o.group_step([A], [G], mu, eta, 0.5, policy=policy)
+        o.group_step([Bl], [G], mu, eta, 0.5, policy=policy, weight_decay=lam)
+        assert np.array_equal(A.M, Bl.M) and np.array_equal(A.Q, Bl.Q)
+        np.testing.assert_allclose(Bl.X - A.X, (d - 1.0) * X0, rtol=0, atol=1e-14)
+
+
 ALL_CHECKS = [check_golden, check_orthogonalize_is_qr_factor,
               check_orthogonalize_matches_gram_schmidt, check_column_normalize,
               check_frobenius_norm, check_rmmc_definition, check_rmmc_zero_when_unchanged,
               check_rmmc_scale_invariance, check_power_iteration_converges,
               check_full_rank_momentum, check_rank_one_closed_form,
               check_local_branch_closed_form, check_gate,
-              check_first_step_syncs_and_global_max, check_policies_match_algorithms]
+              check_first_step_syncs_and_global_max, check_policies_match_algorithms,
+              check_weight_decay_decoupled]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda c: c.__name__)
@@ -344,30 +370,30 @@ def _m_r_from_ptilde(B, Q_prev):
     return Pt, P, B.T @ Pt
 
 
-def _m_sqrt_n_over_m(B, X, Q_prev, mu, eta):
+def _m_sqrt_n_over_m(B, X, Q_prev, mu, eta, x_decay=1.0):
     B = np.asarray(B, dtype=np.float64)
     m, n = B.shape
     Pt, P, R = OC.power_iteration(B, Q_prev)
     Q = OC.column_normalize(R)
-    return dict(M=B - (1 - mu) * (P @ R.T), X=X - eta * math.sqrt(n / m) * (P @ Q.T),
+    return dict(M=B - (1 - mu) * (P @ R.T), X=x_decay * X - eta * math.sqrt(n / m) * (P @ Q.T),
                 Q=Q, P=P, P_tilde=Pt, R=R)
 
 
-def _m_mu_instead_of_one_minus_mu(B, X, Q_prev, mu, eta):
+def _m_mu_instead_of_one_minus_mu(B, X, Q_prev, mu, eta, x_decay=1.0):
     B = np.asarray(B, dtype=np.float64)
     m, n = B.shape
     Pt, P, R = OC.power_iteration(B, Q_prev)
     Q = OC.column_normalize(R)
-    return dict(M=B - mu * (P @ R.T), X=X - eta * math.sqrt(m / n) * (P @ Q.T),
+    return dict(M=B - mu * (P @ R.T), X=x_decay * X - eta * math.sqrt(m / n) * (P @ Q.T),
                 Q=Q, P=P, P_tilde=Pt, R=R)
 
 
-def _m_x_uses_r(B, X, Q_prev, mu, eta):
+def _m_x_uses_r(B, X, Q_prev, mu, eta, x_decay=1.0):
     B = np.asarray(B, dtype=np.float64)
     m, n = B.shape
     Pt, P, R = OC.power_iteration(B, Q_prev)
     Q = OC.column_normalize(R)
-    return dict(M=B - (1 - mu) * (P @ R.T), X=X - eta * math.sqrt(m / n) * (P @ R.T),
+    return dict(M=B - (1 - mu) * (P @ R.T), X=x_decay * X - eta * math.sqrt(m / n) * (P @ R.T),
                 Q=Q, P=P, P_tilde=Pt, R=R)
 
 
@@ -398,13 +424,25 @@ def _m_gate_mean(rmmc_values, tau, policy=0, step=1, H=1):
     return g, bool(g > tau) if policy == 0 else OC.gate(rmmc_values, tau, policy, step, H)[1]
 
 
-def _m_local_no_g(B, G, X, eta_local):
-    return dict(M=np.asarray(B, dtype=np.float64).copy(), X=np.asarray(X, dtype=np.float64).copy())
+def _m_local_no_g(B, G, X, eta_local, x_decay=1.0):
+    return dict(M=np.asarray(B, dtype=np.float64).copy(), X=x_decay * np.asarray(X, dtype=np.float64))
 
 
-def _m_local_decays(B, G, X, eta_local):
+def _m_local_decays(B, G, X, eta_local, x_decay=1.0):
     return dict(M=0.95 * np.asarray(B, dtype=np.float64),
-                X=np.asarray(X, dtype=np.float64) - eta_local * np.asarray(G, dtype=np.float64))
+                X=x_decay * np.asarray(X, dtype=np.float64) - eta_local * np.asarray(G, dtype=np.float64))
+
+
+def _m_weight_decay_on_m(B, X, Q_prev, mu, eta, x_decay=1.0):
+    out = OC.sync_update(B, X, Q_prev, mu, eta, x_decay)
+    out["M"] = x_decay * out["M"]
+    return out
+
+
+def _m_weight_decay_after_update(B, X, Q_prev, mu, eta, x_decay=1.0):
+    out = OC.sync_update(B, X, Q_prev, mu, eta, 1.0)
+    out["X"] = x_decay * out["X"]
+    return out
 
 
 MUTANTS = {
@@ -421,6 +459,8 @@ MUTANTS = {
     "gate_mean": dict(gate=_m_gate_mean),
     "local_drops_G": dict(local_update=_m_local_no_g),
     "local_decays_M": dict(local_update=_m_local_decays),
+    "weight_decay_on_M": dict(sync_update=_m_weight_decay_on_m),
+    "weight_decay_after_update": dict(sync_update=_m_weight_decay_after_update),
 }
 
 
