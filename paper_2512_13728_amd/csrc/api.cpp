@@ -114,6 +114,16 @@ struct Timer {
     for (auto& r : recs) { pool.push_back(r.a); pool.push_back(r.b); }
     recs.clear();
   }
+  // create events ahead of time so that a timed region creates none
+  hipError_t reserve(size_t n) {
+    while (pool.size() < n) {
+      hipEvent_t e = nullptr;
+      const hipError_t err = hipEventCreate(&e);
+      if (err != hipSuccess) return err;
+      pool.push_back(e);
+    }
+    return hipSuccess;
+  }
   ~Timer() {
     release();
     for (hipEvent_t e : pool) (void)hipEventDestroy(e);
@@ -782,10 +792,9 @@ cd_status cd_group_destroy(cd_group* group) {
 cd_status cd_group_set_timing(cd_group* group, int enable) {
   if (!group) return fail(CD_EINVAL, "group is NULL");
   DeviceGuard dg(group->device);
-  if (!group->timer.recs.empty()) {
-    CD_HIP(hipEventSynchronize(group->timer.recs.back().b));
-    group->timer.release();
-  }
+  for (const auto& r : group->timer.recs) CD_HIP(hipEventSynchronize(r.b));
+  group->timer.release();
+  if (enable) CD_HIP(group->timer.reserve(2048));
   group->timer.on = enable != 0;
   return CD_OK;
 }
@@ -799,7 +808,7 @@ cd_status cd_group_kernel_times(cd_group* group, cd_kernel_time* out, int max_ki
     std::memset(&agg[k], 0, sizeof(agg[k]));
     std::snprintf(agg[k].name, sizeof(agg[k].name), "%s", kKindName[k]);
   }
-  if (!t.recs.empty()) CD_HIP(hipEventSynchronize(t.recs.back().b));
+  for (const auto& r : t.recs) CD_HIP(hipEventSynchronize(r.b));   // each launch's stream
   for (const auto& r : t.recs) {
     float ms = 0.f;
     CD_HIP(hipEventElapsedTime(&ms, r.a, r.b));
