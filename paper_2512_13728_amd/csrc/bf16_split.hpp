@@ -77,6 +77,38 @@ struct Stage {
   __device__ __forceinline__ void load(const float* __restrict__ src, int ld, bool kc, int r0, int nrows,
                                        int k0, int kend, int tid) {
     const bool vec = (ld & 3) == 0;
+    // interior stage (every row and k in range, 16-byte rows): no per-element
+    // checks; the condition is uniform over the workgroup
+    if (vec && r0 + ROWS <= nrows && k0 + BK16 <= kend) {
+      if (kc) {
+#pragma unroll
+        for (int i = 0; i < KC_PER; ++i) {
+          const int slot = tid + i * NT;
+          if (KC_SLOTS % NT == 0 || slot < KC_SLOTS) {
+            const int row = slot / (BK16 / 4), kq = (slot % (BK16 / 4)) * 4;
+            const float4 f =
+                *reinterpret_cast<const float4*>(src + static_cast<long long>(r0 + row) * ld + k0 + kq);
+            v[4 * i] = f.x; v[4 * i + 1] = f.y; v[4 * i + 2] = f.z; v[4 * i + 3] = f.w;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < T_PER; ++i) {
+          const int slot = tid + i * NT;
+          if (T_SLOTS % NT == 0 || slot < T_SLOTS) {
+            const int rq = (slot % (ROWS / 4)) * 4, kq = (slot / (ROWS / 4)) * 4;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+              const float4 f = *reinterpret_cast<const float4*>(
+                  src + static_cast<long long>(k0 + kq + kk) * ld + r0 + rq);
+              v[16 * i + 4 * kk + 0] = f.x; v[16 * i + 4 * kk + 1] = f.y;
+              v[16 * i + 4 * kk + 2] = f.z; v[16 * i + 4 * kk + 3] = f.w;
+            }
+          }
+        }
+      }
+      return;
+    }
     if (kc) {
 #pragma unroll
       for (int i = 0; i < KC_PER; ++i) {
