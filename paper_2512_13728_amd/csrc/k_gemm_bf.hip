@@ -11,7 +11,9 @@
 namespace cd {
 namespace {
 
-template <int S, int BM, int BN, bool A_KC, bool B_KC>
+// W64: the result is written as fp64 (one split only); a separate
+// instantiation, so the common fp32 kernel carries no second store path.
+template <int S, int BM, int BN, bool A_KC, bool B_KC, bool W64>
 __global__ __launch_bounds__(256, 2) void k_gemm_bf(GemmArgs g) {
   constexpr int WN_WAVES = (BN >= 64) ? 2 : 1;
   constexpr int WM_WAVES = 4 / WN_WAVES;
@@ -54,9 +56,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf(GemmArgs g) {
       sa.load(A, g.lda, A_KC, m0, g.M, k0 + BK16, ke, tid);
       sb.load(Bm, g.ldb, B_KC, n0, g.N, k0 + BK16, ke, tid);
     }
+    // The multiply phase runs at raised priority: the co-resident
+    // workgroup's staging work then fills the issue slots between the MFMAs.
     // A fragments stay in registers for the whole stage; B fragments are
     // fetched one 16-column block at a time (wide wave tiles would not hold
-    // them all)
+    // them all).
+    __builtin_amdgcn_s_setprio(1);
     bf16x8 a[TM][S];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -75,27 +80,37 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf(GemmArgs g) {
 #pragma unroll
           for (int i = 0; i < TM; ++i) acc[i][j] = mfma_bf16(a[i][p], b[sum - p], acc[i][j]);
     }
+    __builtin_amdgcn_s_setprio(0);
     __syncthreads();
   }
 
-  // fp32 split partials, or the result (fp32, or fp64 when out64)
-  float* C = static_cast<float*>(g.C[layer]) + static_cast<long long>(blockIdx.y) * g.split_stride;
-  double* C64 = static_cast<double*>(g.C[layer]);
-  const bool wide = g.out64 && g.splits == 1;
+  // fp32 split partials, or the result (fp32, or fp64 for W64).  The
+  // whole-tile test is uniform over the block, so the interior store loop is
+  // free of per-element branches.
+  auto put = [&](auto* C) {
+    const int rb = m0 + wm0 + 4 * (lane >> 4), cb = n0 + wn0 + (lane & 15);
+    if (m0 + BM <= g.M && n0 + BN <= g.N) {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = m0 + wm0 + i * 16 + 4 * (lane >> 4) + v;
-        const int col = n0 + wn0 + j * 16 + (lane & 15);
-        if (row < g.M && col < g.N) {
-          const long long o = static_cast<long long>(row) * g.ldc + col;
-          if (wide) C64[o] = acc[i][j][v];
-          else C[o] = acc[i][j][v];
-        }
-      }
+          for (int v = 0; v < 4; ++v)
+            C[static_cast<long long>(rb + i * 16 + v) * g.ldc + cb + j * 16] = acc[i][j][v];
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int row = rb + i * 16 + v, col = cb + j * 16;
+            if (row < g.M && col < g.N) C[static_cast<long long>(row) * g.ldc + col] = acc[i][j][v];
+          }
+    }
+  };
+  if constexpr (W64) put(static_cast<double*>(g.C[layer]));
+  else put(static_cast<float*>(g.C[layer]) + static_cast<long long>(blockIdx.y) * g.split_stride);
 }
 
 // bf16 planes of an fp32 matrix (rows x r): plane s holds the s-th split piece,
@@ -321,10 +336,21 @@ template <int S, int BM, int BN>
 hipError_t launch_bm(const GemmArgs& g, int nl, hipStream_t s) {
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   const dim3 grid(xcd_grid(tiles), g.splits, nl);
-  if (g.a_kc && !g.b_kc) hipLaunchKernelGGL((k_gemm_bf<S, BM, BN, true, false>), grid, dim3(256), 0, s, g);
-  else if (!g.a_kc && !g.b_kc) hipLaunchKernelGGL((k_gemm_bf<S, BM, BN, false, false>), grid, dim3(256), 0, s, g);
-  else if (g.a_kc && g.b_kc) hipLaunchKernelGGL((k_gemm_bf<S, BM, BN, true, true>), grid, dim3(256), 0, s, g);
-  else hipLaunchKernelGGL((k_gemm_bf<S, BM, BN, false, true>), grid, dim3(256), 0, s, g);
+  if (g.out64 && g.splits == 1) {
+    // fp64 results are only asked of the three-piece Gram (both operands
+    // transposed); other combinations are refused
+    if constexpr (S == 3) {
+      if (!g.a_kc && !g.b_kc) {
+        hipLaunchKernelGGL((k_gemm_bf<S, BM, BN, false, false, true>), grid, dim3(256), 0, s, g);
+        return hipGetLastError();
+      }
+    }
+    return hipErrorInvalidValue;
+  }
+  if (g.a_kc && !g.b_kc) hipLaunchKernelGGL((k_gemm_bf<S, BM, BN, true, false, false>), grid, dim3(256), 0, s, g);
+  else if (!g.a_kc && !g.b_kc) hipLaunchKernelGGL((k_gemm_bf<S, BM, BN, false, false, false>), grid, dim3(256), 0, s, g);
+  else if (g.a_kc && g.b_kc) hipLaunchKernelGGL((k_gemm_bf<S, BM, BN, true, true, false>), grid, dim3(256), 0, s, g);
+  else hipLaunchKernelGGL((k_gemm_bf<S, BM, BN, false, true, false>), grid, dim3(256), 0, s, g);
   return hipGetLastError();
 }
 
