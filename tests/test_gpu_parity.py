@@ -233,6 +233,47 @@ def test_group_mixed_shapes_rmmc_gate():
     assert any(flags) and not all(flags)
 
 
+def test_group_wider_than_one_launch():
+    """More layers of one shape than one launch takes (32): 40 of 96 x 160 and
+    3 of 130 x 70, so every stage runs in two chunks for the first shape and
+    the batched Cholesky covers 43 layers; sync and local steps against the
+    oracle, every layer checked."""
+    shapes = [(96, 160)] * 40 + [(130, 70)] * 3
+    r = 16
+    tau = 0.3
+    w = S.Workload("wide", tuple(shapes), r=r, grad_dtype="f32", steps=6, k=4, tau=tau, stream_id=93)
+    Ls = [cdl.Layer(m, n, r, tau=tau) for m, n in shapes]
+    Gp = cdl.Group(Ls)
+    st = [_state(w, i) for i in range(len(shapes))]
+    OLs = [O.OracleLayer.from_arrays(f64(s[0]), f64(s[1]), f64(s[2])) for s in st]
+    streams = [S.GradientStream(w, i, device="cpu") for i in range(len(shapes))]
+    flags = []
+    for t in range(w.steps):
+        Gs = [s.next() for s in streams]
+        g, flag, per, _ = Gp.step([G.to(DEV) for G in Gs], [s[0] for s in st], [s[1] for s in st],
+                                  [s[2] for s in st], w.mu, w.eta, r)
+        torch.cuda.synchronize()
+        res = O.group_step(OLs, [f64(G) for G in Gs], f32(w.mu), f32(w.eta), tau, with_kappa=True)
+        flags.append(flag)
+        assert flag == res["flag"]
+        assert abs(res["g"] - tau) / tau > 1e-4
+        assert len(per) == len(shapes)
+        for a, b in zip(per, res["rmmc"]):
+            assert_rmmc_close(a, b)
+        worst = {"M": 0.0, "X": 0.0, "Q": 0.0}
+        for i, (s, OL) in enumerate(zip(st, OLs)):
+            worst["M"] = max(worst["M"], rel(f64(s[0]), OL.M))
+            worst["X"] = max(worst["X"], rel(f64(s[1]), OL.X))
+            eq = rel(f64(s[2]), OL.Q)
+            assert eq <= (qr_tol(res["kappa"][i]) if flag else 0.0), (i, eq, res["kappa"][i] if flag else None)
+            worst["Q"] = max(worst["Q"], eq)
+            # teacher forcing: the oracle continues from the GPU state
+            OL.M, OL.X, OL.Q = f64(s[0]), f64(s[1]), f64(s[2])
+        print(f"step {t + 1} flag={flag} worst {worst}", flush=True)
+        assert worst["M"] <= 1e-5 and worst["X"] <= 1e-5
+    assert any(flags) and not all(flags)
+
+
 @pytest.mark.parametrize("policy", [O.POLICY_RMMC, O.POLICY_ALWAYS_SYNC])
 @pytest.mark.parametrize("m,n,r", [(512, 1536, 64), (2048, 512, 256), (300, 700, 37)])
 def test_bf16_gradient_steps(m, n, r, policy):
