@@ -146,8 +146,8 @@ __global__ __launch_bounds__(256) void k_split_planes(PlaneArgs a) {
 
 // M = B - (1 - mu) P R^T and X -= c P Q^T on a 128 x BN tile of the m x n
 // matrices; K = r.  P, R, Q come as bf16 planes (k_split_planes), so a stage
-// is plain 16-byte loads into LDS; the P planes of a 128-row panel are shared
-// by the BN-column tiles that the XCD-aware order keeps on one XCD.
+// is plain 16-byte loads into LDS; the XCD-aware grouped tile order keeps the
+// P, R and Q slices of the tiles in flight on one XCD inside its L2.
 constexpr int UBM = 128;
 typedef float nt4 __attribute__((ext_vector_type(4)));
 
@@ -184,10 +184,15 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
   __bf16* Ls = reinterpret_cast<__bf16*>(smem);   // [S][ROWS][BLD]
   const int l = blockIdx.z;
   const int tiles_n = (u.n + BN - 1) / BN;
-  const int ntiles = ((u.m + UBM - 1) / UBM) * tiles_n;
+  const int tiles_m = (u.m + UBM - 1) / UBM;
+  const int ntiles = tiles_m * tiles_n;
   const int t = xcd_tile(blockIdx.x, ntiles);
   if (t >= ntiles) return;
-  const int tm = t / tiles_n, tn = t - tm * tiles_n;
+  // bands of 16 tile rows, columns advancing inside a band: the tiles one XCD
+  // holds at a time share 16 P slices and a few R/Q slices, which stay in its
+  // L2 (half the fetched bytes of row-major order, and 6% less time)
+  int tm, tn;
+  grouped_tile(t, tiles_m, tiles_n, 16, tm, tn);
   const int m0 = tm * UBM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 64, wn0 = (wave & 1) * (BN / 2);
