@@ -376,3 +376,55 @@ def test_state_roundtrip_and_every_h_policy():
     assert s == 6 and p > 0
     L.set_state(123.0, 41)
     assert L.get_state() == (123.0, 41)
+
+
+def test_nonfinite_gradient_takes_the_local_branch():
+    """A NaN (and an Inf) in G: ‖B‖ is not finite, so RMMC is NaN, the gate's
+    NaN > tau is false and the local branch runs (the literal IEEE reading of
+    Alg. 2); the step reports CD_ENONFINITE, prev_norm becomes NaN and the next
+    steps stay local.  In a group the NaN of one layer makes the maximum NaN,
+    so every layer takes the local branch; the finite layer's outputs still
+    match the oracle exactly as a local step."""
+    m, n, r = 200, 300, 8
+    w = S.Workload("nan", ((m, n), (m, n)), r=r, grad_dtype="f32", steps=3, k=4, tau=0.5, stream_id=95)
+    st = [_state(w, i) for i in range(2)]
+    OLs = [O.OracleLayer.from_arrays(f64(s[0]), f64(s[1]), f64(s[2])) for s in st]
+    Ls = [cdl.Layer(m, n, r, tau=0.5) for _ in range(2)]
+    Gp = cdl.Group(Ls)
+    streams = [S.GradientStream(w, i, device="cpu") for i in range(2)]
+    for t in range(3):
+        Gs = [s.next() for s in streams]
+        if t >= 1:
+            Gs[1][3, 5] = float("nan")
+            Gs[1][7, 11] = float("inf")
+        Q0 = [s[2].clone() for s in st]
+        X0 = [f64(s[1]) for s in st]
+        g, flag, per, status = Gp.step([G.to(DEV) for G in Gs], [s[0] for s in st], [s[1] for s in st],
+                                       [s[2] for s in st], w.mu, w.eta, r)
+        torch.cuda.synchronize()
+        res = O.group_step(OLs, [f64(G) for G in Gs], f32(w.mu), f32(w.eta), 0.5)
+        assert flag == res["flag"]
+        if t == 0:
+            assert flag and status == cdl.CD_OK
+            for s, OL in zip(st, OLs):
+                OL.M, OL.X, OL.Q = f64(s[0]), f64(s[1]), f64(s[2])
+            continue
+        assert not flag and status == cdl.CD_ENONFINITE
+        assert math.isnan(g) and math.isnan(per[1]) and math.isfinite(per[0])
+        assert_rmmc_close(per[0], res["rmmc"][0])
+        for i in range(2):
+            assert torch.equal(st[i][2], Q0[i])                      # Q untouched
+            Mg, Xg = f64(st[i][0]), f64(st[i][1])
+            # NaN / Inf positions propagate exactly as in the oracle
+            assert np.array_equal(np.isnan(Mg), np.isnan(OLs[i].M))
+            assert np.array_equal(np.isnan(Xg), np.isnan(OLs[i].X))
+            assert np.array_equal(np.isinf(Xg), np.isinf(OLs[i].X))
+            fin = np.isfinite(OLs[i].M)
+            assert rel(Mg[fin], OLs[i].M[fin]) <= 1e-6
+            finx = np.isfinite(OLs[i].X)
+            scale = np.max(np.abs(X0[i][np.isfinite(X0[i])]))
+            assert np.max(np.abs(Xg[finx] - OLs[i].X[finx])) <= 1e-6 * scale
+            OLs[i].M, OLs[i].X = Mg, Xg
+    p, _ = Ls[1].get_state()
+    assert math.isnan(p)
+    assert math.isfinite(Ls[0].get_state()[0])
