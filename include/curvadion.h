@@ -30,6 +30,10 @@
  * after the RMMC gate, to read the decision back (the single device-to-host
  * crossing that stands in for the max all-reduce); it returns as soon as the
  * chosen branch is enqueued.  Read M, X, Q only after synchronising the stream.
+ * The sync branch's kernels may still run when the call returns, so the next
+ * step of the same layer or group must go to the same stream (or the caller
+ * orders the two streams); the library's workspace and the caller's M, X, Q
+ * are shared between consecutive steps.
  *
  * Errors: arguments are checked before anything is enqueued; CD_EINVAL leaves
  * every buffer and the layer state untouched.  No C++ exception crosses this
