@@ -428,3 +428,39 @@ def test_nonfinite_gradient_takes_the_local_branch():
     p, _ = Ls[1].get_state()
     assert math.isnan(p)
     assert math.isfinite(Ls[0].get_state()[0])
+
+
+def _random_cases(count, seed):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(count):
+        m, n = (int(x) for x in rng.integers(1, 700, size=2))
+        r = int(rng.integers(1, min(m, n, 96) + 1))
+        cases.append((m, n, r, "bf16" if rng.random() < 0.4 else "f32"))
+    # the degenerate corners: one row, one column, r = min(m, n)
+    cases += [(1, 257, 1, "f32"), (333, 1, 1, "bf16"), (40, 40, 40, "f32"), (65, 129, 65, "f32")]
+    return cases
+
+
+@pytest.mark.parametrize("m,n,r,gd", _random_cases(14, 2026))
+def test_random_shapes_sync_then_skip(m, n, r, gd):
+    """Seeded random shapes (every tile size hits a ragged tail somewhere):
+    an always-sync step, then two RMMC-gated steps, teacher-forced against
+    the oracle with the bounds of this module."""
+    w = S.small_workload(m, n, r, grad_dtype=gd, k=3, stream_id=97)
+    M, X, Q = _state(w, 0)
+    bf = gd == "bf16"
+    stream = S.GradientStream(w, 0, device="cpu")
+    L = cdl.Layer(m, n, r, grad_dtype=gd, policy=cdl.POLICY_ALWAYS_SYNC)
+    d = step_and_compare(L, stream.next().to(DEV), M, X, Q, 0.95, 0.01, r, 0.5, O.POLICY_ALWAYS_SYNC)
+    _print(f"random {m}x{n} r={r} {gd} sync", d)
+    _check_step(d, 0.5, O.POLICY_ALWAYS_SYNC, bf16=bf)
+    # the same state under the RMMC gate (a fresh layer: prev_norm = 0 syncs
+    # first, then the statistic decides)
+    L2 = cdl.Layer(m, n, r, grad_dtype=gd, policy=cdl.POLICY_RMMC, tau=0.5)
+    for t in range(2):
+        d = step_and_compare(L2, stream.next().to(DEV), M, X, Q, 0.95, 0.01, r, 0.5, O.POLICY_RMMC)
+        _print(f"random {m}x{n} r={r} {gd} rmmc t={t + 1}", d)
+        if math.isfinite(d["rmmc_oracle"]) and abs(d["rmmc_oracle"] - 0.5) / 0.5 <= (1e-2 if bf else 1e-4):
+            continue   # too close to tau to compare decisions
+        _check_step(d, 0.5, O.POLICY_RMMC, bf16=bf)
