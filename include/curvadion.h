@@ -36,9 +36,18 @@
  * are shared between consecutive steps.
  *
  * Errors: arguments are checked before anything is enqueued; CD_EINVAL leaves
- * every buffer and the layer state untouched.  No C++ exception crosses this
- * interface.  cd_last_error() returns a thread-local message for the last
- * failing call on the calling thread.
+ * every buffer and the layer state untouched.  The library cannot see the
+ * extent of a device buffer: a buffer smaller than the sizes above is read or
+ * written out of bounds.  A HIP failure (CD_EHIP) after the gate has run
+ * leaves the step half done (prev_norm and the step counter advanced, the
+ * branch partly enqueued); restore M, X, Q and the layer state from a
+ * checkpoint before going on.  No C++ exception crosses this interface.
+ * cd_last_error() returns a thread-local message for the last failing call on
+ * the calling thread.
+ *
+ * Threads: calls on different layers and groups may come from different host
+ * threads; one layer (or a group, or groups that share a layer) must not be
+ * stepped from two threads at once.
  */
 #ifndef CURVADION_H
 #define CURVADION_H
@@ -145,7 +154,7 @@ cd_status cd_layer_set_state(cd_layer* layer, double prev_norm, long long step);
  * its next step or cd_destroy.  For inspection and tests. */
 cd_status cd_layer_last_factors(const cd_layer* layer, const float** P, const float** R);
 
-/* Waits for the layer's last step to finish, then sets *flag = 1 if the last
+/* Waits for all work queued on the layer's device, then sets *flag = 1 if the last
  * sync step found P~ numerically rank deficient (a Cholesky pivot at or below
  * 1e-13 times the largest Gram diagonal): M, X and Q were still written, but
  * columns of P beyond the numerical rank are not orthonormal and their values

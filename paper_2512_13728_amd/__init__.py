@@ -16,7 +16,7 @@ from typing import Optional, Sequence, Tuple
 __all__ = [
     "LibraryNotBuilt", "CurvaDionError", "Layer", "Group", "lib", "library_path",
     "POLICY_RMMC", "POLICY_ALWAYS_SYNC", "POLICY_NEVER_SYNC", "POLICY_EVERY_H",
-    "F32", "BF16", "EXPORTED_SYMBOLS", "PointerArray",
+    "F32", "BF16", "EXPORTED_SYMBOLS", "PointerArray", "check_operand",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -114,6 +114,31 @@ def _ptr(t) -> int:
     return t.data_ptr()
 
 
+def check_operand(t, role: str, m: int, n: int, r: int, grad_dtype: str, device=None) -> None:
+    """Raise ValueError unless tensor `t` can be handed to the library as
+    operand `role` ("G", "M", "X" or "Q") of an m x n layer stepped at rank r:
+    G, M, X are m x n and Q is n x r, row-major contiguous, on a GPU (the
+    layer's, when `device` is given); M, X, Q fp32 and G of the layer's
+    gradient dtype.  The kernels index these buffers by (m, n, r) alone, so a
+    tensor of another shape or layout would be read out of bounds.  A plain
+    int is a raw device address and is passed through unchecked."""
+    if isinstance(t, int):
+        return
+    want_shape = (n, r) if role == "Q" else (m, n)
+    shape = tuple(t.shape)
+    if shape != want_shape:
+        raise ValueError(f"{role}: expected shape {want_shape}, got {shape}")
+    want_dtype = ("bfloat16" if grad_dtype == "bf16" else "float32") if role == "G" else "float32"
+    if str(t.dtype) != "torch." + want_dtype:
+        raise ValueError(f"{role}: expected {want_dtype}, got {str(t.dtype).replace('torch.', '')}")
+    if not t.is_contiguous():
+        raise ValueError(f"{role}: must be contiguous (row-major, leading dimension = columns)")
+    if t.device.type != "cuda":
+        raise ValueError(f"{role}: must be a GPU tensor, got device {t.device}")
+    if device is not None and t.device.index != device:
+        raise ValueError(f"{role}: on GPU {t.device.index}, the layer lives on GPU {device}")
+
+
 def _stream_handle(stream) -> Optional[int]:
     if stream is None:
         import torch
@@ -137,6 +162,12 @@ class Layer:
         self._h = h
         self.m, self.n, self.r_max = m, n, r_max
         self.grad_dtype = grad_dtype
+        import torch
+        self.device = torch.cuda.current_device()   # the device cd_layer_create used
+
+    def check(self, t, role: str, r: int) -> None:
+        """check_operand for this layer."""
+        check_operand(t, role, self.m, self.n, r, self.grad_dtype, self.device)
 
     @property
     def handle(self) -> ctypes.c_void_p:
@@ -146,6 +177,8 @@ class Layer:
              stream=None) -> Tuple[float, bool, int]:
         """One CurvaDion step; returns (rmmc, sync_flag, status)."""
         r = Q.shape[1] if r is None and hasattr(Q, "shape") else r
+        for t, role in ((G, "G"), (M, "M"), (X, "X"), (Q, "Q")):
+            self.check(t, role, r)
         res = Result()
         st = lib().cd_step(self._h, _ptr(G), _ptr(M), _ptr(X), _ptr(Q), mu, eta, r,
                            _stream_handle(stream), ctypes.byref(res))
@@ -190,6 +223,7 @@ class PointerArray:
     def __init__(self, array, keep):
         self.array = array
         self._keep = list(keep)
+        self._checked = set()      # (role, r) pairs the tensors were checked for
 
     def __len__(self):
         return len(self.array)
@@ -206,6 +240,12 @@ class Group:
         _check(lib().cd_group_create(arr, len(layers), ctypes.byref(h)))
         self._h = h
 
+    def _check_all(self, tensors, role: str, r: int) -> None:
+        if len(tensors) != len(self.layers):
+            raise ValueError(f"{role}: expected {len(self.layers)} tensors, got {len(tensors)}")
+        for L, t in zip(self.layers, tensors):
+            L.check(t, role, r)
+
     def pack(self, tensors) -> "PointerArray":
         """The device addresses of one tensor per layer, marshalled once: pass
         the result to step() in place of the list while those tensors live."""
@@ -218,10 +258,21 @@ class Group:
         """One step over every layer; returns (rmmc_max, sync_flag, rmmc_per_layer, status).
         G, M, X, Q are lists with one tensor (or address) per layer, or pack() results."""
         n = len(self.layers)
-        mk = lambda ts: ts.array if isinstance(ts, PointerArray) else (ctypes.c_void_p * n)(*[_ptr(t) for t in ts])
+
+        def mk(ts, role):
+            # a packed array is checked once per role and rank, a list on every call
+            if isinstance(ts, PointerArray):
+                if (role, r) not in ts._checked:
+                    self._check_all(ts._keep, role, r)
+                    ts._checked.add((role, r))
+                return ts.array
+            self._check_all(ts, role, r)
+            return (ctypes.c_void_p * n)(*[_ptr(t) for t in ts])
+
+        arrays = [mk(G, "G"), mk(M, "M"), mk(X, "X"), mk(Q, "Q")]
         per = (ctypes.c_double * n)()
         res = Result()
-        st = lib().cd_group_step(self._h, mk(G), mk(M), mk(X), mk(Q), mu, eta, r,
+        st = lib().cd_group_step(self._h, *arrays, mu, eta, r,
                                  _stream_handle(stream), per, ctypes.byref(res))
         _check(st, allow=(CD_OK, CD_ENONFINITE))
         return res.rmmc, bool(res.sync_flag), list(per), st

@@ -154,7 +154,6 @@ struct cd_layer {
   __bf16* planes = nullptr;     // bf16 split planes of P, R, Q for the update
   float* colnrm = nullptr;      // r_max column norms
   cd_group* self = nullptr;     // one-layer group used by cd_step
-  hipStream_t last_stream = nullptr;
   int last_r = 0;
 };
 
@@ -596,7 +595,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   CD_HIP(hipEventSynchronize(g->ev));
   const cd::GateOut* go = static_cast<const cd::GateOut*>(g->out_host);
   const double* rm = reinterpret_cast<const double*>(go + 1);
-  for (cd_layer* L : g->layers) { L->step += 1; L->last_stream = s; }
+  for (cd_layer* L : g->layers) L->step += 1;
   const long long step = g->layers[0]->step;
   bool sync = false;
   switch (g->policy) {
@@ -857,7 +856,9 @@ cd_status cd_layer_last_factors(const cd_layer* layer, const float** P, const fl
 cd_status cd_layer_rank_deficient(const cd_layer* layer, int* flag) {
   if (!layer || !flag) return fail(CD_EINVAL, "NULL argument");
   DeviceGuard dg(layer->device);
-  CD_HIP(hipStreamSynchronize(layer->last_stream));
+  // the whole device, not the last step's stream: the caller may have
+  // destroyed that stream since
+  CD_HIP(hipDeviceSynchronize());
   CD_HIP(hipMemcpy(flag, layer->rankdef, sizeof(int), hipMemcpyDeviceToHost));
   return CD_OK;
 }

@@ -110,3 +110,32 @@ def test_package_does_not_import_oracle():
             if f.endswith((".py", ".cpp", ".hip", ".hpp", ".h")):
                 text = open(os.path.join(dirpath, f), errors="replace").read()
                 assert "oracle" not in text.lower().replace("oracles", ""), f
+
+
+def test_operand_check_refuses_what_the_kernels_would_misread():
+    """The binding's operand check: the kernels index G, M, X (m x n) and Q
+    (n x r) by the sizes alone, so a wrong shape, dtype or layout is refused
+    before the library sees the pointer."""
+    import torch
+    m, n, r = 48, 40, 8
+    ok = dict(G=torch.zeros(m, n), M=torch.zeros(m, n), X=torch.zeros(m, n), Q=torch.zeros(n, r))
+    bad = [
+        ("M", torch.zeros(n, m), "shape"),                    # transposed shape
+        ("Q", torch.zeros(n, r + 1), "shape"),                # Q wider than the step's rank
+        ("X", torch.zeros(m, n, dtype=torch.float64), "float32"),
+        ("G", torch.zeros(m, n, dtype=torch.bfloat16), "float32"),   # fp32-gradient layer
+        ("M", torch.zeros(n, m).t(), "contiguous"),           # right shape, column-major
+        ("Q", torch.zeros(n, 2 * r)[:, :r], "contiguous"),    # a column slice
+        ("G", torch.zeros(m, n), "GPU"),                      # host memory
+    ]
+    for role, t, msg in bad:
+        with pytest.raises(ValueError, match=msg):
+            cdl.check_operand(t, role, m, n, r, "f32")
+    # raw addresses pass through unchecked (the C ABI's contract)
+    cdl.check_operand(0x1000, "M", m, n, r, "f32")
+    # every check before the device check passes for well-formed host tensors
+    for role, t in ok.items():
+        with pytest.raises(ValueError, match="GPU"):
+            cdl.check_operand(t, role, m, n, r, "f32")
+    with pytest.raises(ValueError, match="GPU"):
+        cdl.check_operand(torch.zeros(m, n, dtype=torch.bfloat16), "G", m, n, r, "bf16")

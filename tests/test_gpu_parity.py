@@ -364,6 +364,36 @@ def test_packed_pointers_match_lists():
         Gp.pack(M[:1])
 
 
+def test_wrong_operands_are_refused_before_any_work():
+    """A transposed, mistyped or wrongly-sized operand raises ValueError in the
+    binding; the layer's state (prev_norm, step counter) and every buffer stay
+    as they were, and a packed array is re-checked for a new rank."""
+    m, n, r = 96, 64, 8
+    w = S.small_workload(m, n, r)
+    L = cdl.Layer(m, n, r)
+    M, X, Q = _state(w, 0)
+    G = S.GradientStream(w, 0, device="cpu").next().to(DEV)
+    before = [t.clone() for t in (M, X, Q)]
+    bad = [dict(M=M.t()), dict(X=X.double()), dict(G=G.bfloat16()), dict(Q=Q[:, : r // 2]),
+           dict(G=G.cpu())]
+    for kw in bad:
+        args = dict(G=G, M=M, X=X, Q=Q)
+        args.update(kw)
+        with pytest.raises(ValueError):
+            L.step(args["G"], args["M"], args["X"], args["Q"], 0.95, 0.01, r)
+    torch.cuda.synchronize()
+    assert L.get_state() == (0.0, 0)
+    for a, b in zip(before, (M, X, Q)):
+        assert torch.equal(a, b)
+    Gp = cdl.Group([L])
+    pQ = Gp.pack([Q])
+    Gp.step([G], [M], [X], pQ, 0.95, 0.01, r)
+    with pytest.raises(ValueError, match="shape"):
+        Gp.step([G], [M], [X], pQ, 0.95, 0.01, r // 2)     # Q is n x r, not n x r/2
+    torch.cuda.synchronize()
+    assert L.get_state()[1] == 1
+
+
 def test_state_roundtrip_and_every_h_policy():
     m, n, r = 64, 64, 4
     L = cdl.Layer(m, n, r, policy=cdl.POLICY_EVERY_H, H=3)
