@@ -156,9 +156,11 @@ cd_status cd_layer_last_factors(const cd_layer* layer, const float** P, const fl
 
 /* Waits for all work queued on the layer's device, then sets *flag = 1 if the last
  * sync step found P~ numerically rank deficient (a Cholesky pivot at or below
- * 1e-13 times the largest Gram diagonal): M, X and Q were still written, but
- * columns of P beyond the numerical rank are not orthonormal and their values
- * are not unique.  *flag = 0 otherwise. */
+ * 1e-13 times the largest Gram diagonal).  M, X and Q were still written and P
+ * still has orthonormal columns: past the numerical rank it is completed with
+ * fixed pseudo-random directions orthonormalised against the other columns
+ * (as a Householder QR factor is completed), so those columns, and the
+ * matching columns of R and Q, are not unique.  *flag = 0 otherwise. */
 cd_status cd_layer_rank_deficient(const cd_layer* layer, int* flag);
 
 /* Kernel timing, for measurement.  While timing is on, every kernel launch of

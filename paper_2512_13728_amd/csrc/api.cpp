@@ -138,6 +138,7 @@ struct cd_layer {
   long long step = 0;
   double* prev = nullptr;       // device, 1 double
   int* rankdef = nullptr;       // device, 1 int
+  int* rowok = nullptr;         // device, r_max ints: rows of T whose pivot was not floored
   double* pa = nullptr;         // m x r_max fp64: P~
   float* pb = nullptr;          // m x r_max: P~ after the first CholQR pass
   float* Uf = nullptr;          // r_max^2: inverse Cholesky factor (fp32) for the bf16 apply
@@ -186,6 +187,7 @@ struct cd_group {
   int2* trsm_tiles = nullptr;           // (layer, 64-row tile of m) pairs
   int2* trtri_tiles = nullptr;          // (layer, 64-row tile of r_max) pairs
   int ntiles = 0, ntiles_r = 0;
+  int mmax = 0;                         // largest m of the layers
   Timer timer;
 };
 
@@ -193,7 +195,7 @@ namespace {
 
 void free_layer(cd_layer* L) {
   if (!L) return;
-  void* ptrs[] = {L->prev, L->rankdef, L->pa, L->pb, L->Uf, L->P, L->R, L->W, L->Dinv, L->floor_,
+  void* ptrs[] = {L->prev, L->rankdef, L->rowok, L->pa, L->pb, L->Uf, L->P, L->R, L->W, L->Dinv, L->floor_,
                   L->gram_part, L->split_part, L->colsq, L->colnrm, L->planes};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
@@ -253,10 +255,11 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
     cd_layer* L = layers[i];
     np[i] = static_cast<int>(blocks_for(1LL * L->d.m * L->d.n));
     pv[i] = L->prev;
-    ct[i] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef};
+    ct[i] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok};
     t0[i] = cd::TrsmTab{L->pa, L->pb, L->W, L->Dinv, L->d.m};
     t1[i] = cd::TrsmTab{nullptr, L->Uf, L->W, L->Dinv, L->d.r_max};
     t2[i] = cd::TrsmTab{L->pb, L->P, L->W, L->Dinv, L->d.m};
+    g->mmax = std::max(g->mmax, L->d.m);
     for (int rt = 0; rt < (L->d.m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) tiles.push_back(int2{i, rt});
     for (int rt = 0; rt < (L->d.r_max + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) rtiles.push_back(int2{i, rt});
   }
@@ -630,6 +633,14 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
         st = enqueue_factor(g, r, stage == 1 ? 0 : 1, s);
         if (st != CD_OK) return st;
       }
+      if (stage == 2) {
+        // P1 is complete for every layer: new directions for the columns of
+        // floored pass-0 pivots (layers without any return at once)
+        st = run(g, K_CHOL, 4.0 * g->L, 0.0, s, [&] {
+          return cd::launch_fill_dead(g->chol_tab, g->trsm_tab[0], g->L, g->mmax, r, s);
+        });
+        if (st != CD_OK) return st;
+      }
     }
     for (cd_layer* Ly : g->layers) Ly->last_r = r;
   } else if (!spec) {
@@ -692,6 +703,7 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = dalloc(&L->prev, 1);
     if (e == hipSuccess) e = dalloc(&L->rankdef, 1);
+    if (e == hipSuccess) e = dalloc(&L->rowok, static_cast<size_t>(rm));
     if (e == hipSuccess) e = dalloc(&L->pa, 1ULL * m * rm);
     if (e == hipSuccess) e = dalloc(&L->pb, 1ULL * m * rm);
     if (e == hipSuccess) e = dalloc(&L->Uf, 1ULL * rm * rm);

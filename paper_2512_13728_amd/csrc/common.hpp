@@ -121,6 +121,7 @@ struct CholTab {
   double* Dinv;                    // ceil(r / CHOL_BLOCK) blocks of 64 x 64
   double* floor_;                  // pivot floor of the current factorisation
   int* rankdef;                    // set to 1 when a pivot was raised to the floor
+  int* rowok;                      // r: 0 for the rows of floored pivots, else 1
 };
 // All CHOL_BLOCK steps for `nlayers` layers of rank r; `pass` 0 clears rankdef.
 hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s);
@@ -135,6 +136,10 @@ struct TrsmTab {
 };
 // tiles: one (layer, 64-row tile) pair per workgroup.  ident: Pin is the
 // identity (the result is T^{-1}); mlimit > 0 caps every layer's row count.
+// Between the CholQR passes: columns of P1 (TrsmTab::Pout, fp32 m x r) whose
+// pivot was floored get fixed pseudo-random directions (layers with
+// rankdef == 0 are left alone).  mmax: the largest m of the layers.
+hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, int mmax, int r, hipStream_t s);
 hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r, bool in64, bool out64,
                        hipStream_t s, bool ident = false, int mlimit = 0);
 

@@ -7,9 +7,11 @@
 //   chol_diag  (one wave per layer)  T_kk = chol(W_kk) in registers and its
 //              inverse D_k = T_kk^{-1}; the first block also sets the pivot
 //              floor max(1e-13 * max_i W_ii, 1e-60) (smaller or NaN pivots are raised to
-//              it and the layer is flagged rank deficient; the absolute floor
-//              keeps T^{-1} finite in fp32 when P~ is numerically zero)
-//   chol_panel X = D_k^T W[k, k+1:]: the k-th block row of T       (fp64 MFMA)
+//              it, the rest of their row of T is zero, and the layer is flagged
+//              rank deficient; the absolute floor keeps T^{-1} finite in fp32
+//              when P~ is numerically zero)
+//   chol_panel X = D_k^T W[k, k+1:]: the k-th block row of T, zero in the
+//              rows of floored pivots                              (fp64 MFMA)
 //   chol_trail W[k+1:, k+1:] -= X^T X, upper tiles only            (fp64 MFMA)
 // and the triangular solve, one launch per block column c:
 //   P[:, c] = (P~[:, c] - P[:, :c] T[:c, c]) D_c                   (fp64 MFMA)
@@ -25,15 +27,33 @@ constexpr int CB = CHOL_BLOCK;
 // (upper triangle; rows past the matrix padded with the identity) in
 // registers.  Right-looking Cholesky: at pivot p the lanes publish row p of
 // the updated block in LDS and every lane reads it back with uniform-address
-// loads (a broadcast), then updates its own column.  D = T^{-1} follows by
-// back substitution, lane c solving T d = e_c, with T read from LDS.  The
-// loops are unrolled so that the register arrays are indexed by constants.
+// loads (a broadcast), then updates its own column.  The register array is
+// shifted by one row per pivot inside the update (a[i] holds row p + i), so
+// the pivot row is always a[0] and every index is a constant while the pivot
+// loop itself stays rolled: the kernel is a few KB of code instead of a
+// fully unrolled 100 KB that the instruction cache cannot hold.
+//
+// A pivot at or below the floor is raised to it and the rest of its row of T
+// is set to zero (as is the row of the block row that k_chol_panel forms,
+// through rowok): the numerically dependent direction then adds nothing to
+// the trailing matrix.  Dividing its rounding-level residuals by the floor's
+// square root instead would subtract their squares from the next pivots,
+// which fall under the floor in turn, and the entries grow without bound.
+//
+// D = T^{-1} follows by back substitution, lane c solving T d = e_c from the
+// last row up, with T read from LDS and the unknowns shifted the same way;
+// the columns of floored pivots are stored as zero, so that P~ T^{-1} is
+// zero in those columns (k_fill_dead then gives them new directions).
 constexpr int TLD = CB + 1;   // padded row of T in LDS (column stores hit distinct banks)
+constexpr int TPAD = CB;      // leading doubles: back-substitution reads above row 0 stay in the array
 
-__global__ __launch_bounds__(64) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
                                                   int pass) {
-  __shared__ __attribute__((aligned(16))) double rowb[CB];
-  __shared__ double Ts[CB * TLD];   // Ts[j * TLD + i] = T[i][j]
+  __shared__ __attribute__((aligned(16))) double rowb[2 * CB];   // row p, then zeros
+  __shared__ double Tsb[TPAD + CB * TLD];
+  __shared__ double pinv[CB];                                     // 1 / T[p][p]
+  __shared__ int okb[CB];                                         // pivot p not floored
+  double* const Ts = Tsb + TPAD;   // Ts[j * TLD + i] = T[i][j]
   const CholTab t = tab[blockIdx.x];
   const int j = threadIdx.x;
   const long long ld = r;
@@ -52,50 +72,73 @@ __global__ __launch_bounds__(64) void k_chol_diag(const CholTab* __restrict__ ta
   } else {
     fl = *t.floor_;
   }
-  double a[CB];
+  double a[CB];   // a[i] = A[p + i][j] at pivot p
 #pragma unroll
   for (int i = 0; i < CB; ++i) {
     if (i < nb && j < nb) a[i] = i <= j ? t.W[(k0 + i) * ld + k0 + j] : 0.0;
     else a[i] = i == j ? 1.0 : 0.0;
   }
+  rowb[CB + j] = 0.0;
+  Tsb[j] = 0.0;
   bool def = false;
-#pragma unroll
+#pragma unroll 1
   for (int p = 0; p < CB; ++p) {
-    rowb[j] = a[p];
+    rowb[j] = a[0];
     __syncthreads();
     double d = rowb[p];
-    if (p < nb && !(d > fl)) { d = fl; def = true; }
+    const bool floored = p < nb && !(d > fl);   // uniform over the wave
+    if (floored) { d = fl; def = true; }
     const double piv = sqrt(d);
-    a[p] = (j == p) ? piv : a[p] / piv;   // row p of T (lanes j > p)
+    const double inv = 1.0 / piv;
+    // row p of T (zero left of the diagonal, and right of a floored pivot)
+    const double tp = j == p ? piv : (j > p && !floored ? a[0] * inv : 0.0);
+    Ts[j * TLD + p] = tp;
+    if (j == p) {
+      pinv[p] = inv;
+      okb[p] = floored ? 0 : 1;
+      if (p < nb) t.rowok[k0 + p] = floored ? 0 : 1;
+    }
     __syncthreads();
-    rowb[j] = a[p];
+    rowb[j] = tp;
     __syncthreads();
-    // rows below p: A[i][j] -= T[p][i] T[p][j]; lanes j < i only touch the
-    // (unused) lower triangle
+    // rows below p: A[p + i][j] -= T[p][p + i] T[p][j], shifted up one row;
+    // lanes j < p + i only touch the (unused) lower triangle.  The row is read
+    // whole before the update (one LDS round trip, not one per pair).
+    double rv[CB];
 #pragma unroll
-    for (int i = p + 1; i < CB; ++i) a[i] = fma(-rowb[i], a[p], a[i]);
+    for (int i = 1; i < CB; ++i) rv[i] = rowb[p + i];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 1; i < CB; ++i) a[i - 1] = fma(-rv[i], tp, a[i]);
+    a[CB - 1] = 0.0;
     __syncthreads();
   }
+  // f[k] = d[p - k] at step p; entries with k > p lie above row 0 and are
+  // never stored
+  double f[CB];
 #pragma unroll
-  for (int i = 0; i < CB; ++i) Ts[j * TLD + i] = a[i];
-  __syncthreads();
-  double e[CB];
-#pragma unroll
-  for (int i = 0; i < CB; ++i) e[i] = i == j ? 1.0 : 0.0;
-#pragma unroll
-  for (int p = CB - 1; p >= 0; --p) {
-    const double* col = Ts + p * TLD;   // column p of T: T[i][p] = col[i]
-    e[p] = e[p] / col[p];
-#pragma unroll
-    for (int i = 0; i < p; ++i) e[i] = fma(-col[i], e[p], e[i]);
-  }
+  for (int k = 0; k < CB; ++k) f[k] = k == CB - 1 - j ? 1.0 : 0.0;
   double* D = t.Dinv + static_cast<long long>(kb) * CB * CB;
+  // the column of a floored pivot is stored as zero: P~ T^{-1} then has a
+  // zero column there and the other columns are unchanged (with row p of T
+  // zero right of the diagonal, column j != p of T^{-1} is zero in row p)
+  const bool cin = j < nb && okb[j];
+#pragma unroll 1
+  for (int p = CB - 1; p >= 0; --p) {
+    const double x = f[0] * pinv[p];
+    D[p * CB + j] = (p < nb && cin) ? x : 0.0;
+    const double* col = Ts + p * TLD + p;   // col[-k] = T[p - k][p]
+    double cv[CB];
 #pragma unroll
-  for (int i = 0; i < CB; ++i) {
-    const bool in = i < nb && j < nb;
-    if (in && i <= j) t.W[(k0 + i) * ld + k0 + j] = a[i];
-    D[i * CB + j] = in ? e[i] : 0.0;
+    for (int k = 1; k < CB; ++k) cv[k] = col[-k];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int k = 1; k < CB; ++k) f[k - 1] = fma(-cv[k], x, f[k]);
+    f[CB - 1] = 0.0;
   }
+#pragma unroll 4
+  for (int i = 0; i < nb; ++i)
+    if (j < nb && i <= j) t.W[(k0 + i) * ld + k0 + j] = Ts[j * TLD + i];
   if (j == 0 && def) *t.rankdef = 1;
 }
 
@@ -158,7 +201,8 @@ __global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ 
       for (int v = 0; v < 4; ++v) {
         const int row = wm0 + i * 16 + Mfma<double>::out_row(lane, v);
         const int col = j0 + wn0 + j * 16 + (lane & 15);
-        if (row < nb && col < r) t.W[static_cast<long long>(k0 + row) * r + col] = T.acc[i][j][v];
+        if (row < nb && col < r)
+          t.W[static_cast<long long>(k0 + row) * r + col] = t.rowok[k0 + row] ? T.acc[i][j][v] : 0.0;
       }
 }
 
@@ -195,6 +239,41 @@ __global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ 
         const int col = j0 + wn0 + j * 16 + (lane & 15);
         if (row < r && col < r) t.W[static_cast<long long>(row) * r + col] -= T.acc[i][j][v];
       }
+}
+
+// Completion of the basis past the numerical rank, between the two CholQR
+// passes: a column of P1 = P~ T^{-1} whose pivot was floored is zero; it is
+// replaced by a fixed pseudo-random vector of unit expected norm, which the
+// second pass orthonormalises against the other columns.  P then has
+// orthonormal columns, as a Householder QR factor of a rank-deficient P~
+// does, and the columns of Q that belong to them are not lost for the later
+// steps.  Workgroups of layers whose factorisation floored no pivot return
+// at once.
+constexpr int FILL_ROWS = 64;
+
+__device__ __forceinline__ float fill_value(unsigned i, unsigned j, float scale) {
+  // integer hash of (row, column): xorshift-multiply rounds
+  unsigned h = i * 0x9E3779B1u + j * 0x85EBCA77u + 0x27D4EB2Fu;
+  h ^= h >> 16; h *= 0x7FEB352Du;
+  h ^= h >> 15; h *= 0x846CA68Bu;
+  h ^= h >> 16;
+  return scale * (static_cast<float>(h >> 8) * (2.0f / 16777216.0f) - 1.0f);   // uniform in [-1, 1)
+}
+
+__global__ __launch_bounds__(256) void k_fill_dead(const CholTab* __restrict__ ct,
+                                                   const TrsmTab* __restrict__ tt, int r) {
+  const CholTab c = ct[blockIdx.y];
+  if (*c.rankdef == 0) return;
+  const TrsmTab t = tt[blockIdx.y];
+  float* P1 = static_cast<float*>(t.Pout);
+  const int i0 = blockIdx.x * FILL_ROWS;
+  const int rows = min(FILL_ROWS, t.m - i0);
+  if (rows <= 0) return;
+  const float scale = sqrtf(3.0f / static_cast<float>(t.m));
+  for (int e = threadIdx.x; e < rows * r; e += 256) {
+    const int i = i0 + e / r, j = e % r;
+    if (!c.rowok[j]) P1[static_cast<long long>(i) * r + j] = fill_value(i, j, scale);
+  }
 }
 
 // Block column c of P = P~ T^{-1}; one 64-row tile of one layer per workgroup.
@@ -320,6 +399,12 @@ hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hip
     hipLaunchKernelGGL(k_chol_panel, dim3(nt, nlayers), dim3(256), 0, s, tab, r, kb);
     hipLaunchKernelGGL(k_chol_trail, dim3(nt * (nt + 1) / 2, nlayers), dim3(256), 0, s, tab, r, kb);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, int mmax, int r, hipStream_t s) {
+  if (nlayers <= 0 || mmax <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_dead, dim3((mmax + FILL_ROWS - 1) / FILL_ROWS, nlayers), dim3(256), 0, s, ct, tt, r);
   return hipGetLastError();
 }
 

@@ -177,6 +177,82 @@ def test_zero_buffer_sync_is_defined():
     assert L.rank_deficient()
 
 
+@pytest.mark.parametrize("gd", ["f32", "bf16"])
+def test_rank_deficient_buffer_is_completed(gd):
+    """B of exact rank k < r (only its first k rows are nonzero, in either
+    gradient dtype) on a sync step: P~ = B Q has rank k, so r - k pass-0
+    Cholesky pivots fall under the floor, in both 64-column blocks of r = 96.
+    Like a Householder QR factor, P still has orthonormal columns: the first k
+    are unique and match the oracle (as do those of R and Q, and M = mu B),
+    the others complete the basis orthogonally to B's column space (so the
+    matching columns of R are zero to rounding).  The completion is not
+    unique (the oracle's Q_j there is normalised rounding noise), so X is held
+    to the unique part plus at most eta sqrt(m/n) per such column.
+
+    R = B^T P lies in B's k-dimensional row space, and so does every column of
+    Q after this step (in the oracle too), so a full-rank gradient next still
+    meets a rank-k P~.  The completed P makes R = B^T P full rank again in that
+    step, and the step after it is a plain full-rank step that matches the
+    oracle: no column of Q is lost for good."""
+    from gpu_util import device_to_numpy
+    m, n, r, k = 192, 160, 96, 5
+    gen = torch.Generator().manual_seed(77)
+    G = torch.zeros(m, n)
+    G[:k] = torch.randn(k, n, generator=gen) * 0.01
+    G = G.to(torch.bfloat16 if gd == "bf16" else torch.float32)
+    X0 = torch.randn(m, n, generator=gen) * 0.02
+    Q0 = torch.linalg.qr(torch.randn(n, r, generator=gen, dtype=torch.float64))[0].float()
+    M = torch.zeros(m, n, device=DEV)
+    X, Q = X0.to(DEV), Q0.to(DEV).contiguous()
+    mu, eta = 0.95, 0.01
+    L = cdl.Layer(m, n, r, grad_dtype=gd, policy=cdl.POLICY_ALWAYS_SYNC)
+    _, flag, _ = L.step(G.to(DEV), M, X, Q, mu, eta, r)
+    torch.cuda.synchronize()
+    assert flag and L.rank_deficient()
+    Pa, Ra = L.last_factors()
+    Pg = device_to_numpy(Pa, (m, r)).astype(np.float64)
+    Rg = device_to_numpy(Ra, (n, r)).astype(np.float64)
+    Mg, Xg, Qg = f64(M), f64(X), f64(Q)
+    for name, a in (("P", Pg), ("R", Rg), ("M", Mg), ("X", Xg), ("Q", Qg)):
+        assert np.isfinite(a).all(), name
+    B = f64(G.float())
+    _, Po, Ro = O.power_iteration(B, f64(Q0))
+    Qo = O.column_normalize(Ro)
+    tol = 2e-2 if gd == "bf16" else 1e-5
+    orth = np.abs(Pg.T @ Pg - np.eye(r)).max()
+    print(f"rank-deficient {gd}: P {rel(Pg[:, :k], Po[:, :k]):.3g} R {rel(Rg[:, :k], Ro[:, :k]):.3g} "
+          f"Q {rel(Qg[:, :k], Qo[:, :k]):.3g} M {rel(Mg, mu * B):.3g} |P^T P - I| {orth:.3g} "
+          f"|R_j|/|R| past the rank {np.linalg.norm(Rg[:, k:]) / np.linalg.norm(Rg):.3g}", flush=True)
+    assert rel(Pg[:, :k], Po[:, :k]) <= tol
+    assert rel(Rg[:, :k], Ro[:, :k]) <= tol
+    assert rel(Qg[:, :k], Qo[:, :k]) <= tol
+    assert rel(Mg, mu * B) <= tol
+    assert orth <= (1e-4 if gd == "bf16" else 1e-5)
+    assert np.linalg.norm(Rg[:, k:]) <= (1e-3 if gd == "bf16" else 1e-5) * np.linalg.norm(Rg)
+    c = eta * math.sqrt(m / n)
+    X_unique = f64(X0) - c * Po[:, :k] @ Qo[:, :k].T
+    extra = np.linalg.norm(Xg - X_unique)
+    assert extra <= c * (r - k) * 1.01 + tol * np.linalg.norm(Xg), extra
+    sv = np.linalg.svd(Qo, compute_uv=False)
+    assert int(np.sum(sv > 1e-8 * sv[0])) == k      # the oracle's Q spans B's row space only
+    for t in range(2):
+        Gt = (torch.randn(m, n, generator=gen) * 0.01).to(G.dtype).to(DEV)
+        if t == 0:
+            L.step(Gt, M, X, Q, mu, eta, r)
+            torch.cuda.synchronize()
+            for name, a in (("M", M), ("X", X), ("Q", Q)):
+                assert torch.isfinite(a).all(), name
+            P2 = device_to_numpy(L.last_factors()[0], (m, r)).astype(np.float64)
+            assert np.abs(P2.T @ P2 - np.eye(r)).max() <= (1e-4 if gd == "bf16" else 1e-5)
+            sv = np.linalg.svd(f64(Q), compute_uv=False)
+            assert int(np.sum(sv > 1e-8 * sv[0])) == r   # full rank again
+        else:
+            d = step_and_compare(L, Gt, M, X, Q, mu, eta, r, 0.5, O.POLICY_ALWAYS_SYNC)
+            _print(f"two steps after the deficiency {gd}", d)
+            assert not L.rank_deficient()
+            _check_step(d, 0.5, O.POLICY_ALWAYS_SYNC, bf16=gd == "bf16")
+
+
 @pytest.mark.parametrize("tau,policy", [(0.5, O.POLICY_RMMC), (0.1, O.POLICY_RMMC),
                                         (0.5, O.POLICY_ALWAYS_SYNC)])
 def test_single256_trajectory(tau, policy):
