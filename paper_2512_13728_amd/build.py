@@ -44,8 +44,28 @@ def _compile(src: str) -> str:
     return obj
 
 
+C_CLIENT_SRC = os.path.join(ROOT, "tests", "c", "cd_c_step.c")
+C_CLIENT = os.path.join(ROOT, "tests", "c", "cd_c_step")
+
+
+def build_c_client() -> str:
+    """The plain-C99 client of the ABI that the tests run (gcc, no HIP
+    compiler: the header and the HIP runtime's C API only)."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    cmd = ["gcc", "-std=c99", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(ROOT, "include"), "-I", os.path.join(rocm, "include"), C_CLIENT_SRC,
+           "-L", HERE, "-lcurvadion", "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN/../../paper_2512_13728_amd", "-Wl,-rpath," + os.path.join(rocm, "lib"),
+           "-o", C_CLIENT]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"C client build failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+    return C_CLIENT
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every source and link the shared library; returns its path."""
+    """Compile every source and link the shared library (then the C client
+    the tests use); returns the library's path."""
     os.makedirs(OBJDIR, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
@@ -55,8 +75,9 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
     os.replace(tmp, LIB)
+    build_c_client()
     if verbose:
-        print("built", LIB)
+        print("built", LIB, "and", C_CLIENT)
     return LIB
 
 

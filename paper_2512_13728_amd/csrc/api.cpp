@@ -356,11 +356,11 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   // pieces > 0: fp32 operands on the bf16 MFMA with `pieces`-way splits
   auto gemm = [&](int tkind, double flops, double bytes, cd::GemmKind kind, int Mr, int Nr, int K,
                   bool a_kc, int lda, bool b_kc, int ldb, bool upper, auto Aof, auto Bof, auto Cof,
-                  auto Pof, int pieces = 0, bool bf_out64 = false) -> cd_status {
+                  auto Pof, int pieces = 0, bool bf_out64 = false, bool b_upper = false) -> cd_status {
     const bool acc64 = pieces == 0 && cd::gemm_acc64(kind);
     cd::GemmArgs ga{};
     ga.M = Mr; ga.N = Nr; ga.K = K; ga.lda = lda; ga.ldb = ldb; ga.ldc = Nr;
-    ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper; ga.out64 = bf_out64;
+    ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper; ga.out64 = bf_out64; ga.b_upper = b_upper;
     ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk, pieces, upper);
     ga.split_stride = 1LL * Mr * Nr;
     if (ga.splits > 1) {
@@ -438,8 +438,10 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
     if (!fast) return CD_OK;   // fp32 layers: fp64 triangular solves in enqueue_factor
     auto In = [&](int j) { return static_cast<const void*>(stage == 2 ? lay(j)->P : lay(j)->pb); };
     auto Out = [&](int j) { return static_cast<void*>(stage == 2 ? lay(j)->pb : lay(j)->P); };
+    // U is upper triangular: output column j takes k <= j only
     return gemm(K_APPLY_BF, mr * r, 12.0 * mr + 4.0 * rr, cd::GemmKind::F32, m, r, r, true, r, false, r,
-                false, In, [&](int j) { return static_cast<const void*>(lay(j)->Uf); }, Out, part, 3);
+                false, In, [&](int j) { return static_cast<const void*>(lay(j)->Uf); }, Out, part, 3,
+                false, true);
   }
   if (stage == 3) {
     auto In = [&](int j) { return static_cast<const void*>(lay(j)->pb); };
@@ -447,7 +449,9 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
       return gemm(K_GRAM, mr * (r + 1), 4.0 * mr + 8.0 * rr, cd::GemmKind::F64_FROM_F32, r, r, m, false,
                   r, false, r, true, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); },
                   [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
-    // pass-1 Gram matrix of the nearly orthonormal P1, fp32-accurate, into fp64 W
+    // pass-1 Gram matrix of the nearly orthonormal P1, fp32-accurate, into
+    // fp64 W (all tiles: with upper tiles only the launch takes more K-splits
+    // and their reduction costs more than the skipped tiles save)
     return gemm(K_GRAM_BF, 2.0 * mr * r, 4.0 * mr + 8.0 * rr, cd::GemmKind::F32, r, r, m, false, r, false,
                 r, false, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); }, part, 3, true);
   }

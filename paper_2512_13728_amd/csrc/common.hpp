@@ -82,8 +82,10 @@ struct GemmArgs {
   int kchunk;                      // K per split (multiple of GBK)
   long long split_stride;          // elements between split partials
   bool a_kc, b_kc;
-  bool upper_only;                 // skip tiles strictly below the diagonal
+  bool upper_only;                 // fp32/fp64 kernels: skip tiles strictly below the diagonal
   bool out64;                      // bf16-split kernels: write the result as fp64
+  bool b_upper;                    // bf16-split kernels: B is upper triangular (K x N),
+                                   // so output column j needs k <= j only
   const void* A[MAXB];
   const void* B[MAXB];
   void* C[MAXB];                   // result (splits == 1) or partials (splits > 1)

@@ -30,7 +30,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf(GemmArgs g) {
   const int tm = t / tiles_n, tn = t - tm * tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
   const int kb = blockIdx.y * g.kchunk;
-  const int ke = min(g.K, kb + g.kchunk);
+  // an upper-triangular B contributes nothing past the tile's last column; a
+  // split left with an empty range still writes its (zero) partial
+  const int ke = g.b_upper ? min(min(g.K, kb + g.kchunk), n0 + BN) : min(g.K, kb + g.kchunk);
   const float* A = static_cast<const float*>(g.A[layer]);
   const float* Bm = static_cast<const float*>(g.B[layer]);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;

@@ -139,3 +139,17 @@ def test_operand_check_refuses_what_the_kernels_would_misread():
             cdl.check_operand(t, role, m, n, r, "f32")
     with pytest.raises(ValueError, match="GPU"):
         cdl.check_operand(torch.zeros(m, n, dtype=torch.bfloat16), "G", m, n, r, "bf16")
+
+
+def test_plain_c_client_check():
+    """A C99 program that includes only include/curvadion.h (and the HIP
+    runtime's C API) compiles with gcc -Werror, links against the library and
+    sees CD_EINVAL with a message for invalid descriptors and NULL arguments."""
+    from paper_2512_13728_amd import build
+    exe = build.C_CLIENT
+    if not os.path.exists(exe):
+        build.build_c_client()
+    out = subprocess.run([exe, "check"], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stderr
+    assert "check ok" in out.stdout
+    assert out.stdout.count("CD_EINVAL") == 8
