@@ -152,3 +152,83 @@ def test_sweep4096_ranks(r):
     w1 = S.Workload(f"sweep4096-r{r}", w.shapes, r=r, grad_dtype="f32", steps=2, k=w.k, sigma=w.sigma,
                     tau=w.tau, stream_id=w.stream_id)
     _group_case(w1, O.POLICY_ALWAYS_SYNC, 2, log=f"sweep r={r}")
+
+
+def _chunked_norm(M, G, rows=2048):
+    """||M + float(G)||_F in fp64, a row block at a time."""
+    s = 0.0
+    for i in range(0, M.shape[0], rows):
+        s += float(torch.sum((M[i:i + rows] + G[i:i + rows].float()).double() ** 2))
+    return math.sqrt(s)
+
+
+def test_layer_past_32bit_indexing():
+    """One bf16-gradient layer of 46341 x 46341 = 2^31 + 4633 elements (about
+    25 GB with M, X and G), r = 8: every kernel's element index exceeds 32 bits.
+    The oracle cannot run at this size, so the check uses what holds at any
+    size.  Step 1 syncs (prev_norm starts at 0): ||B|| against a chunked fp64
+    norm; P orthonormal and spanning P~ = B Q0 with an upper-triangular,
+    positive-diagonal factor P^T P~; R = B^T P on sampled columns; M =
+    B - (1 - mu) P R^T and X = X0 - eta sqrt(m/n) P Q^T on sampled rows;
+    Q = ColumnNormalize(R).  Step 2 takes the local branch: M = M + G and
+    X = X - eta G bit-exact on sampled rows, RMMC from the two fp64 norms."""
+    m = n = 46341
+    r, mu, eta = 8, 0.95, 0.01
+    assert m * n > 2 ** 31
+    gen = torch.Generator(device=DEV).manual_seed(4242)
+    M = torch.randn(m, n, generator=gen, device=DEV) * 0.02
+    X = torch.randn(m, n, generator=gen, device=DEV) * 0.02
+    G = (torch.randn(m, n, generator=gen, device=DEV) * 0.01).to(torch.bfloat16)
+    Q0 = torch.linalg.qr(torch.randn(n, r, generator=gen, device=DEV, dtype=torch.float64))[0]
+    Q = Q0.float().contiguous()
+    rows = [0, 1, m // 2, m - 2, m - 1]
+    cols = [0, 3, n // 2, n - 1]
+    B_rows = (M[rows] + G[rows].float()).double()
+    B_cols = (M[:, cols] + G[:, cols].float()).double()
+    X0_rows = X[rows].double()
+    nb1 = _chunked_norm(M, G)
+    # P~ = B Q0 in fp64, a row block at a time
+    Pt = torch.empty(m, r, dtype=torch.float64, device=DEV)
+    for i in range(0, m, 2048):
+        Pt[i:i + 2048] = (M[i:i + 2048] + G[i:i + 2048].float()).double() @ Q0
+    L = cdl.Layer(m, n, r, grad_dtype="bf16", tau=1e6)
+    print(f"32-bit-index case: {m} x {n} bf16, r = {r}", flush=True)
+    rm, flag, st = L.step(G, M, X, Q, mu, eta, r)
+    torch.cuda.synchronize()
+    assert flag and st == cdl.CD_OK
+    prev1, step1 = L.get_state()
+    assert step1 == 1 and abs(prev1 - nb1) <= 1e-6 * nb1, (prev1, nb1)
+    Pa, Ra = L.last_factors()
+    P = torch.from_numpy(device_to_numpy(Pa, (m, r))).double().to(DEV)
+    R = torch.from_numpy(device_to_numpy(Ra, (n, r))).double().to(DEV)
+    assert float((P.T @ P - torch.eye(r, device=DEV, dtype=torch.float64)).abs().max()) <= 1e-4
+    C = P.T @ Pt                                   # the R-factor of P~ = P C
+    assert float(torch.linalg.norm(Pt - P @ C) / torch.linalg.norm(Pt)) <= 1e-3
+    assert float(torch.tril(C, -1).abs().max()) <= 1e-3 * float(C.abs().max())
+    assert bool((torch.diagonal(C) > 0).all())
+    # R = B^T P on sampled columns (two-piece bf16 products: about 2^-16)
+    R_cols = B_cols.T @ P
+    assert float(torch.linalg.norm(R[cols] - R_cols) / torch.linalg.norm(R_cols)) <= 1e-3
+    # M and X on sampled rows (plain bf16 products in the rank-r update)
+    Qd = Q.double()
+    colnrm = torch.linalg.norm(R, dim=0)
+    assert float((Qd - R / colnrm).abs().max()) <= 1e-5
+    # (the corrections are about 1e-4 of B and X here, so they are compared
+    # themselves, at the bound of plain bf16 products)
+    dM = (1 - f32(mu)) * P[rows] @ R.T
+    dX = f32(eta) * math.sqrt(m / n) * P[rows] @ Qd.T
+    assert float(torch.linalg.norm((B_rows - M[rows].double()) - dM) / torch.linalg.norm(dM)) <= 2e-2
+    assert float(torch.linalg.norm((X0_rows - X[rows].double()) - dX) / torch.linalg.norm(dX)) <= 2e-2
+    # step 2: the local branch, bit-exact on sampled rows
+    M1_rows, X1_rows = M[rows].clone(), X[rows].clone()
+    G.copy_((torch.randn(m, n, generator=gen, device=DEV) * 0.01).to(torch.bfloat16))
+    nb2 = _chunked_norm(M, G)
+    rm2, flag2, _ = L.step(G, M, X, Q, mu, eta, r)
+    torch.cuda.synchronize()
+    assert not flag2
+    assert abs(rm2 - abs(nb2 - prev1) / (prev1 + 1e-8)) <= 1e-5 * rm2 + 1e-9
+    Gr = G[rows].float()
+    assert torch.equal(M[rows], M1_rows + Gr)
+    # X - eta G is one fused multiply-add in fp32: within 1 ulp of the fp64 value
+    Xref = X1_rows.double() - f32(eta) * Gr.double()
+    assert bool(((X[rows].double() - Xref).abs() <= Xref.abs() * 2.0 ** -23 + 1e-30).all())
