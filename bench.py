@@ -464,6 +464,21 @@ def main():
             branches[name]["compulsory_bytes"] = nbytes
             branches[name]["algorithmic_GBps"] = gbps
             branches[name]["frac_of_hbm_peak"] = gbps / PEAK_HBM_GBPS
+    if branches["sync"]["count"]:
+        # a sync step is MFMA work: the method's flops (P~ = BQ, R = B^T P and
+        # the rank-r M and X corrections, 8 r flops per parameter, plus two
+        # CholQR passes of 2 m r^2 + r^3 / 3 each) against the fp32 MFMA peak an
+        # fp32 implementation would be bound by; and the MFMA time the executed
+        # products (every bf16 piece product, fp64 where used) need at their
+        # peaks, as a fraction of the step
+        t_sync = branches["sync"]["median_ms"] * 1e-3
+        alg = sum(8.0 * w.r * m * n + 2.0 * (2.0 * m * w.r ** 2 + w.r ** 3 / 3.0) for m, n in w.shapes)
+        busy = sum(mult * kt[k]["flops"] / n_sync / (PEAK_TFLOPS[prec] * 1e12)
+                   for k in kt for bound, prec, mult in [KIND_BOUND.get(k, ("hbm", None, 1))]
+                   if bound == "mfma")
+        branches["sync"].update(algorithmic_flops=alg, algorithmic_TFLOPs=alg / t_sync / 1e12,
+                                frac_of_fp32_mfma_peak=alg / t_sync / 1e12 / PEAK_TFLOPS["f32"],
+                                mfma_busy_frac=busy / t_sync)
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -25,15 +25,20 @@
  * P~/P/R panels, Gram and factor matrices, partial sums) and the per-layer
  * prev_norm; both live until cd_destroy.
  *
- * Ordering: all work is enqueued on the HIP stream passed to a step call
+ * Ordering: all work is ordered on the HIP stream passed to a step call
  * (NULL = the default stream).  A step blocks the calling host thread once,
  * after the RMMC gate, to read the decision back (the single device-to-host
  * crossing that stands in for the max all-reduce); it returns as soon as the
- * chosen branch is enqueued.  Read M, X, Q only after synchronising the stream.
- * The sync branch's kernels may still run when the call returns, so the next
- * step of the same layer or group must go to the same stream (or the caller
- * orders the two streams); the library's workspace and the caller's M, X, Q
- * are shared between consecutive steps.
+ * chosen branch is enqueued.  In a group with layers of several shapes (or
+ * more than 32 layers of one shape) the sync branch runs each batch of layers
+ * of one shape on its own stream: the caller's stream and up to three streams
+ * the group owns (default priority), which wait for the caller's stream before
+ * they start and which the caller's stream waits for before anything enqueued
+ * after the step; the caller sees one ordered stream either way.  Read M, X, Q
+ * only after synchronising the stream.  The sync branch's kernels may still
+ * run when the call returns, so the next step of the same layer or group must
+ * go to the same stream (or the caller orders the two streams); the library's
+ * workspace and the caller's M, X, Q are shared between consecutive steps.
  *
  * Errors: arguments are checked before anything is enqueued; CD_EINVAL leaves
  * every buffer and the layer state untouched.  The library cannot see the

@@ -6,8 +6,11 @@
 //   2. gate kernel: fixed-order norms, RMMC_l, prev_norm update, max, flag
 //   3. one device-to-host copy of {max, flag, RMMC_l}: the decision point that
 //      stands in for the max all-reduce at one worker
-//   4. sync branch, per shape class: P~ = B Q; CholQR twice (fp64 Gram,
-//      Cholesky + inverse, apply); R = B^T P; ColumnNormalize; M/X update.
+//   4. sync branch, per unit (up to MAXB layers of one shape), each unit's
+//      whole pipeline on one stream and up to four units at a time: P~ = B Q;
+//      CholQR twice (fp64 Gram, Cholesky + inverse, apply); R = B^T P;
+//      ColumnNormalize; M/X update.  The latency-bound factorisation of one
+//      unit overlaps the GEMMs of the others.
 //      local branch: X -= eta_local G (M already holds B).
 // Layers of equal (m, n) share every launch (up to MAXB per launch).
 #include <hip/hip_runtime.h>
@@ -163,6 +166,18 @@ struct ShapeClass {
   std::vector<int> idx;  // positions in the group
 };
 
+// A batch of at most MAXB layers of one shape: the sync branch enqueues a
+// unit's whole pipeline on one stream.  Its layers occupy the contiguous
+// range [off, off + sel.size()) of the group's factor tables, and its tile
+// lists index the layers relative to `off`.
+struct Unit {
+  int sc;                // shape class
+  std::vector<int> sel;  // positions in the group
+  int off;               // first factor-table entry
+  int toff, nt;          // its (layer, 64-row tile of m) pairs in trsm_tiles
+  int rtoff, nrt;        // its (layer, 64-row tile of r_max) pairs in trtri_tiles
+};
+
 struct cd_group {
   std::vector<cd_layer*> layers;
   std::vector<ShapeClass> shapes;
@@ -182,12 +197,19 @@ struct cd_group {
   cd::GateOut* out_dev = nullptr;
   void* out_host = nullptr;     // pinned
   hipEvent_t ev = nullptr;
-  cd::CholTab* chol_tab = nullptr;      // [L] static workspace pointers
+  std::vector<Unit> units;
+  cd::CholTab* chol_tab = nullptr;      // [L] static workspace pointers, in unit order
   cd::TrsmTab* trsm_tab[3] = {nullptr, nullptr, nullptr};  // P1 = P~ T^-1; U = T^-1; P = P1 T^-1
-  int2* trsm_tiles = nullptr;           // (layer, 64-row tile of m) pairs
-  int2* trtri_tiles = nullptr;          // (layer, 64-row tile of r_max) pairs
-  int ntiles = 0, ntiles_r = 0;
-  int mmax = 0;                         // largest m of the layers
+  int2* trsm_tiles = nullptr;           // per unit: (layer in the unit, 64-row tile of m) pairs
+  int2* trtri_tiles = nullptr;          // per unit: (layer in the unit, 64-row tile of r_max) pairs
+  // groups of several units: the sync branch runs unit u on stream
+  // stream_of(u) (the caller's stream or one of these, default priority),
+  // forked from and joined back to the caller's stream
+  static constexpr int NSIDE = 3;
+  int nside = 0;
+  hipStream_t side[NSIDE] = {nullptr, nullptr, nullptr};
+  hipEvent_t fork_ev = nullptr;
+  hipEvent_t join_ev[NSIDE] = {nullptr, nullptr, nullptr};
   Timer timer;
 };
 
@@ -218,6 +240,11 @@ void free_group(cd_group* g) {
   if (g->trsm_tab[2]) (void)hipFree(g->trsm_tab[2]);
   if (g->trsm_tiles) (void)hipFree(g->trsm_tiles);
   if (g->trtri_tiles) (void)hipFree(g->trtri_tiles);
+  for (int i = 0; i < cd_group::NSIDE; ++i) {
+    if (g->side[i]) (void)hipStreamDestroy(g->side[i]);
+    if (g->join_ev[i]) (void)hipEventDestroy(g->join_ev[i]);
+  }
+  if (g->fork_ev) (void)hipEventDestroy(g->fork_ev);
   delete g;
 }
 
@@ -252,19 +279,37 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   std::vector<cd::TrsmTab> t0(n), t1(n), t2(n);
   std::vector<int2> tiles, rtiles;
   for (int i = 0; i < n; ++i) {
-    cd_layer* L = layers[i];
-    np[i] = static_cast<int>(blocks_for(1LL * L->d.m * L->d.n));
-    pv[i] = L->prev;
-    ct[i] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok};
-    t0[i] = cd::TrsmTab{L->pa, L->pb, L->W, L->Dinv, L->d.m};
-    t1[i] = cd::TrsmTab{nullptr, L->Uf, L->W, L->Dinv, L->d.r_max};
-    t2[i] = cd::TrsmTab{L->pb, L->P, L->W, L->Dinv, L->d.m};
-    g->mmax = std::max(g->mmax, L->d.m);
-    for (int rt = 0; rt < (L->d.m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) tiles.push_back(int2{i, rt});
-    for (int rt = 0; rt < (L->d.r_max + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) rtiles.push_back(int2{i, rt});
+    np[i] = static_cast<int>(blocks_for(1LL * layers[i]->d.m * layers[i]->d.n));
+    pv[i] = layers[i]->prev;
   }
-  g->ntiles = static_cast<int>(tiles.size());
-  g->ntiles_r = static_cast<int>(rtiles.size());
+  // units (chunks of at most MAXB layers of one shape) and their factor tables
+  int off = 0;
+  for (int c = 0; c < static_cast<int>(g->shapes.size()); ++c) {
+    const ShapeClass& sc = g->shapes[c];
+    for (size_t c0 = 0; c0 < sc.idx.size(); c0 += cd::MAXB) {
+      Unit u;
+      u.sc = c;
+      u.sel.assign(sc.idx.begin() + c0, sc.idx.begin() + std::min(sc.idx.size(), c0 + cd::MAXB));
+      u.off = off;
+      u.toff = static_cast<int>(tiles.size());
+      u.rtoff = static_cast<int>(rtiles.size());
+      for (int j = 0; j < static_cast<int>(u.sel.size()); ++j) {
+        cd_layer* L = layers[u.sel[j]];
+        const int k = off + j;
+        ct[k] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok};
+        t0[k] = cd::TrsmTab{L->pa, L->pb, L->W, L->Dinv, L->d.m};
+        t1[k] = cd::TrsmTab{nullptr, L->Uf, L->W, L->Dinv, L->d.r_max};
+        t2[k] = cd::TrsmTab{L->pb, L->P, L->W, L->Dinv, L->d.m};
+        for (int rt = 0; rt < (L->d.m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) tiles.push_back(int2{j, rt});
+        for (int rt = 0; rt < (L->d.r_max + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt)
+          rtiles.push_back(int2{j, rt});
+      }
+      u.nt = static_cast<int>(tiles.size()) - u.toff;
+      u.nrt = static_cast<int>(rtiles.size()) - u.rtoff;
+      off += static_cast<int>(u.sel.size());
+      g->units.push_back(std::move(u));
+    }
+  }
   hipError_t e = hipSuccess;
   if (e == hipSuccess) e = dalloc(&g->parts, static_cast<size_t>(n) * g->nparts_stride);
   if (e == hipSuccess) e = dalloc(&g->nparts, n);
@@ -292,6 +337,14 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
     e = hipMemcpy(g->trtri_tiles, rtiles.data(), sizeof(int2) * rtiles.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess)
     e = hipMemcpy(g->trsm_tiles, tiles.data(), sizeof(int2) * tiles.size(), hipMemcpyHostToDevice);
+  if (g->units.size() > 1) {
+    g->nside = std::min(static_cast<int>(g->units.size()) - 1, cd_group::NSIDE);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&g->fork_ev, hipEventDisableTiming);
+    for (int i = 0; i < g->nside && e == hipSuccess; ++i) {
+      e = hipStreamCreateWithFlags(&g->side[i], hipStreamNonBlocking);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&g->join_ev[i], hipEventDisableTiming);
+    }
+  }
   if (e != hipSuccess) {
     free_group(g);
     return fail(e == hipErrorOutOfMemory ? CD_ENOMEM : CD_EHIP, "group setup: %s",
@@ -510,25 +563,27 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
 // Between the stages of CholQR pass `pass`, over every layer: Cholesky of each
 // W, then either the fp64 triangular solve (fp32 layers: P1 = P~ T^-1, then
 // P = P1 T^-1) or the inverse U = T^-1 in fp32 for the bf16 x 6 apply.
-cd_status enqueue_factor(cd_group* g, int r, int pass, hipStream_t s) {
-  const double L = g->L, rr = 1.0 * r * r;
+cd_status enqueue_factor(cd_group* g, const Unit& u, int r, int pass, hipStream_t s) {
+  const int nl = static_cast<int>(u.sel.size());
+  const double L = nl, rr = 1.0 * r * r;
+  const cd::CholTab* ct = g->chol_tab + u.off;
   cd_status st = run(g, K_CHOL, 16.0 * rr * L, (1.0 / 3.0) * rr * r * L, s,
-                     [&] { return cd::launch_cholesky(g->chol_tab, g->L, r, pass, s); });
+                     [&] { return cd::launch_cholesky(ct, nl, r, pass, s); });
   if (st != CD_OK) return st;
   if (!g->g_bf16) {
     double flops = 0, bytes = 0;
-    for (const cd_layer* Ly : g->layers) {
-      const double mr = 1.0 * Ly->d.m * r;
+    for (int li : u.sel) {
+      const double mr = 1.0 * g->layers[li]->d.m * r;
       flops += mr * r;
       bytes += (pass == 0 ? 8.0 : 4.0) * mr + 4.0 * mr + 4.0 * rr;
     }
     return run(g, K_TRSM, bytes, flops, s, [&] {
-      return cd::launch_trsm(g->trsm_tab[pass == 0 ? 0 : 2], g->trsm_tiles, g->ntiles, r, pass == 0,
-                             false, s);
+      return cd::launch_trsm(g->trsm_tab[pass == 0 ? 0 : 2] + u.off, g->trsm_tiles + u.toff, u.nt, r,
+                             pass == 0, false, s);
     });
   }
   return run(g, K_TRTRI, 12.0 * rr * L, rr * r / 3.0 * L, s, [&] {
-    return cd::launch_trsm(g->trsm_tab[1], g->trtri_tiles, g->ntiles_r, r, true, false, s, true, r);
+    return cd::launch_trsm(g->trsm_tab[1] + u.off, g->trtri_tiles + u.rtoff, u.nrt, r, true, false, s, true, r);
   });
 }
 
@@ -616,54 +671,67 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   if (rmmc_per_layer) std::memcpy(rmmc_per_layer, rm, sizeof(double) * g->L);
 
   // 4. branch
-  auto for_chunks = [&](auto&& fn) -> cd_status {
-    for (const ShapeClass& sc : g->shapes) {
-      for (size_t c0 = 0; c0 < sc.idx.size(); c0 += cd::MAXB) {
-        const int nl = static_cast<int>(std::min<size_t>(cd::MAXB, sc.idx.size() - c0));
-        std::vector<int> sel(sc.idx.begin() + c0, sc.idx.begin() + c0 + nl);
-        cd_status st = fn(sc, sel);
+  if (sync) {
+    // Each unit's pipeline in stage order on its own stream: the first unit
+    // on the caller's stream, the others on the group's side streams, forked
+    // from the caller's stream here and joined back to it below.  Units are
+    // independent (no workspace is shared between layers), so the results do
+    // not depend on how their kernels interleave.
+    const int nu = static_cast<int>(g->units.size());
+    auto stream_of = [&](int u) -> hipStream_t {
+      const int k = u % (g->nside + 1);
+      return k == 0 ? s : g->side[k - 1];
+    };
+    if (g->nside > 0) {
+      CD_HIP(hipEventRecord(g->fork_ev, s));
+      for (int i = 0; i < g->nside; ++i) CD_HIP(hipStreamWaitEvent(g->side[i], g->fork_ev, 0));
+    }
+    for (int stage = 0; stage < 6; ++stage) {
+      for (int ui = 0; ui < nu; ++ui) {
+        const Unit& u = g->units[ui];
+        const hipStream_t su = stream_of(ui);
+        cd_status st = enqueue_sync(g, g->shapes[u.sc], u.sel, G, spec ? eta : 0.0f, M, X, Q, mu, eta, r,
+                                    stage, su);
         if (st != CD_OK) return st;
+        if (stage == 1 || stage == 3) {
+          st = enqueue_factor(g, u, r, stage == 1 ? 0 : 1, su);
+          if (st != CD_OK) return st;
+        }
+        if (stage == 2) {
+          // P1 is complete for the unit: new directions for the columns of
+          // floored pass-0 pivots (layers without any return at once)
+          const int nl = static_cast<int>(u.sel.size());
+          const int mu_rows = g->shapes[u.sc].m;
+          st = run(g, K_CHOL, 4.0 * nl, 0.0, su, [&] {
+            return cd::launch_fill_dead(g->chol_tab + u.off, g->trsm_tab[0] + u.off, nl, mu_rows, r, su);
+          });
+          if (st != CD_OK) return st;
+        }
       }
     }
-    return CD_OK;
-  };
-  if (sync) {
-    for (int stage = 0; stage < 6; ++stage) {
-      cd_status st = for_chunks([&](const ShapeClass& sc, const std::vector<int>& sel) {
-        return enqueue_sync(g, sc, sel, G, spec ? eta : 0.0f, M, X, Q, mu, eta, r, stage, s);
-      });
-      if (st != CD_OK) return st;
-      if (stage == 1 || stage == 3) {
-        st = enqueue_factor(g, r, stage == 1 ? 0 : 1, s);
-        if (st != CD_OK) return st;
-      }
-      if (stage == 2) {
-        // P1 is complete for every layer: new directions for the columns of
-        // floored pass-0 pivots (layers without any return at once)
-        st = run(g, K_CHOL, 4.0 * g->L, 0.0, s, [&] {
-          return cd::launch_fill_dead(g->chol_tab, g->trsm_tab[0], g->L, g->mmax, r, s);
-        });
-        if (st != CD_OK) return st;
-      }
+    for (int i = 0; i < g->nside; ++i) {
+      CD_HIP(hipEventRecord(g->join_ev[i], g->side[i]));
+      CD_HIP(hipStreamWaitEvent(s, g->join_ev[i], 0));
     }
     for (cd_layer* Ly : g->layers) Ly->last_r = r;
   } else if (!spec) {
-    cd_status st = for_chunks([&](const ShapeClass& sc, const std::vector<int>& sel) -> cd_status {
-      const int nl = static_cast<int>(sel.size());
+    for (const Unit& u : g->units) {
+      const ShapeClass& sc = g->shapes[u.sc];
+      const int nl = static_cast<int>(u.sel.size());
       cd::LocalArgs la{};
       la.numel = 1LL * sc.m * sc.n;
       la.blocks_per_layer = static_cast<int>(blocks_for(la.numel));
       for (int j = 0; j < nl; ++j) {
-        const int li = sel[j];
+        const int li = u.sel[j];
         la.X[j] = X[li]; la.G[j] = G[li];
         la.coef[j] = static_cast<float>(g->layers[li]->d.eta_local_scale * static_cast<double>(eta));
         la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * g->layers[li]->d.weight_decay);
       }
       const double lb = static_cast<double>(la.numel) * nl * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
-      return run(g, K_LOCAL, lb, 2.0 * la.numel * nl, s,
-                 [&] { return cd::launch_local_update(la, nl, g->g_bf16, s); });
-    });
-    if (st != CD_OK) return st;
+      cd_status st = run(g, K_LOCAL, lb, 2.0 * la.numel * nl, s,
+                         [&] { return cd::launch_local_update(la, nl, g->g_bf16, s); });
+      if (st != CD_OK) return st;
+    }
   }
   g->predict_skip = !sync;
   if (out) { out->rmmc = gmax; out->sync_flag = sync ? 1 : 0; }
