@@ -137,7 +137,10 @@ def summarize_trace(d: str, bench_json: str, out: str):
              f"#   rocprofv3 --kernel-trace --stats -f csv -d {d} -o bench -- python3 bench.py > {bench_json}",
              f"#   python3 bench.py --summarize-trace {d} {bench_json} {out}",
              "# calls include the warmup steps; torch kernels (input generation, state reset)",
-             f"# are left out below: {other_ns / 1e6:.1f} ms in total.", "",
+             f"# are left out below: {other_ns / 1e6:.1f} ms in total.",
+             "# sync-step kernels of different shape batches run concurrently (up to four",
+             "# streams): their durations overlap and do not add up to the step time; the",
+             "# skip-step kernels (form_buffer, gate) run alone.", "",
              f"{'kernel':64s} {'calls':>6s} {'avg_us':>10s} {'total_ms':>10s}"]
     for r in sorted(ours, key=lambda r: -float(r["TotalDurationNs"])):
         lines.append(f"{_kernel_name(r['Name'])[:64]:64s} {int(r['Calls']):6d} "
@@ -371,8 +374,9 @@ def main():
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
     # addresses marshalled once (the state tensors and every resident gradient set)
-    pM, pX, pQ = group.pack(M), group.pack(X), group.pack(Q)
-    pG = [group.pack(gs) for gs in grads]
+    # (and checked against the layers here, outside the timed steps)
+    pM, pX, pQ = group.pack(M, "M"), group.pack(X, "X"), group.pack(Q, "Q", w.r)
+    pG = [group.pack(gs, "G") for gs in grads]
     flags, rmmcs = [], []
     group.set_timing(True)
     if streamed:
@@ -383,7 +387,7 @@ def main():
               for _ in range(K)]
         wall = 0.0
         for t in range(K):
-            G = pG[0] if t == 0 else group.pack([st.next() for st in streams])
+            G = pG[0] if t == 0 else group.pack([st.next() for st in streams], "G")
             if t == 0:
                 for st in streams:
                     st.next()

@@ -246,13 +246,23 @@ class Group:
         for L, t in zip(self.layers, tensors):
             L.check(t, role, r)
 
-    def pack(self, tensors) -> "PointerArray":
+    def pack(self, tensors, role: Optional[str] = None, r: Optional[int] = None) -> "PointerArray":
         """The device addresses of one tensor per layer, marshalled once: pass
-        the result to step() in place of the list while those tensors live."""
+        the result to step() in place of the list while those tensors live.
+        With `role` ("G", "M", "X" or "Q"; Q also takes its rank r, by default
+        its column count) the tensors are checked here, once; otherwise on the
+        first step() that uses the array."""
         n = len(self.layers)
         if len(tensors) != n:
             raise ValueError(f"expected {n} tensors, got {len(tensors)}")
-        return PointerArray((ctypes.c_void_p * n)(*[_ptr(t) for t in tensors]), tensors)
+        pa = PointerArray((ctypes.c_void_p * n)(*[_ptr(t) for t in tensors]), tensors)
+        if role is not None:
+            if role == "Q" and r is None:
+                r = next((t.shape[1] for t in tensors if not isinstance(t, int)), None)
+            key = r if role == "Q" else None
+            self._check_all(tensors, role, r if r is not None else 1)
+            pa._checked.add((role, key))
+        return pa
 
     def step(self, G, M, X, Q, mu: float, eta: float, r: int, stream=None):
         """One step over every layer; returns (rmmc_max, sync_flag, rmmc_per_layer, status).
@@ -260,11 +270,12 @@ class Group:
         n = len(self.layers)
 
         def mk(ts, role):
-            # a packed array is checked once per role and rank, a list on every call
+            # a packed array is checked once (per rank, for Q), a list on every call
             if isinstance(ts, PointerArray):
-                if (role, r) not in ts._checked:
+                key = (role, r if role == "Q" else None)
+                if key not in ts._checked:
                     self._check_all(ts._keep, role, r)
-                    ts._checked.add((role, r))
+                    ts._checked.add(key)
                 return ts.array
             self._check_all(ts, role, r)
             return (ctypes.c_void_p * n)(*[_ptr(t) for t in ts])

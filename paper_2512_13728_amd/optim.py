@@ -90,8 +90,8 @@ class CurvaDion(torch.optim.Optimizer):
         if len(set(ranks)) != 1:
             # one cd_group_step takes one r: step matrices of each rank separately
             raise ValueError("all matrices of one gradient dtype must share the rank; pass an int rank")
-        return dict(group=grp, layers=layers, params=list(params), M=grp.pack(Ms),
-                    X=grp.pack(list(params)), Q=grp.pack(Qs), r=ranks[0])
+        return dict(group=grp, layers=layers, params=list(params), M=grp.pack(Ms, "M"),
+                    X=grp.pack(list(params), "X"), Q=grp.pack(Qs, "Q", ranks[0]), r=ranks[0])
 
     @torch.no_grad()
     def step(self, closure: Optional[callable] = None):

@@ -466,6 +466,10 @@ def test_wrong_operands_are_refused_before_any_work():
     Gp.step([G], [M], [X], pQ, 0.95, 0.01, r)
     with pytest.raises(ValueError, match="shape"):
         Gp.step([G], [M], [X], pQ, 0.95, 0.01, r // 2)     # Q is n x r, not n x r/2
+    with pytest.raises(ValueError, match="shape"):
+        Gp.pack([M.t()], "M")                              # checked when packed with a role
+    with pytest.raises(ValueError, match="float32"):
+        Gp.pack([X.double()], "X")
     torch.cuda.synchronize()
     assert L.get_state()[1] == 1
 
