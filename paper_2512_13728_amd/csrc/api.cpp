@@ -159,6 +159,7 @@ struct cd_layer {
   float* colnrm = nullptr;      // r_max column norms
   cd_group* self = nullptr;     // one-layer group used by cd_step
   int last_r = 0;
+  bool prev_zero = true;        // prev_norm is known to be 0 (new layer, or set so)
 };
 
 struct ShapeClass {
@@ -610,11 +611,14 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   // to be "skip", X -= eta_local G rides along in the buffer pass, which saves
   // the second read of G; should the step sync after all, the sync update
   // first adds eta_local G back (in fp32, one rounding).  The RMMC policy
-  // predicts the previous step's branch.
+  // predicts the previous step's branch, except that a layer whose prev_norm
+  // is 0 (its first step) has RMMC = ||B|| / eps: that step syncs unless B = 0.
   const long long next_step = g->layers[0]->step + 1;
+  bool any_prev_zero = false;
+  for (const cd_layer* Ly : g->layers) any_prev_zero = any_prev_zero || Ly->prev_zero;
   bool spec = false;
   switch (g->policy) {
-    case CD_POLICY_RMMC: spec = g->predict_skip; break;
+    case CD_POLICY_RMMC: spec = g->predict_skip && !any_prev_zero; break;
     case CD_POLICY_ALWAYS_SYNC: spec = false; break;
     case CD_POLICY_NEVER_SYNC: spec = true; break;
     case CD_POLICY_EVERY_H: spec = (next_step % g->H) != 0; break;
@@ -657,7 +661,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   CD_HIP(hipEventSynchronize(g->ev));
   const cd::GateOut* go = static_cast<const cd::GateOut*>(g->out_host);
   const double* rm = reinterpret_cast<const double*>(go + 1);
-  for (cd_layer* L : g->layers) L->step += 1;
+  for (cd_layer* L : g->layers) { L->step += 1; L->prev_zero = false; }
   const long long step = g->layers[0]->step;
   bool sync = false;
   switch (g->policy) {
@@ -927,6 +931,7 @@ cd_status cd_layer_set_state(cd_layer* layer, double prev_norm, long long step) 
   CD_HIP(hipDeviceSynchronize());
   CD_HIP(hipMemcpy(layer->prev, &prev_norm, sizeof(double), hipMemcpyHostToDevice));
   layer->step = step;
+  layer->prev_zero = prev_norm == 0.0;
   return CD_OK;
 }
 
