@@ -350,6 +350,47 @@ def test_group_wider_than_one_launch():
     assert any(flags) and not all(flags)
 
 
+@pytest.mark.parametrize("gd", ["f32", "bf16"])
+def test_more_shape_batches_than_streams(gd):
+    """Seven shapes of two layers each: the sync branch runs seven batches on
+    four streams (the caller's and three of the group's), three streams taking
+    two batches each.  Always-sync steps: every layer's M, X, Q against the
+    oracle (teacher-forced), and a second group on the same inputs gives
+    bit-identical results (the batches share no memory, so how their kernels
+    interleave does not matter)."""
+    shapes = [(96, 160), (160, 96), (130, 70), (64, 64), (200, 120), (72, 300), (256, 128)]
+    shapes = [s for s in shapes for _ in range(2)]
+    r = 16
+    w = S.Workload("many", tuple(shapes), r=r, grad_dtype=gd, steps=3, k=4, tau=0.3, stream_id=97)
+    runs = []
+    for rep in range(2):
+        Ls = [cdl.Layer(m, n, r, grad_dtype=gd, policy=cdl.POLICY_ALWAYS_SYNC) for m, n in shapes]
+        Gp = cdl.Group(Ls)
+        st = [_state(w, i) for i in range(len(shapes))]
+        streams = [S.GradientStream(w, i, device="cpu") for i in range(len(shapes))]
+        OLs = [O.OracleLayer.from_arrays(f64(s[0]), f64(s[1]), f64(s[2])) for s in st]
+        for t in range(w.steps):
+            Gs = [s.next() for s in streams]
+            _, flag, _, _ = Gp.step([G.to(DEV) for G in Gs], [s[0] for s in st], [s[1] for s in st],
+                                    [s[2] for s in st], w.mu, w.eta, r)
+            torch.cuda.synchronize()
+            assert flag
+            if rep == 0:
+                res = O.group_step(OLs, [f64(G) for G in Gs], f32(w.mu), f32(w.eta), 0.3,
+                                   policy=O.POLICY_ALWAYS_SYNC, with_kappa=True)
+                tol = 2e-2 if gd == "bf16" else 1e-5
+                for i, (s, OL) in enumerate(zip(st, OLs)):
+                    assert rel(f64(s[0]), OL.M) <= tol, (t, i)
+                    assert rel(f64(s[1]), OL.X) <= tol, (t, i)
+                    qt = 2e-2 if gd == "bf16" else qr_tol(res["kappa"][i])
+                    assert rel(f64(s[2]), OL.Q) <= qt, (t, i)
+                    OL.M, OL.X, OL.Q = f64(s[0]), f64(s[1]), f64(s[2])
+        runs.append([f64(t) for s in st for t in s])
+        print(f"{gd} run {rep + 1}: 7 shape batches, {w.steps} sync steps", flush=True)
+    for a, b in zip(*runs):
+        assert np.array_equal(a, b)
+
+
 @pytest.mark.parametrize("policy", [O.POLICY_RMMC, O.POLICY_ALWAYS_SYNC])
 @pytest.mark.parametrize("m,n,r", [(512, 1536, 64), (2048, 512, 256), (300, 700, 37)])
 def test_bf16_gradient_steps(m, n, r, policy):
