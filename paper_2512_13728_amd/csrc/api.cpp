@@ -2,7 +2,8 @@
 // group lifetimes, workspace, launch planning and the per-step schedule.
 //
 // One group step (Algorithm 2 of the paper):
-//   1. per shape class: B = M + G with per-block partial sums of B^2
+//   1. B = M + G with per-block partial sums of B^2, up to MAXB layers of
+//      any shapes per launch
 //   2. gate kernel: fixed-order norms, RMMC_l, prev_norm update, max, flag
 //   3. one device-to-host copy of {max, flag, RMMC_l}: the decision point that
 //      stands in for the max all-reduce at one worker
@@ -12,7 +13,8 @@
 //      ColumnNormalize; M/X update.  The latency-bound factorisation of one
 //      unit overlaps the GEMMs of the others.
 //      local branch: X -= eta_local G (M already holds B).
-// Layers of equal (m, n) share every launch (up to MAXB per launch).
+// The streaming passes take up to MAXB layers of any shapes per launch; the
+// sync branch's kernels take layers of equal (m, n) (up to MAXB per launch).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -199,6 +201,9 @@ struct cd_group {
   void* out_host = nullptr;     // pinned
   hipEvent_t ev = nullptr;
   std::vector<Unit> units;
+  // the streaming passes (buffer formation, local update): batches of up to
+  // MAXB layers of any shapes, in group order, each at most 2^30 blocks
+  std::vector<std::vector<int>> sbatches;
   cd::CholTab* chol_tab = nullptr;      // [L] static workspace pointers, in unit order
   cd::TrsmTab* trsm_tab[3] = {nullptr, nullptr, nullptr};  // P1 = P~ T^-1; U = T^-1; P = P1 T^-1
   int2* trsm_tiles = nullptr;           // per unit: (layer in the unit, 64-row tile of m) pairs
@@ -310,6 +315,16 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
       off += static_cast<int>(u.sel.size());
       g->units.push_back(std::move(u));
     }
+  }
+  for (int i = 0; i < n; ++i) {
+    const long long nb = blocks_for(1LL * layers[i]->d.m * layers[i]->d.n);
+    long long total = 0;
+    if (!g->sbatches.empty())
+      for (int li : g->sbatches.back()) total += blocks_for(1LL * layers[li]->d.m * layers[li]->d.n);
+    if (g->sbatches.empty() || static_cast<int>(g->sbatches.back().size()) == cd::MAXB ||
+        total + nb > (1LL << 30))
+      g->sbatches.emplace_back();
+    g->sbatches.back().push_back(i);
   }
   hipError_t e = hipSuccess;
   if (e == hipSuccess) e = dalloc(&g->parts, static_cast<size_t>(n) * g->nparts_stride);
@@ -625,25 +640,28 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   }
 
   // 1. B = M + G, partial sums of B^2 (and the speculative skip update)
-  for (const ShapeClass& sc : g->shapes) {
-    const long long numel = 1LL * sc.m * sc.n;
-    for (size_t c0 = 0; c0 < sc.idx.size(); c0 += cd::MAXB) {
-      const int nl = static_cast<int>(std::min<size_t>(cd::MAXB, sc.idx.size() - c0));
-      cd::FormArgs fa{};
-      fa.numel = numel;
-      fa.blocks_per_layer = static_cast<int>(blocks_for(numel));
-      for (int j = 0; j < nl; ++j) {
-        const int li = sc.idx[c0 + j];
-        fa.M[j] = M[li]; fa.G[j] = G[li]; fa.part[j] = g->parts + 1LL * li * g->nparts_stride;
-        fa.X[j] = X[li];
-        fa.coef[j] = static_cast<float>(g->layers[li]->d.eta_local_scale * static_cast<double>(eta));
-        fa.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * g->layers[li]->d.weight_decay);
-      }
-      const double fb = static_cast<double>(numel) * nl * ((spec ? 16.0 : 8.0) + (g->g_bf16 ? 2.0 : 4.0));
-      cd_status st = run(g, spec ? K_FORM_X : K_FORM, fb, (spec ? 5.0 : 3.0) * numel * nl, s,
-                         [&] { return cd::launch_form_buffer(fa, nl, g->g_bf16, spec, s); });
-      if (st != CD_OK) return st;
+  for (const std::vector<int>& batch : g->sbatches) {
+    const int nl = static_cast<int>(batch.size());
+    cd::FormArgs fa{};
+    fa.nl = nl;
+    long long total = 0, blocks = 0;
+    for (int j = 0; j < nl; ++j) {
+      const int li = batch[j];
+      const cd_layer* Ly = g->layers[li];
+      fa.numel[j] = 1LL * Ly->d.m * Ly->d.n;
+      fa.block0[j] = static_cast<int>(blocks);
+      blocks += blocks_for(fa.numel[j]);
+      total += fa.numel[j];
+      fa.M[j] = M[li]; fa.G[j] = G[li]; fa.part[j] = g->parts + 1LL * li * g->nparts_stride;
+      fa.X[j] = X[li];
+      fa.coef[j] = static_cast<float>(Ly->d.eta_local_scale * static_cast<double>(eta));
+      fa.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * Ly->d.weight_decay);
     }
+    fa.block0[nl] = static_cast<int>(blocks);
+    const double fb = static_cast<double>(total) * ((spec ? 16.0 : 8.0) + (g->g_bf16 ? 2.0 : 4.0));
+    cd_status st = run(g, spec ? K_FORM_X : K_FORM, fb, (spec ? 5.0 : 3.0) * total, s,
+                       [&] { return cd::launch_form_buffer(fa, g->g_bf16, spec, s); });
+    if (st != CD_OK) return st;
   }
   // 2. gate
   cd::GateArgs ga{};
@@ -719,21 +737,26 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
     }
     for (cd_layer* Ly : g->layers) Ly->last_r = r;
   } else if (!spec) {
-    for (const Unit& u : g->units) {
-      const ShapeClass& sc = g->shapes[u.sc];
-      const int nl = static_cast<int>(u.sel.size());
+    for (const std::vector<int>& batch : g->sbatches) {
+      const int nl = static_cast<int>(batch.size());
       cd::LocalArgs la{};
-      la.numel = 1LL * sc.m * sc.n;
-      la.blocks_per_layer = static_cast<int>(blocks_for(la.numel));
+      la.nl = nl;
+      long long total = 0, blocks = 0;
       for (int j = 0; j < nl; ++j) {
-        const int li = u.sel[j];
+        const int li = batch[j];
+        const cd_layer* Ly = g->layers[li];
+        la.numel[j] = 1LL * Ly->d.m * Ly->d.n;
+        la.block0[j] = static_cast<int>(blocks);
+        blocks += blocks_for(la.numel[j]);
+        total += la.numel[j];
         la.X[j] = X[li]; la.G[j] = G[li];
-        la.coef[j] = static_cast<float>(g->layers[li]->d.eta_local_scale * static_cast<double>(eta));
-        la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * g->layers[li]->d.weight_decay);
+        la.coef[j] = static_cast<float>(Ly->d.eta_local_scale * static_cast<double>(eta));
+        la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * Ly->d.weight_decay);
       }
-      const double lb = static_cast<double>(la.numel) * nl * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
-      cd_status st = run(g, K_LOCAL, lb, 2.0 * la.numel * nl, s,
-                         [&] { return cd::launch_local_update(la, nl, g->g_bf16, s); });
+      la.block0[nl] = static_cast<int>(blocks);
+      const double lb = static_cast<double>(total) * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
+      cd_status st = run(g, K_LOCAL, lb, 2.0 * total, s,
+                         [&] { return cd::launch_local_update(la, g->g_bf16, s); });
       if (st != CD_OK) return st;
     }
   }

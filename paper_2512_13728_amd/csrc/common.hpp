@@ -16,30 +16,34 @@ constexpr int NTHREADS = 256;     // threads per block for the streaming kernels
 constexpr int GBK = 32;           // GEMM k per LDS stage; split-K slices are multiples
 
 // ---- a1: B = M + G and per-block sum of B^2 -------------------------------
-// Every block covers FORM_CHUNK consecutive elements of one layer.
+// Every block covers FORM_CHUNK consecutive elements of one layer; one launch
+// covers up to MAXB layers of any shapes (the passes are elementwise), layer
+// j owning blocks [block0[j], block0[j + 1]).
 constexpr int FORM_CHUNK = NTHREADS * 4 * 4;   // 4096 elements
 struct FormArgs {
-  long long numel;                 // elements per layer (m*n)
-  int blocks_per_layer;            // ceil(numel / FORM_CHUNK)
+  int nl;                          // layers in this launch
+  long long numel[MAXB];           // elements of each layer (m*n)
+  int block0[MAXB + 1];            // first block of each layer; block0[nl] = blocks of the launch
   float* M[MAXB];                  // in: M_{t-1}; out: B_t
   const void* G[MAXB];             // fp32 or bf16
-  double* part[MAXB];              // out: blocks_per_layer partial sums of B^2
+  double* part[MAXB];              // out: ceil(numel / FORM_CHUNK) partial sums of B^2 per layer
   float* X[MAXB];                  // with_x: the skip-branch update X = xdecay X - coef G, fused
   float coef[MAXB];                // eta_local per layer (with_x only)
   float xdecay[MAXB];              // 1 - eta * weight_decay per layer (with_x only)
 };
-hipError_t launch_form_buffer(const FormArgs& a, int nl, bool g_bf16, bool with_x, hipStream_t s);
+hipError_t launch_form_buffer(const FormArgs& a, bool g_bf16, bool with_x, hipStream_t s);
 
 // ---- local branch: X = X - eta_local G --------------------------------------
-struct LocalArgs {
-  long long numel;
-  int blocks_per_layer;
+struct LocalArgs {                 // launch layout as FormArgs
+  int nl;
+  long long numel[MAXB];
+  int block0[MAXB + 1];
   float* X[MAXB];
   const void* G[MAXB];
   float coef[MAXB];                // eta_local per layer
   float xdecay[MAXB];              // 1 - eta * weight_decay per layer
 };
-hipError_t launch_local_update(const LocalArgs& a, int nl, bool g_bf16, hipStream_t s);
+hipError_t launch_local_update(const LocalArgs& a, bool g_bf16, hipStream_t s);
 
 // ---- gate: fixed-order reduction of the partials, RMMC, prev update, max ----
 struct GateOut {                   // device-side result, copied to the host

@@ -70,19 +70,28 @@ __device__ double block_sum(double v) {
 
 constexpr int VPT = FORM_CHUNK / (NTHREADS * 4);   // float4 groups per thread (4)
 
+// The layer that block b of a launch belongs to (block0 increases; the scan
+// is uniform over the block and reads the kernel arguments only).
+__device__ __forceinline__ int layer_of(const int* block0, int nl, int b) {
+  int l = 0;
+  for (int k = 1; k < nl; ++k) l += b >= block0[k] ? 1 : 0;
+  return l;
+}
+
 // B = M + G in place, the block's partial sum of B^2, and (WX) the skip
 // branch's X = xdecay X - coef G in the same pass over G (xdecay = 1 - eta
 // weight_decay; 1 without weight decay, where the product is exact).
 template <bool BF16, bool WX>
 __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
-  const int l = blockIdx.y;
+  const int l = layer_of(a.block0, a.nl, blockIdx.x);
+  const int lb = blockIdx.x - a.block0[l];   // block within the layer
   float* __restrict__ M = a.M[l];
   const void* __restrict__ G = a.G[l];
   float* __restrict__ X = a.X[l];
   const float c = a.coef[l];
   const float d = a.xdecay[l];
-  const long long base = static_cast<long long>(blockIdx.x) * FORM_CHUNK;
-  const long long end = min(base + FORM_CHUNK, a.numel);
+  const long long base = static_cast<long long>(lb) * FORM_CHUNK;
+  const long long end = min(base + FORM_CHUNK, a.numel[l]);
   double acc = 0.0;
   if (end - base == FORM_CHUNK) {
     float4 m[VPT], g[VPT], x[VPT];
@@ -136,18 +145,18 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
     }
   }
   const double s = block_sum(acc);
-  if (threadIdx.x == 0) a.part[l][blockIdx.x] = s;
+  if (threadIdx.x == 0) a.part[l][lb] = s;
 }
 
 template <bool BF16>
 __global__ __launch_bounds__(NTHREADS) void k_local_update(LocalArgs a) {
-  const int l = blockIdx.y;
+  const int l = layer_of(a.block0, a.nl, blockIdx.x);
   float* __restrict__ X = a.X[l];
   const void* __restrict__ G = a.G[l];
   const float c = a.coef[l];
   const float d = a.xdecay[l];
-  const long long base = static_cast<long long>(blockIdx.x) * FORM_CHUNK;
-  const long long end = min(base + FORM_CHUNK, a.numel);
+  const long long base = static_cast<long long>(blockIdx.x - a.block0[l]) * FORM_CHUNK;
+  const long long end = min(base + FORM_CHUNK, a.numel[l]);
   if (end - base == FORM_CHUNK) {
     float4 x[VPT], g[VPT];
 #pragma unroll
@@ -243,9 +252,9 @@ __global__ __launch_bounds__(GATE_THREADS) void k_gate(GateArgs a) {
 
 }  // namespace
 
-hipError_t launch_form_buffer(const FormArgs& a, int nl, bool g_bf16, bool with_x, hipStream_t s) {
-  if (nl <= 0 || a.blocks_per_layer <= 0) return hipSuccess;
-  const dim3 grid(a.blocks_per_layer, nl), block(NTHREADS);
+hipError_t launch_form_buffer(const FormArgs& a, bool g_bf16, bool with_x, hipStream_t s) {
+  if (a.nl <= 0 || a.nl > MAXB || a.block0[a.nl] <= 0) return a.nl == 0 ? hipSuccess : hipErrorInvalidValue;
+  const dim3 grid(a.block0[a.nl]), block(NTHREADS);
   if (g_bf16) {
     if (with_x) hipLaunchKernelGGL((k_form_buffer<true, true>), grid, block, 0, s, a);
     else hipLaunchKernelGGL((k_form_buffer<true, false>), grid, block, 0, s, a);
@@ -256,9 +265,9 @@ hipError_t launch_form_buffer(const FormArgs& a, int nl, bool g_bf16, bool with_
   return hipGetLastError();
 }
 
-hipError_t launch_local_update(const LocalArgs& a, int nl, bool g_bf16, hipStream_t s) {
-  if (nl <= 0 || a.blocks_per_layer <= 0) return hipSuccess;
-  const dim3 grid(a.blocks_per_layer, nl), block(NTHREADS);
+hipError_t launch_local_update(const LocalArgs& a, bool g_bf16, hipStream_t s) {
+  if (a.nl <= 0 || a.nl > MAXB || a.block0[a.nl] <= 0) return a.nl == 0 ? hipSuccess : hipErrorInvalidValue;
+  const dim3 grid(a.block0[a.nl]), block(NTHREADS);
   if (g_bf16) hipLaunchKernelGGL(k_local_update<true>, grid, block, 0, s, a);
   else hipLaunchKernelGGL(k_local_update<false>, grid, block, 0, s, a);
   return hipGetLastError();
