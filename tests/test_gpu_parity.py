@@ -454,6 +454,34 @@ def test_weight_decay_every_branch(m, n, r, gd):
     assert flags == [True, False, True, False]
 
 
+@pytest.mark.parametrize("gd", ["f32", "bf16"])
+def test_local_scale_and_eps_through_every_x_path(gd):
+    """eta_local = 0.5 eta, eps = 1e-3 and weight decay 0.05 through
+    [sync, skip, skip, sync, skip, skip]: the stand-alone skip update (after a
+    sync the branch is predicted sync), the fused speculative skip update kept
+    (a skip after a skip), its reversal when a spike (G x 40) makes the
+    predicted skip a sync, and both again.  Every step against the oracle
+    with the same eps, eta_local and decay."""
+    m, n, r = 300, 200, 24
+    w = S.small_workload(m, n, r, grad_dtype=gd, k=8)
+    M, X, Q = _state(w, 0)
+    tau, eps, scale, lam = 0.5, 1e-3, 0.5, 0.05
+    L = cdl.Layer(m, n, r, grad_dtype=gd, policy=cdl.POLICY_RMMC, tau=tau, eps=eps,
+                  eta_local_scale=scale, weight_decay=lam)
+    stream = S.GradientStream(w, 0, device="cpu")
+    flags = []
+    for t in range(6):
+        G = stream.next()
+        if t == 3:
+            G = (G.float() * 40.0).to(G.dtype)
+        d = step_and_compare(L, G.to(DEV), M, X, Q, 0.95, 0.01, r, tau, O.POLICY_RMMC, eps=eps,
+                             eta_local_scale=scale, weight_decay=lam)
+        _print(f"eta_local x0.5, eps 1e-3, {gd} t={t + 1}", d)
+        _check_step(d, tau, O.POLICY_RMMC, bf16=gd == "bf16")
+        flags.append(d["flag_gpu"])
+    assert flags == [True, False, False, True, False, False]
+
+
 def test_packed_pointers_match_lists():
     """Group.step with pointer arrays marshalled once (Group.pack) gives the
     bit-identical result of passing the tensor lists."""
