@@ -61,7 +61,7 @@ KIND_BOUND = {
     "update_bf16": ("hbm", None, 1), "gram_bf16x6": ("mfma", "bf16", 6),
     "apply_bf16x6": ("mfma", "bf16", 6), "trtri_f64": ("mfma", "f64", 1),
 }
-POLICIES = {"rmmc": 0, "always": 1, "never": 2}
+POLICIES = {"rmmc": 0, "always": 1, "never": 2, "every_h": 3}
 
 # kernel kind -> (kernel-name pattern in the profiler's output, source files);
 # kinds whose kernel template is shared with other kinds have no pattern
@@ -100,6 +100,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--workload", default="gpt1p3b")
     p.add_argument("--policy", default="rmmc", choices=sorted(POLICIES))
+    p.add_argument("--H", type=int, default=4, help="sync period for --policy every_h (Scheduled Sync Dion)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--pool", type=int, default=20, help="distinct gradient sets kept resident")
     p.add_argument("--rank", type=int, default=0, help="override the workload's rank r")
@@ -342,7 +343,9 @@ def main():
         log(f"[bench] copy calibration: streaming copy b = -a, bytes={a.numel() * 4} read and written")
         del a, b
 
-    layers = [cdl.Layer(m, n, w.r, grad_dtype=w.grad_dtype, tau=w.tau, eps=w.eps, policy=policy)
+    if args.H < 1:
+        sys.exit("--H must be >= 1")
+    layers = [cdl.Layer(m, n, w.r, grad_dtype=w.grad_dtype, tau=w.tau, eps=w.eps, policy=policy, H=args.H)
               for (m, n) in w.shapes]
     group = cdl.Group(layers)
     t0 = time.perf_counter()
@@ -514,7 +517,8 @@ def main():
                                       "accumulation" if w.grad_dtype == "bf16" else
                                       "P~ = BQ, Gram and CholQR in fp64; R and the M/X update on bf16 "
                                       "MFMA with 3-piece fp32 splits"),
-            "policy": args.policy, "tau": w.tau, "trajectory_steps": K,
+            "policy": args.policy + (f" (H = {args.H})" if args.policy == "every_h" else ""),
+            "tau": w.tau, "trajectory_steps": K,
             "sync_steps": n_sync, "local_steps": n_local, "parallelism": "none (1 GPU)",
             "inputs": (f"gradients drawn on the GPU between steps, outside each step's timed interval"
                        if streamed else f"{pool} gradient sets resident in HBM, cycled"),
