@@ -83,13 +83,19 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
   bool def = false;
 #pragma unroll 1
   for (int p = 0; p < CB; ++p) {
-    rowb[j] = a[0];
-    __syncthreads();
-    double d = rowb[p];
+    // the pivot A[p][p] is lane p's a[0]: read across the wave (no LDS trip)
+    const double a0 = a[0];
+    double d = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(a0), p),
+                                __builtin_amdgcn_readlane(__double2loint(a0), p));
     const bool floored = p < nb && !(d > fl);   // uniform over the wave
     if (floored) { d = fl; def = true; }
-    const double piv = sqrt(d);
-    const double inv = 1.0 / piv;
+    // 1/sqrt(d): the hardware estimate refined by two Newton steps (error
+    // squared each step), then sqrt(d) = d / sqrt(d); both within about an
+    // ulp, with no divide in the pivot's dependency chain
+    double inv = __builtin_amdgcn_rsq(d);
+#pragma unroll
+    for (int it = 0; it < 2; ++it) inv = fma(inv, fma(-0.5 * d * inv, inv, 0.5), inv);
+    const double piv = d * inv;
     // row p of T (zero left of the diagonal, and right of a floored pivot)
     const double tp = j == p ? piv : (j > p && !floored ? a[0] * inv : 0.0);
     Ts[j * TLD + p] = tp;
