@@ -315,6 +315,47 @@ def check_weight_decay_decoupled(o):
         np.testing.assert_allclose(Bl.X - A.X, (d - 1.0) * X0, rtol=0, atol=1e-14)
 
 
+def check_sync_update_equivariance(o):
+    """Metamorphic pins of the sync update (no formula retyped): for orthogonal
+    U (m x m) and V (n x n) and c > 0,
+      B -> U B, X -> U X:            P -> U P, R and Q unchanged, M -> U M, X' -> U X'
+      B -> B V, X -> X V, Q0 -> V^T Q0:  P unchanged, R -> V^T R, Q -> V^T Q,
+                                          M -> M V, X' -> X' V
+      B -> c B:                      P, Q and X' unchanged, R -> c R, M -> c M
+    (the positive-diagonal QR factor is equivariant under both rotations and
+    invariant under positive scaling; column norms are rotation invariant)."""
+    rng = _rng(23)
+    mu, eta = 0.9, 0.03
+    for m, n, r in ((9, 7, 3), (7, 9, 3), (12, 12, 5)):
+        B, X = rng.standard_normal((m, n)), rng.standard_normal((m, n))
+        Q0 = np.linalg.qr(rng.standard_normal((n, r)))[0]
+        U = np.linalg.qr(rng.standard_normal((m, m)))[0]
+        V = np.linalg.qr(rng.standard_normal((n, n)))[0]
+        base = o.sync_update(B, X, Q0, mu, eta)
+
+        def close(a, b):
+            np.testing.assert_allclose(a, b, rtol=0, atol=1e-11 * max(1.0, np.abs(b).max()))
+
+        left = o.sync_update(U @ B, U @ X, Q0, mu, eta)
+        close(left["P"], U @ base["P"])
+        close(left["R"], base["R"])
+        close(left["Q"], base["Q"])
+        close(left["M"], U @ base["M"])
+        close(left["X"], U @ base["X"])
+        right = o.sync_update(B @ V, X @ V, V.T @ Q0, mu, eta)
+        close(right["P"], base["P"])
+        close(right["R"], V.T @ base["R"])
+        close(right["Q"], V.T @ base["Q"])
+        close(right["M"], base["M"] @ V)
+        close(right["X"], base["X"] @ V)
+        scaled = o.sync_update(3.0 * B, X, Q0, mu, eta)
+        close(scaled["P"], base["P"])
+        close(scaled["Q"], base["Q"])
+        close(scaled["R"], 3.0 * base["R"])
+        close(scaled["M"], 3.0 * base["M"])
+        close(scaled["X"], base["X"])
+
+
 ALL_CHECKS = [check_golden, check_orthogonalize_is_qr_factor,
               check_orthogonalize_matches_gram_schmidt, check_column_normalize,
               check_frobenius_norm, check_rmmc_definition, check_rmmc_zero_when_unchanged,
@@ -322,7 +363,7 @@ ALL_CHECKS = [check_golden, check_orthogonalize_is_qr_factor,
               check_full_rank_momentum, check_rank_one_closed_form,
               check_local_branch_closed_form, check_gate,
               check_first_step_syncs_and_global_max, check_policies_match_algorithms,
-              check_weight_decay_decoupled]
+              check_weight_decay_decoupled, check_sync_update_equivariance]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda c: c.__name__)
