@@ -188,6 +188,15 @@ typedef struct cd_kernel_time {
 cd_status cd_group_set_timing(cd_group* group, int enable);
 cd_status cd_group_kernel_times(cd_group* group, cd_kernel_time* out, int max_kinds, int* count);
 
+/* Restricts the bracketing to the kernel kinds named in `kinds`, a
+ * comma-separated list of the names cd_group_kernel_times() reports (NULL or
+ * "" = every kind, the default).  The events cost several microseconds of
+ * idle time at each bracketed launch, so a measurement of whole steps
+ * brackets only the kernel it reports.  Applies from the next step; the
+ * setting survives cd_group_set_timing().  CD_EINVAL for an unknown name
+ * (the previous setting is then kept). */
+cd_status cd_group_set_timing_kinds(cd_group* group, const char* kinds);
+
 /* Thread-local text of the last error on this thread ("" if none). */
 const char* cd_last_error(void);
 

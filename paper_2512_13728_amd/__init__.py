@@ -33,7 +33,7 @@ EXPORTED_SYMBOLS = (
     "cd_layer_create", "cd_step", "cd_destroy", "cd_group_create", "cd_group_step",
     "cd_group_destroy", "cd_layer_get_state", "cd_layer_set_state",
     "cd_layer_last_factors", "cd_layer_rank_deficient", "cd_group_set_timing",
-    "cd_group_kernel_times", "cd_last_error", "cd_abi_version",
+    "cd_group_kernel_times", "cd_group_set_timing_kinds", "cd_last_error", "cd_abi_version",
 )
 
 
@@ -90,6 +90,7 @@ def lib() -> ctypes.CDLL:
     L.cd_layer_last_factors.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp)]
     L.cd_layer_rank_deficient.argtypes = [vp, ctypes.POINTER(i)]
     L.cd_group_set_timing.argtypes = [vp, i]
+    L.cd_group_set_timing_kinds.argtypes = [vp, ctypes.c_char_p]
     L.cd_group_kernel_times.argtypes = [vp, ctypes.POINTER(KernelTime), i, ctypes.POINTER(i)]
     L.cd_last_error.restype = ctypes.c_char_p
     L.cd_last_error.argtypes = []
@@ -288,8 +289,11 @@ class Group:
         _check(st, allow=(CD_OK, CD_ENONFINITE))
         return res.rmmc, bool(res.sync_flag), list(per), st
 
-    def set_timing(self, enable: bool) -> None:
-        """Bracket every kernel launch with HIP events (see kernel_times)."""
+    def set_timing(self, enable: bool, kinds=None) -> None:
+        """Bracket kernel launches with HIP events (see kernel_times): every
+        launch, or only those of the kernel kinds named in `kinds`."""
+        spec = None if not kinds else ",".join(kinds).encode()
+        _check(lib().cd_group_set_timing_kinds(self._h, spec))
         _check(lib().cd_group_set_timing(self._h, 1 if enable else 0))
 
     def kernel_times(self) -> dict:

@@ -103,16 +103,23 @@ const char* const kKindName[K_NKINDS] = {
     "form_buffer", "form_buffer_local", "gate", "local_update", "power_bq_f64", "power_bq_bf16x3", "gram_f64",
     "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_bf16x6",
     "power_btp_bf16x3", "reduce_splits", "colnorm", "update_bf16x6", "update_bf16"};
+static_assert(K_NKINDS <= 32, "the timing mask holds one bit per kind");
+
+// Timing events only measure: recording them without the system-scope fence
+// (cache write-back and invalidate) keeps them from stretching the gaps
+// between the kernels they bracket.
+constexpr unsigned kTimingEventFlags = hipEventDisableSystemFence;
 
 struct Timer {
   struct Rec { int kind; hipEvent_t a, b; double bytes, flops; };
   bool on = false;
+  unsigned mask = ~0u;   // kinds that get events while on
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
   hipEvent_t get() {
     hipEvent_t e = nullptr;
     if (!pool.empty()) { e = pool.back(); pool.pop_back(); return e; }
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, kTimingEventFlags) != hipSuccess) return nullptr;
     return e;
   }
   void release() {
@@ -123,7 +130,7 @@ struct Timer {
   hipError_t reserve(size_t n) {
     while (pool.size() < n) {
       hipEvent_t e = nullptr;
-      const hipError_t err = hipEventCreate(&e);
+      const hipError_t err = hipEventCreateWithFlags(&e, kTimingEventFlags);
       if (err != hipSuccess) return err;
       pool.push_back(e);
     }
@@ -391,7 +398,7 @@ cd_status check_desc(const cd_layer_desc* d) {
 // Launch through `launch`, bracketed by timing events when timing is on.
 template <typename F>
 cd_status run(cd_group* g, int kind, double bytes, double flops, hipStream_t s, F&& launch) {
-  if (!g->timer.on) {
+  if (!g->timer.on || !((g->timer.mask >> kind) & 1u)) {
     CD_HIP(launch());
     return CD_OK;
   }
@@ -906,6 +913,29 @@ cd_status cd_group_set_timing(cd_group* group, int enable) {
   group->timer.release();
   if (enable) CD_HIP(group->timer.reserve(2048));
   group->timer.on = enable != 0;
+  return CD_OK;
+}
+
+cd_status cd_group_set_timing_kinds(cd_group* group, const char* kinds) {
+  if (!group) return fail(CD_EINVAL, "group is NULL");
+  if (!kinds || !*kinds) {
+    group->timer.mask = ~0u;
+    return CD_OK;
+  }
+  unsigned mask = 0;
+  const std::string list(kinds);
+  size_t b = 0;
+  while (b <= list.size()) {
+    size_t e = list.find(',', b);
+    if (e == std::string::npos) e = list.size();
+    const std::string name = list.substr(b, e - b);
+    int k = 0;
+    while (k < K_NKINDS && name != kKindName[k]) ++k;
+    if (k == K_NKINDS) return fail(CD_EINVAL, "unknown kernel kind '%s'", name.c_str());
+    mask |= 1u << k;
+    b = e + 1;
+  }
+  group->timer.mask = mask;
   return CD_OK;
 }
 

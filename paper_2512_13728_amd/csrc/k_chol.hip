@@ -81,13 +81,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
   rowb[CB + j] = 0.0;
   Tsb[j] = 0.0;
   bool def = false;
+  // only the block's nb pivots: the identity padding of a last, partial block
+  // would factor to itself, and its rows are never stored
 #pragma unroll 1
-  for (int p = 0; p < CB; ++p) {
+  for (int p = 0; p < nb; ++p) {
     // the pivot A[p][p] is lane p's a[0]: read across the wave (no LDS trip)
     const double a0 = a[0];
     double d = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(a0), p),
                                 __builtin_amdgcn_readlane(__double2loint(a0), p));
-    const bool floored = p < nb && !(d > fl);   // uniform over the wave
+    const bool floored = !(d > fl);   // uniform over the wave
     if (floored) { d = fl; def = true; }
     // 1/sqrt(d): the hardware estimate refined by two Newton steps (error
     // squared each step), then sqrt(d) = d / sqrt(d); both within about an
@@ -102,7 +104,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     if (j == p) {
       pinv[p] = inv;
       okb[p] = floored ? 0 : 1;
-      if (p < nb) t.rowok[k0 + p] = floored ? 0 : 1;
+      t.rowok[k0 + p] = floored ? 0 : 1;
     }
     __syncthreads();
     rowb[j] = tp;
@@ -119,20 +121,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     a[CB - 1] = 0.0;
     __syncthreads();
   }
-  // f[k] = d[p - k] at step p; entries with k > p lie above row 0 and are
-  // never stored
+  // f[k] = d[p - k] at step p, from p = nb - 1 down; entries with k > p lie
+  // above row 0 and are never stored
   double f[CB];
 #pragma unroll
-  for (int k = 0; k < CB; ++k) f[k] = k == CB - 1 - j ? 1.0 : 0.0;
+  for (int k = 0; k < CB; ++k) f[k] = k == nb - 1 - j ? 1.0 : 0.0;
   double* D = t.Dinv + static_cast<long long>(kb) * CB * CB;
   // the column of a floored pivot is stored as zero: P~ T^{-1} then has a
   // zero column there and the other columns are unchanged (with row p of T
   // zero right of the diagonal, column j != p of T^{-1} is zero in row p)
   const bool cin = j < nb && okb[j];
+  for (int p = nb; p < CB; ++p) D[p * CB + j] = 0.0;   // rows past a partial block
 #pragma unroll 1
-  for (int p = CB - 1; p >= 0; --p) {
+  for (int p = nb - 1; p >= 0; --p) {
     const double x = f[0] * pinv[p];
-    D[p * CB + j] = (p < nb && cin) ? x : 0.0;
+    D[p * CB + j] = cin ? x : 0.0;
     const double* col = Ts + p * TLD + p;   // col[-k] = T[p - k][p]
     double cv[CB];
 #pragma unroll

@@ -32,13 +32,40 @@ __global__ __launch_bounds__(256) void k_colsq(ColnormArgs a) {
   a.part[l][static_cast<long long>(chunk) * a.r + j] = (s[0] + s[1]) + (s[2] + s[3]);
 }
 
+// Column norms from the partials: 16 columns per block and 16 threads per
+// column, thread c summing partials c, c + 16, c + 32, ... (four interleaved
+// accumulators, so four loads are in flight), then a fixed-order tree over
+// the 16 sums.  The order depends only on n, not on scheduling.
+constexpr int CN_COLS = 16, CN_LANES = 16;
 __global__ __launch_bounds__(256) void k_colnorm_final(ColnormArgs a) {
+  __shared__ double sh[CN_LANES][CN_COLS + 1];
   const int l = blockIdx.z;
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= a.r) return;
-  double s = 0.0;
-  for (int c = 0; c < a.nchunks; ++c) s += a.part[l][static_cast<long long>(c) * a.r + j];
-  a.nrm[l][j] = static_cast<float>(fmax(sqrt(s), 1e-30));
+  const int jj = threadIdx.x % CN_COLS, cl = threadIdx.x / CN_COLS;
+  const int j = blockIdx.x * CN_COLS + jj;
+  double s[4] = {0.0, 0.0, 0.0, 0.0};
+  if (j < a.r) {
+    const double* p = a.part[l] + j;
+    const long long step = static_cast<long long>(a.r) * CN_LANES;
+    int c = cl;
+    for (; c + 3 * CN_LANES < a.nchunks; c += 4 * CN_LANES) {
+      const double* q = p + static_cast<long long>(c) * a.r;
+      const double v0 = q[0], v1 = q[step], v2 = q[2 * step], v3 = q[3 * step];
+      s[0] += v0; s[1] += v1; s[2] += v2; s[3] += v3;
+    }
+    // at most three left: c, c + 16, c + 32
+    const double* q = p + static_cast<long long>(c) * a.r;
+    if (c < a.nchunks) s[0] += q[0];
+    if (c + CN_LANES < a.nchunks) s[1] += q[step];
+    if (c + 2 * CN_LANES < a.nchunks) s[2] += q[2 * step];
+  }
+  sh[cl][jj] = (s[0] + s[1]) + (s[2] + s[3]);
+  __syncthreads();
+#pragma unroll
+  for (int w = CN_LANES / 2; w >= 1; w >>= 1) {
+    if (cl < w) sh[cl][jj] += sh[cl + w][jj];
+    __syncthreads();
+  }
+  if (cl == 0 && j < a.r) a.nrm[l][j] = static_cast<float>(fmax(sqrt(sh[0][jj]), 1e-30));
 }
 
 // Q = R / norms, and the bf16 planes of R and Q (piece s of a value is
@@ -98,7 +125,7 @@ hipError_t launch_colnorm(const ColnormArgs& a, int nl, hipStream_t s) {
   if (nl <= 0) return hipSuccess;
   if (a.rp % 32 != 0 || a.rp < a.r || a.S < 1 || a.S > 3) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_colsq, dim3(a.nchunks, (a.r + 255) / 256, nl), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(k_colnorm_final, dim3((a.r + 255) / 256, 1, nl), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_colnorm_final, dim3((a.r + CN_COLS - 1) / CN_COLS, 1, nl), dim3(256), 0, s, a);
   long long quads = static_cast<long long>(a.n) * (a.rp / 4);
   long long blocks = (quads + 255) / 256;
   if (blocks > 4096) blocks = 4096;

@@ -121,18 +121,31 @@ hipError_t launch_t(const GemmArgs& g, int nl, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Narrow products (r <= 32) take 64 x 16 or 64 x 32 tiles (one wave column,
+// four waves down): a 64-wide tile would spend most of its MFMAs on padding.
+int tile_n(int N) { return N <= 16 ? 16 : (N <= 32 ? 32 : 64); }
+
+template <typename T, typename TIn, typename TOut>
+hipError_t launch_n(const GemmArgs& g, int nl, hipStream_t s) {
+  switch (tile_n(g.N)) {
+    case 16: return launch_t<T, TIn, TOut, 64, 16>(g, nl, s);
+    case 32: return launch_t<T, TIn, TOut, 64, 32>(g, nl, s);
+    default: return launch_t<T, TIn, TOut, 64, 64>(g, nl, s);
+  }
+}
+
 }  // namespace
 
-// Tile shape of the fp64 kernels (64 x 64).
+// Tile shape of the fp64 kernels: 64 rows, 16 / 32 / 64 columns by N.
 int gemm_bm(int N, bool fp64) { (void)N; (void)fp64; return 64; }
-int gemm_bn(int N, bool fp64) { (void)N; (void)fp64; return 64; }
+int gemm_bn(int N, bool fp64) { (void)fp64; return tile_n(N); }
 
 hipError_t launch_gemm(const GemmArgs& g, int nl, GemmKind kind, hipStream_t s) {
   if (nl <= 0) return hipSuccess;
   switch (kind) {
-    case GemmKind::F64_FROM_F32: return launch_t<double, float, double, 64, 64>(g, nl, s);
-    case GemmKind::F64: return launch_t<double, double, double, 64, 64>(g, nl, s);
-    case GemmKind::F64_TO_F32: return launch_t<double, double, float, 64, 64>(g, nl, s);
+    case GemmKind::F64_FROM_F32: return launch_n<double, float, double>(g, nl, s);
+    case GemmKind::F64: return launch_n<double, double, double>(g, nl, s);
+    case GemmKind::F64_TO_F32: return launch_n<double, double, float>(g, nl, s);
     case GemmKind::F32: break;  // fp32 contractions run on the bf16-split kernels
   }
   return hipErrorInvalidValue;

@@ -85,6 +85,8 @@ def test_null_arguments_are_einval(L):
     assert L.cd_layer_last_factors(None, ctypes.byref(P), ctypes.byref(R)) == cdl.CD_EINVAL
     f = ctypes.c_int()
     assert L.cd_layer_rank_deficient(None, ctypes.byref(f)) == cdl.CD_EINVAL
+    assert L.cd_group_set_timing(None, 1) == cdl.CD_EINVAL
+    assert L.cd_group_set_timing_kinds(None, b"gate") == cdl.CD_EINVAL
     assert L.cd_destroy(None) == cdl.CD_OK
     assert L.cd_group_destroy(None) == cdl.CD_OK
 

@@ -509,6 +509,41 @@ def test_packed_pointers_match_lists():
         Gp.pack(M[:1])
 
 
+def test_kernel_timing_brackets_only_the_named_kinds():
+    """Timing restricted to named kernel kinds records only those kinds, with
+    the launch counts of the unrestricted run; timing changes no result; an
+    unknown kind name is refused."""
+    m, n, r = 256, 384, 16
+    w = S.small_workload(m, n, r)
+    runs = []
+    for kinds in (None, "pick"):
+        L = cdl.Layer(m, n, r)
+        Gp = cdl.Group([L])
+        M, X, Q = _state(w, 0)
+        stream = S.GradientStream(w, 0, device="cpu")
+        if kinds == "pick":
+            upd = [k for k in runs[0][0] if k.startswith("update")]
+            assert len(upd) == 1
+            kinds = ["gate", upd[0]]
+        Gp.set_timing(True, kinds)
+        flags = [Gp.step([stream.next().to(DEV)], [M], [X], [Q], w.mu, w.eta, r)[1] for _ in range(3)]
+        kt = Gp.kernel_times()
+        Gp.set_timing(False)
+        torch.cuda.synchronize()
+        runs.append((kt, flags, [f64(t) for t in (M, X, Q)]))
+        if kinds is not None:
+            with pytest.raises(cdl.CurvaDionError):
+                Gp.set_timing(True, ["no_such_kind"])
+    (k_all, f_all, s_all), (k_sel, f_sel, s_sel) = runs
+    assert f_all == f_sel and f_all[0]
+    assert set(k_sel) == {"gate", [k for k in k_all if k.startswith("update")][0]}
+    for k, v in k_sel.items():
+        assert v["launches"] == k_all[k]["launches"] and v["total_ms"] > 0
+    assert len(k_all) > 5 and k_all["gate"]["launches"] == 3
+    for a, b in zip(s_all, s_sel):
+        assert np.array_equal(a, b)
+
+
 def test_wrong_operands_are_refused_before_any_work():
     """A transposed, mistyped or wrongly-sized operand raises ValueError in the
     binding; the layer's state (prev_norm, step counter) and every buffer stay
