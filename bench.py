@@ -63,6 +63,7 @@ KIND_BOUND = {
     "power_bq_bf16x3": ("mfma", "bf16", 3), "power_btp_bf16x3": ("mfma", "bf16", 3),
     "update_bf16": ("hbm", None, 1), "gram_bf16x6": ("mfma", "bf16", 6),
     "apply_bf16x6": ("mfma", "bf16", 6), "trtri_f64": ("mfma", "f64", 1),
+    "update_f32": ("hbm", None, 1),
 }
 POLICIES = {"rmmc": 0, "always": 1, "never": 2, "every_h": 3}
 
@@ -78,6 +79,7 @@ KIND_KERNEL = {
     "gate": (r"k_gate\b", _STREAM),
     "update_bf16": (r"k_update_pl<1,", _BF),
     "update_bf16x6": (r"k_update_pl<3,", _BF),
+    "update_f32": (r"k_update_vec<", ["k_update_vec.hip", "common.hpp"]),
     "cholesky_f64": (None, ["k_chol.hip", "mfma_tile.hpp", "common.hpp"]),
 }
 COPY_PATTERN = r"neg_kernel"          # the calibration copy: b = -a, fp32, elementwise

@@ -27,9 +27,12 @@
  *
  * Ordering: all work is ordered on the HIP stream passed to a step call
  * (NULL = the default stream).  A step blocks the calling host thread once,
- * after the RMMC gate, to read the decision back (the single device-to-host
- * crossing that stands in for the max all-reduce); it returns as soon as the
- * chosen branch is enqueued.  In a group with layers of several shapes (or
+ * after the RMMC gate, to read the gate's output back (the single
+ * device-to-host crossing that stands in for the max all-reduce).  Under the
+ * RMMC policy the branch is enqueued after that read, as it depends on it;
+ * the other policies fix the branch in advance and enqueue it before the
+ * read, so the GPU does not idle through the round trip.  The call returns
+ * once the branch is enqueued and the output read.  In a group with layers of several shapes (or
  * more than 32 layers of one shape) the sync branch runs each batch of layers
  * of one shape on its own stream: the caller's stream and up to three streams
  * the group owns (default priority), which wait for the caller's stream before

@@ -98,11 +98,12 @@ hipError_t dalloc(T** p, size_t count) {
 
 // ---- optional per-kernel timing (HIP events on the launch stream) ----------
 enum Kind { K_FORM, K_FORM_X, K_GATE, K_LOCAL, K_PBQ, K_PBQ_BF, K_GRAM, K_GRAM_BF, K_CHOL, K_TRSM, K_TRTRI,
-            K_APPLY_BF, K_PBTP, K_PBTP3, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_NKINDS };
+            K_APPLY_BF, K_PBTP, K_PBTP3, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_UPDATE_F32,
+            K_NKINDS };
 const char* const kKindName[K_NKINDS] = {
     "form_buffer", "form_buffer_local", "gate", "local_update", "power_bq_f64", "power_bq_bf16x3", "gram_f64",
     "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_bf16x6",
-    "power_btp_bf16x3", "reduce_splits", "colnorm", "update_bf16x6", "update_bf16"};
+    "power_btp_bf16x3", "reduce_splits", "colnorm", "update_bf16x6", "update_bf16", "update_f32"};
 static_assert(K_NKINDS <= 32, "the timing mask holds one bit per kind");
 
 // Timing events only measure: recording them without the system-scope fence
@@ -544,18 +545,37 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   // planes once, then streamed by the update.
   const int up = fast ? 1 : 3;
   const int rp = (r + 31) / 32 * 32;
+  // fp32 layers at r <= 32: the update runs on the fp32 vector units and
+  // reads P, R, Q as they are (no bf16 planes)
+  const bool vec_update = !fast && cd::update_vec_fits(r);
   // Q = ColumnNormalize(R), with the planes of R and Q in the same pass
   cd::ColnormArgs cn{};
   cn.n = n; cn.r = r; cn.nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
-  cn.S = up; cn.rp = rp;
+  cn.S = vec_update ? 0 : up; cn.rp = rp;
   for (int j = 0; j < nl; ++j) {
     cn.R[j] = lay(j)->R; cn.part[j] = lay(j)->colsq; cn.nrm[j] = lay(j)->colnrm; cn.Q[j] = Q[sel[j]];
     cn.Rpl[j] = lay(j)->planes + 3LL * m * rp;
     cn.Qpl[j] = lay(j)->planes + 3LL * m * rp + 3LL * n * rp;
   }
-  st = run(g, K_COLNORM, (12.0 + 4.0 * up) * nr * nl, 3.0 * nr * nl, s,
+  st = run(g, K_COLNORM, (12.0 + 4.0 * cn.S) * nr * nl, 3.0 * nr * nl, s,
            [&] { return cd::launch_colnorm(cn, nl, s); });
   if (st != CD_OK) return st;
+  const double ub = (16.0 + (eta_local_spec != 0.0f ? (g->g_bf16 ? 2.0 : 4.0) : 0.0)) * mn * nl;
+  if (vec_update) {
+    cd::UpdateVecArgs va{};
+    va.m = m; va.n = n; va.r = r;
+    va.one_minus_mu = static_cast<float>(1.0 - static_cast<double>(mu));
+    va.c = static_cast<float>(static_cast<double>(eta) * std::sqrt(static_cast<double>(m) / n));
+    va.g_bf16 = g->g_bf16 ? 1 : 0;
+    for (int j = 0; j < nl; ++j) {
+      va.G[j] = G[sel[j]];
+      va.gc[j] = static_cast<float>(lay(j)->d.eta_local_scale * static_cast<double>(eta_local_spec));
+      va.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * lay(j)->d.weight_decay);
+      va.M[j] = M[sel[j]]; va.X[j] = X[sel[j]];
+      va.P[j] = lay(j)->P; va.R[j] = lay(j)->R; va.Q[j] = Q[sel[j]];
+    }
+    return run(g, K_UPDATE_F32, ub, 4.0 * mn * r * nl, s, [&] { return cd::launch_update_vec(va, nl, s); });
+  }
   {
     cd::PlaneArgs pa{};
     pa.r = r; pa.rp = rp; pa.S = up;
@@ -578,7 +598,6 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
     ua.R[j] = lay(j)->planes + 3LL * m * rp;
     ua.Q[j] = lay(j)->planes + 3LL * m * rp + 3LL * n * rp;
   }
-  const double ub = (16.0 + (eta_local_spec != 0.0f ? (g->g_bf16 ? 2.0 : 4.0) : 0.0)) * mn * nl;
   return run(g, fast ? K_UPDATE_BF1 : K_UPDATE, ub, 4.0 * mn * r * nl, s,
              [&] { return cd::launch_update_planes(ua, nl, up, s); });
 }
@@ -679,93 +698,104 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
     cd_status st = run(g, K_GATE, 8.0 * g->L * g->nparts_stride, 0.0, s, [&] { return cd::launch_gate(ga, s); });
     if (st != CD_OK) return st;
   }
-  // 3. decision point
+  // 3. decision point: one device-to-host copy of the gate's output
   const size_t out_bytes = sizeof(cd::GateOut) + sizeof(double) * g->L;
   CD_HIP(hipMemcpyAsync(g->out_host, g->out_dev, out_bytes, hipMemcpyDeviceToHost, s));
   CD_HIP(hipEventRecord(g->ev, s));
+  for (cd_layer* L : g->layers) { L->step += 1; L->prev_zero = false; }
+
+  // 4. branch
+  auto enqueue_branch = [&](bool sync) -> cd_status {
+    if (sync) {
+      // Each unit's pipeline in stage order on its own stream: the first unit
+      // on the caller's stream, the others on the group's side streams, forked
+      // from the caller's stream here and joined back to it below.  Units are
+      // independent (no workspace is shared between layers), so the results do
+      // not depend on how their kernels interleave.
+      const int nu = static_cast<int>(g->units.size());
+      auto stream_of = [&](int u) -> hipStream_t {
+        const int k = u % (g->nside + 1);
+        return k == 0 ? s : g->side[k - 1];
+      };
+      if (g->nside > 0) {
+        CD_HIP(hipEventRecord(g->fork_ev, s));
+        for (int i = 0; i < g->nside; ++i) CD_HIP(hipStreamWaitEvent(g->side[i], g->fork_ev, 0));
+      }
+      for (int stage = 0; stage < 6; ++stage) {
+        for (int ui = 0; ui < nu; ++ui) {
+          const Unit& u = g->units[ui];
+          const hipStream_t su = stream_of(ui);
+          cd_status st = enqueue_sync(g, g->shapes[u.sc], u.sel, G, spec ? eta : 0.0f, M, X, Q, mu, eta, r,
+                                      stage, su);
+          if (st != CD_OK) return st;
+          if (stage == 1 || stage == 3) {
+            st = enqueue_factor(g, u, r, stage == 1 ? 0 : 1, su);
+            if (st != CD_OK) return st;
+          }
+          if (stage == 2) {
+            // P1 is complete for the unit: new directions for the columns of
+            // floored pass-0 pivots (layers without any return at once)
+            const int nl = static_cast<int>(u.sel.size());
+            const int mu_rows = g->shapes[u.sc].m;
+            st = run(g, K_CHOL, 4.0 * nl, 0.0, su, [&] {
+              return cd::launch_fill_dead(g->chol_tab + u.off, g->trsm_tab[0] + u.off, nl, mu_rows, r, su);
+            });
+            if (st != CD_OK) return st;
+          }
+        }
+      }
+      for (int i = 0; i < g->nside; ++i) {
+        CD_HIP(hipEventRecord(g->join_ev[i], g->side[i]));
+        CD_HIP(hipStreamWaitEvent(s, g->join_ev[i], 0));
+      }
+      for (cd_layer* Ly : g->layers) Ly->last_r = r;
+    } else if (!spec) {
+      for (const std::vector<int>& batch : g->sbatches) {
+        const int nl = static_cast<int>(batch.size());
+        cd::LocalArgs la{};
+        la.nl = nl;
+        long long total = 0, blocks = 0;
+        for (int j = 0; j < nl; ++j) {
+          const int li = batch[j];
+          const cd_layer* Ly = g->layers[li];
+          la.numel[j] = 1LL * Ly->d.m * Ly->d.n;
+          la.block0[j] = static_cast<int>(blocks);
+          blocks += blocks_for(la.numel[j]);
+          total += la.numel[j];
+          la.X[j] = X[li]; la.G[j] = G[li];
+          la.coef[j] = static_cast<float>(Ly->d.eta_local_scale * static_cast<double>(eta));
+          la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * Ly->d.weight_decay);
+        }
+        la.block0[nl] = static_cast<int>(blocks);
+        const double lb = static_cast<double>(total) * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
+        cd_status st = run(g, K_LOCAL, lb, 2.0 * total, s,
+                           [&] { return cd::launch_local_update(la, g->g_bf16, s); });
+        if (st != CD_OK) return st;
+      }
+    }
+    return CD_OK;
+  };
+  // ALWAYS, NEVER and EVERY_H fix the branch in advance: it is enqueued
+  // before the wait for the gate's output, so the GPU does not idle through
+  // the round trip.  The RMMC policy decides on the output.
+  bool sync = false;
+  const bool fixed = g->policy != CD_POLICY_RMMC;
+  if (fixed) {
+    sync = g->policy == CD_POLICY_ALWAYS_SYNC ||
+           (g->policy == CD_POLICY_EVERY_H && next_step % g->H == 0);
+    const cd_status st = enqueue_branch(sync);
+    if (st != CD_OK) return st;
+  }
   CD_HIP(hipEventSynchronize(g->ev));
   const cd::GateOut* go = static_cast<const cd::GateOut*>(g->out_host);
   const double* rm = reinterpret_cast<const double*>(go + 1);
-  for (cd_layer* L : g->layers) { L->step += 1; L->prev_zero = false; }
-  const long long step = g->layers[0]->step;
-  bool sync = false;
-  switch (g->policy) {
-    case CD_POLICY_RMMC: sync = go->flag != 0; break;
-    case CD_POLICY_ALWAYS_SYNC: sync = true; break;
-    case CD_POLICY_NEVER_SYNC: sync = false; break;
-    case CD_POLICY_EVERY_H: sync = (step % g->H) == 0; break;
-  }
   const double gmax = go->g;
   const bool nonfinite = go->nonfinite != 0;
   if (rmmc_per_layer) std::memcpy(rmmc_per_layer, rm, sizeof(double) * g->L);
-
-  // 4. branch
-  if (sync) {
-    // Each unit's pipeline in stage order on its own stream: the first unit
-    // on the caller's stream, the others on the group's side streams, forked
-    // from the caller's stream here and joined back to it below.  Units are
-    // independent (no workspace is shared between layers), so the results do
-    // not depend on how their kernels interleave.
-    const int nu = static_cast<int>(g->units.size());
-    auto stream_of = [&](int u) -> hipStream_t {
-      const int k = u % (g->nside + 1);
-      return k == 0 ? s : g->side[k - 1];
-    };
-    if (g->nside > 0) {
-      CD_HIP(hipEventRecord(g->fork_ev, s));
-      for (int i = 0; i < g->nside; ++i) CD_HIP(hipStreamWaitEvent(g->side[i], g->fork_ev, 0));
-    }
-    for (int stage = 0; stage < 6; ++stage) {
-      for (int ui = 0; ui < nu; ++ui) {
-        const Unit& u = g->units[ui];
-        const hipStream_t su = stream_of(ui);
-        cd_status st = enqueue_sync(g, g->shapes[u.sc], u.sel, G, spec ? eta : 0.0f, M, X, Q, mu, eta, r,
-                                    stage, su);
-        if (st != CD_OK) return st;
-        if (stage == 1 || stage == 3) {
-          st = enqueue_factor(g, u, r, stage == 1 ? 0 : 1, su);
-          if (st != CD_OK) return st;
-        }
-        if (stage == 2) {
-          // P1 is complete for the unit: new directions for the columns of
-          // floored pass-0 pivots (layers without any return at once)
-          const int nl = static_cast<int>(u.sel.size());
-          const int mu_rows = g->shapes[u.sc].m;
-          st = run(g, K_CHOL, 4.0 * nl, 0.0, su, [&] {
-            return cd::launch_fill_dead(g->chol_tab + u.off, g->trsm_tab[0] + u.off, nl, mu_rows, r, su);
-          });
-          if (st != CD_OK) return st;
-        }
-      }
-    }
-    for (int i = 0; i < g->nside; ++i) {
-      CD_HIP(hipEventRecord(g->join_ev[i], g->side[i]));
-      CD_HIP(hipStreamWaitEvent(s, g->join_ev[i], 0));
-    }
-    for (cd_layer* Ly : g->layers) Ly->last_r = r;
-  } else if (!spec) {
-    for (const std::vector<int>& batch : g->sbatches) {
-      const int nl = static_cast<int>(batch.size());
-      cd::LocalArgs la{};
-      la.nl = nl;
-      long long total = 0, blocks = 0;
-      for (int j = 0; j < nl; ++j) {
-        const int li = batch[j];
-        const cd_layer* Ly = g->layers[li];
-        la.numel[j] = 1LL * Ly->d.m * Ly->d.n;
-        la.block0[j] = static_cast<int>(blocks);
-        blocks += blocks_for(la.numel[j]);
-        total += la.numel[j];
-        la.X[j] = X[li]; la.G[j] = G[li];
-        la.coef[j] = static_cast<float>(Ly->d.eta_local_scale * static_cast<double>(eta));
-        la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * Ly->d.weight_decay);
-      }
-      la.block0[nl] = static_cast<int>(blocks);
-      const double lb = static_cast<double>(total) * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
-      cd_status st = run(g, K_LOCAL, lb, 2.0 * total, s,
-                         [&] { return cd::launch_local_update(la, g->g_bf16, s); });
-      if (st != CD_OK) return st;
-    }
+  if (!fixed) {
+    sync = go->flag != 0;
+    const cd_status st = enqueue_branch(sync);
+    if (st != CD_OK) return st;
   }
   g->predict_skip = !sync;
   if (out) { out->rmmc = gmax; out->sync_flag = sync ? 1 : 0; }

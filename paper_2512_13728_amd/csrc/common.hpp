@@ -167,8 +167,11 @@ hipError_t launch_colnorm(const ColnormArgs& a, int nl, hipStream_t s);
 
 // ---- error-feedback momentum and weight update ------------------------------
 // M = M - (1-mu) P R^T (M holds B on entry); X = X - c P Q^T, c = eta sqrt(m/n)
-struct UpdateArgs {
-  int m, n, r;
+// fp32 operands on the vector units, for r <= 32 (k_update_vec): P m x r,
+// R and Q n x r, all fp32 row-major; band = rows per block (set by the
+// launcher)
+struct UpdateVecArgs {
+  int m, n, r, band;
   float one_minus_mu;
   float c;
   float* M[MAXB];
@@ -176,7 +179,13 @@ struct UpdateArgs {
   const float* P[MAXB];
   const float* R[MAXB];
   const float* Q[MAXB];
+  const void* G[MAXB];   // reversal of a speculative skip update, as below
+  float gc[MAXB];
+  int g_bf16;
+  float xdecay[MAXB];
 };
+bool update_vec_fits(int r);
+hipError_t launch_update_vec(UpdateVecArgs a, int nl, hipStream_t s);
 // bf16 planes of fp32 matrices (rows x r): plane s (s < S <= 3) holds the
 // s-th bf16 piece of each value, rows padded to rp (multiple of 32) with zeros.
 struct PlaneArgs {

@@ -123,7 +123,8 @@ __global__ __launch_bounds__(256) void k_colscale_planes(ColnormArgs a) {
 
 hipError_t launch_colnorm(const ColnormArgs& a, int nl, hipStream_t s) {
   if (nl <= 0) return hipSuccess;
-  if (a.rp % 32 != 0 || a.rp < a.r || a.S < 1 || a.S > 3) return hipErrorInvalidValue;
+  // S = 0: no planes (the fp32 vector update reads R and Q themselves)
+  if (a.rp % 32 != 0 || a.rp < a.r || a.S < 0 || a.S > 3) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_colsq, dim3(a.nchunks, (a.r + 255) / 256, nl), dim3(256), 0, s, a);
   hipLaunchKernelGGL(k_colnorm_final, dim3((a.r + CN_COLS - 1) / CN_COLS, 1, nl), dim3(256), 0, s, a);
   long long quads = static_cast<long long>(a.n) * (a.rp / 4);

@@ -133,7 +133,10 @@ def test_rmmc_exactly_zero_and_deterministic():
 
 
 @pytest.mark.parametrize("m,n,r", [(256, 256, 16), (300, 1000, 37), (1000, 300, 64), (64, 64, 64),
-                                   (97, 513, 1), (2048, 768, 192), (513, 640, 130)])
+                                   (97, 513, 1), (2048, 768, 192), (513, 640, 130),
+                                   # fp32 vector update (r <= 32): ragged column strips of
+                                   # four and of two columns per lane, a tall narrow matrix
+                                   (97, 515, 5), (130, 259, 20), (8197, 6, 3), (300, 1000, 32)])
 def test_sync_step_teacher_forced(m, n, r):
     w = S.small_workload(m, n, r, k=max(2, r // 2))
     M, X, Q = _state(w, 0)
