@@ -14,9 +14,10 @@ Prints ONE JSON line: params updated per second (whole job), per-branch step
 times, the roofline of the kernel with the largest share of the trajectory,
 and the float64 oracle timed on this host's cores on a bounded sample.  An
 untimed profiling pass of the same K steps brackets every launch with HIP
-events (inside the library) to find that kernel and the per-kind table; the
-timed pass then brackets only that kernel's launches, since each bracketed
-launch idles the GPU for several microseconds.
+events (inside the library; the sync branch's shape batches then run one
+after another) to find that kernel and the per-kind table; the timed pass
+then brackets only that kernel's launches, since each bracketed launch idles
+the GPU for several microseconds.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--policy rmmc|always|never]
 
@@ -435,14 +436,16 @@ def main():
         group.set_timing(False)
         return flags, rmmcs, step_ms, wall, kt
 
-    # An untimed profiling pass of the same K steps brackets every launch: the
-    # per-kind table and the dominant kernel.  The events idle the GPU for
-    # several microseconds at each bracketed launch, so the timed pass brackets
-    # only the dominant kernel's launches.
+    # An untimed profiling pass of the same K steps brackets every launch (the
+    # library then runs the sync branch's shape batches one after another, so
+    # that each interval times its kernel alone): the per-kind table and the
+    # dominant kernel.  The events idle the GPU for several microseconds at
+    # each bracketed launch, so the timed pass, on the untimed schedule,
+    # brackets only the dominant kernel's launches.
     _, _, _, prof_wall, kt = trajectory(None)
     dom = max(kt.items(), key=lambda kv: kv[1]["total_ms"])[0]
     log(f"[bench] profiling pass: {K} steps in {prof_wall * 1e3:.2f} ms with every launch "
-        f"bracketed; dominant kernel {dom}")
+        f"bracketed (sync batches serial); dominant kernel {dom}")
     flags, rmmcs, step_ms, elapsed, kt_dom = trajectory([dom])
     log(f"[bench] timed {K} steps in {elapsed * 1e3:.2f} ms; syncs at "
         f"{[t + 1 for t, f in enumerate(flags) if f]}")

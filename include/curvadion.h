@@ -173,7 +173,11 @@ cd_status cd_layer_rank_deficient(const cd_layer* layer, int* flag);
 
 /* Kernel timing, for measurement.  While timing is on, every kernel launch of
  * the group's steps is bracketed by two HIP events recorded on the launch
- * stream.  cd_group_kernel_times() waits for the last recorded event, then
+ * stream.  While every kind is bracketed (the default), the sync branch runs
+ * its batches one after another on the caller's stream, so that each interval
+ * times its kernel alone; with a narrower selection (see below) the schedule
+ * is the untimed one, and a bracketed sync-branch launch also counts the time
+ * it waits for CUs that kernels of other batches hold.  cd_group_kernel_times() waits for the last recorded event, then
  * returns one entry per kernel kind that ran since timing was switched on (or
  * since the previous query): launch count, summed event time, and the
  * algorithmic bytes and flops of those launches (compulsory traffic of the

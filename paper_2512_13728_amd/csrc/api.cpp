@@ -712,14 +712,19 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
       // from the caller's stream here and joined back to it below.  Units are
       // independent (no workspace is shared between layers), so the results do
       // not depend on how their kernels interleave.
+      // While every kernel kind is bracketed by timing events, the units run
+      // one after another on the caller's stream, so that each bracketed
+      // launch times its kernel alone (not its wait for CUs that another
+      // stream's kernels hold).
       const int nu = static_cast<int>(g->units.size());
+      const int nside = (g->timer.on && g->timer.mask == ~0u) ? 0 : g->nside;
       auto stream_of = [&](int u) -> hipStream_t {
-        const int k = u % (g->nside + 1);
+        const int k = u % (nside + 1);
         return k == 0 ? s : g->side[k - 1];
       };
-      if (g->nside > 0) {
+      if (nside > 0) {
         CD_HIP(hipEventRecord(g->fork_ev, s));
-        for (int i = 0; i < g->nside; ++i) CD_HIP(hipStreamWaitEvent(g->side[i], g->fork_ev, 0));
+        for (int i = 0; i < nside; ++i) CD_HIP(hipStreamWaitEvent(g->side[i], g->fork_ev, 0));
       }
       for (int stage = 0; stage < 6; ++stage) {
         for (int ui = 0; ui < nu; ++ui) {
@@ -744,7 +749,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
           }
         }
       }
-      for (int i = 0; i < g->nside; ++i) {
+      for (int i = 0; i < nside; ++i) {
         CD_HIP(hipEventRecord(g->join_ev[i], g->side[i]));
         CD_HIP(hipStreamWaitEvent(s, g->join_ev[i], 0));
       }

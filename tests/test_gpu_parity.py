@@ -547,6 +547,37 @@ def test_kernel_timing_brackets_only_the_named_kinds():
         assert np.array_equal(a, b)
 
 
+def test_full_timing_runs_batches_serially_with_identical_results():
+    """With every kernel kind timed, the shape batches of the sync branch run
+    one after another on the caller's stream; the results are bit-identical
+    to the untimed (concurrent) schedule, and the per-kind table covers the
+    sync-branch kernels of every batch."""
+    shapes = [(256, 384), (384, 256), (100, 300)]
+    r = 16
+    w = S.Workload("timing", tuple(shapes), r=r, grad_dtype="f32", steps=3, k=8, tau=0.3, stream_id=93)
+    outs = []
+    for timed in (False, True):
+        Gp = cdl.Group([cdl.Layer(m, n, r, tau=0.3) for m, n in shapes])
+        st = [_state(w, i) for i in range(len(shapes))]
+        M, X, Q = [t[0] for t in st], [t[1] for t in st], [t[2] for t in st]
+        streams = [S.GradientStream(w, i, device="cpu") for i in range(len(shapes))]
+        if timed:
+            Gp.set_timing(True)
+        res = [Gp.step([s.next().to(DEV) for s in streams], M, X, Q, w.mu, w.eta, r)[:2]
+               for _ in range(w.steps)]
+        kt = Gp.kernel_times() if timed else None
+        Gp.set_timing(False)
+        torch.cuda.synchronize()
+        outs.append((res, [f64(t) for t in M + X + Q], kt))
+    assert outs[0][0] == outs[1][0] and outs[0][0][0][1]
+    for a, b in zip(outs[0][1], outs[1][1]):
+        assert np.array_equal(a, b)
+    kt = outs[1][2]
+    n_sync = sum(f for _, f in outs[0][0])
+    # one update launch per shape batch and sync step
+    assert kt["update_f32"]["launches"] == len(shapes) * n_sync
+
+
 def test_wrong_operands_are_refused_before_any_work():
     """A transposed, mistyped or wrongly-sized operand raises ValueError in the
     binding; the layer's state (prev_norm, step counter) and every buffer stay
