@@ -228,7 +228,7 @@ def summarize_pmc(fdir: str, wdir: str, out: str, workload: str, cal_mib: int):
              f"#   python3 bench.py --summarize-pmc {fdir} {wdir} {out} --copy-calibration {cal_mib}",
              f"# calibration: a streaming copy (b = -a, fp32) of {cal_bytes} B read + {cal_bytes} B written;",
              f"#   FETCH_SIZE x {factor['FETCH_SIZE']:.4f} and WRITE_SIZE x {factor['WRITE_SIZE']:.4f} give bytes",
-             "# all dispatches of the run (warmup and timed steps); bytes are scaled, per dispatch", "",
+             "# all dispatches of the run (warmup steps, profiling pass, timed pass); bytes are scaled, per dispatch", "",
              f"{'kernel':64s} {'disp':>5s} {'fetch_MB':>10s} {'write_MB':>10s}"]
     for name, t in sorted(table.items(), key=lambda kv: -sum(kv[1]["FETCH_SIZE"]) - sum(kv[1]["WRITE_SIZE"])):
         nf = max(len(t["FETCH_SIZE"]), 1)
