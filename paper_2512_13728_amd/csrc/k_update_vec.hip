@@ -1,8 +1,8 @@
 // The M / X update of the Dion sync branch (Algorithm 1 / Algorithm 2) for
 // fp32-gradient layers at small rank (r <= 32), on the fp32 vector units:
 //   M = B - (1 - mu) P R^T,    X -= eta sqrt(m/n) P Q^T
-// At r <= 32 the correction costs 4r flops per element, far under what the
-// vector units give per streamed byte, so the kernel only has to stream M
+// At r <= 32 the correction costs at most 4r = 128 flops per element, well
+// under what the vector units give per streamed byte, so the kernel only has to stream M
 // and X at the HBM rate.  Each lane holds its column's rows of R and Q in
 // registers for the whole launch; the row of P is the same for a whole wave
 // (broadcast across the lanes); M and X move with non-temporal accesses.
@@ -91,6 +91,8 @@ __global__ __launch_bounds__(256) void k_update_vec(UpdateVecArgs u) {
 
 }  // namespace
 
+// up to r = 32: at r = 48 and 64 this form took 0.49-0.50 ms on 4096 x 16384
+// (189 VGPRs, two waves per SIMD) against 0.36 ms for the bf16-split MFMA update
 bool update_vec_fits(int r) { return r >= 1 && r <= 32; }
 
 hipError_t launch_update_vec(UpdateVecArgs u, int nl, hipStream_t s) {

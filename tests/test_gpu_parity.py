@@ -136,7 +136,8 @@ def test_rmmc_exactly_zero_and_deterministic():
                                    (97, 513, 1), (2048, 768, 192), (513, 640, 130),
                                    # fp32 vector update (r <= 32): ragged column strips of
                                    # four and of two columns per lane, a tall narrow matrix
-                                   (97, 515, 5), (130, 259, 20), (8197, 6, 3), (300, 1000, 32)])
+                                   (97, 515, 5), (130, 259, 20), (8197, 6, 3), (300, 1000, 32),
+                                   (257, 333, 48)])
 def test_sync_step_teacher_forced(m, n, r):
     w = S.small_workload(m, n, r, k=max(2, r // 2))
     M, X, Q = _state(w, 0)
