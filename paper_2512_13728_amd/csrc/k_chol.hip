@@ -15,6 +15,8 @@
 //   chol_trail W[k+1:, k+1:] -= X^T X, upper tiles only            (fp64 MFMA)
 // and the triangular solve, one launch per block column c:
 //   P[:, c] = (P~[:, c] - P[:, :c] T[:c, c]) D_c                   (fp64 MFMA)
+#include <type_traits>
+
 #include "common.hpp"
 #include "mfma_tile.hpp"
 
@@ -46,6 +48,7 @@ constexpr int CB = CHOL_BLOCK;
 // zero in those columns (k_fill_dead then gives them new directions).
 constexpr int TLD = CB + 1;   // padded row of T in LDS (column stores hit distinct banks)
 constexpr int TPAD = CB;      // leading doubles: back-substitution reads above row 0 stay in the array
+constexpr int SEG = 16;       // pivots per segment of the diagonal-block loops
 
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
                                                   int pass) {
@@ -81,10 +84,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
   rowb[CB + j] = 0.0;
   Tsb[j] = 0.0;
   bool def = false;
-  // only the block's nb pivots: the identity padding of a last, partial block
-  // would factor to itself, and its rows are never stored
-#pragma unroll 1
-  for (int p = 0; p < nb; ++p) {
+  // Only the block's nb pivots run: the identity padding of a last, partial
+  // block would factor to itself, and its rows are never stored.  At pivot p
+  // only rows p .. 63 remain, so the pivots run in four segments of SEG whose
+  // register arrays carry 64, 48, 32 and 16 rows (five eighths of the
+  // full-width work; rows past the live range stay untouched and unused).
+  auto pivot = [&](auto na, int p) {
+    constexpr int NA = decltype(na)::value;
     // the pivot A[p][p] is lane p's a[0]: read across the wave (no LDS trip)
     const double a0 = a[0];
     double d = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(a0), p),
@@ -112,17 +118,31 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     // rows below p: A[p + i][j] -= T[p][p + i] T[p][j], shifted up one row;
     // lanes j < p + i only touch the (unused) lower triangle.  The row is read
     // whole before the update (one LDS round trip, not one per pair).
-    double rv[CB];
+    double rv[NA];
 #pragma unroll
-    for (int i = 1; i < CB; ++i) rv[i] = rowb[p + i];
+    for (int i = 1; i < NA; ++i) rv[i] = rowb[p + i];
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int i = 1; i < CB; ++i) a[i - 1] = fma(-rv[i], tp, a[i]);
-    a[CB - 1] = 0.0;
+    for (int i = 1; i < NA; ++i) a[i - 1] = fma(-rv[i], tp, a[i]);
+    a[NA - 1] = 0.0;
     __syncthreads();
-  }
+  };
+  using I64 = std::integral_constant<int, CB>;
+  using I48 = std::integral_constant<int, CB - SEG>;
+  using I32 = std::integral_constant<int, CB - 2 * SEG>;
+  using I16 = std::integral_constant<int, CB - 3 * SEG>;
+#pragma unroll 1
+  for (int p = 0; p < min(nb, SEG); ++p) pivot(I64{}, p);
+#pragma unroll 1
+  for (int p = SEG; p < min(nb, 2 * SEG); ++p) pivot(I48{}, p);
+#pragma unroll 1
+  for (int p = 2 * SEG; p < min(nb, 3 * SEG); ++p) pivot(I32{}, p);
+#pragma unroll 1
+  for (int p = 3 * SEG; p < nb; ++p) pivot(I16{}, p);
+
   // f[k] = d[p - k] at step p, from p = nb - 1 down; entries with k > p lie
-  // above row 0 and are never stored
+  // above row 0 and are never stored, so the steps of pivots below
+  // 64 - SEG s carry only 64 - SEG s entries
   double f[CB];
 #pragma unroll
   for (int k = 0; k < CB; ++k) f[k] = k == nb - 1 - j ? 1.0 : 0.0;
@@ -132,19 +152,27 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
   // zero right of the diagonal, column j != p of T^{-1} is zero in row p)
   const bool cin = j < nb && okb[j];
   for (int p = nb; p < CB; ++p) D[p * CB + j] = 0.0;   // rows past a partial block
-#pragma unroll 1
-  for (int p = nb - 1; p >= 0; --p) {
+  auto back = [&](auto nf, int p) {
+    constexpr int NF = decltype(nf)::value;
     const double x = f[0] * pinv[p];
     D[p * CB + j] = cin ? x : 0.0;
     const double* col = Ts + p * TLD + p;   // col[-k] = T[p - k][p]
-    double cv[CB];
+    double cv[NF];
 #pragma unroll
-    for (int k = 1; k < CB; ++k) cv[k] = col[-k];
+    for (int k = 1; k < NF; ++k) cv[k] = col[-k];
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int k = 1; k < CB; ++k) f[k - 1] = fma(-cv[k], x, f[k]);
-    f[CB - 1] = 0.0;
-  }
+    for (int k = 1; k < NF; ++k) f[k - 1] = fma(-cv[k], x, f[k]);
+    f[NF - 1] = 0.0;
+  };
+#pragma unroll 1
+  for (int p = nb - 1; p >= 3 * SEG; --p) back(I64{}, p);
+#pragma unroll 1
+  for (int p = min(nb, 3 * SEG) - 1; p >= 2 * SEG; --p) back(I48{}, p);
+#pragma unroll 1
+  for (int p = min(nb, 2 * SEG) - 1; p >= SEG; --p) back(I32{}, p);
+#pragma unroll 1
+  for (int p = min(nb, SEG) - 1; p >= 0; --p) back(I16{}, p);
 #pragma unroll 4
   for (int i = 0; i < nb; ++i)
     if (j < nb && i <= j) t.W[(k0 + i) * ld + k0 + j] = Ts[j * TLD + i];
