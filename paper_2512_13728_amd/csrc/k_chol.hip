@@ -16,6 +16,7 @@
 // and the triangular solve, one launch per block column c:
 //   P[:, c] = (P~[:, c] - P[:, :c] T[:c, c]) D_c                   (fp64 MFMA)
 #include <type_traits>
+#include <utility>
 
 #include "common.hpp"
 #include "mfma_tile.hpp"
@@ -48,7 +49,17 @@ constexpr int CB = CHOL_BLOCK;
 // zero in those columns (k_fill_dead then gives them new directions).
 constexpr int TLD = CB + 1;   // padded row of T in LDS (column stores hit distinct banks)
 constexpr int TPAD = CB;      // leading doubles: back-substitution reads above row 0 stay in the array
-constexpr int SEG = 16;       // pivots per segment of the diagonal-block loops
+constexpr int SEG = 8;        // pivots per segment of the diagonal-block loops
+
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>), in order
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
                                                   int pass) {
@@ -86,9 +97,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
   bool def = false;
   // Only the block's nb pivots run: the identity padding of a last, partial
   // block would factor to itself, and its rows are never stored.  At pivot p
-  // only rows p .. 63 remain, so the pivots run in four segments of SEG whose
-  // register arrays carry 64, 48, 32 and 16 rows (five eighths of the
-  // full-width work; rows past the live range stay untouched and unused).
+  // only rows p .. 63 remain, so the pivots run in segments of SEG whose
+  // register arrays carry 64, 64 - SEG, ... rows (rows past the live range
+  // stay untouched and unused).
   auto pivot = [&](auto na, int p) {
     constexpr int NA = decltype(na)::value;
     // the pivot A[p][p] is lane p's a[0]: read across the wave (no LDS trip)
@@ -127,18 +138,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     a[NA - 1] = 0.0;
     __syncthreads();
   };
-  using I64 = std::integral_constant<int, CB>;
-  using I48 = std::integral_constant<int, CB - SEG>;
-  using I32 = std::integral_constant<int, CB - 2 * SEG>;
-  using I16 = std::integral_constant<int, CB - 3 * SEG>;
+  // segment s: pivots [s SEG, (s + 1) SEG) with CB - s SEG live rows
+  static_for<CB / SEG>([&](auto sc) {
+    constexpr int S = decltype(sc)::value;
 #pragma unroll 1
-  for (int p = 0; p < min(nb, SEG); ++p) pivot(I64{}, p);
-#pragma unroll 1
-  for (int p = SEG; p < min(nb, 2 * SEG); ++p) pivot(I48{}, p);
-#pragma unroll 1
-  for (int p = 2 * SEG; p < min(nb, 3 * SEG); ++p) pivot(I32{}, p);
-#pragma unroll 1
-  for (int p = 3 * SEG; p < nb; ++p) pivot(I16{}, p);
+    for (int p = S * SEG; p < min(nb, (S + 1) * SEG); ++p) pivot(std::integral_constant<int, CB - S * SEG>{}, p);
+  });
 
   // f[k] = d[p - k] at step p, from p = nb - 1 down; entries with k > p lie
   // above row 0 and are never stored, so the steps of pivots below
@@ -165,14 +170,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     for (int k = 1; k < NF; ++k) f[k - 1] = fma(-cv[k], x, f[k]);
     f[NF - 1] = 0.0;
   };
+  // segments from the last down: segment s carries (s + 1) SEG entries
+  static_for<CB / SEG>([&](auto ic) {
+    constexpr int S = CB / SEG - 1 - decltype(ic)::value;
 #pragma unroll 1
-  for (int p = nb - 1; p >= 3 * SEG; --p) back(I64{}, p);
-#pragma unroll 1
-  for (int p = min(nb, 3 * SEG) - 1; p >= 2 * SEG; --p) back(I48{}, p);
-#pragma unroll 1
-  for (int p = min(nb, 2 * SEG) - 1; p >= SEG; --p) back(I32{}, p);
-#pragma unroll 1
-  for (int p = min(nb, SEG) - 1; p >= 0; --p) back(I16{}, p);
+    for (int p = min(nb, (S + 1) * SEG) - 1; p >= S * SEG; --p) back(std::integral_constant<int, (S + 1) * SEG>{}, p);
+  });
 #pragma unroll 4
   for (int i = 0; i < nb; ++i)
     if (j < nb && i <= j) t.W[(k0 + i) * ld + k0 + j] = Ts[j * TLD + i];
