@@ -2,7 +2,7 @@
 // group lifetimes, workspace, launch planning and the per-step schedule.
 //
 // One group step (Algorithm 2 of the paper):
-//   1. B = M + G with per-block partial sums of B^2, up to MAXB layers of
+//   1. B = M + G with per-block partial sums of B^2, up to MAXS layers of
 //      any shapes per launch
 //   2. gate kernel: fixed-order norms, RMMC_l, prev_norm update, max, flag
 //   3. one device-to-host copy of {max, flag, RMMC_l}: the decision point that
@@ -13,7 +13,7 @@
 //      ColumnNormalize; M/X update.  The latency-bound factorisation of one
 //      unit overlaps the GEMMs of the others.
 //      local branch: X -= eta_local G (M already holds B).
-// The streaming passes take up to MAXB layers of any shapes per launch; the
+// The streaming passes take up to MAXS layers of any shapes per launch; the
 // sync branch's kernels take layers of equal (m, n) (up to MAXB per launch).
 #include <hip/hip_runtime.h>
 
@@ -210,7 +210,7 @@ struct cd_group {
   hipEvent_t ev = nullptr;
   std::vector<Unit> units;
   // the streaming passes (buffer formation, local update): batches of up to
-  // MAXB layers of any shapes, in group order, each at most 2^30 blocks
+  // MAXS layers of any shapes, in group order, each at most 2^30 blocks
   std::vector<std::vector<int>> sbatches;
   cd::CholTab* chol_tab = nullptr;      // [L] static workspace pointers, in unit order
   cd::TrsmTab* trsm_tab[3] = {nullptr, nullptr, nullptr};  // P1 = P~ T^-1; U = T^-1; P = P1 T^-1
@@ -329,7 +329,7 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
     long long total = 0;
     if (!g->sbatches.empty())
       for (int li : g->sbatches.back()) total += blocks_for(1LL * layers[li]->d.m * layers[li]->d.n);
-    if (g->sbatches.empty() || static_cast<int>(g->sbatches.back().size()) == cd::MAXB ||
+    if (g->sbatches.empty() || static_cast<int>(g->sbatches.back().size()) == cd::MAXS ||
         total + nb > (1LL << 30))
       g->sbatches.emplace_back();
     g->sbatches.back().push_back(i);

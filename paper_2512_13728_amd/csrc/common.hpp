@@ -11,37 +11,41 @@
 
 namespace cd {
 
-constexpr int MAXB = 32;          // layers per batched launch
+constexpr int MAXB = 32;          // layers per batched launch of the sync branch (one shape)
+// layers per launch of the streaming passes (any shapes): 64 gave the 160M
+// set's skip step 2% (one launch instead of two) and cost the 1.3B set's 1.7%
+// (64 + 32 layers instead of 3 x 32)
+constexpr int MAXS = 32;
 constexpr int NTHREADS = 256;     // threads per block for the streaming kernels
 constexpr int GBK = 32;           // GEMM k per LDS stage; split-K slices are multiples
 
 // ---- a1: B = M + G and per-block sum of B^2 -------------------------------
 // Every block covers FORM_CHUNK consecutive elements of one layer; one launch
-// covers up to MAXB layers of any shapes (the passes are elementwise), layer
+// covers up to MAXS layers of any shapes (the passes are elementwise), layer
 // j owning blocks [block0[j], block0[j + 1]).
 constexpr int FORM_CHUNK = NTHREADS * 4 * 4;   // 4096 elements
 struct FormArgs {
   int nl;                          // layers in this launch
-  long long numel[MAXB];           // elements of each layer (m*n)
-  int block0[MAXB + 1];            // first block of each layer; block0[nl] = blocks of the launch
-  float* M[MAXB];                  // in: M_{t-1}; out: B_t
-  const void* G[MAXB];             // fp32 or bf16
-  double* part[MAXB];              // out: ceil(numel / FORM_CHUNK) partial sums of B^2 per layer
-  float* X[MAXB];                  // with_x: the skip-branch update X = xdecay X - coef G, fused
-  float coef[MAXB];                // eta_local per layer (with_x only)
-  float xdecay[MAXB];              // 1 - eta * weight_decay per layer (with_x only)
+  long long numel[MAXS];           // elements of each layer (m*n)
+  int block0[MAXS + 1];            // first block of each layer; block0[nl] = blocks of the launch
+  float* M[MAXS];                  // in: M_{t-1}; out: B_t
+  const void* G[MAXS];             // fp32 or bf16
+  double* part[MAXS];              // out: ceil(numel / FORM_CHUNK) partial sums of B^2 per layer
+  float* X[MAXS];                  // with_x: the skip-branch update X = xdecay X - coef G, fused
+  float coef[MAXS];                // eta_local per layer (with_x only)
+  float xdecay[MAXS];              // 1 - eta * weight_decay per layer (with_x only)
 };
 hipError_t launch_form_buffer(const FormArgs& a, bool g_bf16, bool with_x, hipStream_t s);
 
 // ---- local branch: X = X - eta_local G --------------------------------------
 struct LocalArgs {                 // launch layout as FormArgs
   int nl;
-  long long numel[MAXB];
-  int block0[MAXB + 1];
-  float* X[MAXB];
-  const void* G[MAXB];
-  float coef[MAXB];                // eta_local per layer
-  float xdecay[MAXB];              // 1 - eta * weight_decay per layer
+  long long numel[MAXS];
+  int block0[MAXS + 1];
+  float* X[MAXS];
+  const void* G[MAXS];
+  float coef[MAXS];                // eta_local per layer
+  float xdecay[MAXS];              // 1 - eta * weight_decay per layer
 };
 hipError_t launch_local_update(const LocalArgs& a, bool g_bf16, hipStream_t s);
 

@@ -253,7 +253,7 @@ __global__ __launch_bounds__(GATE_THREADS) void k_gate(GateArgs a) {
 }  // namespace
 
 hipError_t launch_form_buffer(const FormArgs& a, bool g_bf16, bool with_x, hipStream_t s) {
-  if (a.nl <= 0 || a.nl > MAXB || a.block0[a.nl] <= 0) return a.nl == 0 ? hipSuccess : hipErrorInvalidValue;
+  if (a.nl <= 0 || a.nl > MAXS || a.block0[a.nl] <= 0) return a.nl == 0 ? hipSuccess : hipErrorInvalidValue;
   const dim3 grid(a.block0[a.nl]), block(NTHREADS);
   if (g_bf16) {
     if (with_x) hipLaunchKernelGGL((k_form_buffer<true, true>), grid, block, 0, s, a);
@@ -266,7 +266,7 @@ hipError_t launch_form_buffer(const FormArgs& a, bool g_bf16, bool with_x, hipSt
 }
 
 hipError_t launch_local_update(const LocalArgs& a, bool g_bf16, hipStream_t s) {
-  if (a.nl <= 0 || a.nl > MAXB || a.block0[a.nl] <= 0) return a.nl == 0 ? hipSuccess : hipErrorInvalidValue;
+  if (a.nl <= 0 || a.nl > MAXS || a.block0[a.nl] <= 0) return a.nl == 0 ? hipSuccess : hipErrorInvalidValue;
   const dim3 grid(a.block0[a.nl]), block(NTHREADS);
   if (g_bf16) hipLaunchKernelGGL(k_local_update<true>, grid, block, 0, s, a);
   else hipLaunchKernelGGL(k_local_update<false>, grid, block, 0, s, a);

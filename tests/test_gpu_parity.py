@@ -314,11 +314,12 @@ def test_group_mixed_shapes_rmmc_gate():
 
 
 def test_group_wider_than_one_launch():
-    """More layers of one shape than one launch takes (32): 40 of 96 x 160 and
-    3 of 130 x 70, so every stage runs in two chunks for the first shape and
-    the batched Cholesky covers 43 layers; sync and local steps against the
-    oracle, every layer checked."""
-    shapes = [(96, 160)] * 40 + [(130, 70)] * 3
+    """More layers than one launch takes: 40 of 96 x 160 and 30 of 130 x 70,
+    so the sync branch runs the first shape in two chunks (32 + 8 layers per
+    launch) and the streaming passes in three launches (32 + 32 + 6 layers, the
+    second of mixed shapes); sync and local steps against the oracle, every
+    layer checked."""
+    shapes = [(96, 160)] * 40 + [(130, 70)] * 30
     r = 16
     tau = 0.3
     w = S.Workload("wide", tuple(shapes), r=r, grad_dtype="f32", steps=6, k=4, tau=tau, stream_id=93)
