@@ -27,8 +27,9 @@
  *
  * Ordering: all work is ordered on the HIP stream passed to a step call
  * (NULL = the default stream).  A step blocks the calling host thread once,
- * after the RMMC gate, to read the gate's output back (the single
- * device-to-host crossing that stands in for the max all-reduce).  Under the
+ * after the RMMC gate, until the gate's output has reached the host (the gate
+ * kernel writes it into pinned host memory; this single device-to-host
+ * crossing stands in for the max all-reduce).  Under the
  * RMMC policy the branch is enqueued after that read, as it depends on it;
  * the other policies fix the branch in advance and enqueue it before the
  * read, so the GPU does not idle through the round trip.  The call returns

@@ -18,6 +18,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -206,7 +207,11 @@ struct cd_group {
   unsigned* counter = nullptr;  // gate completion counter (returns to zero)
   bool predict_skip = false;    // RMMC policy: branch predicted for the next step
   cd::GateOut* out_dev = nullptr;
-  void* out_host = nullptr;     // pinned
+  // pinned, coherent, mapped: GateOut, L doubles, then the sequence number the
+  // gate stores last; out_host_dev is the device view of the same memory
+  void* out_host = nullptr;
+  void* out_host_dev = nullptr;
+  unsigned long long seq = 0;
   hipEvent_t ev = nullptr;
   std::vector<Unit> units;
   // the streaming passes (buffer formation, local update): batches of up to
@@ -343,7 +348,10 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   if (e == hipSuccess) e = hipMemset(g->counter, 0, sizeof(unsigned));
   if (e == hipSuccess)
     e = hipMalloc(reinterpret_cast<void**>(&g->out_dev), sizeof(cd::GateOut) + sizeof(double) * n);
-  if (e == hipSuccess) e = hipHostMalloc(&g->out_host, sizeof(cd::GateOut) + sizeof(double) * n);
+  const size_t host_bytes = sizeof(cd::GateOut) + sizeof(double) * n + sizeof(unsigned long long);
+  if (e == hipSuccess) e = hipHostMalloc(&g->out_host, host_bytes, hipHostMallocMapped | hipHostMallocCoherent);
+  if (e == hipSuccess) std::memset(g->out_host, 0, host_bytes);
+  if (e == hipSuccess) e = hipHostGetDevicePointer(&g->out_host_dev, g->out_host, 0);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&g->ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipMemcpy(g->nparts, np.data(), sizeof(int) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->prev, pv.data(), sizeof(double*) * n, hipMemcpyHostToDevice);
@@ -694,13 +702,18 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   ga.L = g->L; ga.nparts_stride = g->nparts_stride; ga.parts = g->parts; ga.nparts = g->nparts;
   ga.prev = g->prev; ga.eps = g->eps; ga.tau = g->tau; ga.out = g->out_dev;
   ga.norms = g->norms; ga.counter = g->counter;
+  const size_t seq_off = sizeof(cd::GateOut) + sizeof(double) * g->L;
+  ga.host_out = static_cast<cd::GateOut*>(g->out_host_dev);
+  ga.host_seq = reinterpret_cast<unsigned long long*>(static_cast<char*>(g->out_host_dev) + seq_off);
+  ga.seq = ++g->seq;
   {
     cd_status st = run(g, K_GATE, 8.0 * g->L * g->nparts_stride, 0.0, s, [&] { return cd::launch_gate(ga, s); });
     if (st != CD_OK) return st;
   }
-  // 3. decision point: one device-to-host copy of the gate's output
-  const size_t out_bytes = sizeof(cd::GateOut) + sizeof(double) * g->L;
-  CD_HIP(hipMemcpyAsync(g->out_host, g->out_dev, out_bytes, hipMemcpyDeviceToHost, s));
+  // 3. decision point: the gate writes its output into pinned host memory and
+  // stores the step's sequence number last; the host polls that number (the
+  // event after the gate bounds the wait: once it has completed, the output
+  // is there or the step failed)
   CD_HIP(hipEventRecord(g->ev, s));
   for (cd_layer* L : g->layers) { L->step += 1; L->prev_zero = false; }
 
@@ -791,7 +804,18 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
     const cd_status st = enqueue_branch(sync);
     if (st != CD_OK) return st;
   }
-  CD_HIP(hipEventSynchronize(g->ev));
+  {
+    const volatile unsigned long long* hs = reinterpret_cast<const volatile unsigned long long*>(
+        static_cast<const char*>(g->out_host) + seq_off);
+    for (unsigned polls = 1; *hs != ga.seq; ++polls) {
+      if (polls % 4096 != 0) continue;
+      const hipError_t q = hipEventQuery(g->ev);
+      if (q == hipErrorNotReady) continue;
+      if (q != hipSuccess) return fail(CD_EHIP, "gate: %s", hipGetErrorString(q));
+      if (*hs != ga.seq) return fail(CD_EHIP, "gate output did not reach host memory");
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+  }
   const cd::GateOut* go = static_cast<const cd::GateOut*>(g->out_host);
   const double* rm = reinterpret_cast<const double*>(go + 1);
   const double gmax = go->g;

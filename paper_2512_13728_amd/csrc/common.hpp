@@ -50,7 +50,7 @@ struct LocalArgs {                 // launch layout as FormArgs
 hipError_t launch_local_update(const LocalArgs& a, bool g_bf16, hipStream_t s);
 
 // ---- gate: fixed-order reduction of the partials, RMMC, prev update, max ----
-struct GateOut {                   // device-side result, copied to the host
+struct GateOut {                   // result of the gate (device and host copies)
   double g;                        // max over layers of RMMC (NaN if any is NaN)
   int flag;                        // g > tau
   int nonfinite;                   // some ‖B‖ was NaN/Inf
@@ -67,6 +67,11 @@ struct GateArgs {
   GateOut* out;                    // + L doubles after the header
   double* norms;                   // [L] workspace: ‖B‖ per layer
   unsigned* counter;               // zero between launches (the last block resets it)
+  // the same result in pinned, coherent host memory (device view): header and
+  // L doubles, then `seq` at host_seq, stored after everything else is visible
+  GateOut* host_out;
+  unsigned long long* host_seq;
+  unsigned long long seq;
 };
 hipError_t launch_gate(const GateArgs& a, hipStream_t s);
 
