@@ -319,7 +319,7 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
+        print("bench.py measures one GPU: the library has no multi-GPU path "
               "(the data-parallel all-reduces are identities at one worker). "
               "Run without --gpus or with --gpus 1.", file=sys.stderr)
         sys.exit(2)
