@@ -215,7 +215,8 @@ struct cd_group {
   hipEvent_t ev = nullptr;
   std::vector<Unit> units;
   // the streaming passes (buffer formation, local update): batches of up to
-  // MAXS layers of any shapes, in group order, each at most 2^30 blocks
+  // MAXS layers of any shapes, in group order, each at most MAX_STREAM_BLOCKS
+  // blocks
   std::vector<std::vector<int>> sbatches;
   cd::CholTab* chol_tab = nullptr;      // [L] static workspace pointers, in unit order
   cd::TrsmTab* trsm_tab[3] = {nullptr, nullptr, nullptr};  // P1 = P~ T^-1; U = T^-1; P = P1 T^-1
@@ -335,7 +336,7 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
     if (!g->sbatches.empty())
       for (int li : g->sbatches.back()) total += blocks_for(1LL * layers[li]->d.m * layers[li]->d.n);
     if (g->sbatches.empty() || static_cast<int>(g->sbatches.back().size()) == cd::MAXS ||
-        total + nb > (1LL << 30))
+        total + nb > cd::MAX_STREAM_BLOCKS)
       g->sbatches.emplace_back();
     g->sbatches.back().push_back(i);
   }

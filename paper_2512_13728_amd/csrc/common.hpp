@@ -12,10 +12,12 @@
 namespace cd {
 
 constexpr int MAXB = 32;          // layers per batched launch of the sync branch (one shape)
-// layers per launch of the streaming passes (any shapes): 64 gave the 160M
-// set's skip step 2% (one launch instead of two) and cost the 1.3B set's 1.7%
-// (64 + 32 layers instead of 3 x 32)
-constexpr int MAXS = 32;
+// Streaming-pass launches (any shapes): at most MAXS layers and about 420M
+// elements (4 GB of M, X and bf16 G).  On the 1.3B set, launches of 48 or 64
+// layers (600-800M elements) streamed 1.7% slower than 3 x 32 layers (403M
+// each); the 160M set (48 layers, 85M elements) gains 3.4% from one launch.
+constexpr int MAXS = 48;
+constexpr long long MAX_STREAM_BLOCKS = 102400;   // x 4096 elements
 constexpr int NTHREADS = 256;     // threads per block for the streaming kernels
 constexpr int GBK = 32;           // GEMM k per LDS stage; split-K slices are multiples
 

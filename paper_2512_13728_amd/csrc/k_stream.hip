@@ -70,12 +70,17 @@ __device__ double block_sum(double v) {
 
 constexpr int VPT = FORM_CHUNK / (NTHREADS * 4);   // float4 groups per thread (4)
 
-// The layer that block b of a launch belongs to (block0 increases; the scan
-// is uniform over the block and reads the kernel arguments only).
+// The layer that block b of a launch belongs to: block0 increases, so a
+// binary search (uniform over the block, kernel arguments only) finds the
+// last j with block0[j] <= b.
 __device__ __forceinline__ int layer_of(const int* block0, int nl, int b) {
-  int l = 0;
-  for (int k = 1; k < nl; ++k) l += b >= block0[k] ? 1 : 0;
-  return l;
+  int lo = 0, hi = nl - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (b >= block0[mid]) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
 }
 
 // B = M + G in place, the block's partial sum of B^2, and (WX) the skip

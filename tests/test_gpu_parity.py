@@ -316,9 +316,9 @@ def test_group_mixed_shapes_rmmc_gate():
 def test_group_wider_than_one_launch():
     """More layers than one launch takes: 40 of 96 x 160 and 30 of 130 x 70,
     so the sync branch runs the first shape in two chunks (32 + 8 layers per
-    launch) and the streaming passes in three launches (32 + 32 + 6 layers, the
-    second of mixed shapes); sync and local steps against the oracle, every
-    layer checked."""
+    launch) and the streaming passes in two launches (48 + 22 layers, the first
+    of mixed shapes); sync and local steps against the oracle, every layer
+    checked."""
     shapes = [(96, 160)] * 40 + [(130, 70)] * 30
     r = 16
     tau = 0.3
