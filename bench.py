@@ -59,8 +59,9 @@ KIND_BOUND = {
     "local_update": ("hbm", None, 1), "gate": ("hbm", None, 1),
     "reduce_splits": ("hbm", None, 1), "colnorm": ("hbm", None, 1),
     "power_bq_f64": ("mfma", "f64", 1), "gram_f64": ("mfma", "f64", 1), "trsm_f64": ("mfma", "f64", 1),
+    "power_btp_f64": ("mfma", "f64", 1),
     "cholesky_f64": ("mfma", "f64", 1), "power_bq_bf16x6": ("mfma", "bf16", 6),
-    "power_btp_bf16x6": ("mfma", "bf16", 6), "update_bf16x6": ("mfma", "bf16", 6),
+    "update_bf16x6": ("mfma", "bf16", 6),
     "power_bq_bf16x3": ("mfma", "bf16", 3), "power_btp_bf16x3": ("mfma", "bf16", 3),
     "update_bf16": ("hbm", None, 1), "gram_bf16x6": ("mfma", "bf16", 6),
     "apply_bf16x6": ("mfma", "bf16", 6), "trtri_f64": ("mfma", "f64", 1),

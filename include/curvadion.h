@@ -134,6 +134,7 @@ cd_status cd_step(cd_layer* layer, const void* G, float* M, float* X, float* Q,
  * layer first.  NULL is accepted (no-op). */
 cd_status cd_destroy(cd_layer* layer);
 
+
 /* Group layers so that one step takes the max of RMMC over all of them before
  * any layer branches (Algorithm 2).  All layers must share grad_dtype, tau,
  * policy, H and device; the group refers to (does not own) the layers, and

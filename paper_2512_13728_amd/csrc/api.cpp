@@ -29,6 +29,7 @@
 
 #include "../../include/curvadion.h"
 #include "common.hpp"
+#include "plan.hpp"
 
 namespace {
 
@@ -90,20 +91,13 @@ int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk, int pieces 
   return (K + kc - 1) / kc;
 }
 
-template <typename T>
-hipError_t dalloc(T** p, size_t count) {
-  *p = nullptr;
-  if (count == 0) count = 1;
-  return hipMalloc(reinterpret_cast<void**>(p), count * sizeof(T));
-}
-
 // ---- optional per-kernel timing (HIP events on the launch stream) ----------
 enum Kind { K_FORM, K_FORM_X, K_GATE, K_LOCAL, K_PBQ, K_PBQ_BF, K_GRAM, K_GRAM_BF, K_CHOL, K_TRSM, K_TRTRI,
             K_APPLY_BF, K_PBTP, K_PBTP3, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_UPDATE_F32,
             K_NKINDS };
 const char* const kKindName[K_NKINDS] = {
     "form_buffer", "form_buffer_local", "gate", "local_update", "power_bq_f64", "power_bq_bf16x3", "gram_f64",
-    "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_bf16x6",
+    "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_f64",
     "power_btp_bf16x3", "reduce_splits", "colnorm", "update_bf16x6", "update_bf16", "update_f32"};
 static_assert(K_NKINDS <= 32, "the timing mask holds one bit per kind");
 
@@ -150,6 +144,7 @@ struct cd_layer {
   cd_layer_desc d{};
   int device = 0;
   long long step = 0;
+  void* ws = nullptr;           // the one device allocation the pointers below are carved from
   double* prev = nullptr;       // device, 1 double
   int* rankdef = nullptr;       // device, 1 int
   int* rowok = nullptr;         // device, r_max ints: rows of T whose pivot was not floored
@@ -191,6 +186,7 @@ struct Unit {
 };
 
 struct cd_group {
+  void* tables = nullptr;       // the one device allocation the tables below are carved from
   std::vector<cd_layer*> layers;
   std::vector<ShapeClass> shapes;
   int device = 0;
@@ -237,29 +233,15 @@ namespace {
 
 void free_layer(cd_layer* L) {
   if (!L) return;
-  void* ptrs[] = {L->prev, L->rankdef, L->rowok, L->pa, L->pb, L->Uf, L->P, L->R, L->W, L->Dinv, L->floor_,
-                  L->gram_part, L->split_part, L->colsq, L->colnrm, L->planes};
-  for (void* p : ptrs)
-    if (p) (void)hipFree(p);
+  if (L->ws) (void)hipFree(L->ws);
   delete L;
 }
 
 void free_group(cd_group* g) {
   if (!g) return;
-  if (g->parts) (void)hipFree(g->parts);
-  if (g->nparts) (void)hipFree(g->nparts);
-  if (g->prev) (void)hipFree(g->prev);
-  if (g->norms) (void)hipFree(g->norms);
-  if (g->counter) (void)hipFree(g->counter);
-  if (g->out_dev) (void)hipFree(g->out_dev);
+  if (g->tables) (void)hipFree(g->tables);
   if (g->out_host) (void)hipHostFree(g->out_host);
   if (g->ev) (void)hipEventDestroy(g->ev);
-  if (g->chol_tab) (void)hipFree(g->chol_tab);
-  if (g->trsm_tab[0]) (void)hipFree(g->trsm_tab[0]);
-  if (g->trsm_tab[1]) (void)hipFree(g->trsm_tab[1]);
-  if (g->trsm_tab[2]) (void)hipFree(g->trsm_tab[2]);
-  if (g->trsm_tiles) (void)hipFree(g->trsm_tiles);
-  if (g->trtri_tiles) (void)hipFree(g->trtri_tiles);
   for (int i = 0; i < cd_group::NSIDE; ++i) {
     if (g->side[i]) (void)hipStreamDestroy(g->side[i]);
     if (g->join_ev[i]) (void)hipEventDestroy(g->join_ev[i]);
@@ -270,9 +252,149 @@ void free_group(cd_group* g) {
 
 long long blocks_for(long long numel) { return (numel + cd::FORM_CHUNK - 1) / cd::FORM_CHUNK; }
 
-cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
-  cd_group* g = new (std::nothrow) cd_group();
-  if (!g) return fail(CD_ENOMEM, "host allocation failed");
+// Workspace of one layer for ranks up to rm, as byte offsets into one block
+// (every piece 256-byte aligned) that cd_layer_create allocates.
+struct LayerLayout {
+  size_t prev, rankdef, rowok, pa, pb, Uf, P, R, W, Dinv, floor_, gram_part, split_part, colsq, planes, colnrm;
+  size_t split_cap;   // bytes of split_part
+  size_t gram_cap;    // doubles of gram_part
+  size_t total;
+};
+
+struct Carver {
+  size_t off = 0;
+  size_t put(size_t bytes) {
+    const size_t o = off;
+    off += (std::max<size_t>(bytes, 1) + 255) / 256 * 256;
+    return o;
+  }
+};
+
+LayerLayout layer_layout(int m, int n, int rm) {
+  // split-K capacity: the largest partial product any rank r <= rm needs,
+  // for one layer per launch (the most splits) and every piece count (the
+  // tile width, hence the split count, depends on it)
+  size_t split_bytes = 8, gram_cap = 1;
+  for (int r = 1; r <= rm; ++r) {
+    int kc;
+    const size_t mr = static_cast<size_t>(m) * r, nr = static_cast<size_t>(n) * r;
+    split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, true, &kc) * mr * sizeof(double));
+    split_bytes = std::max(split_bytes, plan_splits(n, r, m, 1, true, &kc) * nr * sizeof(double));
+    for (int pieces = 1; pieces <= 3; ++pieces) {
+      split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, false, &kc, pieces) * mr * sizeof(float));
+      split_bytes = std::max(split_bytes, plan_splits(n, r, m, 1, false, &kc, pieces) * nr * sizeof(float));
+      split_bytes = std::max(split_bytes, plan_splits(m, r, r, 1, false, &kc, pieces) * mr * sizeof(float));
+      split_bytes = std::max(split_bytes, plan_splits(r, r, m, 1, false, &kc, pieces) * r * r * sizeof(float));
+    }
+    gram_cap = std::max(gram_cap, static_cast<size_t>(plan_splits(r, r, m, 1, true, &kc, 0, true)) * r * r);
+  }
+  const size_t M = m, N = n, R = rm;
+  const size_t nchunks = (N + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
+  const size_t nblk = (R + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK;
+  const size_t rpm = (R + 31) / 32 * 32;
+  LayerLayout lo{};
+  Carver c;
+  lo.prev = c.put(sizeof(double));
+  lo.rankdef = c.put(sizeof(int));
+  lo.rowok = c.put(sizeof(int) * R);
+  lo.pa = c.put(sizeof(double) * M * R);
+  lo.pb = c.put(sizeof(float) * M * R);
+  lo.Uf = c.put(sizeof(float) * R * R);
+  lo.P = c.put(sizeof(float) * M * R);
+  lo.R = c.put(sizeof(float) * N * R);
+  lo.W = c.put(sizeof(double) * R * R);
+  lo.Dinv = c.put(sizeof(double) * nblk * cd::CHOL_BLOCK * cd::CHOL_BLOCK);
+  lo.floor_ = c.put(sizeof(double));
+  lo.gram_part = c.put(sizeof(double) * gram_cap);
+  lo.split_part = c.put(split_bytes);
+  lo.colsq = c.put(sizeof(double) * nchunks * R);
+  lo.planes = c.put(sizeof(__bf16) * 3 * (M + 2 * N) * rpm);
+  lo.colnrm = c.put(sizeof(float) * R);
+  lo.split_cap = split_bytes;
+  lo.gram_cap = gram_cap;
+  lo.total = c.off;
+  return lo;
+}
+
+void carve_layer(cd_layer* L, char* base, const LayerLayout& lo) {
+  L->prev = reinterpret_cast<double*>(base + lo.prev);
+  L->rankdef = reinterpret_cast<int*>(base + lo.rankdef);
+  L->rowok = reinterpret_cast<int*>(base + lo.rowok);
+  L->pa = reinterpret_cast<double*>(base + lo.pa);
+  L->pb = reinterpret_cast<float*>(base + lo.pb);
+  L->Uf = reinterpret_cast<float*>(base + lo.Uf);
+  L->P = reinterpret_cast<float*>(base + lo.P);
+  L->R = reinterpret_cast<float*>(base + lo.R);
+  L->W = reinterpret_cast<double*>(base + lo.W);
+  L->Dinv = reinterpret_cast<double*>(base + lo.Dinv);
+  L->floor_ = reinterpret_cast<double*>(base + lo.floor_);
+  L->gram_part = reinterpret_cast<double*>(base + lo.gram_part);
+  L->split_part = base + lo.split_part;
+  L->colsq = reinterpret_cast<double*>(base + lo.colsq);
+  L->planes = reinterpret_cast<__bf16*>(base + lo.planes);
+  L->colnrm = reinterpret_cast<float*>(base + lo.colnrm);
+  L->split_cap = lo.split_cap;
+  L->gram_cap = lo.gram_cap;
+}
+
+// The device tables of a group of L layers, as byte offsets into one block.
+struct GroupLayout {
+  size_t parts, nparts, prev, norms, counter, out_dev, chol_tab, trsm_tab[3], trsm_tiles, trtri_tiles;
+  size_t total;
+};
+
+GroupLayout group_layout(int L, int nparts_stride, size_t ntiles, size_t nrtiles) {
+  GroupLayout lo{};
+  Carver c;
+  lo.parts = c.put(sizeof(double) * L * nparts_stride);
+  lo.nparts = c.put(sizeof(int) * L);
+  lo.prev = c.put(sizeof(double*) * L);
+  lo.norms = c.put(sizeof(double) * L);
+  lo.counter = c.put(sizeof(unsigned));
+  lo.out_dev = c.put(sizeof(cd::GateOut) + sizeof(double) * L);
+  lo.chol_tab = c.put(sizeof(cd::CholTab) * L);
+  for (int k = 0; k < 3; ++k) lo.trsm_tab[k] = c.put(sizeof(cd::TrsmTab) * L);
+  lo.trsm_tiles = c.put(sizeof(int2) * ntiles);
+  lo.trtri_tiles = c.put(sizeof(int2) * nrtiles);
+  lo.total = c.off;
+  return lo;
+}
+
+void carve_group(cd_group* g, char* base, const GroupLayout& lo) {
+  g->parts = reinterpret_cast<double*>(base + lo.parts);
+  g->nparts = reinterpret_cast<int*>(base + lo.nparts);
+  g->prev = reinterpret_cast<double**>(base + lo.prev);
+  g->norms = reinterpret_cast<double*>(base + lo.norms);
+  g->counter = reinterpret_cast<unsigned*>(base + lo.counter);
+  g->out_dev = reinterpret_cast<cd::GateOut*>(base + lo.out_dev);
+  g->chol_tab = reinterpret_cast<cd::CholTab*>(base + lo.chol_tab);
+  for (int k = 0; k < 3; ++k) g->trsm_tab[k] = reinterpret_cast<cd::TrsmTab*>(base + lo.trsm_tab[k]);
+  g->trsm_tiles = reinterpret_cast<int2*>(base + lo.trsm_tiles);
+  g->trtri_tiles = reinterpret_cast<int2*>(base + lo.trtri_tiles);
+}
+
+// The triangular-solve tables of one layer.  fp32-gradient layers solve
+// both CholQR passes in place in the fp64 panel pa (P~ -> P1 -> P), so that
+// every block column is formed from fp64 values of the earlier ones; P is
+// rounded to fp32 afterwards.  bf16-gradient layers apply explicit inverses
+// (t1: U = T^-1) and use t0 only to complete P1 (fp32, pb) past the rank.
+void factor_tabs(const cd_layer* L, cd::TrsmTab& t0, cd::TrsmTab& t1, cd::TrsmTab& t2) {
+  if (L->d.grad_dtype == CD_BF16) {
+    t0 = cd::TrsmTab{L->pa, L->pb, L->W, L->Dinv, L->d.m};
+    t2 = cd::TrsmTab{L->pb, L->P, L->W, L->Dinv, L->d.m};
+  } else {
+    t0 = cd::TrsmTab{L->pa, L->pa, L->W, L->Dinv, L->d.m};
+    t2 = cd::TrsmTab{L->pa, L->pa, L->W, L->Dinv, L->d.m};
+  }
+  t1 = cd::TrsmTab{nullptr, L->Uf, L->W, L->Dinv, L->d.r_max};
+}
+
+// Host side of a group: shape classes, units (chunks of at most MAXB layers
+// of one shape) with their rows of the factor tables, and the streaming
+// launches; the table contents go to ct, t0..t2 and the tile lists.
+void plan_group(cd_group* g, cd_layer* const* layers, int n, std::vector<int>& np, std::vector<double*>& pv,
+                std::vector<cd::CholTab>& ct, std::vector<cd::TrsmTab>& t0, std::vector<cd::TrsmTab>& t1,
+                std::vector<cd::TrsmTab>& t2, std::vector<int2>& tiles, std::vector<int2>& rtiles) {
   g->layers.assign(layers, layers + n);
   g->L = n;
   g->device = layers[0]->device;
@@ -281,6 +403,9 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   g->eps = layers[0]->d.eps;
   g->policy = layers[0]->d.policy;
   g->H = layers[0]->d.H;
+  g->shapes.clear();
+  g->units.clear();
+  g->nparts_stride = 0;
   for (int i = 0; i < n; ++i) {
     const cd_layer* L = layers[i];
     auto it = std::find_if(g->shapes.begin(), g->shapes.end(), [&](const ShapeClass& s) {
@@ -291,18 +416,18 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
     g->nparts_stride = std::max<int>(g->nparts_stride,
                                      static_cast<int>(blocks_for(1LL * L->d.m * L->d.n)));
   }
-  DeviceGuard dg(g->device);
-  if (!dg.ok) { free_group(g); return fail(CD_EHIP, "cannot select device %d", g->device); }
-  std::vector<int> np(n);
-  std::vector<double*> pv(n);
-  std::vector<cd::CholTab> ct(n);
-  std::vector<cd::TrsmTab> t0(n), t1(n), t2(n);
-  std::vector<int2> tiles, rtiles;
+  np.assign(n, 0);
+  pv.assign(n, nullptr);
+  ct.assign(n, cd::CholTab{});
+  t0.assign(n, cd::TrsmTab{});
+  t1.assign(n, cd::TrsmTab{});
+  t2.assign(n, cd::TrsmTab{});
+  tiles.clear();
+  rtiles.clear();
   for (int i = 0; i < n; ++i) {
     np[i] = static_cast<int>(blocks_for(1LL * layers[i]->d.m * layers[i]->d.n));
     pv[i] = layers[i]->prev;
   }
-  // units (chunks of at most MAXB layers of one shape) and their factor tables
   int off = 0;
   for (int c = 0; c < static_cast<int>(g->shapes.size()); ++c) {
     const ShapeClass& sc = g->shapes[c];
@@ -317,9 +442,7 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
         cd_layer* L = layers[u.sel[j]];
         const int k = off + j;
         ct[k] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok};
-        t0[k] = cd::TrsmTab{L->pa, L->pb, L->W, L->Dinv, L->d.m};
-        t1[k] = cd::TrsmTab{nullptr, L->Uf, L->W, L->Dinv, L->d.r_max};
-        t2[k] = cd::TrsmTab{L->pb, L->P, L->W, L->Dinv, L->d.m};
+        factor_tabs(L, t0[k], t1[k], t2[k]);
         for (int rt = 0; rt < (L->d.m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) tiles.push_back(int2{j, rt});
         for (int rt = 0; rt < (L->d.r_max + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt)
           rtiles.push_back(int2{j, rt});
@@ -330,25 +453,28 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
       g->units.push_back(std::move(u));
     }
   }
-  for (int i = 0; i < n; ++i) {
-    const long long nb = blocks_for(1LL * layers[i]->d.m * layers[i]->d.n);
-    long long total = 0;
-    if (!g->sbatches.empty())
-      for (int li : g->sbatches.back()) total += blocks_for(1LL * layers[li]->d.m * layers[li]->d.n);
-    if (g->sbatches.empty() || static_cast<int>(g->sbatches.back().size()) == cd::MAXS ||
-        total + nb > cd::MAX_STREAM_BLOCKS)
-      g->sbatches.emplace_back();
-    g->sbatches.back().push_back(i);
+  std::vector<long long> numel(n);
+  for (int i = 0; i < n; ++i) numel[i] = 1LL * layers[i]->d.m * layers[i]->d.n;
+  g->sbatches = cd::plan_stream_batches(numel, cd::MAXS, cd::MAX_STREAM_BLOCKS, cd::FORM_CHUNK);
+}
+
+cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
+  cd_group* g = new (std::nothrow) cd_group();
+  if (!g) return fail(CD_ENOMEM, "host allocation failed");
+  std::vector<int> np;
+  std::vector<double*> pv;
+  std::vector<cd::CholTab> ct;
+  std::vector<cd::TrsmTab> t0, t1, t2;
+  std::vector<int2> tiles, rtiles;
+  plan_group(g, layers, n, np, pv, ct, t0, t1, t2, tiles, rtiles);
+  DeviceGuard dg(g->device);
+  if (!dg.ok) { free_group(g); return fail(CD_EHIP, "cannot select device %d", g->device); }
+  const GroupLayout lo = group_layout(n, g->nparts_stride, tiles.size(), rtiles.size());
+  hipError_t e = hipMalloc(&g->tables, lo.total);
+  if (e == hipSuccess) {
+    carve_group(g, static_cast<char*>(g->tables), lo);
+    e = hipMemset(g->counter, 0, sizeof(unsigned));
   }
-  hipError_t e = hipSuccess;
-  if (e == hipSuccess) e = dalloc(&g->parts, static_cast<size_t>(n) * g->nparts_stride);
-  if (e == hipSuccess) e = dalloc(&g->nparts, n);
-  if (e == hipSuccess) e = dalloc(&g->prev, n);
-  if (e == hipSuccess) e = dalloc(&g->norms, n);
-  if (e == hipSuccess) e = dalloc(&g->counter, 1);
-  if (e == hipSuccess) e = hipMemset(g->counter, 0, sizeof(unsigned));
-  if (e == hipSuccess)
-    e = hipMalloc(reinterpret_cast<void**>(&g->out_dev), sizeof(cd::GateOut) + sizeof(double) * n);
   const size_t host_bytes = sizeof(cd::GateOut) + sizeof(double) * n + sizeof(unsigned long long);
   if (e == hipSuccess) e = hipHostMalloc(&g->out_host, host_bytes, hipHostMallocMapped | hipHostMallocCoherent);
   if (e == hipSuccess) std::memset(g->out_host, 0, host_bytes);
@@ -356,12 +482,6 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   if (e == hipSuccess) e = hipEventCreateWithFlags(&g->ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipMemcpy(g->nparts, np.data(), sizeof(int) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->prev, pv.data(), sizeof(double*) * n, hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = dalloc(&g->chol_tab, n);
-  if (e == hipSuccess) e = dalloc(&g->trsm_tab[0], n);
-  if (e == hipSuccess) e = dalloc(&g->trsm_tab[1], n);
-  if (e == hipSuccess) e = dalloc(&g->trsm_tab[2], n);
-  if (e == hipSuccess) e = dalloc(&g->trsm_tiles, tiles.size());
-  if (e == hipSuccess) e = dalloc(&g->trtri_tiles, rtiles.size());
   if (e == hipSuccess) e = hipMemcpy(g->chol_tab, ct.data(), sizeof(cd::CholTab) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[0], t0.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[1], t1.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
@@ -431,8 +551,10 @@ cd_status run(cd_group* g, int kind, double bytes, double flops, hipStream_t s, 
 // Cholesky factorisations, triangular solves and inverses run between the
 // stages over all layers at once (enqueue_factor); fp32 layers apply T^-1 by
 // fp64 triangular solves there.
+// spec: this step's buffer pass applied the skip branch's X update (the
+// branch was predicted to be local), which the update stage takes back.
 cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>& sel,
-                       const void* const* G, float eta_local_spec,
+                       const void* const* G, bool spec,
                        float* const* M, float* const* X, float* const* Q, float mu, float eta,
                        int r, int stage, hipStream_t s) {
   const int m = sc.m, n = sc.n, nl = static_cast<int>(sel.size());
@@ -530,23 +652,33 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
                 false, true);
   }
   if (stage == 3) {
-    auto In = [&](int j) { return static_cast<const void*>(lay(j)->pb); };
-    if (!fast)
-      return gemm(K_GRAM, mr * (r + 1), 4.0 * mr + 8.0 * rr, cd::GemmKind::F64_FROM_F32, r, r, m, false,
-                  r, false, r, true, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); },
+    if (!fast) {
+      // fp32 layers: P1 is fp64, in pa
+      auto In64 = [&](int j) { return static_cast<const void*>(lay(j)->pa); };
+      return gemm(K_GRAM, mr * (r + 1), 8.0 * mr + 8.0 * rr, cd::GemmKind::F64, r, r, m, false, r, false,
+                  r, true, In64, In64, [&](int j) { return static_cast<void*>(lay(j)->W); },
                   [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
+    }
+    auto In = [&](int j) { return static_cast<const void*>(lay(j)->pb); };
     // pass-1 Gram matrix of the nearly orthonormal P1, fp32-accurate, into
     // fp64 W (all tiles: with upper tiles only the launch takes more K-splits
     // and their reduction costs more than the skipped tiles save)
     return gemm(K_GRAM_BF, 2.0 * mr * r, 4.0 * mr + 8.0 * rr, cd::GemmKind::F32, r, r, m, false, r, false,
                 r, false, In, In, [&](int j) { return static_cast<void*>(lay(j)->W); }, part, 3, true);
   }
-  // R = B^T P
-  cd_status st = gemm(fast ? K_PBTP3 : K_PBTP, 2.0 * mn * r, 4.0 * mn + 4.0 * mr + 4.0 * nr,
-                      cd::GemmKind::F32, n, r, m, false, n, false, r, false,
-                      [&](int j) { return static_cast<const void*>(M[sel[j]]); },
-                      [&](int j) { return static_cast<const void*>(lay(j)->P); },
-                      [&](int j) { return static_cast<void*>(lay(j)->R); }, part, fast ? 2 : 3);
+  // R = B^T P: bf16-gradient layers from the fp32 P with two-piece splits;
+  // fp32 layers from the fp64 P on the fp64 MFMA (R_j = B^T P_j cancels for
+  // the weak directions, by up to ||B||_2 / ||R_j||, which fp32 products and
+  // sums would pass on to Q)
+  cd_status st = fast
+      ? gemm(K_PBTP3, 2.0 * mn * r, 4.0 * mn + 4.0 * mr + 4.0 * nr, cd::GemmKind::F32, n, r, m, false, n,
+             false, r, false, [&](int j) { return static_cast<const void*>(M[sel[j]]); },
+             [&](int j) { return static_cast<const void*>(lay(j)->P); },
+             [&](int j) { return static_cast<void*>(lay(j)->R); }, part, 2)
+      : gemm(K_PBTP, 2.0 * mn * r, 4.0 * mn + 8.0 * mr + 4.0 * nr, cd::GemmKind::F32_F64_TO_F32, n, r, m,
+             false, n, false, r, false, [&](int j) { return static_cast<const void*>(M[sel[j]]); },
+             [&](int j) { return static_cast<const void*>(lay(j)->pa); },
+             [&](int j) { return static_cast<void*>(lay(j)->R); }, part);
   if (st != CD_OK) return st;
   // M = B - (1 - mu) P R^T;  X -= eta sqrt(m/n) P Q^T.  The rank-r
   // corrections are fp32-accurate (6 bf16 piece products) for fp32 layers and
@@ -569,16 +701,23 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   st = run(g, K_COLNORM, (12.0 + 4.0 * cn.S) * nr * nl, 3.0 * nr * nl, s,
            [&] { return cd::launch_colnorm(cn, nl, s); });
   if (st != CD_OK) return st;
-  const double ub = (16.0 + (eta_local_spec != 0.0f ? (g->g_bf16 ? 2.0 : 4.0) : 0.0)) * mn * nl;
+  // eta_local of each layer: what a speculative skip update subtracted
+  auto eta_local = [&](int j) {
+    return static_cast<float>(lay(j)->d.eta_local_scale * static_cast<double>(eta));
+  };
+  bool reads_g = false;
+  for (int j = 0; j < nl && spec; ++j) reads_g = reads_g || eta_local(j) != 0.0f;
+  const double ub = (16.0 + (reads_g ? (g->g_bf16 ? 2.0 : 4.0) : 0.0)) * mn * nl;
   if (vec_update) {
     cd::UpdateVecArgs va{};
     va.m = m; va.n = n; va.r = r;
     va.one_minus_mu = static_cast<float>(1.0 - static_cast<double>(mu));
     va.c = static_cast<float>(static_cast<double>(eta) * std::sqrt(static_cast<double>(m) / n));
     va.g_bf16 = g->g_bf16 ? 1 : 0;
+    va.spec = spec ? 1 : 0;
     for (int j = 0; j < nl; ++j) {
       va.G[j] = G[sel[j]];
-      va.gc[j] = static_cast<float>(lay(j)->d.eta_local_scale * static_cast<double>(eta_local_spec));
+      va.gc[j] = spec ? eta_local(j) : 0.0f;
       va.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * lay(j)->d.weight_decay);
       va.M[j] = M[sel[j]]; va.X[j] = X[sel[j]];
       va.P[j] = lay(j)->P; va.R[j] = lay(j)->R; va.Q[j] = Q[sel[j]];
@@ -598,9 +737,10 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   ua.one_minus_mu = static_cast<float>(1.0 - static_cast<double>(mu));
   ua.c = static_cast<float>(static_cast<double>(eta) * std::sqrt(static_cast<double>(m) / n));
   ua.g_bf16 = g->g_bf16 ? 1 : 0;
+  ua.spec = spec ? 1 : 0;
   for (int j = 0; j < nl; ++j) {
     ua.G[j] = G[sel[j]];
-    ua.gc[j] = static_cast<float>(lay(j)->d.eta_local_scale * static_cast<double>(eta_local_spec));
+    ua.gc[j] = spec ? eta_local(j) : 0.0f;
     ua.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * lay(j)->d.weight_decay);
     ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]];
     ua.P[j] = lay(j)->planes;
@@ -622,26 +762,38 @@ cd_status enqueue_factor(cd_group* g, const Unit& u, int r, int pass, hipStream_
                      [&] { return cd::launch_cholesky(ct, nl, r, pass, s); });
   if (st != CD_OK) return st;
   if (!g->g_bf16) {
+    // in place in the fp64 panel: P1 = P~ T^-1 (pass 0), P = P1 T1^-1 (pass 1)
     double flops = 0, bytes = 0;
     for (int li : u.sel) {
       const double mr = 1.0 * g->layers[li]->d.m * r;
       flops += mr * r;
-      bytes += (pass == 0 ? 8.0 : 4.0) * mr + 4.0 * mr + 4.0 * rr;
+      bytes += 16.0 * mr + 8.0 * rr;
     }
-    return run(g, K_TRSM, bytes, flops, s, [&] {
-      return cd::launch_trsm(g->trsm_tab[pass == 0 ? 0 : 2] + u.off, g->trsm_tiles + u.toff, u.nt, r,
-                             pass == 0, false, s);
+    st = run(g, K_TRSM, bytes, flops, s, [&] {
+      return cd::launch_trsm(g->trsm_tab[pass == 0 ? 0 : 2] + u.off, g->trsm_tiles + u.toff, u.nt, r, true,
+                             true, s);
     });
+    if (st != CD_OK || pass == 0) return st;
+    // P rounded to fp32 (the update's operand planes and cd_layer_last_factors)
+    cd::ReduceArgs ra{};
+    ra.count = 1LL * g->shapes[u.sc].m * r;
+    ra.stride = ra.count;
+    ra.splits = 1;
+    for (int j = 0; j < nl; ++j) {
+      ra.part[j] = g->layers[u.sel[j]]->pa;
+      ra.out[j] = g->layers[u.sel[j]]->P;
+    }
+    return run(g, K_REDUCE, 12.0 * ra.count * nl, 0.0, s,
+               [&] { return cd::launch_reduce_splits(ra, nl, true, false, s); });
   }
   return run(g, K_TRTRI, 12.0 * rr * L, rr * r / 3.0 * L, s, [&] {
     return cd::launch_trsm(g->trsm_tab[1] + u.off, g->trtri_tiles + u.rtoff, u.nrt, r, true, false, s, true, r);
   });
 }
 
-cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, float* const* X,
-                          float* const* Q, float mu, float eta, int r, void* stream,
-                          double* rmmc_per_layer, cd_result* out) {
-  if (!g) return fail(CD_EINVAL, "group is NULL");
+// Argument checks shared by every step entry point (nothing is enqueued yet).
+cd_status check_step_args(const cd_group* g, const void* const* G, float* const* M, float* const* X,
+                          float* const* Q, float mu, float eta, int r) {
   if (!G || !M || !X || !Q) return fail(CD_EINVAL, "pointer array is NULL");
   if (!(mu >= 0.0f && mu <= 1.0f)) return fail(CD_EINVAL, "mu must be in [0, 1] (got %g)", mu);
   if (!std::isfinite(eta) || eta < 0.0f) return fail(CD_EINVAL, "eta must be finite and >= 0 (got %g)", eta);
@@ -653,28 +805,13 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
     if (!aligned16(G[i]) || !aligned16(M[i]) || !aligned16(X[i]) || !aligned16(Q[i]))
       return fail(CD_EINVAL, "matrix pointers of layer %d must be 16-byte aligned", i);
   }
-  DeviceGuard dg(g->device);
-  if (!dg.ok) return fail(CD_EHIP, "cannot select device %d", g->device);
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  return CD_OK;
+}
 
-  // Skip-branch speculation: when the coming decision is known or predicted
-  // to be "skip", X -= eta_local G rides along in the buffer pass, which saves
-  // the second read of G; should the step sync after all, the sync update
-  // first adds eta_local G back (in fp32, one rounding).  The RMMC policy
-  // predicts the previous step's branch, except that a layer whose prev_norm
-  // is 0 (its first step) has RMMC = ||B|| / eps: that step syncs unless B = 0.
-  const long long next_step = g->layers[0]->step + 1;
-  bool any_prev_zero = false;
-  for (const cd_layer* Ly : g->layers) any_prev_zero = any_prev_zero || Ly->prev_zero;
-  bool spec = false;
-  switch (g->policy) {
-    case CD_POLICY_RMMC: spec = g->predict_skip && !any_prev_zero; break;
-    case CD_POLICY_ALWAYS_SYNC: spec = false; break;
-    case CD_POLICY_NEVER_SYNC: spec = true; break;
-    case CD_POLICY_EVERY_H: spec = (next_step % g->H) != 0; break;
-  }
-
-  // 1. B = M + G, partial sums of B^2 (and the speculative skip update)
+// 1. B = M + G, partial sums of B^2 (and, when spec, the skip branch's X
+// update in the same pass).
+cd_status enqueue_form(cd_group* g, const void* const* G, float* const* M, float* const* X, float eta,
+                       bool spec, hipStream_t s) {
   for (const std::vector<int>& batch : g->sbatches) {
     const int nl = static_cast<int>(batch.size());
     cd::FormArgs fa{};
@@ -698,19 +835,137 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
                        [&] { return cd::launch_form_buffer(fa, g->g_bf16, spec, s); });
     if (st != CD_OK) return st;
   }
-  // 2. gate
+  return CD_OK;
+}
+
+// 2. the gate: norms, RMMC, prev_norm, max, flag into g->out_dev; with
+// to_host also into the pinned block, followed by the step's sequence number.
+cd_status enqueue_gate(cd_group* g, hipStream_t s, bool to_host) {
   cd::GateArgs ga{};
   ga.L = g->L; ga.nparts_stride = g->nparts_stride; ga.parts = g->parts; ga.nparts = g->nparts;
   ga.prev = g->prev; ga.eps = g->eps; ga.tau = g->tau; ga.out = g->out_dev;
   ga.norms = g->norms; ga.counter = g->counter;
-  const size_t seq_off = sizeof(cd::GateOut) + sizeof(double) * g->L;
-  ga.host_out = static_cast<cd::GateOut*>(g->out_host_dev);
-  ga.host_seq = reinterpret_cast<unsigned long long*>(static_cast<char*>(g->out_host_dev) + seq_off);
-  ga.seq = ++g->seq;
-  {
-    cd_status st = run(g, K_GATE, 8.0 * g->L * g->nparts_stride, 0.0, s, [&] { return cd::launch_gate(ga, s); });
-    if (st != CD_OK) return st;
+  if (to_host) {
+    const size_t seq_off = sizeof(cd::GateOut) + sizeof(double) * g->L;
+    ga.host_out = static_cast<cd::GateOut*>(g->out_host_dev);
+    ga.host_seq = reinterpret_cast<unsigned long long*>(static_cast<char*>(g->out_host_dev) + seq_off);
+    ga.seq = ++g->seq;
   }
+  return run(g, K_GATE, 8.0 * g->L * g->nparts_stride, 0.0, s, [&] { return cd::launch_gate(ga, s); });
+}
+
+// 4. the branch: the sync branch per unit (each unit's pipeline on its own
+// stream, forked from and joined back to s), or the stand-alone local update
+// (nothing when spec already applied it in the buffer pass).
+cd_status enqueue_branch(cd_group* g, bool sync, bool spec, const void* const* G, float* const* M,
+                         float* const* X, float* const* Q, float mu, float eta, int r, hipStream_t s) {
+  if (sync) {
+    // Each unit's pipeline in stage order on its own stream: the first unit
+    // on the caller's stream, the others on the group's side streams, forked
+    // from the caller's stream here and joined back to it below.  Units are
+    // independent (no workspace is shared between layers), so the results do
+    // not depend on how their kernels interleave.
+    // While every kernel kind is bracketed by timing events, the units run
+    // one after another on the caller's stream, so that each bracketed
+    // launch times its kernel alone (not its wait for CUs that another
+    // stream's kernels hold).
+    const int nu = static_cast<int>(g->units.size());
+    const int nside = (g->timer.on && g->timer.mask == ~0u) ? 0 : g->nside;
+    auto stream_of = [&](int u) -> hipStream_t {
+      const int k = u % (nside + 1);
+      return k == 0 ? s : g->side[k - 1];
+    };
+    if (nside > 0) {
+      CD_HIP(hipEventRecord(g->fork_ev, s));
+      for (int i = 0; i < nside; ++i) CD_HIP(hipStreamWaitEvent(g->side[i], g->fork_ev, 0));
+    }
+    for (int stage = 0; stage < 6; ++stage) {
+      for (int ui = 0; ui < nu; ++ui) {
+        const Unit& u = g->units[ui];
+        const hipStream_t su = stream_of(ui);
+        cd_status st = enqueue_sync(g, g->shapes[u.sc], u.sel, G, spec, M, X, Q, mu, eta, r, stage, su);
+        if (st != CD_OK) return st;
+        if (stage == 1 || stage == 3) {
+          st = enqueue_factor(g, u, r, stage == 1 ? 0 : 1, su);
+          if (st != CD_OK) return st;
+        }
+        if (stage == 2) {
+          // P1 is complete for the unit: new directions for the columns of
+          // floored pass-0 pivots (layers without any return at once)
+          const int nl = static_cast<int>(u.sel.size());
+          const int mu_rows = g->shapes[u.sc].m;
+          st = run(g, K_CHOL, 4.0 * nl, 0.0, su, [&] {
+            return cd::launch_fill_dead(g->chol_tab + u.off, g->trsm_tab[0] + u.off, nl, mu_rows, r,
+                                        !g->g_bf16, su);
+          });
+          if (st != CD_OK) return st;
+        }
+      }
+    }
+    for (int i = 0; i < nside; ++i) {
+      CD_HIP(hipEventRecord(g->join_ev[i], g->side[i]));
+      CD_HIP(hipStreamWaitEvent(s, g->join_ev[i], 0));
+    }
+    for (cd_layer* Ly : g->layers) Ly->last_r = r;
+  } else if (!spec) {
+    for (const std::vector<int>& batch : g->sbatches) {
+      const int nl = static_cast<int>(batch.size());
+      cd::LocalArgs la{};
+      la.nl = nl;
+      long long total = 0, blocks = 0;
+      for (int j = 0; j < nl; ++j) {
+        const int li = batch[j];
+        const cd_layer* Ly = g->layers[li];
+        la.numel[j] = 1LL * Ly->d.m * Ly->d.n;
+        la.block0[j] = static_cast<int>(blocks);
+        blocks += blocks_for(la.numel[j]);
+        total += la.numel[j];
+        la.X[j] = X[li]; la.G[j] = G[li];
+        la.coef[j] = static_cast<float>(Ly->d.eta_local_scale * static_cast<double>(eta));
+        la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * Ly->d.weight_decay);
+      }
+      la.block0[nl] = static_cast<int>(blocks);
+      const double lb = static_cast<double>(total) * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
+      cd_status st = run(g, K_LOCAL, lb, 2.0 * total, s,
+                         [&] { return cd::launch_local_update(la, g->g_bf16, s); });
+      if (st != CD_OK) return st;
+    }
+  }
+  return CD_OK;
+}
+
+// The branch a fixed policy takes at step `step` (1-based); RMMC: unknown.
+bool fixed_policy(const cd_group* g) { return g->policy != CD_POLICY_RMMC; }
+bool fixed_sync(const cd_group* g, long long step) {
+  return g->policy == CD_POLICY_ALWAYS_SYNC || (g->policy == CD_POLICY_EVERY_H && step % g->H == 0);
+}
+
+cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, float* const* X,
+                          float* const* Q, float mu, float eta, int r, void* stream,
+                          double* rmmc_per_layer, cd_result* out) {
+  if (!g) return fail(CD_EINVAL, "group is NULL");
+  cd_status st = check_step_args(g, G, M, X, Q, mu, eta, r);
+  if (st != CD_OK) return st;
+  DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CD_EHIP, "cannot select device %d", g->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  // Skip-branch speculation: when the coming decision is known or predicted
+  // to be "skip", X -= eta_local G rides along in the buffer pass, which saves
+  // the second read of G; should the step sync after all, the sync update
+  // first adds eta_local G back (in fp32, one rounding).  The RMMC policy
+  // predicts the previous step's branch, except that a layer whose prev_norm
+  // is 0 (its first step) has RMMC = ||B|| / eps: that step syncs unless B = 0.
+  const long long next_step = g->layers[0]->step + 1;
+  bool any_prev_zero = false;
+  for (const cd_layer* Ly : g->layers) any_prev_zero = any_prev_zero || Ly->prev_zero;
+  const bool fixed = fixed_policy(g);
+  const bool spec = fixed ? !fixed_sync(g, next_step) : (g->predict_skip && !any_prev_zero);
+
+  st = enqueue_form(g, G, M, X, eta, spec, s);
+  if (st != CD_OK) return st;
+  st = enqueue_gate(g, s, true);
+  if (st != CD_OK) return st;
   // 3. decision point: the gate writes its output into pinned host memory and
   // stores the step's sequence number last; the host polls that number (the
   // event after the gate bounds the wait: once it has completed, the output
@@ -718,102 +973,25 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   CD_HIP(hipEventRecord(g->ev, s));
   for (cd_layer* L : g->layers) { L->step += 1; L->prev_zero = false; }
 
-  // 4. branch
-  auto enqueue_branch = [&](bool sync) -> cd_status {
-    if (sync) {
-      // Each unit's pipeline in stage order on its own stream: the first unit
-      // on the caller's stream, the others on the group's side streams, forked
-      // from the caller's stream here and joined back to it below.  Units are
-      // independent (no workspace is shared between layers), so the results do
-      // not depend on how their kernels interleave.
-      // While every kernel kind is bracketed by timing events, the units run
-      // one after another on the caller's stream, so that each bracketed
-      // launch times its kernel alone (not its wait for CUs that another
-      // stream's kernels hold).
-      const int nu = static_cast<int>(g->units.size());
-      const int nside = (g->timer.on && g->timer.mask == ~0u) ? 0 : g->nside;
-      auto stream_of = [&](int u) -> hipStream_t {
-        const int k = u % (nside + 1);
-        return k == 0 ? s : g->side[k - 1];
-      };
-      if (nside > 0) {
-        CD_HIP(hipEventRecord(g->fork_ev, s));
-        for (int i = 0; i < nside; ++i) CD_HIP(hipStreamWaitEvent(g->side[i], g->fork_ev, 0));
-      }
-      for (int stage = 0; stage < 6; ++stage) {
-        for (int ui = 0; ui < nu; ++ui) {
-          const Unit& u = g->units[ui];
-          const hipStream_t su = stream_of(ui);
-          cd_status st = enqueue_sync(g, g->shapes[u.sc], u.sel, G, spec ? eta : 0.0f, M, X, Q, mu, eta, r,
-                                      stage, su);
-          if (st != CD_OK) return st;
-          if (stage == 1 || stage == 3) {
-            st = enqueue_factor(g, u, r, stage == 1 ? 0 : 1, su);
-            if (st != CD_OK) return st;
-          }
-          if (stage == 2) {
-            // P1 is complete for the unit: new directions for the columns of
-            // floored pass-0 pivots (layers without any return at once)
-            const int nl = static_cast<int>(u.sel.size());
-            const int mu_rows = g->shapes[u.sc].m;
-            st = run(g, K_CHOL, 4.0 * nl, 0.0, su, [&] {
-              return cd::launch_fill_dead(g->chol_tab + u.off, g->trsm_tab[0] + u.off, nl, mu_rows, r, su);
-            });
-            if (st != CD_OK) return st;
-          }
-        }
-      }
-      for (int i = 0; i < nside; ++i) {
-        CD_HIP(hipEventRecord(g->join_ev[i], g->side[i]));
-        CD_HIP(hipStreamWaitEvent(s, g->join_ev[i], 0));
-      }
-      for (cd_layer* Ly : g->layers) Ly->last_r = r;
-    } else if (!spec) {
-      for (const std::vector<int>& batch : g->sbatches) {
-        const int nl = static_cast<int>(batch.size());
-        cd::LocalArgs la{};
-        la.nl = nl;
-        long long total = 0, blocks = 0;
-        for (int j = 0; j < nl; ++j) {
-          const int li = batch[j];
-          const cd_layer* Ly = g->layers[li];
-          la.numel[j] = 1LL * Ly->d.m * Ly->d.n;
-          la.block0[j] = static_cast<int>(blocks);
-          blocks += blocks_for(la.numel[j]);
-          total += la.numel[j];
-          la.X[j] = X[li]; la.G[j] = G[li];
-          la.coef[j] = static_cast<float>(Ly->d.eta_local_scale * static_cast<double>(eta));
-          la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * Ly->d.weight_decay);
-        }
-        la.block0[nl] = static_cast<int>(blocks);
-        const double lb = static_cast<double>(total) * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
-        cd_status st = run(g, K_LOCAL, lb, 2.0 * total, s,
-                           [&] { return cd::launch_local_update(la, g->g_bf16, s); });
-        if (st != CD_OK) return st;
-      }
-    }
-    return CD_OK;
-  };
   // ALWAYS, NEVER and EVERY_H fix the branch in advance: it is enqueued
   // before the wait for the gate's output, so the GPU does not idle through
   // the round trip.  The RMMC policy decides on the output.
   bool sync = false;
-  const bool fixed = g->policy != CD_POLICY_RMMC;
   if (fixed) {
-    sync = g->policy == CD_POLICY_ALWAYS_SYNC ||
-           (g->policy == CD_POLICY_EVERY_H && next_step % g->H == 0);
-    const cd_status st = enqueue_branch(sync);
+    sync = fixed_sync(g, next_step);
+    st = enqueue_branch(g, sync, spec, G, M, X, Q, mu, eta, r, s);
     if (st != CD_OK) return st;
   }
   {
+    const size_t seq_off = sizeof(cd::GateOut) + sizeof(double) * g->L;
     const volatile unsigned long long* hs = reinterpret_cast<const volatile unsigned long long*>(
         static_cast<const char*>(g->out_host) + seq_off);
-    for (unsigned polls = 1; *hs != ga.seq; ++polls) {
+    for (unsigned polls = 1; *hs != g->seq; ++polls) {
       if (polls % 4096 != 0) continue;
       const hipError_t q = hipEventQuery(g->ev);
       if (q == hipErrorNotReady) continue;
       if (q != hipSuccess) return fail(CD_EHIP, "gate: %s", hipGetErrorString(q));
-      if (*hs != ga.seq) return fail(CD_EHIP, "gate output did not reach host memory");
+      if (*hs != g->seq) return fail(CD_EHIP, "gate output did not reach host memory");
     }
     std::atomic_thread_fence(std::memory_order_acquire);
   }
@@ -824,7 +1002,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   if (rmmc_per_layer) std::memcpy(rmmc_per_layer, rm, sizeof(double) * g->L);
   if (!fixed) {
     sync = go->flag != 0;
-    const cd_status st = enqueue_branch(sync);
+    st = enqueue_branch(g, sync, spec, G, M, X, Q, mu, eta, r, s);
     if (st != CD_OK) return st;
   }
   g->predict_skip = !sync;
@@ -847,47 +1025,12 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out) {
     if (!L) return fail(CD_ENOMEM, "host allocation failed");
     L->d = *desc;
     if (hipGetDevice(&L->device) != hipSuccess) { delete L; return fail(CD_EHIP, "hipGetDevice failed"); }
-    const int m = desc->m, n = desc->n, rm = desc->r_max;
-    // split-K capacity: the largest partial product any rank r <= r_max needs,
-    // for one layer per launch (the most splits) and every piece count (the
-    // tile width, hence the split count, depends on it)
-    size_t split_bytes = 8, gram_cap = 1;
-    for (int r = 1; r <= rm; ++r) {
-      int kc;
-      const size_t mr = static_cast<size_t>(m) * r, nr = static_cast<size_t>(n) * r;
-      split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, true, &kc) * mr * sizeof(double));
-      for (int pieces = 1; pieces <= 3; ++pieces) {
-        split_bytes = std::max(split_bytes, plan_splits(m, r, n, 1, false, &kc, pieces) * mr * sizeof(float));
-        split_bytes = std::max(split_bytes, plan_splits(n, r, m, 1, false, &kc, pieces) * nr * sizeof(float));
-        split_bytes = std::max(split_bytes, plan_splits(m, r, r, 1, false, &kc, pieces) * mr * sizeof(float));
-        split_bytes = std::max(split_bytes,
-                               plan_splits(r, r, m, 1, false, &kc, pieces) * r * r * sizeof(float));
-      }
-      gram_cap = std::max(gram_cap, static_cast<size_t>(plan_splits(r, r, m, 1, true, &kc, 0, true)) * r * r);
+    const LayerLayout lo = layer_layout(desc->m, desc->n, desc->r_max);
+    hipError_t e = hipMalloc(&L->ws, lo.total);
+    if (e == hipSuccess) {
+      carve_layer(L, static_cast<char*>(L->ws), lo);
+      e = hipMemset(L->prev, 0, sizeof(double));
     }
-    const size_t nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
-    hipError_t e = hipSuccess;
-    if (e == hipSuccess) e = dalloc(&L->prev, 1);
-    if (e == hipSuccess) e = dalloc(&L->rankdef, 1);
-    if (e == hipSuccess) e = dalloc(&L->rowok, static_cast<size_t>(rm));
-    if (e == hipSuccess) e = dalloc(&L->pa, 1ULL * m * rm);
-    if (e == hipSuccess) e = dalloc(&L->pb, 1ULL * m * rm);
-    if (e == hipSuccess) e = dalloc(&L->Uf, 1ULL * rm * rm);
-    if (e == hipSuccess) e = dalloc(&L->P, 1ULL * m * rm);
-    if (e == hipSuccess) e = dalloc(&L->R, 1ULL * n * rm);
-    if (e == hipSuccess) e = dalloc(&L->W, 1ULL * rm * rm);
-    const size_t nblk = (rm + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK;
-    if (e == hipSuccess) e = dalloc(&L->Dinv, nblk * cd::CHOL_BLOCK * cd::CHOL_BLOCK);
-    if (e == hipSuccess) e = dalloc(&L->floor_, 1);
-    if (e == hipSuccess) e = dalloc(&L->gram_part, gram_cap);
-    if (e == hipSuccess) e = hipMalloc(&L->split_part, split_bytes);
-    L->split_cap = split_bytes;
-    L->gram_cap = gram_cap;
-    if (e == hipSuccess) e = dalloc(&L->colsq, nchunks * rm);
-    const size_t rpm = (rm + 31) / 32 * 32;
-    if (e == hipSuccess) e = dalloc(&L->planes, 3ULL * (m + 2ULL * n) * rpm);
-    if (e == hipSuccess) e = dalloc(&L->colnrm, static_cast<size_t>(rm));
-    if (e == hipSuccess) e = hipMemset(L->prev, 0, sizeof(double));
     if (e == hipSuccess) e = hipMemset(L->rankdef, 0, sizeof(int));
     if (e != hipSuccess) {
       free_layer(L);

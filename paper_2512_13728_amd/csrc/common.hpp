@@ -9,23 +9,16 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "plan.hpp"
+
 namespace cd {
 
-constexpr int MAXB = 32;          // layers per batched launch of the sync branch (one shape)
-// Streaming-pass launches (any shapes): at most MAXS layers and about 420M
-// elements (4 GB of M, X and bf16 G).  On the 1.3B set, launches of 48 or 64
-// layers (600-800M elements) streamed 1.7% slower than 3 x 32 layers (403M
-// each); the 160M set (48 layers, 85M elements) gains 3.4% from one launch.
-constexpr int MAXS = 48;
-constexpr long long MAX_STREAM_BLOCKS = 102400;   // x 4096 elements
-constexpr int NTHREADS = 256;     // threads per block for the streaming kernels
 constexpr int GBK = 32;           // GEMM k per LDS stage; split-K slices are multiples
 
 // ---- a1: B = M + G and per-block sum of B^2 -------------------------------
 // Every block covers FORM_CHUNK consecutive elements of one layer; one launch
 // covers up to MAXS layers of any shapes (the passes are elementwise), layer
 // j owning blocks [block0[j], block0[j + 1]).
-constexpr int FORM_CHUNK = NTHREADS * 4 * 4;   // 4096 elements
 struct FormArgs {
   int nl;                          // layers in this launch
   long long numel[MAXS];           // elements of each layer (m*n)
@@ -70,7 +63,8 @@ struct GateArgs {
   double* norms;                   // [L] workspace: ‖B‖ per layer
   unsigned* counter;               // zero between launches (the last block resets it)
   // the same result in pinned, coherent host memory (device view): header and
-  // L doubles, then `seq` at host_seq, stored after everything else is visible
+  // L doubles, then `seq` at host_seq, stored after everything else is
+  // visible (host_out NULL: device copy only)
   GateOut* host_out;
   unsigned long long* host_seq;
   unsigned long long seq;
@@ -88,7 +82,8 @@ enum class GemmKind {
   F32,          // fp32 operands, fp32 MFMA, fp32 result
   F64_FROM_F32, // fp32 operands, fp64 MFMA, fp64 result
   F64,          // fp64 operands, fp64 MFMA, fp64 result
-  F64_TO_F32    // fp64 operands, fp64 MFMA, result rounded to fp32
+  F64_TO_F32,   // fp64 operands, fp64 MFMA, result rounded to fp32
+  F32_F64_TO_F32  // fp32 A, fp64 B, fp64 MFMA, result rounded to fp32
 };
 struct GemmArgs {
   int M, N, K;
@@ -143,7 +138,10 @@ struct CholTab {
 // All CHOL_BLOCK steps for `nlayers` layers of rank r; `pass` 0 clears rankdef.
 hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s);
 
-// P = P~ T^{-1} by block columns (in place is not allowed: Pin != Pout).
+// P = P~ T^{-1} by block columns.  In place (Pin == Pout, same type) is
+// allowed: the workgroup of a row tile reads its block column of P~ before it
+// writes that block column of P, and reads only finished columns of P
+// besides.
 struct TrsmTab {
   const void* Pin;                 // m x r, fp64 or fp32
   void* Pout;                      // m x r, fp64 or fp32
@@ -156,7 +154,9 @@ struct TrsmTab {
 // Between the CholQR passes: columns of P1 (TrsmTab::Pout, fp32 m x r) whose
 // pivot was floored get fixed pseudo-random directions (layers with
 // rankdef == 0 are left alone).  mmax: the largest m of the layers.
-hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, int mmax, int r, hipStream_t s);
+// p64: P1 is fp64 (fp32-gradient layers), else fp32.
+hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, int mmax, int r, bool p64,
+                            hipStream_t s);
 hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r, bool in64, bool out64,
                        hipStream_t s, bool ident = false, int mlimit = 0);
 
@@ -190,9 +190,14 @@ struct UpdateVecArgs {
   const float* P[MAXB];
   const float* R[MAXB];
   const float* Q[MAXB];
-  const void* G[MAXB];   // reversal of a speculative skip update, as below
+  // spec = 1: the buffer pass already applied the skip branch's
+  // X = xdecay X - eta_local G (the decay included); the update first adds
+  // gc G back (gc = eta_local; no read of G when it is 0).  spec = 0: X
+  // still needs the decay, X = xdecay X, before the rank-r correction.
+  const void* G[MAXB];
   float gc[MAXB];
   int g_bf16;
+  int spec;
   float xdecay[MAXB];
 };
 bool update_vec_fits(int r);
@@ -217,13 +222,14 @@ struct UpdatePlArgs {
   const __bf16* P[MAXB];
   const __bf16* R[MAXB];
   const __bf16* Q[MAXB];
-  // reversal of a speculative skip-branch update: X += gc G before the rank-r
-  // correction (gc = 0: none)
+  // spec = 1: the buffer pass already applied the skip branch's
+  // X = xdecay X - eta_local G (the decay included); the update first adds
+  // gc G back (gc = eta_local; no read of G when it is 0).  spec = 0: the
+  // decoupled weight decay X = xdecay X comes first.
   const void* G[MAXB];
   float gc[MAXB];
   int g_bf16;
-  // decoupled weight decay of X when no speculative update preceded (with one,
-  // X already carries it): X = xdecay X before the rank-r correction
+  int spec;
   float xdecay[MAXB];
 };
 hipError_t launch_update_planes(const UpdatePlArgs& a, int nl, int pieces, hipStream_t s);

@@ -300,19 +300,20 @@ __device__ __forceinline__ float fill_value(unsigned i, unsigned j, float scale)
   return scale * (static_cast<float>(h >> 8) * (2.0f / 16777216.0f) - 1.0f);   // uniform in [-1, 1)
 }
 
+template <typename T>
 __global__ __launch_bounds__(256) void k_fill_dead(const CholTab* __restrict__ ct,
                                                    const TrsmTab* __restrict__ tt, int r) {
   const CholTab c = ct[blockIdx.y];
   if (*c.rankdef == 0) return;
   const TrsmTab t = tt[blockIdx.y];
-  float* P1 = static_cast<float*>(t.Pout);
+  T* P1 = static_cast<T*>(t.Pout);
   const int i0 = blockIdx.x * FILL_ROWS;
   const int rows = min(FILL_ROWS, t.m - i0);
   if (rows <= 0) return;
   const float scale = sqrtf(3.0f / static_cast<float>(t.m));
   for (int e = threadIdx.x; e < rows * r; e += 256) {
     const int i = i0 + e / r, j = e % r;
-    if (!c.rowok[j]) P1[static_cast<long long>(i) * r + j] = fill_value(i, j, scale);
+    if (!c.rowok[j]) P1[static_cast<long long>(i) * r + j] = static_cast<T>(fill_value(i, j, scale));
   }
 }
 
@@ -442,9 +443,12 @@ hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hip
   return hipGetLastError();
 }
 
-hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, int mmax, int r, hipStream_t s) {
+hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, int mmax, int r, bool p64,
+                            hipStream_t s) {
   if (nlayers <= 0 || mmax <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_fill_dead, dim3((mmax + FILL_ROWS - 1) / FILL_ROWS, nlayers), dim3(256), 0, s, ct, tt, r);
+  const dim3 grid((mmax + FILL_ROWS - 1) / FILL_ROWS, nlayers);
+  if (p64) hipLaunchKernelGGL(k_fill_dead<double>, grid, dim3(256), 0, s, ct, tt, r);
+  else hipLaunchKernelGGL(k_fill_dead<float>, grid, dim3(256), 0, s, ct, tt, r);
   return hipGetLastError();
 }
 

@@ -2,6 +2,7 @@
 // branch) on MFMA:
 //   P~ = B Q            (m x n . n x r; A = B row-major, k contiguous)
 //   W  = P~^T P~        (Gram matrix, upper tiles only)
+//   R  = B^T P          (fp32-gradient layers: B fp32, P fp64, R rounded to fp32)
 // These run in fp64 (v_mfma_f64_16x16x4_f64 on fp32 or fp64 operands): P~
 // is the ill-conditioned panel, and keeping it, its Gram matrix and the CholQR
 // passes in fp64 makes the orthonormal P accurate to fp32 rounding whatever
@@ -15,7 +16,8 @@
 namespace cd {
 namespace {
 
-template <typename T, typename TIn, typename TOut, int BM, int BN, bool A_KC, bool B_KC>
+// TIn: element type of the A operand; TInB: of the B operand.
+template <typename T, typename TIn, typename TOut, int BM, int BN, bool A_KC, bool B_KC, typename TInB = TIn>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   constexpr int WN_WAVES = (BN >= 64) ? 2 : 1;
   constexpr int WM_WAVES = 4 / WN_WAVES;
@@ -35,7 +37,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   const int kb = blockIdx.y * g.kchunk;
   const int ke = min(g.K, kb + g.kchunk);
   const TIn* A = static_cast<const TIn*>(g.A[layer]);
-  const TIn* Bm = static_cast<const TIn*>(g.B[layer]);
+  const TInB* Bm = static_cast<const TInB*>(g.B[layer]);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave / WN_WAVES) * WM, wn0 = (wave % WN_WAVES) * WN;
 
@@ -46,7 +48,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     for (int j = 0; j < TN; ++j) acc[i][j] = typename Mfma<T>::acc_t{};
 
   Prefetch<TIn, BM, 256, A_KC> pa;
-  Prefetch<TIn, BN, 256, B_KC> pb;
+  Prefetch<TInB, BN, 256, B_KC> pb;
   if (kb < ke) {
     pa.load(A, g.lda, m0, g.M, kb, ke, tid);
     pb.load(Bm, g.ldb, n0, g.N, kb, ke, tid);
@@ -108,14 +110,14 @@ __global__ __launch_bounds__(256) void k_reduce(ReduceArgs a) {
   }
 }
 
-template <typename T, typename TIn, typename TOut, int BM, int BN>
+template <typename T, typename TIn, typename TOut, int BM, int BN, typename TInB = TIn>
 hipError_t launch_t(const GemmArgs& g, int nl, hipStream_t s) {
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   const dim3 grid(xcd_grid(tiles), g.splits, nl);
   if (g.a_kc && !g.b_kc)
-    hipLaunchKernelGGL((k_gemm<T, TIn, TOut, BM, BN, true, false>), grid, dim3(256), 0, s, g);
+    hipLaunchKernelGGL((k_gemm<T, TIn, TOut, BM, BN, true, false, TInB>), grid, dim3(256), 0, s, g);
   else if (!g.a_kc && !g.b_kc)
-    hipLaunchKernelGGL((k_gemm<T, TIn, TOut, BM, BN, false, false>), grid, dim3(256), 0, s, g);
+    hipLaunchKernelGGL((k_gemm<T, TIn, TOut, BM, BN, false, false, TInB>), grid, dim3(256), 0, s, g);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -125,12 +127,12 @@ hipError_t launch_t(const GemmArgs& g, int nl, hipStream_t s) {
 // four waves down): a 64-wide tile would spend most of its MFMAs on padding.
 int tile_n(int N) { return N <= 16 ? 16 : (N <= 32 ? 32 : 64); }
 
-template <typename T, typename TIn, typename TOut>
+template <typename T, typename TIn, typename TOut, typename TInB = TIn>
 hipError_t launch_n(const GemmArgs& g, int nl, hipStream_t s) {
   switch (tile_n(g.N)) {
-    case 16: return launch_t<T, TIn, TOut, 64, 16>(g, nl, s);
-    case 32: return launch_t<T, TIn, TOut, 64, 32>(g, nl, s);
-    default: return launch_t<T, TIn, TOut, 64, 64>(g, nl, s);
+    case 16: return launch_t<T, TIn, TOut, 64, 16, TInB>(g, nl, s);
+    case 32: return launch_t<T, TIn, TOut, 64, 32, TInB>(g, nl, s);
+    default: return launch_t<T, TIn, TOut, 64, 64, TInB>(g, nl, s);
   }
 }
 
@@ -146,6 +148,7 @@ hipError_t launch_gemm(const GemmArgs& g, int nl, GemmKind kind, hipStream_t s) 
     case GemmKind::F64_FROM_F32: return launch_n<double, float, double>(g, nl, s);
     case GemmKind::F64: return launch_n<double, double, double>(g, nl, s);
     case GemmKind::F64_TO_F32: return launch_n<double, double, float>(g, nl, s);
+    case GemmKind::F32_F64_TO_F32: return launch_n<double, float, float, double>(g, nl, s);
     case GemmKind::F32: break;  // fp32 contractions run on the bf16-split kernels
   }
   return hipErrorInvalidValue;

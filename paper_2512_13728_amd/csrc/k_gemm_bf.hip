@@ -297,8 +297,9 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
     const float coef = which == 0 ? -u.one_minus_mu : -u.c;
     // X only: first undo a speculative skip-branch update (X += gc G; that
     // update already applied the weight decay), else apply the decay
-    const float gc = which == 0 ? 0.f : u.gc[l];
-    const float xd = which == 0 ? 1.f : u.xdecay[l];
+    const bool spec = which == 1 && u.spec != 0;
+    const float gc = spec ? u.gc[l] : 0.f;
+    const float xd = (which == 0 || spec) ? 1.f : u.xdecay[l];
     const void* const G = u.G[l];
     const bool gbf = u.g_bf16 != 0;
 #pragma unroll 4
@@ -317,7 +318,7 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
           const float4 g = load_g4(G, gbf, off);
           w.x = fmaf(gc, g.x, w.x); w.y = fmaf(gc, g.y, w.y);
           w.z = fmaf(gc, g.z, w.z); w.w = fmaf(gc, g.w, w.w);
-        } else {
+        } else if (!spec) {
           w.x *= xd; w.y *= xd; w.z *= xd; w.w *= xd;
         }
         w.x = fmaf(coef, a.x, w.x); w.y = fmaf(coef, a.y, w.y);
@@ -330,7 +331,7 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
           if (gcol + c >= u.n) continue;
           float w = y[c];
           if (gc != 0.f) w = fmaf(gc, load_g1(G, gbf, off + c), w);
-          else w *= xd;
+          else if (!spec) w *= xd;
           y[c] = fmaf(coef, av[c], w);
         }
       }

@@ -252,10 +252,13 @@ __global__ __launch_bounds__(GATE_THREADS) void k_gate(GateArgs a) {
     a.out->g = g;
     a.out->flag = (g > a.tau) ? 1 : 0;
     a.out->nonfinite = (flags & 2) ? 1 : 0;
-    a.host_out->g = g;
-    a.host_out->flag = (g > a.tau) ? 1 : 0;
-    a.host_out->nonfinite = (flags & 2) ? 1 : 0;
+    if (a.host_out) {
+      a.host_out->g = g;
+      a.host_out->flag = (g > a.tau) ? 1 : 0;
+      a.host_out->nonfinite = (flags & 2) ? 1 : 0;
+    }
   }
+  if (!a.host_out) return;
   // the host copy: every value first, then (once all of them are visible at
   // system scope) the step's sequence number, which the host polls
   double* host_rm = reinterpret_cast<double*>(a.host_out + 1);
@@ -289,7 +292,7 @@ hipError_t launch_local_update(const LocalArgs& a, bool g_bf16, hipStream_t s) {
 }
 
 hipError_t launch_gate(const GateArgs& a, hipStream_t s) {
-  if (a.L <= 0 || !a.counter || !a.norms || !a.host_out || !a.host_seq) return hipErrorInvalidValue;
+  if (a.L <= 0 || !a.counter || !a.norms || !a.out || (a.host_out && !a.host_seq)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_gate, dim3(a.L), dim3(GATE_THREADS), 0, s, a);
   return hipGetLastError();
 }

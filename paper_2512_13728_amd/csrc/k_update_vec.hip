@@ -53,7 +53,8 @@ __global__ __launch_bounds__(256) void k_update_vec(UpdateVecArgs u) {
   float* const Xo = u.X[l];
   const void* const G = u.G[l];
   const bool gbf = u.g_bf16 != 0;
-  const float gc = u.gc[l], xd = u.xdecay[l];
+  const bool spec = u.spec != 0;
+  const float gc = spec ? u.gc[l] : 0.0f, xd = spec ? 1.0f : u.xdecay[l];
   const float cm = -u.one_minus_mu, cx = -u.c;
   const int i_end = min(m, (blockIdx.y + 1) * u.band);
   for (int i = blockIdx.y * u.band + wave; i < i_end; i += 4 * U) {
@@ -81,7 +82,7 @@ __global__ __launch_bounds__(256) void k_update_vec(UpdateVecArgs u) {
       if (!in) continue;
       const long long off = static_cast<long long>(row) * n + j;
       // undo a speculative skip-branch update (it already applied the weight
-      // decay), else apply the decay
+      // decay), else apply the decay (xd = 1 after a speculative update)
       const float xv = gc != 0.0f ? fmaf(gc, load_g(G, gbf, off), x[t]) : x[t] * xd;
       __builtin_nontemporal_store(fmaf(cm, sm, w[t]), Mo + off);
       __builtin_nontemporal_store(fmaf(cx, sx, xv), Xo + off);

@@ -155,3 +155,33 @@ def test_plain_c_client_check():
     assert out.returncode == 0, out.stderr
     assert "check ok" in out.stdout
     assert out.stdout.count("CD_EINVAL") == 8
+
+
+def _stream_plan(shapes, tmp_path):
+    """Streaming-pass launches the library plans for `shapes`: the planning
+    header compiled with g++ (it has no HIP dependency) and run on the CPU."""
+    exe = tmp_path / "plan_check"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-Wall", "-Werror", "-I",
+                    os.path.join(ROOT, "paper_2512_13728_amd", "csrc"),
+                    os.path.join(ROOT, "tests", "c", "plan_check.cpp"), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], input="".join(f"{m} {n}\n" for m, n in shapes),
+                         capture_output=True, text=True, check=True).stdout
+    return [tuple(int(x) for x in line.split()) for line in out.splitlines()]
+
+
+def test_streaming_launch_plan_of_the_workloads(tmp_path):
+    """The buffer pass and the local update launch whole layers in group order,
+    at most 48 layers and 98304 blocks of 4096 elements per launch: the
+    1.3B-shaped set (96 matrices, 24 blocks of 2048x6144, 2048x2048,
+    2048x8192, 8192x2048) runs as 3 launches of 32 layers (8 transformer
+    blocks, 402.7M elements each), the 160M-shaped set (48 matrices) as one
+    launch, and a layer beyond the block cap as a launch of its own."""
+    import synthetic as S
+    assert _stream_plan(S.WORKLOADS["gpt1p3b"].shapes, tmp_path) == [(32, 98304)] * 3
+    assert _stream_plan(S.WORKLOADS["gpt160m"].shapes, tmp_path) == [(48, 20736)]
+    assert _stream_plan([(256, 256)], tmp_path) == [(1, 16)]
+    # 46341^2 elements (2^31 + 4633): 524290 blocks, alone; the next layer starts a launch
+    assert _stream_plan([(13, 7), (46341, 46341), (300, 1000)], tmp_path) == [(1, 1), (1, 524290), (1, 74)]
+    # 49 small layers: the layer cap splits them 48 + 1
+    assert _stream_plan([(64, 64)] * 49, tmp_path) == [(48, 48), (1, 1)]
+
