@@ -134,6 +134,41 @@ cd_status cd_step(cd_layer* layer, const void* G, float* M, float* X, float* Q,
  * layer first.  NULL is accepted (no-op). */
 cd_status cd_destroy(cd_layer* layer);
 
+/* For callers that cannot allocate memory while they step (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): one
+ * step of one layer as cd_step computes it, that allocates nothing.  Every
+ * buffer the step needs besides its inputs and outputs lives in one fixed
+ * array of CD_STATIC_SCRATCH_BYTES per device, which the library holds from
+ * its first use on a device until the process ends; the first call on a
+ * device looks up that array's address.
+ *
+ * There is no layer object: `desc` describes the layer (as for
+ * cd_layer_create; r <= desc->r_max), and the caller owns its state,
+ * `prev_norm` (a DEVICE pointer to one double, 0 before the first step, read
+ * and written by the step) and `*step` (host, the number of steps taken,
+ * incremented).  G, M, X, Q, mu, eta, r, stream and out as for cd_step.  The
+ * call blocks the host until the gate's output has been copied back
+ * (hipMemcpyAsync into the call's stack, then a stream synchronisation), then
+ * enqueues the branch and returns.  Without state between calls there is no
+ * branch prediction: under CD_POLICY_RMMC the skip update is a pass of its
+ * own (fixed policies fuse it as cd_step does), so results match cd_step's
+ * to within an fp32 rounding of X.  Rank deficiency is handled as in cd_step
+ * but not reported.
+ *
+ * CD_EINVAL (nothing enqueued) for the descriptor and argument errors of
+ * cd_layer_create and cd_step, a NULL or misaligned prev_norm, a NULL step,
+ * and for a layer whose workspace at rank r exceeds CD_STATIC_SCRATCH_BYTES
+ * (the message gives both sizes; such layers need cd_step).
+ *
+ * Every call on one device uses that device's one array, whose contents the
+ * next call overwrites: calls whose work overlaps on one device (different
+ * streams, or different host threads on streams not ordered with each other)
+ * race, and must be ordered by the caller.  Calls from several host threads
+ * are serialised on the host. */
+#define CD_STATIC_SCRATCH_BYTES (64u << 20)
+cd_status cd_step_static(const cd_layer_desc* desc, double* prev_norm, long long* step, const void* G,
+                         float* M, float* X, float* Q, float mu, float eta, int r, void* stream,
+                         cd_result* out);
 
 /* Group layers so that one step takes the max of RMMC over all of them before
  * any layer branches (Algorithm 2).  All layers must share grad_dtype, tau,

@@ -16,7 +16,8 @@ from typing import Optional, Sequence, Tuple
 __all__ = [
     "LibraryNotBuilt", "CurvaDionError", "Layer", "Group", "lib", "library_path",
     "POLICY_RMMC", "POLICY_ALWAYS_SYNC", "POLICY_NEVER_SYNC", "POLICY_EVERY_H",
-    "F32", "BF16", "EXPORTED_SYMBOLS", "PointerArray", "check_operand",
+    "F32", "BF16", "EXPORTED_SYMBOLS", "PointerArray", "check_operand", "step_static",
+    "STATIC_SCRATCH_BYTES",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -34,6 +35,7 @@ EXPORTED_SYMBOLS = (
     "cd_group_destroy", "cd_layer_get_state", "cd_layer_set_state",
     "cd_layer_last_factors", "cd_layer_rank_deficient", "cd_group_set_timing",
     "cd_group_kernel_times", "cd_group_set_timing_kinds", "cd_last_error", "cd_abi_version",
+    "cd_step_static",
 )
 
 
@@ -80,6 +82,8 @@ def lib() -> ctypes.CDLL:
     L.cd_layer_create.argtypes = [ctypes.POINTER(LayerDesc), ctypes.POINTER(vp)]
     L.cd_step.argtypes = [vp, vp, vp, vp, vp, f, f, i, vp, ctypes.POINTER(Result)]
     L.cd_destroy.argtypes = [vp]
+    L.cd_step_static.argtypes = [ctypes.POINTER(LayerDesc), vp, ctypes.POINTER(ctypes.c_longlong), vp, vp,
+                                 vp, vp, f, f, i, vp, ctypes.POINTER(Result)]
     L.cd_group_create.argtypes = [ctypes.POINTER(vp), i, ctypes.POINTER(vp)]
     L.cd_group_step.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
                                 ctypes.POINTER(vp), f, f, i, vp, ctypes.POINTER(d),
@@ -215,6 +219,35 @@ class Layer:
             self.close()
         except Exception:
             pass
+
+
+#: size of the per-device workspace of cd_step_static (CD_STATIC_SCRATCH_BYTES)
+STATIC_SCRATCH_BYTES = 64 << 20
+
+
+def step_static(m: int, n: int, r_max: int, prev_norm, step: int, G, M, X, Q, mu: float, eta: float,
+                r: Optional[int] = None, *, grad_dtype: str = "f32", tau: float = 0.5, eps: float = 1e-8,
+                eta_local_scale: float = 1.0, policy: int = POLICY_RMMC, H: int = 1,
+                weight_decay: float = 0.0, stream=None) -> Tuple[float, bool, int, int]:
+    """One step of one layer through cd_step_static, the entry point that
+    allocates nothing (its workspace is a fixed per-device array).  The
+    caller owns the layer state: `prev_norm` is a one-element fp64 GPU tensor
+    (or a device address), `step` the steps taken so far.  Returns
+    (rmmc, sync_flag, status, step + 1)."""
+    r = Q.shape[1] if r is None and hasattr(Q, "shape") else r
+    for t, role in ((G, "G"), (M, "M"), (X, "X"), (Q, "Q")):
+        check_operand(t, role, m, n, r, grad_dtype)
+    if not isinstance(prev_norm, int):
+        if str(prev_norm.dtype) != "torch.float64" or prev_norm.numel() != 1 or prev_norm.device.type != "cuda":
+            raise ValueError("prev_norm: expected one float64 element on a GPU")
+    desc = LayerDesc(m, n, r_max, BF16 if grad_dtype == "bf16" else F32, tau, eps, eta_local_scale,
+                     policy, H, weight_decay)
+    st_c = ctypes.c_longlong(step)
+    res = Result()
+    st = lib().cd_step_static(ctypes.byref(desc), _ptr(prev_norm), ctypes.byref(st_c), _ptr(G), _ptr(M),
+                              _ptr(X), _ptr(Q), mu, eta, r, _stream_handle(stream), ctypes.byref(res))
+    _check(st, allow=(CD_OK, CD_ENONFINITE))
+    return res.rmmc, bool(res.sync_flag), st, st_c.value
 
 
 class PointerArray:

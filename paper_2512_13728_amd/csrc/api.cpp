@@ -23,6 +23,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -253,7 +254,8 @@ void free_group(cd_group* g) {
 long long blocks_for(long long numel) { return (numel + cd::FORM_CHUNK - 1) / cd::FORM_CHUNK; }
 
 // Workspace of one layer for ranks up to rm, as byte offsets into one block
-// (every piece 256-byte aligned) that cd_layer_create allocates.
+// (every piece 256-byte aligned).  cd_layer_create allocates the block; the
+// allocation-free step carves it from the static scratch array.
 struct LayerLayout {
   size_t prev, rankdef, rowok, pa, pb, Uf, P, R, W, Dinv, floor_, gram_part, split_part, colsq, planes, colnrm;
   size_t split_cap;   // bytes of split_part
@@ -1011,6 +1013,186 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   return CD_OK;
 }
 
+// ---- the allocation-free step (cd_step_static) -------------------------------
+// All workspace of one layer's step and the device tables of its one-layer
+// group live in one fixed array per device.  Host code never uses the
+// array's name as an address: its device address comes from
+// hipGetSymbolAddress, once per device, and every kernel argument is carved
+// from that address.
+static __device__ __align__(256) unsigned char scratch[CD_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+// Per device: the array's device address and the host-side layer and group
+// objects the step reuses (their vectors keep their one-element capacity, so
+// a call after the first allocates nothing on the host either).
+struct StaticSlot {
+  std::mutex mu;
+  void* base = nullptr;
+  cd_layer layer;
+  cd_group group;
+};
+StaticSlot g_static[kMaxDevices];
+
+// Writes the one-layer group's device tables (a kernel instead of host-to-
+// device copies, so that the step needs no staging memory).
+struct StaticSetup {
+  int* nparts;
+  int np;
+  double** prev_tab;
+  double* prev;
+  unsigned* counter;
+  cd::CholTab* ct;
+  cd::CholTab ctv;
+  cd::TrsmTab* tt[3];
+  cd::TrsmTab ttv[3];
+  int2* tiles;
+  int ntiles;
+  int2* rtiles;
+  int nrtiles;
+};
+
+__global__ __launch_bounds__(256) void k_static_setup(StaticSetup a) {
+  const int t = threadIdx.x;
+  if (t == 0) {
+    *a.nparts = a.np;
+    *a.prev_tab = a.prev;
+    *a.counter = 0u;   // the gate's completion counter starts at zero
+    *a.ct = a.ctv;
+    for (int k = 0; k < 3; ++k) *a.tt[k] = a.ttv[k];
+  }
+  for (int i = t; i < a.ntiles; i += 256) a.tiles[i] = int2{0, i};
+  for (int i = t; i < a.nrtiles; i += 256) a.rtiles[i] = int2{0, i};
+}
+
+// The one-layer group of a static step, planned in place.
+void plan_static(cd_group* g, cd_layer* L, int r, int ntiles, int nrtiles) {
+  g->layers.resize(1);
+  g->layers[0] = L;
+  g->L = 1;
+  g->device = L->device;
+  g->g_bf16 = L->d.grad_dtype == CD_BF16;
+  g->tau = L->d.tau;
+  g->eps = L->d.eps;
+  g->policy = L->d.policy;
+  g->H = L->d.H;
+  g->nparts_stride = static_cast<int>(blocks_for(1LL * L->d.m * L->d.n));
+  g->shapes.resize(1);
+  g->shapes[0].m = L->d.m;
+  g->shapes[0].n = L->d.n;
+  g->shapes[0].idx.resize(1);
+  g->shapes[0].idx[0] = 0;
+  g->units.resize(1);
+  Unit& u = g->units[0];
+  u.sc = 0;
+  u.sel.resize(1);
+  u.sel[0] = 0;
+  u.off = 0;
+  u.toff = 0;
+  u.nt = ntiles;
+  u.rtoff = 0;
+  u.nrt = nrtiles;
+  g->sbatches.resize(1);
+  g->sbatches[0].resize(1);
+  g->sbatches[0][0] = 0;
+  g->nside = 0;
+  g->out_host = nullptr;
+  g->out_host_dev = nullptr;
+  g->ev = nullptr;
+  g->timer.on = false;
+  (void)r;
+}
+
+cd_status static_step_impl(const cd_layer_desc* desc, double* prev_norm, long long* step, const void* G,
+                           float* M, float* X, float* Q, float mu, float eta, int r, void* stream,
+                           cd_result* out) {
+  cd_status st = check_desc(desc);
+  if (st != CD_OK) return st;
+  if (!prev_norm || !step) return fail(CD_EINVAL, "prev_norm and step must not be NULL");
+  if ((reinterpret_cast<uintptr_t>(prev_norm) & 7u) != 0) return fail(CD_EINVAL, "prev_norm must be 8-byte aligned");
+  if (*step < 0) return fail(CD_EINVAL, "step must be >= 0");
+  if (r < 1 || r > desc->r_max) return fail(CD_EINVAL, "r must be in [1, r_max] (got %d)", r);
+  const int m = desc->m, n = desc->n;
+  const int ntiles = (m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK;
+  const int nrtiles = (r + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK;
+  const LayerLayout lo = layer_layout(m, n, r);
+  const GroupLayout glo = group_layout(1, static_cast<int>(blocks_for(1LL * m * n)), ntiles, nrtiles);
+  const size_t need = lo.total + glo.total;
+  if (need > CD_STATIC_SCRATCH_BYTES)
+    return fail(CD_EINVAL,
+                "a %d x %d layer at rank %d needs %zu bytes of workspace; the allocation-free step has "
+                "%zu (CD_STATIC_SCRATCH_BYTES): use cd_step",
+                m, n, r, need, static_cast<size_t>(CD_STATIC_SCRATCH_BYTES));
+  int dev = -1;
+  CD_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(CD_EINVAL, "device %d is beyond the %d supported", dev, kMaxDevices);
+  StaticSlot& slot = g_static[dev];
+  std::lock_guard<std::mutex> lock(slot.mu);
+  if (!slot.base) {
+    void* ptr = nullptr;
+    CD_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    slot.base = ptr;
+  }
+  char* base = static_cast<char*>(slot.base);
+  cd_layer* L = &slot.layer;
+  L->d = *desc;
+  L->d.r_max = r;   // the workspace is laid out for this rank
+  L->device = dev;
+  L->step = *step;
+  carve_layer(L, base, lo);
+  L->prev = prev_norm;
+  L->prev_zero = false;
+  cd_group* g = &slot.group;
+  plan_static(g, L, r, ntiles, nrtiles);
+  carve_group(g, base + lo.total, glo);
+  const void* Ga[1] = {G};
+  float* Ma[1] = {M};
+  float* Xa[1] = {X};
+  float* Qa[1] = {Q};
+  st = check_step_args(g, Ga, Ma, Xa, Qa, mu, eta, r);
+  if (st != CD_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  StaticSetup su{};
+  su.nparts = g->nparts;
+  su.np = g->nparts_stride;
+  su.prev_tab = g->prev;
+  su.prev = prev_norm;
+  su.counter = g->counter;
+  su.ct = g->chol_tab;
+  su.ctv = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok};
+  su.tt[0] = g->trsm_tab[0];
+  su.tt[1] = g->trsm_tab[1];
+  su.tt[2] = g->trsm_tab[2];
+  factor_tabs(L, su.ttv[0], su.ttv[1], su.ttv[2]);
+  su.tiles = g->trsm_tiles;
+  su.ntiles = ntiles;
+  su.rtiles = g->trtri_tiles;
+  su.nrtiles = nrtiles;
+  hipLaunchKernelGGL(k_static_setup, dim3(1), dim3(256), 0, s, su);
+  CD_HIP(hipGetLastError());
+
+  // no branch prediction without state between calls: the buffer pass fuses
+  // the skip update only when a fixed policy says the step is local
+  const long long next_step = *step + 1;
+  const bool fixed = fixed_policy(g);
+  const bool spec = fixed && !fixed_sync(g, next_step);
+  st = enqueue_form(g, Ga, Ma, Xa, eta, spec, s);
+  if (st != CD_OK) return st;
+  st = enqueue_gate(g, s, false);
+  if (st != CD_OK) return st;
+  struct { cd::GateOut h; double rm; } hb;
+  CD_HIP(hipMemcpyAsync(&hb, g->out_dev, sizeof(hb), hipMemcpyDeviceToHost, s));
+  CD_HIP(hipStreamSynchronize(s));
+  *step = next_step;
+  const bool sync = fixed ? fixed_sync(g, next_step) : hb.h.flag != 0;
+  st = enqueue_branch(g, sync, spec, Ga, Ma, Xa, Qa, mu, eta, r, s);
+  if (st != CD_OK) return st;
+  if (out) { out->rmmc = hb.h.g; out->sync_flag = sync ? 1 : 0; }
+  if (hb.h.nonfinite) return fail(CD_ENONFINITE, "the layer norm ||B|| was not finite");
+  return CD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1058,6 +1240,16 @@ cd_status cd_step(cd_layer* layer, const void* G, float* M, float* X, float* Q, 
     return group_step_impl(layer->self, Ga, Ma, Xa, Qa, mu, eta, r, stream, nullptr, out);
   } catch (...) {
     return fail(CD_ENOMEM, "exception in cd_step");
+  }
+}
+
+cd_status cd_step_static(const cd_layer_desc* desc, double* prev_norm, long long* step, const void* G,
+                         float* M, float* X, float* Q, float mu, float eta, int r, void* stream,
+                         cd_result* out) {
+  try {
+    return static_step_impl(desc, prev_norm, step, G, M, X, Q, mu, eta, r, stream, out);
+  } catch (...) {
+    return fail(CD_ENOMEM, "exception in cd_step_static");
   }
 }
 

@@ -185,3 +185,26 @@ def test_streaming_launch_plan_of_the_workloads(tmp_path):
     # 49 small layers: the layer cap splits them 48 + 1
     assert _stream_plan([(64, 64)] * 49, tmp_path) == [(48, 48), (1, 1)]
 
+
+def test_static_step_refuses_before_touching_the_gpu(L):
+    """cd_step_static checks the descriptor, its state arguments and the
+    workspace size against the fixed array before anything else (so these
+    errors need no GPU)."""
+    st = ctypes.c_longlong(0)
+    res = cdl.Result()
+    big = _desc(m=8192, n=8192, r_max=1024)
+    rc = L.cd_step_static(ctypes.byref(big), 4096, ctypes.byref(st), 16, 16, 16, 16, 0.95, 0.01, 1024, None,
+                          ctypes.byref(res))
+    assert rc == cdl.CD_EINVAL and b"CD_STATIC_SCRATCH_BYTES" in L.cd_last_error()
+    small = _desc()
+    assert L.cd_step_static(ctypes.byref(small), None, ctypes.byref(st), 16, 16, 16, 16, 0.95, 0.01, 4, None,
+                            ctypes.byref(res)) == cdl.CD_EINVAL
+    assert L.cd_step_static(ctypes.byref(small), 4096, None, 16, 16, 16, 16, 0.95, 0.01, 4, None,
+                            ctypes.byref(res)) == cdl.CD_EINVAL
+    assert L.cd_step_static(ctypes.byref(small), 4100, ctypes.byref(st), 16, 16, 16, 16, 0.95, 0.01, 4, None,
+                            ctypes.byref(res)) == cdl.CD_EINVAL     # misaligned prev_norm
+    assert L.cd_step_static(ctypes.byref(small), 4096, ctypes.byref(st), 16, 16, 16, 16, 0.95, 0.01, 9, None,
+                            ctypes.byref(res)) == cdl.CD_EINVAL     # r > r_max
+    assert L.cd_step_static(None, 4096, ctypes.byref(st), 16, 16, 16, 16, 0.95, 0.01, 4, None,
+                            ctypes.byref(res)) == cdl.CD_EINVAL
+    assert st.value == 0
