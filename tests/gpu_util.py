@@ -13,9 +13,24 @@ import paper_2512_13728_amd as cdl
 
 U32 = 2.0 ** -24  # unit roundoff of fp32
 
-TOL_F32 = 1e-5    # M, X, P, Q, dM, dX with fp32 gradients (global rel-Frobenius)
-TILE_F32 = 3e-5   # the largest 128 x 64 tile (64-row panel of P) error, fp32 gradients
-TOL_BF16 = 2e-2   # every quantity, global and per tile, with bf16 gradients
+# Bounds (rel-Frobenius against the oracle; the largest measured values over
+# the GPU suite in brackets).  fp32 gradients: the power iteration, both
+# CholQR passes and R = B^T P run in fp64 and everything is stored in fp32,
+# so P, Q and M carry a few fp32 roundings [P 2.7e-8 at kappa 1.2e6, Q 5.2e-8,
+# M 3.7e-8]; the rank-r corrections use fp32-accurate split products
+# [dM 1.1e-6, its largest 128 x 64 tile 1.5e-6]; X [8.3e-7] and dX carry
+# the fp32 rounding of X itself (x_floor).
+TIGHT_F32 = 5e-7   # P, Q, M with fp32 gradients
+TOL_F32 = 1e-5     # X, dM, dX with fp32 gradients (the stated fp32 tolerance)
+TILE_F32 = 1.5e-5  # the largest tile of dM, dX, P with fp32 gradients
+# bf16 gradients: the power products use two-piece splits (about 2^-16), so
+# P, Q and dX move by about kappa(P~) 2^-16 times a small factor [1.5e-2 at
+# kappa 2e6]: the stated 2e-2; the rank-r corrections use plain bf16
+# products [dM 2.9e-3, tile 3.0e-3], which reach M and X only through that
+# (1 - mu) and eta-scaled correction [M 1.5e-4, X 7.1e-4].
+TOL_BF16 = 2e-2    # P, Q, dM, dX and every tile with bf16 gradients
+M_BF16 = 2e-3
+X_BF16 = 5e-3
 
 _hip = None
 
@@ -252,19 +267,22 @@ def check_errors(d, bf16=False):
     the local-branch errors), given the decision the step took."""
     d = {k: v for k, v in d.items() if k != "ref"}
     if bf16:
-        for k in ("err_M", "err_X", "err_P", "err_Q", "err_dM", "err_dX", "tile_dM", "tile_dX", "tile_P"):
+        assert d["err_M"] <= M_BF16, d
+        assert d["err_X"] <= X_BF16, d
+        for k in ("err_P", "err_Q", "err_dM", "err_dX", "tile_dM", "tile_dX", "tile_P"):
             if k in d:
                 assert d[k] <= TOL_BF16, (k, d)
         if d["flag_oracle"]:
             assert d["orth_P"] <= 1e-4 and d["colnorm_dev"] <= 1e-5, d
         return
-    assert d["err_M"] <= TOL_F32, d
+    assert d["err_M"] <= TIGHT_F32, d
     assert d["err_X"] <= TOL_F32, d
     if d["flag_oracle"]:
         assert d["orth_P"] <= 1e-5, d
         assert d["colnorm_dev"] <= 1e-5, d
-        for k in ("err_P", "err_Q", "err_dM"):
-            assert d[k] <= TOL_F32, (k, d)
+        for k in ("err_P", "err_Q"):
+            assert d[k] <= TIGHT_F32, (k, d)
+        assert d["err_dM"] <= TOL_F32, d
         assert d["err_dX"] <= TOL_F32 + d["dx_floor"], d
         for k in ("tile_dM", "tile_P"):
             assert d[k] <= TILE_F32, (k, d)
