@@ -75,8 +75,8 @@ CSRC = os.path.join(ROOT, "paper_2512_13728_amd", "csrc")
 _STREAM = ["k_stream.hip", "common.hpp"]
 _BF = ["k_gemm_bf.hip", "bf16_split.hpp", "mfma_tile.hpp", "common.hpp"]
 KIND_KERNEL = {
-    "form_buffer": (r"k_form_buffer<\w+, false>", _STREAM),
-    "form_buffer_local": (r"k_form_buffer<\w+, true>", _STREAM),
+    "form_buffer": (r"k_form_buffer<\w+, 0>", _STREAM),
+    "form_buffer_local": (r"k_form_buffer<\w+, 1>", _STREAM),
     "local_update": (r"k_local_update<", _STREAM),
     "gate": (r"k_gate\b", _STREAM),
     "update_bf16": (r"k_update_pl<1,", _BF),
@@ -111,6 +111,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--pool", type=int, default=20, help="distinct gradient sets kept resident")
     p.add_argument("--rank", type=int, default=0, help="override the workload's rank r")
+    p.add_argument("--async", dest="async_steps", action="store_true",
+                   help="timed steps asynchronous (no host output: both branches enqueued, every kernel "
+                        "predicated on the gate's decision in device memory); the decisions are those of "
+                        "the blocking profiling pass over the same inputs, checked against the last step's")
     p.add_argument("--stream-inputs", action="store_true",
                    help="draw every step's gradients on the GPU just before the step (outside its "
                         "timed interval) instead of cycling a resident pool; the default for "
@@ -165,6 +169,49 @@ def summarize_trace(d: str, bench_json: str, out: str):
         lines.append(f"#   {k}: {json.dumps(v)}")
     open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+
+def _pmc_dispatches(d: str, counter: str):
+    """[(dispatch id, kernel name, value)] of one counter, in dispatch order
+    (values of one dispatch summed over the rows the profiler writes)."""
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        sys.exit(f"no *counter_collection.csv under {d}")
+    per = {}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            key = int(r["Dispatch_Id"])
+            per.setdefault(key, [r["Kernel_Name"], 0.0])[1] += float(r["Counter_Value"])
+    return [(k, v[0], v[1]) for k, v in sorted(per.items())]
+
+
+# kernels of the step's two streaming passes and its gate; every other
+# library kernel belongs to the sync branch
+STEP_COMMON = (r"k_form_buffer<", r"k_gate\b", r"k_local_update<")
+
+
+def steps_of(dispatches):
+    """Library dispatches (in order) cut into steps: a step starts at its
+    first buffer-pass launch (k_form_buffer) and runs until the next step's.
+    Returns [(kind, [indices])], kind "sync" when a sync-branch kernel ran."""
+    steps, cur, prev_form = [], None, False
+    for i, (_, name, _) in enumerate(dispatches):
+        if "cd::" not in name:
+            continue
+        form = re.search(r"k_form_buffer<", name) is not None
+        if form and not prev_form:
+            cur = []
+            steps.append(cur)
+        prev_form = form
+        if cur is not None:
+            cur.append(i)
+    out = []
+    for idx in steps:
+        sync = any(not any(re.search(p, dispatches[i][1]) for p in STEP_COMMON) for i in idx)
+        out.append(("sync" if sync else "local", idx))
+    return out
 
 
 def _pmc_rows(d: str, counter: str):
@@ -236,9 +283,45 @@ def summarize_pmc(fdir: str, wdir: str, out: str, workload: str, cal_mib: int):
         nw = max(len(t["WRITE_SIZE"]), 1)
         lines.append(f"{name[:64]:64s} {len(t['FETCH_SIZE']):5d} {sum(t['FETCH_SIZE']) / nf / 1e6:10.2f} "
                      f"{sum(t['WRITE_SIZE']) / nw / 1e6:10.2f}")
-    lines += ["", "json " + json.dumps({"workload": workload, "factor": factor, "kinds": kinds})]
+    # HBM bytes per step, by branch: the two runs dispatch the same sequence
+    fd = _pmc_dispatches(fdir, "FETCH_SIZE")
+    wd = _pmc_dispatches(wdir, "WRITE_SIZE")
+    fs, ws = steps_of(fd), steps_of(wd)
+    if len(fs) != len(ws) or any(a[0] != b[0] or len(a[1]) != len(b[1]) for a, b in zip(fs, ws)):
+        sys.exit("the FETCH_SIZE and WRITE_SIZE runs dispatched different step sequences")
+    per_branch = {}
+    for (kind, fi), (_, wi) in zip(fs, ws):
+        fb = sum(fd[i][2] for i in fi) * 1024.0 * factor["FETCH_SIZE"]
+        wb = sum(wd[i][2] for i in wi) * 1024.0 * factor["WRITE_SIZE"]
+        per_branch.setdefault(kind, []).append((fb, wb))
+    steps = {"source_digest": source_digest(ALL_SOURCES)}
+    lines += ["", "# HBM bytes per step (every library kernel of the step, the dispatch sequence cut at each",
+              "# step's first buffer-pass launch), median over the steps of each branch in the run:"]
+    for kind, v in sorted(per_branch.items()):
+        fmed = sorted(x[0] for x in v)[len(v) // 2]
+        wmed = sorted(x[1] for x in v)[len(v) // 2]
+        steps[kind] = {"fetch_bytes": fmed, "write_bytes": wmed, "bytes": fmed + wmed, "steps": len(v)}
+        lines.append(f"#   {kind:6s} steps {len(v):4d}  fetch {fmed / 1e9:8.3f} GB  write {wmed / 1e9:8.3f} GB")
+    lines += ["", "json " + json.dumps({"workload": workload, "factor": factor, "kinds": kinds, "steps": steps})]
     open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+
+ALL_SOURCES = sorted(f for f in os.listdir(CSRC) if f.endswith((".hip", ".hpp", ".cpp")))
+
+
+def counted_step_bytes(workload: str):
+    """Counted HBM bytes per sync and per local step from the committed
+    counter summary, or {} if there is none or any kernel source changed since."""
+    path = PMC_PROFILE.format(workload=workload)
+    if not os.path.exists(path):
+        return {}
+    for line in open(path):
+        if line.startswith("json "):
+            st = json.loads(line[5:]).get("steps", {})
+            if st.get("source_digest") == source_digest(ALL_SOURCES):
+                return {k: v["bytes"] for k, v in st.items() if k in ("sync", "local")}
+    return {}
 
 
 def counted_traffic(workload: str, kind: str):
@@ -390,9 +473,10 @@ def main():
     pM, pX, pQ = group.pack(M, "M"), group.pack(X, "X"), group.pack(Q, "Q", w.r)
     pG = [group.pack(gs, "G") for gs in grads]
 
-    def trajectory(timing_kinds):
+    def trajectory(timing_kinds, asyn=False):
         """Steps 1..K from the initial state; kernel launches of the kinds in
-        `timing_kinds` (None = every kind) bracketed by HIP events."""
+        `timing_kinds` (None = every kind) bracketed by HIP events.  asyn: the
+        steps are asynchronous (no per-step outcome on the host)."""
         reset()
         flags, rmmcs = [], []
         group.set_timing(True, timing_kinds)
@@ -426,10 +510,13 @@ def main():
             t_start = time.perf_counter()
             ev[0].record(stream)
             for t in range(K):
-                g, flag, _, _ = group.step(pG[t % pool], pM, pX, pQ, w.mu, w.eta, w.r, sh)
+                if asyn:
+                    group.step(pG[t % pool], pM, pX, pQ, w.mu, w.eta, w.r, sh, wait=False)
+                else:
+                    g, flag, _, _ = group.step(pG[t % pool], pM, pX, pQ, w.mu, w.eta, w.r, sh)
+                    flags.append(flag)
+                    rmmcs.append(g)
                 ev[t + 1].record(stream)
-                flags.append(flag)
-                rmmcs.append(g)
             torch.cuda.synchronize()
             wall = time.perf_counter() - t_start
             step_ms = [ev[t].elapsed_time(ev[t + 1]) for t in range(K)]
@@ -443,11 +530,18 @@ def main():
     # dominant kernel.  The events idle the GPU for several microseconds at
     # each bracketed launch, so the timed pass, on the untimed schedule,
     # brackets only the dominant kernel's launches.
-    _, _, _, prof_wall, kt = trajectory(None)
+    prof_flags, prof_rmmcs, _, prof_wall, kt = trajectory(None)
     dom = max(kt.items(), key=lambda kv: kv[1]["total_ms"])[0]
     log(f"[bench] profiling pass: {K} steps in {prof_wall * 1e3:.2f} ms with every launch "
         f"bracketed (sync batches serial); dominant kernel {dom}")
-    flags, rmmcs, step_ms, elapsed, kt_dom = trajectory([dom])
+    asyn = args.async_steps and not streamed
+    flags, rmmcs, step_ms, elapsed, kt_dom = trajectory([dom], asyn)
+    if asyn:
+        g_last, f_last, _, _ = group.last_result()
+        if f_last != prof_flags[-1] or g_last != prof_rmmcs[-1]:
+            sys.exit(f"asynchronous steps diverged from the blocking pass: {g_last} {f_last} vs "
+                     f"{prof_rmmcs[-1]} {prof_flags[-1]}")
+        flags, rmmcs = prof_flags, prof_rmmcs
     log(f"[bench] timed {K} steps in {elapsed * 1e3:.2f} ms; syncs at "
         f"{[t + 1 for t, f in enumerate(flags) if f]}")
 
@@ -455,8 +549,6 @@ def main():
     n_local = K - n_sync
     sync_ms = [x for x, f in zip(step_ms, flags) if f]
     local_ms = [x for x, f in zip(step_ms, flags) if not f]
-    total_bytes = sum(v["bytes"] for v in kt.values())
-    total_flops = sum(v["flops"] for v in kt.values())
     log("[bench] per kind, profiling pass (every launch bracketed):")
     for name, v in sorted(kt.items(), key=lambda kv: -kv[1]["total_ms"]):
         log(f"[bench]   {name:16s} launches {v['launches']:5d}  {v['total_ms']:9.3f} ms  "
@@ -484,10 +576,14 @@ def main():
         if not ms_list:
             return {"count": 0}
         med = float(np.median(ms_list))
-        return {"count": count, "median_ms": round(med, 4), "min_ms": round(min(ms_list), 4),
-                "max_ms": round(max(ms_list), 4), "params_per_s": w.params / (med * 1e-3)}
+        return {"count": count, "median_ms": round(med, 4),
+                "p10_ms": round(float(np.percentile(ms_list, 10)), 4),
+                "p90_ms": round(float(np.percentile(ms_list, 90)), 4),
+                "min_ms": round(min(ms_list), 4), "max_ms": round(max(ms_list), 4),
+                "params_per_s": w.params / (med * 1e-3)}
 
     branches = {"sync": branch(sync_ms, n_sync), "local": branch(local_ms, n_local)}
+    counted = counted_step_bytes(w.name)
     # compulsory bytes per step: read G, M, X and write M, X; a sync step also
     # reads and writes Q (n x r per layer)
     gb = 2 if w.grad_dtype == "bf16" else 4
@@ -495,25 +591,38 @@ def main():
     sync_bytes = skip_bytes + 8 * sum(n * w.r for _, n in w.shapes)
     for name, nbytes in (("local", skip_bytes), ("sync", sync_bytes)):
         if branches[name]["count"]:
-            gbps = nbytes / (branches[name]["median_ms"] * 1e-3) / 1e9
+            t_med = branches[name]["median_ms"] * 1e-3
+            gbps = nbytes / t_med / 1e9
             branches[name]["compulsory_bytes"] = nbytes
             branches[name]["algorithmic_GBps"] = gbps
-            branches[name]["frac_of_hbm_peak"] = gbps / PEAK_HBM_GBPS
+            branches[name]["algorithmic_frac_of_hbm_peak"] = gbps / PEAK_HBM_GBPS
+            # hardware-counted bytes of such a step (FETCH_SIZE + WRITE_SIZE,
+            # profiles/), null when the kernels changed since they were counted
+            cb = counted.get(name)
+            branches[name]["counted_bytes"] = cb
+            branches[name]["counted_GBps"] = cb / t_med / 1e9 if cb else None
     if branches["sync"]["count"]:
         # a sync step is MFMA work: the method's flops (P~ = BQ, R = B^T P and
         # the rank-r M and X corrections, 8 r flops per parameter, plus two
-        # CholQR passes of 2 m r^2 + r^3 / 3 each) against the fp32 MFMA peak an
-        # fp32 implementation would be bound by; and the MFMA time the executed
-        # products (every bf16 piece product, fp64 where used) need at their
-        # peaks, as a fraction of the step
+        # CholQR passes of 2 m r^2 + r^3 / 3 each), and, as a model (not a
+        # counter), the time the executed MFMA products (every bf16 piece
+        # product at the bf16 peak, fp64 products at the fp64 peak) would need
+        # at the published peaks, as a fraction of the step; the counted MFMA
+        # busy fraction per kernel is in profiles/
         t_sync = branches["sync"]["median_ms"] * 1e-3
         alg = sum(8.0 * w.r * m * n + 2.0 * (2.0 * m * w.r ** 2 + w.r ** 3 / 3.0) for m, n in w.shapes)
-        busy = sum(mult * kt[k]["flops"] / n_sync / (PEAK_TFLOPS[prec] * 1e12)
-                   for k in kt for bound, prec, mult in [KIND_BOUND.get(k, ("hbm", None, 1))]
-                   if bound == "mfma")
+        executed = {}
+        for k in kt:
+            bound, prec, mult = KIND_BOUND.get(k, ("hbm", None, 1))
+            if bound == "mfma":
+                executed[prec] = executed.get(prec, 0.0) + mult * kt[k]["flops"] / n_sync
+        busy = sum(f / (PEAK_TFLOPS[prec] * 1e12) for prec, f in executed.items())
         branches["sync"].update(algorithmic_flops=alg, algorithmic_TFLOPs=alg / t_sync / 1e12,
-                                frac_of_fp32_mfma_peak=alg / t_sync / 1e12 / PEAK_TFLOPS["f32"],
-                                mfma_busy_frac=busy / t_sync)
+                                executed_mfma_flops={p: f for p, f in executed.items()},
+                                executed_TFLOPs={p: f / t_sync / 1e12 for p, f in executed.items()},
+                                executed_frac_of_peak={p: f / t_sync / 1e12 / PEAK_TFLOPS[p]
+                                                       for p, f in executed.items()},
+                                mfma_time_model_frac=busy / t_sync)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -533,7 +642,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        # the contractions of bf16-gradient layers run on the bf16 MFMA (split
+        # fp32 operands for the power iteration, plain bf16 for the rank-r
+        # update); fp32-gradient layers compute in fp32 and fp64
+        "dtype": "bf16" if w.grad_dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {
             "workload": (f"{w.name}: {L} matrices of the 1.3B-shaped GPT set (d_model 2048, 24 blocks)"
@@ -546,13 +658,18 @@ def main():
                                       "P~ = BQ, Gram and CholQR in fp64; R and the M/X update on bf16 "
                                       "MFMA with 3-piece fp32 splits"),
             "policy": args.policy + (f" (H = {args.H})" if args.policy == "every_h" else ""),
+            "steps_mode": "asynchronous (no host read per step)" if asyn else "blocking (gate read per step)",
             "tau": w.tau, "trajectory_steps": K,
             "sync_steps": n_sync, "local_steps": n_local, "parallelism": "none (1 GPU)",
             "inputs": (f"gradients drawn on the GPU between steps, outside each step's timed interval"
                        if streamed else f"{pool} gradient sets resident in HBM, cycled"),
         },
-        "hbm_GBps": total_bytes / elapsed / 1e9,
-        "achieved_TFLOPs": total_flops / elapsed / 1e12,
+        # whole trajectory: compulsory bytes (algorithmic) and, where the
+        # committed counter summary matches the sources, counted bytes
+        "algorithmic_GBps": (n_sync * sync_bytes + n_local * skip_bytes) / elapsed / 1e9,
+        "counted_GBps": ((n_sync * counted["sync"] if n_sync else 0.0) +
+                         (n_local * counted["local"] if n_local else 0.0)) / elapsed / 1e9
+        if (not n_sync or "sync" in counted) and (not n_local or "local" in counted) else None,
         "branches": branches,
         "roofline": roofline,
         "kernels_profiling_pass": {k: {"launches": v["launches"], "total_ms": round(v["total_ms"], 4)}

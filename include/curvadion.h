@@ -26,14 +26,26 @@
  * prev_norm; both live until cd_destroy.
  *
  * Ordering: all work is ordered on the HIP stream passed to a step call
- * (NULL = the default stream).  A step blocks the calling host thread once,
- * after the RMMC gate, until the gate's output has reached the host (the gate
- * kernel writes it into pinned host memory; this single device-to-host
- * crossing stands in for the max all-reduce).  Under the
- * RMMC policy the branch is enqueued after that read, as it depends on it;
- * the other policies fix the branch in advance and enqueue it before the
- * read, so the GPU does not idle through the round trip.  The call returns
- * once the branch is enqueued and the output read.  In a group with layers of several shapes (or
+ * (NULL = the default stream).
+ *
+ * Blocking and asynchronous steps.  A step call that asks for a result on
+ * the host (`out`, or `rmmc_per_layer` of a group step, not NULL) blocks the
+ * calling host thread once, after the RMMC gate, until the gate's output has
+ * reached the host (the gate kernel writes it into pinned host memory; this
+ * single device-to-host crossing stands in for the max all-reduce).  Under
+ * the RMMC policy the branch is enqueued after that read, as it depends on
+ * it; the other policies fix the branch in advance and enqueue it before the
+ * read, so the GPU does not idle through the round trip.  A step call with no
+ * host output is asynchronous: it enqueues the whole step and returns without
+ * waiting for anything.  The gate then leaves its decision in device memory,
+ * and under the RMMC policy both branches are enqueued, each of their kernels
+ * returning at once when its branch was not taken (a few microseconds per
+ * kernel on the GPU's timeline: the price of not waiting).  The results are
+ * bit-identical to those of blocking steps over the same inputs.
+ * cd_layer_last_result / cd_group_last_result read the outcome of the last
+ * step later (and report CD_ENONFINITE and CD_ERANKDEF).
+ *
+ * The call returns once the branch is enqueued.  In a group with layers of several shapes (or
  * more than 32 layers of one shape) the sync branch runs each batch of layers
  * of one shape on its own stream: the caller's stream and up to three streams
  * the group owns (default priority), which wait for the caller's stream before
@@ -65,7 +77,7 @@
 extern "C" {
 #endif
 
-#define CD_ABI_VERSION 2
+#define CD_ABI_VERSION 3
 
 typedef enum cd_status {
   CD_OK = 0,
@@ -73,8 +85,9 @@ typedef enum cd_status {
   CD_ENOMEM = -2,      /* device or host allocation failed */
   CD_EHIP = -3,        /* a HIP runtime call failed; see cd_last_error() */
   CD_ENONFINITE = -4,  /* some ‖B‖ was NaN/Inf; the step still ran (local branch) */
-  CD_ERANKDEF = -5     /* reserved: rank deficiency is reported by
-                          cd_layer_rank_deficient(), not by a step's status */
+  CD_ERANKDEF = -5     /* from cd_*_last_result: the last step synced and some
+                          layer's P~ was numerically rank deficient; every
+                          output was still written (see cd_layer_rank_deficient) */
 } cd_status;
 
 typedef enum cd_dtype { CD_F32 = 0, CD_BF16 = 1 } cd_dtype;
@@ -124,9 +137,10 @@ cd_status cd_layer_create(const cd_layer_desc* desc, cd_layer** out);
 /* One step for one layer (Algorithm 2 with the max taken over this layer
  * alone).  G: m x n of desc.grad_dtype; M, X: m x n fp32; Q: n x r fp32.
  * mu in [0, 1], eta finite and >= 0, 1 <= r <= r_max.  `stream` is a
- * hipStream_t (NULL = default stream).  `out` (host, may be NULL) receives
- * the statistic and the branch taken.  Returns CD_OK or CD_ENONFINITE after a
- * completed step, or an error before any work. */
+ * hipStream_t (NULL = default stream).  `out` (host) receives the statistic
+ * and the branch taken; NULL makes the step asynchronous (see the top of this
+ * header).  Returns CD_OK, or CD_ENONFINITE after a blocking step whose norm
+ * was not finite, or an error before any work. */
 cd_status cd_step(cd_layer* layer, const void* G, float* M, float* X, float* Q,
                   float mu, float eta, int r, void* stream, cd_result* out);
 
@@ -180,13 +194,26 @@ cd_status cd_group_create(cd_layer* const* layers, int n_layers, cd_group** out)
  * n_layers DEVICE pointers, in the order the group was created with; shapes as
  * for cd_step with each layer's (m, n) and the common rank r (1 <= r <= every
  * layer's r_max).  `rmmc_per_layer` (host, may be NULL) receives n_layers
- * values of RMMC_l.  Returns CD_OK or CD_ENONFINITE after a completed step, or
- * an error before any work. */
+ * values of RMMC_l.  With both `rmmc_per_layer` and `out` NULL the step is
+ * asynchronous.  Returns CD_OK, or CD_ENONFINITE after a blocking step, or an
+ * error before any work. */
 cd_status cd_group_step(cd_group* group, const void* const* G, float* const* M,
                         float* const* X, float* const* Q, float mu, float eta, int r,
                         void* stream, double* rmmc_per_layer, cd_result* out);
 
 cd_status cd_group_destroy(cd_group* group);
+
+/* The outcome of the group's last step (of the layer's last cd_step): waits
+ * until that step's work has finished on the device (its completion event;
+ * other work on the device is not waited for), then writes the gate
+ * statistic and the branch taken to `out` and, for a group, the n_layers
+ * values of RMMC_l to `rmmc_per_layer` (both host, may be NULL).  Returns
+ * CD_OK, CD_ENONFINITE (some ‖B‖ was not finite: the local branch ran),
+ * CD_ERANKDEF (the step synced and some layer's P~ was numerically rank
+ * deficient; the outputs were still written), or CD_EINVAL before the first
+ * step. */
+cd_status cd_group_last_result(cd_group* group, double* rmmc_per_layer, cd_result* out);
+cd_status cd_layer_last_result(cd_layer* layer, cd_result* out);
 
 /* Checkpoint support: the library-owned state of a layer is prev_norm (the
  * last ‖B‖_F) and the step counter; M, X and Q belong to the caller.  These
@@ -199,9 +226,10 @@ cd_status cd_layer_set_state(cd_layer* layer, double prev_norm, long long step);
  * its next step or cd_destroy.  For inspection and tests. */
 cd_status cd_layer_last_factors(const cd_layer* layer, const float** P, const float** R);
 
-/* Waits for all work queued on the layer's device, then sets *flag = 1 if the last
- * sync step found P~ numerically rank deficient (a Cholesky pivot at or below
- * 1e-13 times the largest Gram diagonal).  M, X and Q were still written and P
+/* Waits until the layer's last step has finished on the device (the
+ * completion event of the group that took it, not the whole device), then
+ * sets *flag = 1 if the last sync step found P~ numerically rank deficient (a
+ * Cholesky pivot at or below 1e-13 times the largest Gram diagonal).  M, X and Q were still written and P
  * still has orthonormal columns: past the numerical rank it is completed with
  * fixed pseudo-random directions orthonormalised against the other columns
  * (as a Householder QR factor is completed), so those columns, and the

@@ -35,7 +35,7 @@ EXPORTED_SYMBOLS = (
     "cd_group_destroy", "cd_layer_get_state", "cd_layer_set_state",
     "cd_layer_last_factors", "cd_layer_rank_deficient", "cd_group_set_timing",
     "cd_group_kernel_times", "cd_group_set_timing_kinds", "cd_last_error", "cd_abi_version",
-    "cd_step_static",
+    "cd_step_static", "cd_group_last_result", "cd_layer_last_result",
 )
 
 
@@ -89,6 +89,8 @@ def lib() -> ctypes.CDLL:
                                 ctypes.POINTER(vp), f, f, i, vp, ctypes.POINTER(d),
                                 ctypes.POINTER(Result)]
     L.cd_group_destroy.argtypes = [vp]
+    L.cd_group_last_result.argtypes = [vp, ctypes.POINTER(d), ctypes.POINTER(Result)]
+    L.cd_layer_last_result.argtypes = [vp, ctypes.POINTER(Result)]
     L.cd_layer_get_state.argtypes = [vp, ctypes.POINTER(d), ctypes.POINTER(ctypes.c_longlong)]
     L.cd_layer_set_state.argtypes = [vp, d, ctypes.c_longlong]
     L.cd_layer_last_factors.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp)]
@@ -179,15 +181,25 @@ class Layer:
         return self._h
 
     def step(self, G, M, X, Q, mu: float, eta: float, r: Optional[int] = None,
-             stream=None) -> Tuple[float, bool, int]:
-        """One CurvaDion step; returns (rmmc, sync_flag, status)."""
+             stream=None, wait: bool = True):
+        """One CurvaDion step; returns (rmmc, sync_flag, status).  wait=False
+        enqueues the whole step without reading its outcome (the asynchronous
+        step) and returns None; last_result() reads it later."""
         r = Q.shape[1] if r is None and hasattr(Q, "shape") else r
         for t, role in ((G, "G"), (M, "M"), (X, "X"), (Q, "Q")):
             self.check(t, role, r)
         res = Result()
         st = lib().cd_step(self._h, _ptr(G), _ptr(M), _ptr(X), _ptr(Q), mu, eta, r,
-                           _stream_handle(stream), ctypes.byref(res))
+                           _stream_handle(stream), ctypes.byref(res) if wait else None)
         _check(st, allow=(CD_OK, CD_ENONFINITE))
+        return (res.rmmc, bool(res.sync_flag), st) if wait else None
+
+    def last_result(self) -> Tuple[float, bool, int]:
+        """(rmmc, sync_flag, status) of the last step, once its work has
+        finished; status CD_OK, CD_ENONFINITE or CD_ERANKDEF."""
+        res = Result()
+        st = lib().cd_layer_last_result(self._h, ctypes.byref(res))
+        _check(st, allow=(CD_OK, CD_ENONFINITE, CD_ERANKDEF))
         return res.rmmc, bool(res.sync_flag), st
 
     def get_state(self) -> Tuple[float, int]:
@@ -298,9 +310,10 @@ class Group:
             pa._checked.add((role, key))
         return pa
 
-    def step(self, G, M, X, Q, mu: float, eta: float, r: int, stream=None):
+    def step(self, G, M, X, Q, mu: float, eta: float, r: int, stream=None, wait: bool = True):
         """One step over every layer; returns (rmmc_max, sync_flag, rmmc_per_layer, status).
-        G, M, X, Q are lists with one tensor (or address) per layer, or pack() results."""
+        G, M, X, Q are lists with one tensor (or address) per layer, or pack() results.
+        wait=False: the asynchronous step (returns None; see last_result)."""
         n = len(self.layers)
 
         def mk(ts, role):
@@ -315,11 +328,24 @@ class Group:
             return (ctypes.c_void_p * n)(*[_ptr(t) for t in ts])
 
         arrays = [mk(G, "G"), mk(M, "M"), mk(X, "X"), mk(Q, "Q")]
+        if not wait:
+            _check(lib().cd_group_step(self._h, *arrays, mu, eta, r, _stream_handle(stream), None, None))
+            return None
         per = (ctypes.c_double * n)()
         res = Result()
         st = lib().cd_group_step(self._h, *arrays, mu, eta, r,
                                  _stream_handle(stream), per, ctypes.byref(res))
         _check(st, allow=(CD_OK, CD_ENONFINITE))
+        return res.rmmc, bool(res.sync_flag), list(per), st
+
+    def last_result(self):
+        """(rmmc_max, sync_flag, rmmc_per_layer, status) of the last step, once
+        its work has finished; status CD_OK, CD_ENONFINITE or CD_ERANKDEF."""
+        n = len(self.layers)
+        per = (ctypes.c_double * n)()
+        res = Result()
+        st = lib().cd_group_last_result(self._h, per, ctypes.byref(res))
+        _check(st, allow=(CD_OK, CD_ENONFINITE, CD_ERANKDEF))
         return res.rmmc, bool(res.sync_flag), list(per), st
 
     def set_timing(self, enable: bool, kinds=None) -> None:

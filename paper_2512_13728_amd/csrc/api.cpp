@@ -167,6 +167,12 @@ struct cd_layer {
   cd_group* self = nullptr;     // one-layer group used by cd_step
   int last_r = 0;
   bool prev_zero = true;        // prev_norm is known to be 0 (new layer, or set so)
+  // the group that stepped the layer last (its completion event and pinned
+  // rank-deficiency mirror answer cd_layer_rank_deficient), the layer's
+  // index there, and the mirror's last value once that group is destroyed
+  cd_group* last_group = nullptr;
+  int last_index = 0;
+  int rankdef_cached = 0;
 };
 
 struct ShapeClass {
@@ -202,10 +208,18 @@ struct cd_group {
   double** prev = nullptr;      // [L] device pointers to each layer's prev_norm
   double* norms = nullptr;      // [L] gate workspace
   unsigned* counter = nullptr;  // gate completion counter (returns to zero)
-  bool predict_skip = false;    // RMMC policy: branch predicted for the next step
+  cd::StepCtl* ctl = nullptr;   // the step's decision on the device (see cd::StepCtl)
+  // RMMC policy: the branch predicted for the next step, when the host knows
+  // the last decision (after a step that read it, or a last-result call);
+  // otherwise the buffer pass takes the device's prediction
+  bool predict_skip = false;
+  bool pred_known = true;
+  hipEvent_t done_ev = nullptr; // recorded after each step's last kernel
+  bool stepped = false;
   cd::GateOut* out_dev = nullptr;
-  // pinned, coherent, mapped: GateOut, L doubles, then the sequence number the
-  // gate stores last; out_host_dev is the device view of the same memory
+  // pinned, coherent, mapped: GateOut, L doubles, the sequence number the
+  // gate stores last, then L ints mirroring each layer's rank-deficiency
+  // flag; out_host_dev is the device view of the same memory
   void* out_host = nullptr;
   void* out_host_dev = nullptr;
   unsigned long long seq = 0;
@@ -232,6 +246,11 @@ struct cd_group {
 
 namespace {
 
+// Offsets inside a group's pinned host block.
+size_t host_seq_off(int L) { return sizeof(cd::GateOut) + sizeof(double) * L; }
+size_t host_rankdef_off(int L) { return host_seq_off(L) + sizeof(unsigned long long); }
+size_t host_bytes(int L) { return host_rankdef_off(L) + sizeof(int) * L; }
+
 void free_layer(cd_layer* L) {
   if (!L) return;
   if (L->ws) (void)hipFree(L->ws);
@@ -240,7 +259,19 @@ void free_layer(cd_layer* L) {
 
 void free_group(cd_group* g) {
   if (!g) return;
+  // layers whose last step this group took keep its rank-deficiency flags
+  for (int i = 0; i < static_cast<int>(g->layers.size()); ++i) {
+    cd_layer* L = g->layers[i];
+    if (L && L->last_group == g) {
+      if (g->done_ev) (void)hipEventSynchronize(g->done_ev);
+      L->rankdef_cached = g->out_host ? static_cast<const int*>(static_cast<const void*>(
+                                            static_cast<const char*>(g->out_host) + host_rankdef_off(g->L)))[i]
+                                      : 0;
+      L->last_group = nullptr;
+    }
+  }
   if (g->tables) (void)hipFree(g->tables);
+  if (g->done_ev) (void)hipEventDestroy(g->done_ev);
   if (g->out_host) (void)hipHostFree(g->out_host);
   if (g->ev) (void)hipEventDestroy(g->ev);
   for (int i = 0; i < cd_group::NSIDE; ++i) {
@@ -341,7 +372,7 @@ void carve_layer(cd_layer* L, char* base, const LayerLayout& lo) {
 
 // The device tables of a group of L layers, as byte offsets into one block.
 struct GroupLayout {
-  size_t parts, nparts, prev, norms, counter, out_dev, chol_tab, trsm_tab[3], trsm_tiles, trtri_tiles;
+  size_t parts, nparts, prev, norms, counter, ctl, out_dev, chol_tab, trsm_tab[3], trsm_tiles, trtri_tiles;
   size_t total;
 };
 
@@ -353,6 +384,7 @@ GroupLayout group_layout(int L, int nparts_stride, size_t ntiles, size_t nrtiles
   lo.prev = c.put(sizeof(double*) * L);
   lo.norms = c.put(sizeof(double) * L);
   lo.counter = c.put(sizeof(unsigned));
+  lo.ctl = c.put(sizeof(cd::StepCtl));
   lo.out_dev = c.put(sizeof(cd::GateOut) + sizeof(double) * L);
   lo.chol_tab = c.put(sizeof(cd::CholTab) * L);
   for (int k = 0; k < 3; ++k) lo.trsm_tab[k] = c.put(sizeof(cd::TrsmTab) * L);
@@ -368,6 +400,7 @@ void carve_group(cd_group* g, char* base, const GroupLayout& lo) {
   g->prev = reinterpret_cast<double**>(base + lo.prev);
   g->norms = reinterpret_cast<double*>(base + lo.norms);
   g->counter = reinterpret_cast<unsigned*>(base + lo.counter);
+  g->ctl = reinterpret_cast<cd::StepCtl*>(base + lo.ctl);
   g->out_dev = reinterpret_cast<cd::GateOut*>(base + lo.out_dev);
   g->chol_tab = reinterpret_cast<cd::CholTab*>(base + lo.chol_tab);
   for (int k = 0; k < 3; ++k) g->trsm_tab[k] = reinterpret_cast<cd::TrsmTab*>(base + lo.trsm_tab[k]);
@@ -394,9 +427,11 @@ void factor_tabs(const cd_layer* L, cd::TrsmTab& t0, cd::TrsmTab& t1, cd::TrsmTa
 // Host side of a group: shape classes, units (chunks of at most MAXB layers
 // of one shape) with their rows of the factor tables, and the streaming
 // launches; the table contents go to ct, t0..t2 and the tile lists.
+// rankdef_host: the device view of the group's L-int rank-deficiency mirror.
 void plan_group(cd_group* g, cd_layer* const* layers, int n, std::vector<int>& np, std::vector<double*>& pv,
                 std::vector<cd::CholTab>& ct, std::vector<cd::TrsmTab>& t0, std::vector<cd::TrsmTab>& t1,
-                std::vector<cd::TrsmTab>& t2, std::vector<int2>& tiles, std::vector<int2>& rtiles) {
+                std::vector<cd::TrsmTab>& t2, std::vector<int2>& tiles, std::vector<int2>& rtiles,
+                int* rankdef_host) {
   g->layers.assign(layers, layers + n);
   g->L = n;
   g->device = layers[0]->device;
@@ -443,7 +478,8 @@ void plan_group(cd_group* g, cd_layer* const* layers, int n, std::vector<int>& n
       for (int j = 0; j < static_cast<int>(u.sel.size()); ++j) {
         cd_layer* L = layers[u.sel[j]];
         const int k = off + j;
-        ct[k] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok};
+        ct[k] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok,
+                            rankdef_host ? rankdef_host + u.sel[j] : nullptr};
         factor_tabs(L, t0[k], t1[k], t2[k]);
         for (int rt = 0; rt < (L->d.m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) tiles.push_back(int2{j, rt});
         for (int rt = 0; rt < (L->d.r_max + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt)
@@ -468,20 +504,27 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   std::vector<cd::CholTab> ct;
   std::vector<cd::TrsmTab> t0, t1, t2;
   std::vector<int2> tiles, rtiles;
-  plan_group(g, layers, n, np, pv, ct, t0, t1, t2, tiles, rtiles);
+  g->device = layers[0]->device;
   DeviceGuard dg(g->device);
   if (!dg.ok) { free_group(g); return fail(CD_EHIP, "cannot select device %d", g->device); }
+  hipError_t e = hipHostMalloc(&g->out_host, host_bytes(n), hipHostMallocMapped | hipHostMallocCoherent);
+  if (e == hipSuccess) std::memset(g->out_host, 0, host_bytes(n));
+  if (e == hipSuccess) e = hipHostGetDevicePointer(&g->out_host_dev, g->out_host, 0);
+  if (e != hipSuccess) {
+    free_group(g);
+    return fail(e == hipErrorOutOfMemory ? CD_ENOMEM : CD_EHIP, "group setup: %s", hipGetErrorString(e));
+  }
+  plan_group(g, layers, n, np, pv, ct, t0, t1, t2, tiles, rtiles,
+             reinterpret_cast<int*>(static_cast<char*>(g->out_host_dev) + host_rankdef_off(n)));
   const GroupLayout lo = group_layout(n, g->nparts_stride, tiles.size(), rtiles.size());
-  hipError_t e = hipMalloc(&g->tables, lo.total);
+  e = hipMalloc(&g->tables, lo.total);
   if (e == hipSuccess) {
     carve_group(g, static_cast<char*>(g->tables), lo);
     e = hipMemset(g->counter, 0, sizeof(unsigned));
   }
-  const size_t host_bytes = sizeof(cd::GateOut) + sizeof(double) * n + sizeof(unsigned long long);
-  if (e == hipSuccess) e = hipHostMalloc(&g->out_host, host_bytes, hipHostMallocMapped | hipHostMallocCoherent);
-  if (e == hipSuccess) std::memset(g->out_host, 0, host_bytes);
-  if (e == hipSuccess) e = hipHostGetDevicePointer(&g->out_host_dev, g->out_host, 0);
+  if (e == hipSuccess) e = hipMemset(g->ctl, 0, sizeof(cd::StepCtl));
   if (e == hipSuccess) e = hipEventCreateWithFlags(&g->ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&g->done_ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipMemcpy(g->nparts, np.data(), sizeof(int) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->prev, pv.data(), sizeof(double*) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->chol_tab, ct.data(), sizeof(cd::CholTab) * n, hipMemcpyHostToDevice);
@@ -553,12 +596,15 @@ cd_status run(cd_group* g, int kind, double bytes, double flops, hipStream_t s, 
 // Cholesky factorisations, triangular solves and inverses run between the
 // stages over all layers at once (enqueue_factor); fp32 layers apply T^-1 by
 // fp64 triangular solves there.
-// spec: this step's buffer pass applied the skip branch's X update (the
-// branch was predicted to be local), which the update stage takes back.
+// spec: whether this step's buffer pass applied the skip branch's X update
+// (the branch was predicted to be local), which the update stage takes back:
+// 0, 1, or 2 = as the control word says.  run_if: NULL, or &ctl->flag when
+// the branch is enqueued before the decision is known (every kernel then
+// returns at once on a local step).
 cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>& sel,
-                       const void* const* G, bool spec,
+                       const void* const* G, int spec,
                        float* const* M, float* const* X, float* const* Q, float mu, float eta,
-                       int r, int stage, hipStream_t s) {
+                       int r, int stage, hipStream_t s, const int* run_if) {
   const int m = sc.m, n = sc.n, nl = static_cast<int>(sel.size());
   auto lay = [&](int j) { return g->layers[sel[j]]; };
 
@@ -571,6 +617,7 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
     cd::GemmArgs ga{};
     ga.M = Mr; ga.N = Nr; ga.K = K; ga.lda = lda; ga.ldb = ldb; ga.ldc = Nr;
     ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper; ga.out64 = bf_out64; ga.b_upper = b_upper;
+    ga.run_if = run_if;
     ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk, pieces, upper);
     ga.split_stride = 1LL * Mr * Nr;
     if (ga.splits > 1) {
@@ -595,7 +642,7 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
     if (st2 != CD_OK) return st2;
     if (ga.splits > 1) {
       cd::ReduceArgs ra{};
-      ra.count = 1LL * Mr * Nr; ra.stride = ga.split_stride; ra.splits = ga.splits;
+      ra.count = 1LL * Mr * Nr; ra.stride = ga.split_stride; ra.splits = ga.splits; ra.run_if = run_if;
       for (int j = 0; j < nl; ++j) { ra.part[j] = Pof(j); ra.out[j] = Cof(j); }
       const bool out64 = pieces == 0 ? (kind == cd::GemmKind::F64 || kind == cd::GemmKind::F64_FROM_F32)
                                      : bf_out64;
@@ -695,6 +742,7 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   cd::ColnormArgs cn{};
   cn.n = n; cn.r = r; cn.nchunks = (n + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
   cn.S = vec_update ? 0 : up; cn.rp = rp;
+  cn.run_if = run_if;
   for (int j = 0; j < nl; ++j) {
     cn.R[j] = lay(j)->R; cn.part[j] = lay(j)->colsq; cn.nrm[j] = lay(j)->colnrm; cn.Q[j] = Q[sel[j]];
     cn.Rpl[j] = lay(j)->planes + 3LL * m * rp;
@@ -708,7 +756,8 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
     return static_cast<float>(lay(j)->d.eta_local_scale * static_cast<double>(eta));
   };
   bool reads_g = false;
-  for (int j = 0; j < nl && spec; ++j) reads_g = reads_g || eta_local(j) != 0.0f;
+  for (int j = 0; j < nl && spec != 0; ++j) reads_g = reads_g || eta_local(j) != 0.0f;
+  cd::StepCtl* const uctl = run_if ? g->ctl : nullptr;
   const double ub = (16.0 + (reads_g ? (g->g_bf16 ? 2.0 : 4.0) : 0.0)) * mn * nl;
   if (vec_update) {
     cd::UpdateVecArgs va{};
@@ -716,10 +765,11 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
     va.one_minus_mu = static_cast<float>(1.0 - static_cast<double>(mu));
     va.c = static_cast<float>(static_cast<double>(eta) * std::sqrt(static_cast<double>(m) / n));
     va.g_bf16 = g->g_bf16 ? 1 : 0;
-    va.spec = spec ? 1 : 0;
+    va.spec = spec;
+    va.ctl = uctl;
     for (int j = 0; j < nl; ++j) {
       va.G[j] = G[sel[j]];
-      va.gc[j] = spec ? eta_local(j) : 0.0f;
+      va.gc[j] = spec != 0 ? eta_local(j) : 0.0f;
       va.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * lay(j)->d.weight_decay);
       va.M[j] = M[sel[j]]; va.X[j] = X[sel[j]];
       va.P[j] = lay(j)->P; va.R[j] = lay(j)->R; va.Q[j] = Q[sel[j]];
@@ -729,6 +779,7 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   {
     cd::PlaneArgs pa{};
     pa.r = r; pa.rp = rp; pa.S = up;
+    pa.run_if = run_if;
     pa.rows = m;
     for (int j = 0; j < nl; ++j) { pa.src[j] = lay(j)->P; pa.dst[j] = lay(j)->planes; }
     st = run(g, K_COLNORM, (4.0 + 2.0 * up) * mr * nl, 0.0, s, [&] { return cd::launch_split_planes(pa, nl, s); });
@@ -739,10 +790,11 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   ua.one_minus_mu = static_cast<float>(1.0 - static_cast<double>(mu));
   ua.c = static_cast<float>(static_cast<double>(eta) * std::sqrt(static_cast<double>(m) / n));
   ua.g_bf16 = g->g_bf16 ? 1 : 0;
-  ua.spec = spec ? 1 : 0;
+  ua.spec = spec;
+  ua.ctl = uctl;
   for (int j = 0; j < nl; ++j) {
     ua.G[j] = G[sel[j]];
-    ua.gc[j] = spec ? eta_local(j) : 0.0f;
+    ua.gc[j] = spec != 0 ? eta_local(j) : 0.0f;
     ua.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * lay(j)->d.weight_decay);
     ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]];
     ua.P[j] = lay(j)->planes;
@@ -756,12 +808,12 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
 // Between the stages of CholQR pass `pass`, over every layer: Cholesky of each
 // W, then either the fp64 triangular solve (fp32 layers: P1 = P~ T^-1, then
 // P = P1 T^-1) or the inverse U = T^-1 in fp32 for the bf16 x 6 apply.
-cd_status enqueue_factor(cd_group* g, const Unit& u, int r, int pass, hipStream_t s) {
+cd_status enqueue_factor(cd_group* g, const Unit& u, int r, int pass, hipStream_t s, const int* run_if) {
   const int nl = static_cast<int>(u.sel.size());
   const double L = nl, rr = 1.0 * r * r;
   const cd::CholTab* ct = g->chol_tab + u.off;
   cd_status st = run(g, K_CHOL, 16.0 * rr * L, (1.0 / 3.0) * rr * r * L, s,
-                     [&] { return cd::launch_cholesky(ct, nl, r, pass, s); });
+                     [&] { return cd::launch_cholesky(ct, nl, r, pass, s, run_if); });
   if (st != CD_OK) return st;
   if (!g->g_bf16) {
     // in place in the fp64 panel: P1 = P~ T^-1 (pass 0), P = P1 T1^-1 (pass 1)
@@ -773,7 +825,7 @@ cd_status enqueue_factor(cd_group* g, const Unit& u, int r, int pass, hipStream_
     }
     st = run(g, K_TRSM, bytes, flops, s, [&] {
       return cd::launch_trsm(g->trsm_tab[pass == 0 ? 0 : 2] + u.off, g->trsm_tiles + u.toff, u.nt, r, true,
-                             true, s);
+                             true, s, false, 0, run_if);
     });
     if (st != CD_OK || pass == 0) return st;
     // P rounded to fp32 (the update's operand planes and cd_layer_last_factors)
@@ -781,6 +833,7 @@ cd_status enqueue_factor(cd_group* g, const Unit& u, int r, int pass, hipStream_
     ra.count = 1LL * g->shapes[u.sc].m * r;
     ra.stride = ra.count;
     ra.splits = 1;
+    ra.run_if = run_if;
     for (int j = 0; j < nl; ++j) {
       ra.part[j] = g->layers[u.sel[j]]->pa;
       ra.out[j] = g->layers[u.sel[j]]->P;
@@ -789,7 +842,8 @@ cd_status enqueue_factor(cd_group* g, const Unit& u, int r, int pass, hipStream_
                [&] { return cd::launch_reduce_splits(ra, nl, true, false, s); });
   }
   return run(g, K_TRTRI, 12.0 * rr * L, rr * r / 3.0 * L, s, [&] {
-    return cd::launch_trsm(g->trsm_tab[1] + u.off, g->trtri_tiles + u.rtoff, u.nrt, r, true, false, s, true, r);
+    return cd::launch_trsm(g->trsm_tab[1] + u.off, g->trtri_tiles + u.rtoff, u.nrt, r, true, false, s, true, r,
+                           run_if);
   });
 }
 
@@ -810,14 +864,16 @@ cd_status check_step_args(const cd_group* g, const void* const* G, float* const*
   return CD_OK;
 }
 
-// 1. B = M + G, partial sums of B^2 (and, when spec, the skip branch's X
-// update in the same pass).
+// 1. B = M + G, partial sums of B^2 and, by spec_mode, the skip branch's X
+// update in the same pass (0: no, 1: yes, 2: as the control word predicts).
 cd_status enqueue_form(cd_group* g, const void* const* G, float* const* M, float* const* X, float eta,
-                       bool spec, hipStream_t s) {
+                       int spec_mode, hipStream_t s) {
+  const bool with_x = spec_mode == 1 || (spec_mode == 2 && g->predict_skip);   // for the byte count
   for (const std::vector<int>& batch : g->sbatches) {
     const int nl = static_cast<int>(batch.size());
     cd::FormArgs fa{};
     fa.nl = nl;
+    fa.ctl = g->ctl;
     long long total = 0, blocks = 0;
     for (int j = 0; j < nl; ++j) {
       const int li = batch[j];
@@ -832,36 +888,70 @@ cd_status enqueue_form(cd_group* g, const void* const* G, float* const* M, float
       fa.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * Ly->d.weight_decay);
     }
     fa.block0[nl] = static_cast<int>(blocks);
-    const double fb = static_cast<double>(total) * ((spec ? 16.0 : 8.0) + (g->g_bf16 ? 2.0 : 4.0));
-    cd_status st = run(g, spec ? K_FORM_X : K_FORM, fb, (spec ? 5.0 : 3.0) * total, s,
-                       [&] { return cd::launch_form_buffer(fa, g->g_bf16, spec, s); });
+    const double fb = static_cast<double>(total) * ((with_x ? 16.0 : 8.0) + (g->g_bf16 ? 2.0 : 4.0));
+    cd_status st = run(g, with_x ? K_FORM_X : K_FORM, fb, (with_x ? 5.0 : 3.0) * total, s,
+                       [&] { return cd::launch_form_buffer(fa, g->g_bf16, spec_mode, s); });
     if (st != CD_OK) return st;
   }
   return CD_OK;
 }
 
-// 2. the gate: norms, RMMC, prev_norm, max, flag into g->out_dev; with
-// to_host also into the pinned block, followed by the step's sequence number.
-cd_status enqueue_gate(cd_group* g, hipStream_t s, bool to_host) {
+// 2. the gate: norms, RMMC, prev_norm, max, the branch (g > tau, or
+// fixed_flag >= 0 for a fixed policy) into g->out_dev and the control word;
+// with to_host also into the pinned block, followed by the step's sequence
+// number.
+cd_status enqueue_gate(cd_group* g, hipStream_t s, bool to_host, int spec_mode, int fixed_flag) {
   cd::GateArgs ga{};
   ga.L = g->L; ga.nparts_stride = g->nparts_stride; ga.parts = g->parts; ga.nparts = g->nparts;
   ga.prev = g->prev; ga.eps = g->eps; ga.tau = g->tau; ga.out = g->out_dev;
   ga.norms = g->norms; ga.counter = g->counter;
+  ga.ctl = g->ctl; ga.spec_mode = spec_mode; ga.fixed_flag = fixed_flag;
   if (to_host) {
-    const size_t seq_off = sizeof(cd::GateOut) + sizeof(double) * g->L;
     ga.host_out = static_cast<cd::GateOut*>(g->out_host_dev);
-    ga.host_seq = reinterpret_cast<unsigned long long*>(static_cast<char*>(g->out_host_dev) + seq_off);
+    ga.host_seq = reinterpret_cast<unsigned long long*>(static_cast<char*>(g->out_host_dev) + host_seq_off(g->L));
     ga.seq = ++g->seq;
   }
   return run(g, K_GATE, 8.0 * g->L * g->nparts_stride, 0.0, s, [&] { return cd::launch_gate(ga, s); });
 }
 
-// 4. the branch: the sync branch per unit (each unit's pipeline on its own
-// stream, forked from and joined back to s), or the stand-alone local update
-// (nothing when spec already applied it in the buffer pass).
-cd_status enqueue_branch(cd_group* g, bool sync, bool spec, const void* const* G, float* const* M,
+// 4. the branch.  BR_SYNC: the sync branch per unit (each unit's pipeline
+// on its own stream, forked from and joined back to s).  BR_LOCAL: the
+// stand-alone local update, unless spec already applied it in the buffer
+// pass.  BR_BOTH (the decision is not known on the host): both, every kernel
+// predicated on the control word, spec taken from it.
+enum Branch { BR_LOCAL = 0, BR_SYNC = 1, BR_BOTH = 2 };
+
+cd_status enqueue_branch(cd_group* g, int branch, int spec, const void* const* G, float* const* M,
                          float* const* X, float* const* Q, float mu, float eta, int r, hipStream_t s) {
-  if (sync) {
+  if (branch == BR_LOCAL || branch == BR_BOTH) {
+    for (const std::vector<int>& batch : g->sbatches) {
+      if (branch == BR_LOCAL && spec != 0) break;
+      const int nl = static_cast<int>(batch.size());
+      cd::LocalArgs la{};
+      la.nl = nl;
+      la.ctl = branch == BR_BOTH ? g->ctl : nullptr;
+      long long total = 0, blocks = 0;
+      for (int j = 0; j < nl; ++j) {
+        const int li = batch[j];
+        const cd_layer* Ly = g->layers[li];
+        la.numel[j] = 1LL * Ly->d.m * Ly->d.n;
+        la.block0[j] = static_cast<int>(blocks);
+        blocks += blocks_for(la.numel[j]);
+        total += la.numel[j];
+        la.X[j] = X[li]; la.G[j] = G[li];
+        la.coef[j] = static_cast<float>(Ly->d.eta_local_scale * static_cast<double>(eta));
+        la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * Ly->d.weight_decay);
+      }
+      la.block0[nl] = static_cast<int>(blocks);
+      const double lb = static_cast<double>(total) * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
+      cd_status st = run(g, K_LOCAL, lb, 2.0 * total, s,
+                         [&] { return cd::launch_local_update(la, g->g_bf16, s); });
+      if (st != CD_OK) return st;
+    }
+  }
+  if (branch == BR_SYNC || branch == BR_BOTH) {
+    const int* run_if = branch == BR_BOTH ? &g->ctl->flag : nullptr;
+    const int uspec = branch == BR_BOTH ? 2 : spec;
     // Each unit's pipeline in stage order on its own stream: the first unit
     // on the caller's stream, the others on the group's side streams, forked
     // from the caller's stream here and joined back to it below.  Units are
@@ -885,10 +975,10 @@ cd_status enqueue_branch(cd_group* g, bool sync, bool spec, const void* const* G
       for (int ui = 0; ui < nu; ++ui) {
         const Unit& u = g->units[ui];
         const hipStream_t su = stream_of(ui);
-        cd_status st = enqueue_sync(g, g->shapes[u.sc], u.sel, G, spec, M, X, Q, mu, eta, r, stage, su);
+        cd_status st = enqueue_sync(g, g->shapes[u.sc], u.sel, G, uspec, M, X, Q, mu, eta, r, stage, su, run_if);
         if (st != CD_OK) return st;
         if (stage == 1 || stage == 3) {
-          st = enqueue_factor(g, u, r, stage == 1 ? 0 : 1, su);
+          st = enqueue_factor(g, u, r, stage == 1 ? 0 : 1, su, run_if);
           if (st != CD_OK) return st;
         }
         if (stage == 2) {
@@ -898,7 +988,7 @@ cd_status enqueue_branch(cd_group* g, bool sync, bool spec, const void* const* G
           const int mu_rows = g->shapes[u.sc].m;
           st = run(g, K_CHOL, 4.0 * nl, 0.0, su, [&] {
             return cd::launch_fill_dead(g->chol_tab + u.off, g->trsm_tab[0] + u.off, nl, mu_rows, r,
-                                        !g->g_bf16, su);
+                                        !g->g_bf16, su, run_if);
           });
           if (st != CD_OK) return st;
         }
@@ -909,29 +999,6 @@ cd_status enqueue_branch(cd_group* g, bool sync, bool spec, const void* const* G
       CD_HIP(hipStreamWaitEvent(s, g->join_ev[i], 0));
     }
     for (cd_layer* Ly : g->layers) Ly->last_r = r;
-  } else if (!spec) {
-    for (const std::vector<int>& batch : g->sbatches) {
-      const int nl = static_cast<int>(batch.size());
-      cd::LocalArgs la{};
-      la.nl = nl;
-      long long total = 0, blocks = 0;
-      for (int j = 0; j < nl; ++j) {
-        const int li = batch[j];
-        const cd_layer* Ly = g->layers[li];
-        la.numel[j] = 1LL * Ly->d.m * Ly->d.n;
-        la.block0[j] = static_cast<int>(blocks);
-        blocks += blocks_for(la.numel[j]);
-        total += la.numel[j];
-        la.X[j] = X[li]; la.G[j] = G[li];
-        la.coef[j] = static_cast<float>(Ly->d.eta_local_scale * static_cast<double>(eta));
-        la.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * Ly->d.weight_decay);
-      }
-      la.block0[nl] = static_cast<int>(blocks);
-      const double lb = static_cast<double>(total) * (8.0 + (g->g_bf16 ? 2.0 : 4.0));
-      cd_status st = run(g, K_LOCAL, lb, 2.0 * total, s,
-                         [&] { return cd::launch_local_update(la, g->g_bf16, s); });
-      if (st != CD_OK) return st;
-    }
   }
   return CD_OK;
 }
@@ -942,6 +1009,26 @@ bool fixed_sync(const cd_group* g, long long step) {
   return g->policy == CD_POLICY_ALWAYS_SYNC || (g->policy == CD_POLICY_EVERY_H && step % g->H == 0);
 }
 
+// Waits for the gate output of the group's last step in the pinned block
+// (the event after the gate bounds the wait: once it has completed, the
+// output is there or the step failed).
+cd_status wait_gate(cd_group* g) {
+  const volatile unsigned long long* hs = reinterpret_cast<const volatile unsigned long long*>(
+      static_cast<const char*>(g->out_host) + host_seq_off(g->L));
+  for (unsigned polls = 1; *hs != g->seq; ++polls) {
+    if (polls % 4096 != 0) continue;
+    const hipError_t q = hipEventQuery(g->ev);
+    if (q == hipErrorNotReady) continue;
+    if (q != hipSuccess) return fail(CD_EHIP, "gate: %s", hipGetErrorString(q));
+    if (*hs != g->seq) return fail(CD_EHIP, "gate output did not reach host memory");
+  }
+  std::atomic_thread_fence(std::memory_order_acquire);
+  return CD_OK;
+}
+
+// The step's results from the pinned block (after wait_gate).
+const cd::GateOut* gate_out(const cd_group* g) { return static_cast<const cd::GateOut*>(g->out_host); }
+
 cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, float* const* X,
                           float* const* Q, float mu, float eta, int r, void* stream,
                           double* rmmc_per_layer, cd_result* out) {
@@ -951,6 +1038,9 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   DeviceGuard dg(g->device);
   if (!dg.ok) return fail(CD_EHIP, "cannot select device %d", g->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // a step with no host output is asynchronous: everything is enqueued and
+  // nothing waits; cd_group_last_result reads the outcome later
+  const bool blocking = out != nullptr || rmmc_per_layer != nullptr;
 
   // Skip-branch speculation: when the coming decision is known or predicted
   // to be "skip", X -= eta_local G rides along in the buffer pass, which saves
@@ -958,58 +1048,90 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   // first adds eta_local G back (in fp32, one rounding).  The RMMC policy
   // predicts the previous step's branch, except that a layer whose prev_norm
   // is 0 (its first step) has RMMC = ||B|| / eps: that step syncs unless B = 0.
+  // When the host has not read the previous decision (after an asynchronous
+  // step) the buffer pass takes the same prediction from the control word.
   const long long next_step = g->layers[0]->step + 1;
   bool any_prev_zero = false;
   for (const cd_layer* Ly : g->layers) any_prev_zero = any_prev_zero || Ly->prev_zero;
   const bool fixed = fixed_policy(g);
-  const bool spec = fixed ? !fixed_sync(g, next_step) : (g->predict_skip && !any_prev_zero);
+  const bool fsync = fixed && fixed_sync(g, next_step);
+  int spec_mode;
+  if (fixed) spec_mode = fsync ? 0 : 1;
+  else if (any_prev_zero) spec_mode = 0;
+  else if (g->pred_known) spec_mode = g->predict_skip ? 1 : 0;
+  else spec_mode = 2;
 
-  st = enqueue_form(g, G, M, X, eta, spec, s);
+  st = enqueue_form(g, G, M, X, eta, spec_mode, s);
   if (st != CD_OK) return st;
-  st = enqueue_gate(g, s, true);
+  st = enqueue_gate(g, s, true, spec_mode, fixed ? (fsync ? 1 : 0) : -1);
   if (st != CD_OK) return st;
-  // 3. decision point: the gate writes its output into pinned host memory and
-  // stores the step's sequence number last; the host polls that number (the
-  // event after the gate bounds the wait: once it has completed, the output
-  // is there or the step failed)
   CD_HIP(hipEventRecord(g->ev, s));
-  for (cd_layer* L : g->layers) { L->step += 1; L->prev_zero = false; }
+  for (int i = 0; i < g->L; ++i) {
+    cd_layer* L = g->layers[i];
+    L->step += 1;
+    L->prev_zero = false;
+    L->last_group = g;
+    L->last_index = i;
+  }
+  g->stepped = true;
 
-  // ALWAYS, NEVER and EVERY_H fix the branch in advance: it is enqueued
-  // before the wait for the gate's output, so the GPU does not idle through
-  // the round trip.  The RMMC policy decides on the output.
-  bool sync = false;
+  // ALWAYS, NEVER and EVERY_H fix the branch in advance, and an asynchronous
+  // step enqueues both branches predicated on the control word: either way
+  // the branch is enqueued before any wait for the gate's output, so the GPU
+  // does not idle through the round trip.  A blocking RMMC step decides on
+  // the output (3. the decision point, standing in for the max all-reduce).
+  bool sync = fsync;
   if (fixed) {
-    sync = fixed_sync(g, next_step);
-    st = enqueue_branch(g, sync, spec, G, M, X, Q, mu, eta, r, s);
+    st = enqueue_branch(g, fsync ? BR_SYNC : BR_LOCAL, spec_mode, G, M, X, Q, mu, eta, r, s);
+    if (st != CD_OK) return st;
+  } else if (!blocking) {
+    st = enqueue_branch(g, BR_BOTH, 2, G, M, X, Q, mu, eta, r, s);
     if (st != CD_OK) return st;
   }
-  {
-    const size_t seq_off = sizeof(cd::GateOut) + sizeof(double) * g->L;
-    const volatile unsigned long long* hs = reinterpret_cast<const volatile unsigned long long*>(
-        static_cast<const char*>(g->out_host) + seq_off);
-    for (unsigned polls = 1; *hs != g->seq; ++polls) {
-      if (polls % 4096 != 0) continue;
-      const hipError_t q = hipEventQuery(g->ev);
-      if (q == hipErrorNotReady) continue;
-      if (q != hipSuccess) return fail(CD_EHIP, "gate: %s", hipGetErrorString(q));
-      if (*hs != g->seq) return fail(CD_EHIP, "gate output did not reach host memory");
+  if (blocking) {
+    st = wait_gate(g);
+    if (st != CD_OK) return st;
+    const cd::GateOut* go = gate_out(g);
+    if (!fixed) {
+      sync = go->flag != 0;
+      st = enqueue_branch(g, sync ? BR_SYNC : BR_LOCAL, go->spec, G, M, X, Q, mu, eta, r, s);
+      if (st != CD_OK) return st;
     }
-    std::atomic_thread_fence(std::memory_order_acquire);
+    if (rmmc_per_layer) std::memcpy(rmmc_per_layer, go + 1, sizeof(double) * g->L);
+    if (out) { out->rmmc = go->g; out->sync_flag = sync ? 1 : 0; }
   }
-  const cd::GateOut* go = static_cast<const cd::GateOut*>(g->out_host);
-  const double* rm = reinterpret_cast<const double*>(go + 1);
-  const double gmax = go->g;
-  const bool nonfinite = go->nonfinite != 0;
-  if (rmmc_per_layer) std::memcpy(rmmc_per_layer, rm, sizeof(double) * g->L);
-  if (!fixed) {
-    sync = go->flag != 0;
-    st = enqueue_branch(g, sync, spec, G, M, X, Q, mu, eta, r, s);
-    if (st != CD_OK) return st;
+  CD_HIP(hipEventRecord(g->done_ev, s));
+  if (fixed || blocking) {
+    g->pred_known = true;
+    g->predict_skip = !sync;
+  } else {
+    g->pred_known = false;
   }
-  g->predict_skip = !sync;
-  if (out) { out->rmmc = gmax; out->sync_flag = sync ? 1 : 0; }
-  if (nonfinite) return fail(CD_ENONFINITE, "a layer norm ||B|| was not finite");
+  if (blocking && gate_out(g)->nonfinite != 0) return fail(CD_ENONFINITE, "a layer norm ||B|| was not finite");
+  return CD_OK;
+}
+
+// The outcome of the group's last step: waits for that step's last kernel
+// (its completion event, not the device), then reads the pinned block.
+cd_status group_last_result(cd_group* g, double* rmmc_per_layer, cd_result* out) {
+  if (!g) return fail(CD_EINVAL, "group is NULL");
+  if (!g->stepped) return fail(CD_EINVAL, "the group has not been stepped");
+  DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CD_EHIP, "cannot select device %d", g->device);
+  CD_HIP(hipEventSynchronize(g->done_ev));
+  cd_status st = wait_gate(g);
+  if (st != CD_OK) return st;
+  const cd::GateOut* go = gate_out(g);
+  if (rmmc_per_layer) std::memcpy(rmmc_per_layer, go + 1, sizeof(double) * g->L);
+  if (out) { out->rmmc = go->g; out->sync_flag = go->flag; }
+  g->pred_known = true;
+  g->predict_skip = go->flag == 0;
+  if (go->nonfinite) return fail(CD_ENONFINITE, "a layer norm ||B|| was not finite");
+  if (go->flag) {
+    const int* rd = reinterpret_cast<const int*>(static_cast<const char*>(g->out_host) + host_rankdef_off(g->L));
+    for (int i = 0; i < g->L; ++i)
+      if (rd[i]) return fail(CD_ERANKDEF, "layer %d: P~ was numerically rank deficient", i);
+  }
   return CD_OK;
 }
 
@@ -1160,7 +1282,7 @@ cd_status static_step_impl(const cd_layer_desc* desc, double* prev_norm, long lo
   su.prev = prev_norm;
   su.counter = g->counter;
   su.ct = g->chol_tab;
-  su.ctv = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok};
+  su.ctv = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok, nullptr};
   su.tt[0] = g->trsm_tab[0];
   su.tt[1] = g->trsm_tab[1];
   su.tt[2] = g->trsm_tab[2];
@@ -1177,16 +1299,16 @@ cd_status static_step_impl(const cd_layer_desc* desc, double* prev_norm, long lo
   const long long next_step = *step + 1;
   const bool fixed = fixed_policy(g);
   const bool spec = fixed && !fixed_sync(g, next_step);
-  st = enqueue_form(g, Ga, Ma, Xa, eta, spec, s);
+  st = enqueue_form(g, Ga, Ma, Xa, eta, spec ? 1 : 0, s);
   if (st != CD_OK) return st;
-  st = enqueue_gate(g, s, false);
+  st = enqueue_gate(g, s, false, spec ? 1 : 0, fixed ? (fixed_sync(g, next_step) ? 1 : 0) : -1);
   if (st != CD_OK) return st;
   struct { cd::GateOut h; double rm; } hb;
   CD_HIP(hipMemcpyAsync(&hb, g->out_dev, sizeof(hb), hipMemcpyDeviceToHost, s));
   CD_HIP(hipStreamSynchronize(s));
   *step = next_step;
-  const bool sync = fixed ? fixed_sync(g, next_step) : hb.h.flag != 0;
-  st = enqueue_branch(g, sync, spec, Ga, Ma, Xa, Qa, mu, eta, r, s);
+  const bool sync = hb.h.flag != 0;
+  st = enqueue_branch(g, sync ? BR_SYNC : BR_LOCAL, spec ? 1 : 0, Ga, Ma, Xa, Qa, mu, eta, r, s);
   if (st != CD_OK) return st;
   if (out) { out->rmmc = hb.h.g; out->sync_flag = sync ? 1 : 0; }
   if (hb.h.nonfinite) return fail(CD_ENONFINITE, "the layer norm ||B|| was not finite");
@@ -1392,12 +1514,34 @@ cd_status cd_layer_last_factors(const cd_layer* layer, const float** P, const fl
 
 cd_status cd_layer_rank_deficient(const cd_layer* layer, int* flag) {
   if (!layer || !flag) return fail(CD_EINVAL, "NULL argument");
-  DeviceGuard dg(layer->device);
-  // the whole device, not the last step's stream: the caller may have
-  // destroyed that stream since
-  CD_HIP(hipDeviceSynchronize());
-  CD_HIP(hipMemcpy(flag, layer->rankdef, sizeof(int), hipMemcpyDeviceToHost));
+  const cd_group* g = layer->last_group;
+  if (!g) {
+    *flag = layer->rankdef_cached;
+    return CD_OK;
+  }
+  DeviceGuard dg(g->device);
+  // the last step of that group only (its completion event), not the device
+  CD_HIP(hipEventSynchronize(g->done_ev));
+  const int* rd = reinterpret_cast<const int*>(static_cast<const char*>(g->out_host) + host_rankdef_off(g->L));
+  *flag = rd[layer->last_index];
   return CD_OK;
+}
+
+cd_status cd_group_last_result(cd_group* group, double* rmmc_per_layer, cd_result* out) {
+  try {
+    return group_last_result(group, rmmc_per_layer, out);
+  } catch (...) {
+    return fail(CD_ENOMEM, "exception in cd_group_last_result");
+  }
+}
+
+cd_status cd_layer_last_result(cd_layer* layer, cd_result* out) {
+  if (!layer) return fail(CD_EINVAL, "layer is NULL");
+  try {
+    return group_last_result(layer->self, nullptr, out);
+  } catch (...) {
+    return fail(CD_ENOMEM, "exception in cd_layer_last_result");
+  }
 }
 
 const char* cd_last_error(void) { return g_err.c_str(); }

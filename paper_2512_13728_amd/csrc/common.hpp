@@ -15,6 +15,22 @@ namespace cd {
 
 constexpr int GBK = 32;           // GEMM k per LDS stage; split-K slices are multiples
 
+// ---- the step's device-resident control word ---------------------------------
+// Written by the gate kernel of every step, read by the kernels that follow
+// it on the device, so that a step can be enqueued whole without the host
+// reading the decision first (the asynchronous step): each kernel of either
+// branch then checks the decision and returns at once when its branch was not
+// taken.
+struct StepCtl {
+  int flag;        // the branch of the last gated step: 1 = sync
+  int spec_next;   // prediction for the next step: 1 = local (fuse the skip update)
+  int spec_cur;    // 1 when this step's buffer pass applied the skip update
+  int pad;
+};
+// Where a kernel may return at once: run_if NULL = always run; else run only
+// when *run_if != 0 (the sync branch's kernels take &ctl->flag).
+__device__ __forceinline__ bool skip_launch(const int* run_if) { return run_if != nullptr && *run_if == 0; }
+
 // ---- a1: B = M + G and per-block sum of B^2 -------------------------------
 // Every block covers FORM_CHUNK consecutive elements of one layer; one launch
 // covers up to MAXS layers of any shapes (the passes are elementwise), layer
@@ -29,8 +45,10 @@ struct FormArgs {
   float* X[MAXS];                  // with_x: the skip-branch update X = xdecay X - coef G, fused
   float coef[MAXS];                // eta_local per layer (with_x only)
   float xdecay[MAXS];              // 1 - eta * weight_decay per layer (with_x only)
+  const StepCtl* ctl;              // spec_mode 2: with_x = ctl->spec_next
 };
-hipError_t launch_form_buffer(const FormArgs& a, bool g_bf16, bool with_x, hipStream_t s);
+// spec_mode: 0 = buffer only, 1 = with the skip update, 2 = as ctl->spec_next says
+hipError_t launch_form_buffer(const FormArgs& a, bool g_bf16, int spec_mode, hipStream_t s);
 
 // ---- local branch: X = X - eta_local G --------------------------------------
 struct LocalArgs {                 // launch layout as FormArgs
@@ -41,14 +59,18 @@ struct LocalArgs {                 // launch layout as FormArgs
   const void* G[MAXS];
   float coef[MAXS];                // eta_local per layer
   float xdecay[MAXS];              // 1 - eta * weight_decay per layer
+  const StepCtl* ctl;              // NULL: run; else only when the step took the local
+                                   // branch and its buffer pass did not apply the update
 };
 hipError_t launch_local_update(const LocalArgs& a, bool g_bf16, hipStream_t s);
 
 // ---- gate: fixed-order reduction of the partials, RMMC, prev update, max ----
 struct GateOut {                   // result of the gate (device and host copies)
   double g;                        // max over layers of RMMC (NaN if any is NaN)
-  int flag;                        // g > tau
+  int flag;                        // the branch: g > tau, or the fixed policy's
   int nonfinite;                   // some ‖B‖ was NaN/Inf
+  int spec;                        // the step's buffer pass applied the skip update
+  int pad;
   // followed by L doubles: RMMC per layer
 };
 struct GateArgs {
@@ -68,6 +90,9 @@ struct GateArgs {
   GateOut* host_out;
   unsigned long long* host_seq;
   unsigned long long seq;
+  StepCtl* ctl;                    // the decision for the kernels that follow
+  int spec_mode;                   // as the step's buffer pass (0, 1, or 2 = ctl->spec_next)
+  int fixed_flag;                  // -1: flag = g > tau; else the fixed policy's branch
 };
 hipError_t launch_gate(const GateArgs& a, hipStream_t s);
 
@@ -99,6 +124,7 @@ struct GemmArgs {
   const void* A[MAXB];
   const void* B[MAXB];
   void* C[MAXB];                   // result (splits == 1) or partials (splits > 1)
+  const int* run_if;               // see skip_launch
 };
 hipError_t launch_gemm(const GemmArgs& a, int nl, GemmKind kind, hipStream_t s);
 int gemm_bm(int N, bool fp64);     // tile rows the launcher uses for this N
@@ -120,6 +146,7 @@ struct ReduceArgs {
   int splits;
   const void* part[MAXB];
   void* out[MAXB];
+  const int* run_if;
 };
 hipError_t launch_reduce_splits(const ReduceArgs& a, int nl, bool part64, bool out64, hipStream_t s);
 
@@ -134,9 +161,11 @@ struct CholTab {
   double* floor_;                  // pivot floor of the current factorisation
   int* rankdef;                    // set to 1 when a pivot was raised to the floor
   int* rowok;                      // r: 0 for the rows of floored pivots, else 1
+  int* rankdef_host;               // NULL, or a mirror of rankdef in pinned host memory
 };
 // All CHOL_BLOCK steps for `nlayers` layers of rank r; `pass` 0 clears rankdef.
-hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s);
+hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s,
+                           const int* run_if = nullptr);
 
 // P = P~ T^{-1} by block columns.  In place (Pin == Pout, same type) is
 // allowed: the workgroup of a row tile reads its block column of P~ before it
@@ -156,9 +185,9 @@ struct TrsmTab {
 // rankdef == 0 are left alone).  mmax: the largest m of the layers.
 // p64: P1 is fp64 (fp32-gradient layers), else fp32.
 hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, int mmax, int r, bool p64,
-                            hipStream_t s);
+                            hipStream_t s, const int* run_if = nullptr);
 hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r, bool in64, bool out64,
-                       hipStream_t s, bool ident = false, int mlimit = 0);
+                       hipStream_t s, bool ident = false, int mlimit = 0, const int* run_if = nullptr);
 
 // ---- ColumnNormalize --------------------------------------------------------
 constexpr int COLNORM_ROWS = 64;   // rows per partial
@@ -173,6 +202,7 @@ struct ColnormArgs {
   int S, rp;
   __bf16* Rpl[MAXB];
   __bf16* Qpl[MAXB];
+  const int* run_if;
 };
 hipError_t launch_colnorm(const ColnormArgs& a, int nl, hipStream_t s);
 
@@ -197,8 +227,9 @@ struct UpdateVecArgs {
   const void* G[MAXB];
   float gc[MAXB];
   int g_bf16;
-  int spec;
+  int spec;              // 0, 1, or 2 = ctl->spec_cur
   float xdecay[MAXB];
+  const StepCtl* ctl;    // NULL: run; else only on a sync step
 };
 bool update_vec_fits(int r);
 hipError_t launch_update_vec(UpdateVecArgs a, int nl, hipStream_t s);
@@ -208,6 +239,7 @@ struct PlaneArgs {
   int rows, r, rp, S;
   const float* src[MAXB];
   __bf16* dst[MAXB];               // S * rows * rp elements
+  const int* run_if;
 };
 hipError_t launch_split_planes(const PlaneArgs& a, int nl, hipStream_t s);
 
@@ -229,8 +261,9 @@ struct UpdatePlArgs {
   const void* G[MAXB];
   float gc[MAXB];
   int g_bf16;
-  int spec;
+  int spec;              // 0, 1, or 2 = ctl->spec_cur
   float xdecay[MAXB];
+  const StepCtl* ctl;    // NULL: run; else only on a sync step
 };
 hipError_t launch_update_planes(const UpdatePlArgs& a, int nl, int pieces, hipStream_t s);
 

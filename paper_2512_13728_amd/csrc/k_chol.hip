@@ -62,12 +62,13 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
-                                                  int pass) {
+                                                  int pass, const int* run_if) {
   __shared__ __attribute__((aligned(16))) double rowb[2 * CB];   // row p, then zeros
   __shared__ double Tsb[TPAD + CB * TLD];
   __shared__ double pinv[CB];                                     // 1 / T[p][p]
   __shared__ int okb[CB];                                         // pivot p not floored
   double* const Ts = Tsb + TPAD;   // Ts[j * TLD + i] = T[i][j]
+  if (skip_launch(run_if)) return;
   const CholTab t = tab[blockIdx.x];
   const int j = threadIdx.x;
   const long long ld = r;
@@ -81,7 +82,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     fl = fmax(1e-13 * md, 1e-60);
     if (j == 0) {
       *t.floor_ = fl;
-      if (pass == 0) *t.rankdef = 0;
+      if (pass == 0) {
+        *t.rankdef = 0;
+        if (t.rankdef_host) *t.rankdef_host = 0;
+      }
     }
   } else {
     fl = *t.floor_;
@@ -179,7 +183,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 #pragma unroll 4
   for (int i = 0; i < nb; ++i)
     if (j < nb && i <= j) t.W[(k0 + i) * ld + k0 + j] = Ts[j * TLD + i];
-  if (j == 0 && def) *t.rankdef = 1;
+  if (j == 0 && def) {
+    *t.rankdef = 1;
+    if (t.rankdef_host) *t.rankdef_host = 1;
+  }
 }
 
 // 64 x 64 fp64 MFMA tile: acc += A(64 x K) B(K x 64) with both operands staged
@@ -213,9 +220,11 @@ struct Tile64 {
   }
 };
 
-__global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ tab, int r, int kb) {
+__global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ tab, int r, int kb,
+                                                    const int* run_if) {
   __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
   __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
+  if (skip_launch(run_if)) return;
   const CholTab t = tab[blockIdx.y];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
@@ -246,9 +255,11 @@ __global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ 
       }
 }
 
-__global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ tab, int r, int kb) {
+__global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ tab, int r, int kb,
+                                                    const int* run_if) {
   __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
   __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
+  if (skip_launch(run_if)) return;
   const CholTab t = tab[blockIdx.y];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
@@ -302,7 +313,8 @@ __device__ __forceinline__ float fill_value(unsigned i, unsigned j, float scale)
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_fill_dead(const CholTab* __restrict__ ct,
-                                                   const TrsmTab* __restrict__ tt, int r) {
+                                                   const TrsmTab* __restrict__ tt, int r, const int* run_if) {
+  if (skip_launch(run_if)) return;
   const CholTab c = ct[blockIdx.y];
   if (*c.rankdef == 0) return;
   const TrsmTab t = tt[blockIdx.y];
@@ -322,11 +334,12 @@ __global__ __launch_bounds__(256) void k_fill_dead(const CholTab* __restrict__ c
 // mlimit > 0 caps the row count (the identity has r rows).
 template <typename TIn, typename TOut, bool IDENT>
 __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, const int2* __restrict__ tiles,
-                                              int r, int cb, int mlimit) {
+                                              int r, int cb, int mlimit, const int* run_if) {
   constexpr int YLD = CB + 4;
   __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
   __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
   __shared__ __attribute__((aligned(16))) double Ys[CB * YLD];
+  if (skip_launch(run_if)) return;
   const int2 lt = tiles[blockIdx.x];
   const TrsmTab t = tab[lt.x];
   const int m = mlimit > 0 ? min(t.m, mlimit) : t.m;
@@ -428,47 +441,47 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
 
 }  // namespace
 
-hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s) {
+hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s, const int* run_if) {
   if (nlayers <= 0) return hipSuccess;
   if (r < 1) return hipErrorInvalidValue;
   const int nblk = (r + CB - 1) / CB;
   for (int kb = 0; kb < nblk; ++kb) {
-    hipLaunchKernelGGL(k_chol_diag, dim3(nlayers), dim3(64), 0, s, tab, r, kb, pass);
+    hipLaunchKernelGGL(k_chol_diag, dim3(nlayers), dim3(64), 0, s, tab, r, kb, pass, run_if);
     const int k1 = min(r, (kb + 1) * CB);
     if (k1 >= r) break;
     const int nt = (r - k1 + CB - 1) / CB;
-    hipLaunchKernelGGL(k_chol_panel, dim3(nt, nlayers), dim3(256), 0, s, tab, r, kb);
-    hipLaunchKernelGGL(k_chol_trail, dim3(nt * (nt + 1) / 2, nlayers), dim3(256), 0, s, tab, r, kb);
+    hipLaunchKernelGGL(k_chol_panel, dim3(nt, nlayers), dim3(256), 0, s, tab, r, kb, run_if);
+    hipLaunchKernelGGL(k_chol_trail, dim3(nt * (nt + 1) / 2, nlayers), dim3(256), 0, s, tab, r, kb, run_if);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, int mmax, int r, bool p64,
-                            hipStream_t s) {
+                            hipStream_t s, const int* run_if) {
   if (nlayers <= 0 || mmax <= 0) return hipSuccess;
   const dim3 grid((mmax + FILL_ROWS - 1) / FILL_ROWS, nlayers);
-  if (p64) hipLaunchKernelGGL(k_fill_dead<double>, grid, dim3(256), 0, s, ct, tt, r);
-  else hipLaunchKernelGGL(k_fill_dead<float>, grid, dim3(256), 0, s, ct, tt, r);
+  if (p64) hipLaunchKernelGGL(k_fill_dead<double>, grid, dim3(256), 0, s, ct, tt, r, run_if);
+  else hipLaunchKernelGGL(k_fill_dead<float>, grid, dim3(256), 0, s, ct, tt, r, run_if);
   return hipGetLastError();
 }
 
 hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r, bool in64, bool out64,
-                       hipStream_t s, bool ident, int mlimit) {
+                       hipStream_t s, bool ident, int mlimit, const int* run_if) {
   if (ntiles <= 0) return hipSuccess;
   const int nblk = (r + CB - 1) / CB;
   const dim3 grid(ntiles), block(256);
   for (int cb = 0; cb < nblk; ++cb) {
     if (ident) {
-      if (out64) hipLaunchKernelGGL((k_trsm<double, double, true>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
-      else hipLaunchKernelGGL((k_trsm<double, float, true>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+      if (out64) hipLaunchKernelGGL((k_trsm<double, double, true>), grid, block, 0, s, tab, tiles, r, cb, mlimit, run_if);
+      else hipLaunchKernelGGL((k_trsm<double, float, true>), grid, block, 0, s, tab, tiles, r, cb, mlimit, run_if);
     } else if (in64 && out64) {
-      hipLaunchKernelGGL((k_trsm<double, double, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+      hipLaunchKernelGGL((k_trsm<double, double, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit, run_if);
     } else if (in64) {
-      hipLaunchKernelGGL((k_trsm<double, float, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+      hipLaunchKernelGGL((k_trsm<double, float, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit, run_if);
     } else if (out64) {
-      hipLaunchKernelGGL((k_trsm<float, double, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+      hipLaunchKernelGGL((k_trsm<float, double, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit, run_if);
     } else {
-      hipLaunchKernelGGL((k_trsm<float, float, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit);
+      hipLaunchKernelGGL((k_trsm<float, float, false>), grid, block, 0, s, tab, tiles, r, cb, mlimit, run_if);
     }
   }
   return hipGetLastError();

@@ -11,6 +11,7 @@ namespace {
 // column j; four interleaved accumulators (row i goes to i % 4) keep 16 loads
 // in flight and are combined in a fixed order.
 __global__ __launch_bounds__(256) void k_colsq(ColnormArgs a) {
+  if (skip_launch(a.run_if)) return;
   const int l = blockIdx.z, chunk = blockIdx.x;
   const int j = blockIdx.y * 256 + threadIdx.x;
   if (j >= a.r) return;
@@ -39,6 +40,7 @@ __global__ __launch_bounds__(256) void k_colsq(ColnormArgs a) {
 constexpr int CN_COLS = 16, CN_LANES = 16;
 __global__ __launch_bounds__(256) void k_colnorm_final(ColnormArgs a) {
   __shared__ double sh[CN_LANES][CN_COLS + 1];
+  if (skip_launch(a.run_if)) return;
   const int l = blockIdx.z;
   const int jj = threadIdx.x % CN_COLS, cl = threadIdx.x / CN_COLS;
   const int j = blockIdx.x * CN_COLS + jj;
@@ -72,6 +74,7 @@ __global__ __launch_bounds__(256) void k_colnorm_final(ColnormArgs a) {
 // bf16(value - pieces < s), as for every split operand): one pass over R.
 // Four consecutive columns per thread; columns r..rp-1 of the planes are zero.
 __global__ __launch_bounds__(256) void k_colscale_planes(ColnormArgs a) {
+  if (skip_launch(a.run_if)) return;
   const int l = blockIdx.z;
   const int qpr = a.rp / 4;   // quads per row
   const long long quads = static_cast<long long>(a.n) * qpr;

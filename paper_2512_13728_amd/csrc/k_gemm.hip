@@ -26,6 +26,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   static_assert(TM >= 1 && TN >= 1, "tile too small");
   __shared__ __attribute__((aligned(16))) T As[tile_elems<BM>()];
   __shared__ __attribute__((aligned(16))) T Bs[tile_elems<BN>()];
+  if (skip_launch(g.run_if)) return;
 
   const int layer = blockIdx.z;
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
@@ -100,6 +101,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 
 template <typename TP, typename TO>
 __global__ __launch_bounds__(256) void k_reduce(ReduceArgs a) {
+  if (skip_launch(a.run_if)) return;
   const int l = blockIdx.y;
   const TP* p = static_cast<const TP*>(a.part[l]);
   TO* o = static_cast<TO*>(a.out[l]);

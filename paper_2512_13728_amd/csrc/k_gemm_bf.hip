@@ -22,6 +22,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf(GemmArgs g) {
   static_assert(TM >= 1 && TN >= 1, "tile too small");
   __shared__ __attribute__((aligned(16))) __bf16 As[S * BM * BLD];
   __shared__ __attribute__((aligned(16))) __bf16 Bs[S * BN * BLD];
+  if (skip_launch(g.run_if)) return;
 
   const int layer = blockIdx.z;
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
@@ -118,6 +119,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf(GemmArgs g) {
 // bf16 planes of an fp32 matrix (rows x r): plane s holds the s-th split piece,
 // row stride rp (r rounded up to 32, padding zero-filled).
 __global__ __launch_bounds__(256) void k_split_planes(PlaneArgs a) {
+  if (skip_launch(a.run_if)) return;
   const int l = blockIdx.y;
   const long long quads = static_cast<long long>(a.rows) * (a.rp / 4);
   const long long plane = static_cast<long long>(a.rows) * a.rp;
@@ -183,6 +185,7 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
   constexpr int CHUNKS = S * ROWS * (BK16 / 8);   // 16-byte chunks per stage
   constexpr int CPT = (CHUNKS + 255) / 256;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  if (u.ctl != nullptr && u.ctl->flag == 0) return;   // not a sync step
   __bf16* Ls = reinterpret_cast<__bf16*>(smem);   // [S][ROWS][BLD]
   const int l = blockIdx.z;
   const int tiles_n = (u.n + BN - 1) / BN;
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
     const float coef = which == 0 ? -u.one_minus_mu : -u.c;
     // X only: first undo a speculative skip-branch update (X += gc G; that
     // update already applied the weight decay), else apply the decay
-    const bool spec = which == 1 && u.spec != 0;
+    const bool spec = which == 1 && (u.spec == 2 ? u.ctl->spec_cur : u.spec) != 0;
     const float gc = spec ? u.gc[l] : 0.f;
     const float xd = (which == 0 || spec) ? 1.f : u.xdecay[l];
     const void* const G = u.G[l];

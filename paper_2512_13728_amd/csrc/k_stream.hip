@@ -83,11 +83,14 @@ __device__ __forceinline__ int layer_of(const int* block0, int nl, int b) {
   return lo;
 }
 
-// B = M + G in place, the block's partial sum of B^2, and (WX) the skip
+// B = M + G in place, the block's partial sum of B^2, and (wx) the skip
 // branch's X = xdecay X - coef G in the same pass over G (xdecay = 1 - eta
-// weight_decay; 1 without weight decay, where the product is exact).
-template <bool BF16, bool WX>
+// weight_decay; 1 without weight decay, where the product is exact).  WXM:
+// 0 = no X update, 1 = with it, 2 = as the control word predicts (uniform
+// over the launch).
+template <bool BF16, int WXM>
 __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
+  const bool wx = WXM == 1 || (WXM == 2 && a.ctl->spec_next != 0);
   const int l = layer_of(a.block0, a.nl, blockIdx.x);
   const int lb = blockIdx.x - a.block0[l];   // block within the layer
   float* __restrict__ M = a.M[l];
@@ -105,7 +108,7 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
       const long long i = base + 4LL * (threadIdx.x + v * NTHREADS);
       m[v] = ld_nt(M + i);
       g[v] = load_g4<BF16>(G, i);
-      if constexpr (WX) x[v] = ld_nt(X + i);
+      if (wx) x[v] = ld_nt(X + i);
     }
 #pragma unroll
     for (int v = 0; v < VPT; ++v) {
@@ -115,7 +118,7 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
       b.z = m[v].z + g[v].z; b.w = m[v].w + g[v].w;
       st_nt(M + i, b);
       acc += sq(b.x); acc += sq(b.y); acc += sq(b.z); acc += sq(b.w);
-      if constexpr (WX) {
+      if (wx) {
         float4 y;
         y.x = fmaf(-c, g[v].x, d * x[v].x); y.y = fmaf(-c, g[v].y, d * x[v].y);
         y.z = fmaf(-c, g[v].z, d * x[v].z); y.w = fmaf(-c, g[v].w, d * x[v].w);
@@ -131,7 +134,7 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
         b.x = mv.x + gv.x; b.y = mv.y + gv.y; b.z = mv.z + gv.z; b.w = mv.w + gv.w;
         *reinterpret_cast<float4*>(M + i) = b;
         acc += sq(b.x); acc += sq(b.y); acc += sq(b.z); acc += sq(b.w);
-        if constexpr (WX) {
+        if (wx) {
           const float4 xv = *reinterpret_cast<const float4*>(X + i);
           float4 y;
           y.x = fmaf(-c, gv.x, d * xv.x); y.y = fmaf(-c, gv.y, d * xv.y);
@@ -144,7 +147,7 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
           const float b = M[j] + gj;
           M[j] = b;
           acc += sq(b);
-          if constexpr (WX) X[j] = fmaf(-c, gj, d * X[j]);
+          if (wx) X[j] = fmaf(-c, gj, d * X[j]);
         }
       }
     }
@@ -155,6 +158,7 @@ __global__ __launch_bounds__(NTHREADS) void k_form_buffer(FormArgs a) {
 
 template <bool BF16>
 __global__ __launch_bounds__(NTHREADS) void k_local_update(LocalArgs a) {
+  if (a.ctl != nullptr && (a.ctl->flag != 0 || a.ctl->spec_cur != 0)) return;
   const int l = layer_of(a.block0, a.nl, blockIdx.x);
   float* __restrict__ X = a.X[l];
   const void* __restrict__ G = a.G[l];
@@ -249,13 +253,22 @@ __global__ __launch_bounds__(GATE_THREADS) void k_gate(GateArgs a) {
 #pragma unroll
     for (int i = 0; i < GATE_THREADS / 64; ++i) { g = fmax(g, wmax[i]); flags |= wflags[i]; }
     if (flags & 1) g = NAN;
+    // the branch and the speculation this step used, for the kernels after
+    // the gate, and the prediction for the next step (its previous branch)
+    const int flag = a.fixed_flag >= 0 ? a.fixed_flag : ((g > a.tau) ? 1 : 0);
+    const int spec = a.spec_mode == 2 ? a.ctl->spec_next : a.spec_mode;
+    a.ctl->flag = flag;
+    a.ctl->spec_cur = spec;
+    a.ctl->spec_next = flag ? 0 : 1;
     a.out->g = g;
-    a.out->flag = (g > a.tau) ? 1 : 0;
+    a.out->flag = flag;
     a.out->nonfinite = (flags & 2) ? 1 : 0;
+    a.out->spec = spec;
     if (a.host_out) {
       a.host_out->g = g;
-      a.host_out->flag = (g > a.tau) ? 1 : 0;
+      a.host_out->flag = flag;
       a.host_out->nonfinite = (flags & 2) ? 1 : 0;
+      a.host_out->spec = spec;
     }
   }
   if (!a.host_out) return;
@@ -270,15 +283,18 @@ __global__ __launch_bounds__(GATE_THREADS) void k_gate(GateArgs a) {
 
 }  // namespace
 
-hipError_t launch_form_buffer(const FormArgs& a, bool g_bf16, bool with_x, hipStream_t s) {
+hipError_t launch_form_buffer(const FormArgs& a, bool g_bf16, int spec_mode, hipStream_t s) {
   if (a.nl <= 0 || a.nl > MAXS || a.block0[a.nl] <= 0) return a.nl == 0 ? hipSuccess : hipErrorInvalidValue;
+  if (spec_mode < 0 || spec_mode > 2 || (spec_mode == 2 && !a.ctl)) return hipErrorInvalidValue;
   const dim3 grid(a.block0[a.nl]), block(NTHREADS);
   if (g_bf16) {
-    if (with_x) hipLaunchKernelGGL((k_form_buffer<true, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_form_buffer<true, false>), grid, block, 0, s, a);
+    if (spec_mode == 1) hipLaunchKernelGGL((k_form_buffer<true, 1>), grid, block, 0, s, a);
+    else if (spec_mode == 2) hipLaunchKernelGGL((k_form_buffer<true, 2>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_form_buffer<true, 0>), grid, block, 0, s, a);
   } else {
-    if (with_x) hipLaunchKernelGGL((k_form_buffer<false, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_form_buffer<false, false>), grid, block, 0, s, a);
+    if (spec_mode == 1) hipLaunchKernelGGL((k_form_buffer<false, 1>), grid, block, 0, s, a);
+    else if (spec_mode == 2) hipLaunchKernelGGL((k_form_buffer<false, 2>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_form_buffer<false, 0>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }
@@ -292,7 +308,9 @@ hipError_t launch_local_update(const LocalArgs& a, bool g_bf16, hipStream_t s) {
 }
 
 hipError_t launch_gate(const GateArgs& a, hipStream_t s) {
-  if (a.L <= 0 || !a.counter || !a.norms || !a.out || (a.host_out && !a.host_seq)) return hipErrorInvalidValue;
+  if (a.L <= 0 || !a.counter || !a.norms || !a.out || !a.ctl || (a.host_out && !a.host_seq) ||
+      a.spec_mode < 0 || a.spec_mode > 2)
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_gate, dim3(a.L), dim3(GATE_THREADS), 0, s, a);
   return hipGetLastError();
 }

@@ -30,6 +30,7 @@ __device__ __forceinline__ float load_g(const void* G, bool bf, long long i) {
 template <int RMAX, int U>
 __global__ __launch_bounds__(256) void k_update_vec(UpdateVecArgs u) {
   static_assert(RMAX <= 64, "P's row is spread over the lanes of one wave");
+  if (u.ctl != nullptr && u.ctl->flag == 0) return;   // not a sync step
   const int l = blockIdx.z;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int lane = threadIdx.x & 63;
@@ -53,7 +54,7 @@ __global__ __launch_bounds__(256) void k_update_vec(UpdateVecArgs u) {
   float* const Xo = u.X[l];
   const void* const G = u.G[l];
   const bool gbf = u.g_bf16 != 0;
-  const bool spec = u.spec != 0;
+  const bool spec = (u.spec == 2 ? u.ctl->spec_cur : u.spec) != 0;
   const float gc = spec ? u.gc[l] : 0.0f, xd = spec ? 1.0f : u.xdecay[l];
   const float cm = -u.one_minus_mu, cx = -u.c;
   const int i_end = min(m, (blockIdx.y + 1) * u.band);

@@ -14,6 +14,12 @@
  *       writes DIR/M.bin, X.bin, Q.bin and DIR/steps.txt (one line per step:
  *       RMMC, branch, status).
  *
+ *   cd_c_step async DIR ...
+ *       the same steps, each asynchronous (no result argument: the call
+ *       enqueues the whole step and returns), every gradient in its own
+ *       device buffer; then cd_layer_last_result, whose outcome is the one
+ *       line of DIR/steps.txt.
+ *
  * Exit status 0 on success; any unexpected status prints the library's
  * message and exits 1.
  */
@@ -76,6 +82,7 @@ static int check(void) {
   if (cd_step(NULL, NULL, NULL, NULL, NULL, 0.9f, 0.01f, 4, NULL, NULL) != CD_EINVAL) bad = 1;
   if (cd_group_create(NULL, 1, NULL) != CD_EINVAL) bad = 1;
   if (cd_destroy(NULL) != CD_OK || cd_group_destroy(NULL) != CD_OK) bad = 1;
+  if (cd_layer_last_result(NULL, NULL) != CD_EINVAL || cd_group_last_result(NULL, NULL, NULL) != CD_EINVAL) bad = 1;
   if (!bad) printf("check ok (ABI %d)\n", cd_abi_version());
   return bad;
 }
@@ -109,9 +116,10 @@ static int write_file(const char* dir, const char* name, const void* buf, size_t
   return w != bytes;
 }
 
-static int run(int argc, char** argv) {
+static int run(int argc, char** argv, int async) {
   const char* dir;
   int m, n, r, steps, policy, t, rc = 1;
+  void** dGs = NULL;
   int bf16;
   double tau;
   float mu, eta;
@@ -125,7 +133,7 @@ static int run(int argc, char** argv) {
   hipError_t e;
 
   if (argc != 12) {
-    fprintf(stderr, "usage: %s run DIR M N R STEPS f32|bf16 POLICY TAU MU ETA\n", argv[0]);
+    fprintf(stderr, "usage: %s run|async DIR M N R STEPS f32|bf16 POLICY TAU MU ETA\n", argv[0]);
     return 2;
   }
   dir = argv[2];
@@ -162,11 +170,34 @@ static int run(int argc, char** argv) {
   snprintf(path, sizeof(path), "%s/steps.txt", dir);
   log = fopen(path, "w");
   if (!log) { fprintf(stderr, "cannot create %s\n", path); goto done; }
+  if (async) {
+    /* every gradient in a buffer of its own, copied before the first step:
+       an asynchronous step may still read its G when the next one is
+       enqueued */
+    dGs = (void**)calloc((size_t)steps, sizeof(void*));
+    if (!dGs) goto done;
+    for (t = 0; t < steps; ++t) {
+      char name[64];
+      void* hG;
+      snprintf(name, sizeof(name), "G%d.bin", t);
+      hG = read_file(dir, name, g_bytes);
+      if (!hG) goto done;
+      if ((e = hipMalloc(&dGs[t], g_bytes)) != hipSuccess) { free(hG); rc = fail_hip("hipMalloc G", e); goto done; }
+      e = hipMemcpy(dGs[t], hG, g_bytes, hipMemcpyHostToDevice);
+      free(hG);
+      if (e != hipSuccess) { rc = fail_hip("copy G", e); goto done; }
+    }
+  }
   for (t = 0; t < steps; ++t) {
     char name[64];
     void* hG;
     cd_result res;
     cd_status st;
+    if (async) {
+      st = cd_step(L, dGs[t], (float*)dM, (float*)dX, (float*)dQ, mu, eta, r, NULL, NULL);
+      if (st != CD_OK) { fprintf(stderr, "async step %d: %s\n", t, cd_last_error()); goto done; }
+      continue;
+    }
     snprintf(name, sizeof(name), "G%d.bin", t);
     hG = read_file(dir, name, g_bytes);
     if (!hG) goto done;
@@ -177,6 +208,16 @@ static int run(int argc, char** argv) {
     if (st != CD_OK && st != CD_ENONFINITE) { fprintf(stderr, "step %d: %s\n", t, cd_last_error()); goto done; }
     fprintf(log, "%.17g %d %d\n", res.rmmc, res.sync_flag, (int)st);
     printf("step %d: rmmc %.6g %s\n", t + 1, res.rmmc, res.sync_flag ? "sync" : "local");
+  }
+  if (async) {
+    cd_result res;
+    const cd_status st = cd_layer_last_result(L, &res);
+    if (st != CD_OK && st != CD_ENONFINITE && st != CD_ERANKDEF) {
+      fprintf(stderr, "last result: %s\n", cd_last_error());
+      goto done;
+    }
+    fprintf(log, "%.17g %d %d\n", res.rmmc, res.sync_flag, (int)st);
+    printf("%d asynchronous steps; last: rmmc %.6g %s\n", steps, res.rmmc, res.sync_flag ? "sync" : "local");
   }
   if ((e = hipDeviceSynchronize()) != hipSuccess) { rc = fail_hip("synchronize", e); goto done; }
   if ((e = hipMemcpy(hM, dM, mn_bytes, hipMemcpyDeviceToHost)) != hipSuccess) { rc = fail_hip("copy M back", e); goto done; }
@@ -193,13 +234,19 @@ done:
   if (dM) (void)hipFree(dM);
   if (dX) (void)hipFree(dX);
   if (dQ) (void)hipFree(dQ);
+  if (dGs) {
+    for (t = 0; t < steps; ++t)
+      if (dGs[t]) (void)hipFree(dGs[t]);
+    free(dGs);
+  }
   free(hM); free(hX); free(hQ);
   return rc;
 }
 
 int main(int argc, char** argv) {
   if (argc >= 2 && strcmp(argv[1], "check") == 0) return check();
-  if (argc >= 2 && strcmp(argv[1], "run") == 0) return run(argc, argv);
-  fprintf(stderr, "usage: %s check | run DIR M N R STEPS f32|bf16 POLICY TAU MU ETA\n", argv[0]);
+  if (argc >= 2 && strcmp(argv[1], "run") == 0) return run(argc, argv, 0);
+  if (argc >= 2 && strcmp(argv[1], "async") == 0) return run(argc, argv, 1);
+  fprintf(stderr, "usage: %s check | run|async DIR M N R STEPS f32|bf16 POLICY TAU MU ETA\n", argv[0]);
   return 2;
 }

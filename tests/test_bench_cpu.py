@@ -58,7 +58,7 @@ def _write_pmc(dirpath, counter, rows):
 def test_pmc_summary_scales_by_the_calibration_copy(tmp_path, monkeypatch):
     cal_mib = 4
     cal = cal_mib << 20
-    form = "void cd::(anonymous namespace)::k_form_buffer<true, true>(cd::FormArgs)"
+    form = "void cd::(anonymous namespace)::k_form_buffer<true, 1>(cd::FormArgs)"
     copy = "void neg_kernel(float*, float const*, long)"
     # FETCH_SIZE reads half of the copy's bytes (factor 2), WRITE_SIZE all of them
     fetch_rows = [(copy, cal / 2 / 1024), (form, 3000.0), (form, 3100.0)]
@@ -104,7 +104,7 @@ def test_trace_summary(tmp_path):
     with open(d / "bench_kernel_stats.csv", "w", newline="") as fh:
         w = csv.writer(fh)
         w.writerow(["Name", "Calls", "TotalDurationNs", "AverageNs"])
-        w.writerow(["void cd::(anonymous namespace)::k_form_buffer<true, true>(cd::FormArgs)", 4, 3.6e6, 9.0e5])
+        w.writerow(["void cd::(anonymous namespace)::k_form_buffer<true, 1>(cd::FormArgs)", 4, 3.6e6, 9.0e5])
         w.writerow(["void cd::(anonymous namespace)::k_gate(cd::GateArgs)", 2, 2.0e4, 1.0e4])
         w.writerow(["void at::native::elementwise_kernel<...>", 10, 5.0e6, 5.0e5])
     line = {"value": 2.4e11, "ms_per_step": 5.0,
@@ -118,8 +118,49 @@ def test_trace_summary(tmp_path):
     bench.summarize_trace(str(d), str(bj), str(out))
     text = out.read_text()
     rows = [ln for ln in text.splitlines() if ln.startswith("cd::")]
-    assert rows[0].startswith("cd::k_form_buffer<true, true>")          # largest total first
+    assert rows[0].startswith("cd::k_form_buffer<true, 1>")          # largest total first
     assert "900.0" in rows[0] and "3.600" in rows[0]
     assert len(rows) == 2                                                 # torch kernels left out
     assert "5.0 ms in total" in text
     assert "form_buffer_local: avg launch 900.0 us" in text
+
+
+def test_counted_bytes_per_step_by_branch(tmp_path, monkeypatch):
+    """The counter summary cuts the dispatch sequence into steps at each
+    step's first buffer-pass launch and adds every library kernel of a step
+    (torch kernels left out); a step with a sync-branch kernel is a sync
+    step.  The bench line reads the per-branch medians back while no kernel
+    source has changed."""
+    cal_mib = 4
+    cal = cal_mib << 20
+    copy = "void neg_kernel(float*, float const*, long)"
+    form0 = "void cd::(anonymous namespace)::k_form_buffer<true, 0>(cd::FormArgs)"
+    form1 = "void cd::(anonymous namespace)::k_form_buffer<true, 1>(cd::FormArgs)"
+    gate = "void cd::(anonymous namespace)::k_gate(cd::GateArgs)"
+    gemm = "void cd::(anonymous namespace)::k_gemm_bf<2, 128, 256, true, false, false>(cd::GemmArgs)"
+    upd = "void cd::(anonymous namespace)::k_update_pl<1, 64>(cd::UpdatePlArgs)"
+    torch_k = "void at::native::elementwise_kernel<128, 4>(int)"
+    # step 1 sync: form0 x2, gate, gemm, update; step 2 local: form0, gate, torch noise;
+    # step 3 local (fused): form1 x2, gate
+    seq = [(copy, cal / 2 / 1024), (form0, 100.0), (form0, 100.0), (gate, 1.0), (gemm, 50.0), (upd, 300.0),
+           (form0, 100.0), (gate, 1.0), (torch_k, 999.0), (form1, 200.0), (form1, 200.0), (gate, 1.0)]
+    wseq = [(copy, cal / 1024)] + [(n, v / 2) for n, v in seq[1:]]
+    fdir, wdir = str(tmp_path / "f"), str(tmp_path / "w")
+    _write_pmc(fdir, "FETCH_SIZE", seq)
+    _write_pmc(wdir, "WRITE_SIZE", wseq)
+    out = str(tmp_path / "gpt1p3b_hbm_traffic_pmc.txt")
+    bench.summarize_pmc(fdir, wdir, out, "gpt1p3b", cal_mib)
+    info = json.loads([ln for ln in open(out).read().splitlines() if ln.startswith("json ")][0][5:])
+    st = info["steps"]
+    k = 1024.0
+    assert st["sync"]["steps"] == 1 and st["local"]["steps"] == 2
+    assert st["sync"]["fetch_bytes"] == pytest.approx(2.0 * 551.0 * k)
+    assert st["sync"]["write_bytes"] == pytest.approx(551.0 / 2 * k)
+    # local steps: 101 and 401 KiB fetched (x2); the median of two is the larger
+    assert st["local"]["fetch_bytes"] == pytest.approx(2.0 * 401.0 * k)
+    monkeypatch.setattr(bench, "PMC_PROFILE", str(tmp_path / "{workload}_hbm_traffic_pmc.txt"))
+    got = bench.counted_step_bytes("gpt1p3b")
+    assert got["sync"] == pytest.approx(2.0 * 551.0 * k + 551.0 / 2 * k)
+    assert bench.counted_step_bytes("gpt160m") == {}
+    monkeypatch.setattr(bench, "source_digest", lambda files: "0000000000000000")
+    assert bench.counted_step_bytes("gpt1p3b") == {}
