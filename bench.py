@@ -124,6 +124,9 @@ def parse():
                         "the reference for the hardware byte counters")
     p.add_argument("--summarize-trace", nargs=3, metavar=("DIR", "BENCH_JSON", "OUT"),
                    help="write the kernel statistics of a rocprofv3 --kernel-trace --stats run")
+    p.add_argument("--summarize-mfma", nargs=2, metavar=("DIR", "OUT"),
+                   help="write the per-kernel MFMA busy fraction of a rocprofv3 --pmc "
+                        "SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES GRBM_GUI_ACTIVE run")
     p.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"),
                    help="write the per-kernel HBM traffic of two rocprofv3 --pmc runs (give the "
                         "same --copy-calibration size)")
@@ -144,9 +147,11 @@ def summarize_trace(d: str, bench_json: str, out: str):
     ours = [r for r in rows if "cd::" in r["Name"]]
     other_ns = sum(float(r["TotalDurationNs"]) for r in rows if "cd::" not in r["Name"])
     b = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    wl = b["config"].get("workload_name", "gpt1p3b")
     lines = [f"# rocprofv3 kernel statistics: {b['config']['workload']}",
              "# commands (from the repository root):",
-             f"#   rocprofv3 --kernel-trace --stats -f csv -d {d} -o bench -- python3 bench.py > {bench_json}",
+             f"#   rocprofv3 --kernel-trace --stats -f csv -d {d} -o bench -- python3 bench.py "
+             f"{WORKLOAD_ARGS.get(wl, '')}> {bench_json}",
              f"#   python3 bench.py --summarize-trace {d} {bench_json} {out}",
              "# calls include the warmup steps and the untimed profiling pass (the same",
              "# trajectory once more); torch kernels (input generation, state reset)",
@@ -269,10 +274,10 @@ def summarize_pmc(fdir: str, wdir: str, out: str, workload: str, cal_mib: int):
                            "dispatches": len(f_all), "source_digest": source_digest(files)}
     lines = [f"# rocprofv3 hardware counters: HBM bytes per dispatch, workload {workload}",
              "# commands (from the repository root):",
-             f"#   rocprofv3 --pmc FETCH_SIZE -f csv -d {fdir} -o pmc -- python3 bench.py "
-             f"--no-cpu-baseline --copy-calibration {cal_mib}",
-             f"#   rocprofv3 --pmc WRITE_SIZE -f csv -d {wdir} -o pmc -- python3 bench.py "
-             f"--no-cpu-baseline --copy-calibration {cal_mib}",
+             f"#   rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'cd::|neg_kernel' -f csv -d {fdir} -o pmc "
+             f"-- python3 bench.py {WORKLOAD_ARGS.get(workload, '')}--no-cpu-baseline --copy-calibration {cal_mib}",
+             f"#   rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'cd::|neg_kernel' -f csv -d {wdir} -o pmc "
+             f"-- python3 bench.py {WORKLOAD_ARGS.get(workload, '')}--no-cpu-baseline --copy-calibration {cal_mib}",
              f"#   python3 bench.py --summarize-pmc {fdir} {wdir} {out} --copy-calibration {cal_mib}",
              f"# calibration: a streaming copy (b = -a, fp32) of {cal_bytes} B read + {cal_bytes} B written;",
              f"#   FETCH_SIZE x {factor['FETCH_SIZE']:.4f} and WRITE_SIZE x {factor['WRITE_SIZE']:.4f} give bytes",
@@ -322,6 +327,48 @@ def counted_step_bytes(workload: str):
             if st.get("source_digest") == source_digest(ALL_SOURCES):
                 return {k: v["bytes"] for k, v in st.items() if k in ("sync", "local")}
     return {}
+
+
+N_CU, N_XCD, SIMD_PER_CU = 256, 8, 4
+# the bench arguments that select each profiled workload (default: the 1.3B set)
+WORKLOAD_ARGS = {"gpt1p3b": "", "gpt160m": "--workload gpt160m --steps 50 ",
+                 "mixed1p3b": "--workload mixed1p3b --steps 200 ", "single256": "--workload single256 "}
+
+
+def summarize_mfma(d: str, out: str, workload: str):
+    """Per kernel of the library: the MFMA busy fraction counted by the
+    hardware, SQ_VALU_MFMA_BUSY_CYCLES / (SIMDs x cycles the kernel ran),
+    with the kernel's cycles from GRBM_GUI_ACTIVE (which counts on every XCD:
+    divided by their number).  Dispatches of one kernel name are summed."""
+    counters = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE")
+    vals = {c: _pmc_dispatches(d, c) for c in counters}
+    table = {}
+    for i, (did, name, mfma) in enumerate(vals["SQ_VALU_MFMA_BUSY_CYCLES"]):
+        if "cd::" not in name:
+            continue
+        t = table.setdefault(_kernel_name(name), {"n": 0, "mfma": 0.0, "busy": 0.0, "gui": 0.0})
+        t["n"] += 1
+        t["mfma"] += mfma
+        t["busy"] += vals["SQ_BUSY_CYCLES"][i][2]
+        t["gui"] += vals["GRBM_GUI_ACTIVE"][i][2]
+    lines = [f"# rocprofv3 hardware counters: MFMA busy per kernel, workload {workload}",
+             "# commands (from the repository root):",
+             f"#   rocprofv3 --pmc {' '.join(counters)} --kernel-include-regex 'cd::' -f csv -d {d} -o pmc "
+             f"-- python3 bench.py {WORKLOAD_ARGS.get(workload, '')}--no-cpu-baseline --steps 2 --warmup 1 "
+             "--policy always",
+             f"#   python3 bench.py --summarize-mfma {d} {out}",
+             f"# mfma_busy = SQ_VALU_MFMA_BUSY_CYCLES / ({N_CU * SIMD_PER_CU} SIMDs x GRBM_GUI_ACTIVE / {N_XCD} XCDs):",
+             "# the fraction of the kernel's cycles in which an average SIMD's matrix unit was busy", "",
+             f"{'kernel':64s} {'disp':>5s} {'cycles/disp':>12s} {'mfma_busy':>10s}"]
+    summary = {}
+    for name, t in sorted(table.items(), key=lambda kv: -kv[1]["gui"]):
+        cyc = t["gui"] / N_XCD
+        frac = t["mfma"] / (N_CU * SIMD_PER_CU * cyc) if cyc > 0 else 0.0
+        summary[name] = {"dispatches": t["n"], "cycles": cyc, "mfma_busy": frac}
+        lines.append(f"{name[:64]:64s} {t['n']:5d} {cyc / t['n']:12.4g} {frac:10.4f}")
+    lines += ["", "json " + json.dumps({"workload": workload, "kernels": summary})]
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def counted_traffic(workload: str, kind: str):
@@ -397,6 +444,9 @@ def main():
     args = parse()
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma, workload=args.workload)
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, workload=args.workload, cal_mib=args.copy_calibration)
@@ -650,6 +700,7 @@ def main():
         "config": {
             "workload": (f"{w.name}: {L} matrices of the 1.3B-shaped GPT set (d_model 2048, 24 blocks)"
                          if w.name == "gpt1p3b" else w.name),
+            "workload_name": w.name,
             "params": w.params, "rank": w.r, "grad_dtype": w.grad_dtype, "state_dtype": "f32",
             "power_iteration_dtype": ("P~ = BQ and R = B^T P on bf16 MFMA with 2-piece fp32 splits "
                                       "(3 products, ~2^-16 relative); CholQR2 pass 0 Gram + Cholesky in fp64, pass 1 "
