@@ -66,6 +66,8 @@ KIND_BOUND = {
     "update_bf16": ("hbm", None, 1), "gram_bf16x6": ("mfma", "bf16", 6),
     "apply_bf16x6": ("mfma", "bf16", 6), "trtri_f64": ("mfma", "f64", 1),
     "update_f32": ("hbm", None, 1),
+    # small layers: one workgroup per layer, latency-bound; priced against the fp64 peak
+    "small_cholqr": ("alu", "f64", 1), "small_update": ("hbm", None, 1),
 }
 POLICIES = {"rmmc": 0, "always": 1, "never": 2, "every_h": 3}
 

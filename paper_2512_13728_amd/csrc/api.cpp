@@ -95,11 +95,12 @@ int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk, int pieces 
 // ---- optional per-kernel timing (HIP events on the launch stream) ----------
 enum Kind { K_FORM, K_FORM_X, K_GATE, K_LOCAL, K_PBQ, K_PBQ_BF, K_GRAM, K_GRAM_BF, K_CHOL, K_TRSM, K_TRTRI,
             K_APPLY_BF, K_PBTP, K_PBTP3, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_UPDATE_F32,
-            K_NKINDS };
+            K_SMALL_QR, K_SMALL_UPD, K_NKINDS };
 const char* const kKindName[K_NKINDS] = {
     "form_buffer", "form_buffer_local", "gate", "local_update", "power_bq_f64", "power_bq_bf16x3", "gram_f64",
     "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_f64",
-    "power_btp_bf16x3", "reduce_splits", "colnorm", "update_bf16x6", "update_bf16", "update_f32"};
+    "power_btp_bf16x3", "reduce_splits", "colnorm", "update_bf16x6", "update_bf16", "update_f32",
+    "small_cholqr", "small_update"};
 static_assert(K_NKINDS <= 32, "the timing mask holds one bit per kind");
 
 // Timing events only measure: recording them without the system-scope fence
@@ -607,6 +608,8 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
                        int r, int stage, hipStream_t s, const int* run_if) {
   const int m = sc.m, n = sc.n, nl = static_cast<int>(sel.size());
   auto lay = [&](int j) { return g->layers[sel[j]]; };
+  // small layers: four launches (see below), their products without split-K
+  const bool small = cd::small_sync_fits(m, n, r);
 
   // skinny GEMM C = A.B with optional split-K and fixed-order reduction
   // pieces > 0: fp32 operands on the bf16 MFMA with `pieces`-way splits
@@ -618,7 +621,12 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
     ga.M = Mr; ga.N = Nr; ga.K = K; ga.lda = lda; ga.ldb = ldb; ga.ldc = Nr;
     ga.a_kc = a_kc; ga.b_kc = b_kc; ga.upper_only = upper; ga.out64 = bf_out64; ga.b_upper = b_upper;
     ga.run_if = run_if;
-    ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk, pieces, upper);
+    if (small) {
+      ga.splits = 1;
+      ga.kchunk = (K + cd::GBK - 1) / cd::GBK * cd::GBK;
+    } else {
+      ga.splits = plan_splits(Mr, Nr, K, nl, acc64, &ga.kchunk, pieces, upper);
+    }
     ga.split_stride = 1LL * Mr * Nr;
     if (ga.splits > 1) {
       // the partials must fit the workspace sized at create time
@@ -654,6 +662,58 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   };
   auto part = [&](int j) { return lay(j)->split_part; };
   const double mn = 1.0 * m * n, mr = 1.0 * m * r, nr = 1.0 * n * r, rr = 1.0 * r * r;
+  // eta_local of each layer: what a speculative skip update subtracted
+  auto eta_local = [&](int j) {
+    return static_cast<float>(lay(j)->d.eta_local_scale * static_cast<double>(eta));
+  };
+  if (small) {
+    // P~ = B Q (fp64) -> CholQR2 in one workgroup per layer -> R = B^T P
+    // (fp64 products) -> column norms, Q and the M / X update in one launch
+    if (stage == 0)
+      return gemm(K_PBQ, 2.0 * mn * r, 4.0 * mn + 4.0 * nr + 8.0 * mr, cd::GemmKind::F64_FROM_F32, m, r,
+                  n, true, n, false, r, false,
+                  [&](int j) { return static_cast<const void*>(M[sel[j]]); },
+                  [&](int j) { return static_cast<const void*>(Q[sel[j]]); },
+                  [&](int j) { return static_cast<void*>(lay(j)->pa); }, part);
+    if (stage == 1) {
+      cd::SmallQrArgs qa{};
+      qa.m = m; qa.r = r; qa.run_if = run_if;
+      int* mirror = g->out_host_dev ? reinterpret_cast<int*>(static_cast<char*>(g->out_host_dev) +
+                                                             host_rankdef_off(g->L))
+                                    : nullptr;
+      for (int j = 0; j < nl; ++j) {
+        qa.Pt[j] = lay(j)->pa; qa.P64[j] = lay(j)->pa; qa.P32[j] = lay(j)->P;
+        qa.rankdef[j] = lay(j)->rankdef;
+        qa.rankdef_host[j] = mirror ? mirror + sel[j] : nullptr;
+      }
+      return run(g, K_SMALL_QR, (16.0 * mr + 4.0 * mr) * nl, 4.0 * (2.0 * mr * r + rr * r / 3.0) * nl, s,
+                 [&] { return cd::launch_small_cholqr(qa, nl, s); });
+    }
+    if (stage != 5) return CD_OK;
+    cd_status st = gemm(K_PBTP, 2.0 * mn * r, 4.0 * mn + 8.0 * mr + 4.0 * nr, cd::GemmKind::F32_F64_TO_F32, n,
+                        r, m, false, n, false, r, false,
+                        [&](int j) { return static_cast<const void*>(M[sel[j]]); },
+                        [&](int j) { return static_cast<const void*>(lay(j)->pa); },
+                        [&](int j) { return static_cast<void*>(lay(j)->R); }, part);
+    if (st != CD_OK) return st;
+    cd::SmallUpdArgs ua{};
+    ua.m = m; ua.n = n; ua.r = r;
+    ua.one_minus_mu = static_cast<float>(1.0 - static_cast<double>(mu));
+    ua.c = static_cast<float>(static_cast<double>(eta) * std::sqrt(static_cast<double>(m) / n));
+    ua.g_bf16 = g->g_bf16 ? 1 : 0;
+    ua.spec = spec;
+    ua.ctl = run_if ? g->ctl : nullptr;
+    bool reads_g = false;
+    for (int j = 0; j < nl; ++j) {
+      ua.M[j] = M[sel[j]]; ua.X[j] = X[sel[j]]; ua.P[j] = lay(j)->P; ua.R[j] = lay(j)->R; ua.Q[j] = Q[sel[j]];
+      ua.G[j] = G[sel[j]];
+      ua.gc[j] = spec != 0 ? eta_local(j) : 0.0f;
+      ua.xdecay[j] = static_cast<float>(1.0 - static_cast<double>(eta) * lay(j)->d.weight_decay);
+      reads_g = reads_g || (spec != 0 && eta_local(j) != 0.0f);
+    }
+    const double ub = (16.0 + (reads_g ? (g->g_bf16 ? 2.0 : 4.0) : 0.0)) * mn * nl + 8.0 * nr * nl;
+    return run(g, K_SMALL_UPD, ub, 4.0 * mn * r * nl, s, [&] { return cd::launch_small_update(ua, nl, s); });
+  }
   // bf16-gradient layers: the power-iteration products P~ = B Q and R = B^T P
   // use two-piece splits (three bf16 products, relative error about 2^-16,
   // an order below what the plain-bf16 rank-r update of M contributes);
@@ -751,10 +811,6 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
   st = run(g, K_COLNORM, (12.0 + 4.0 * cn.S) * nr * nl, 3.0 * nr * nl, s,
            [&] { return cd::launch_colnorm(cn, nl, s); });
   if (st != CD_OK) return st;
-  // eta_local of each layer: what a speculative skip update subtracted
-  auto eta_local = [&](int j) {
-    return static_cast<float>(lay(j)->d.eta_local_scale * static_cast<double>(eta));
-  };
   bool reads_g = false;
   for (int j = 0; j < nl && spec != 0; ++j) reads_g = reads_g || eta_local(j) != 0.0f;
   cd::StepCtl* const uctl = run_if ? g->ctl : nullptr;
@@ -977,6 +1033,7 @@ cd_status enqueue_branch(cd_group* g, int branch, int spec, const void* const* G
         const hipStream_t su = stream_of(ui);
         cd_status st = enqueue_sync(g, g->shapes[u.sc], u.sel, G, uspec, M, X, Q, mu, eta, r, stage, su, run_if);
         if (st != CD_OK) return st;
+        if (cd::small_sync_fits(g->shapes[u.sc].m, g->shapes[u.sc].n, r)) continue;
         if (stage == 1 || stage == 3) {
           st = enqueue_factor(g, u, r, stage == 1 ? 0 : 1, su, run_if);
           if (st != CD_OK) return st;

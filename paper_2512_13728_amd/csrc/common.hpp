@@ -31,6 +31,18 @@ struct StepCtl {
 // when *run_if != 0 (the sync branch's kernels take &ctl->flag).
 __device__ __forceinline__ bool skip_launch(const int* run_if) { return run_if != nullptr && *run_if == 0; }
 
+// A pointer that a kernel reads from a device-side table is generic to the
+// compiler, which then accesses it with flat instructions; a flat access also
+// counts against the LDS wait counter, so every wait for an LDS result waits
+// for the outstanding global loads and stores as well (a prefetch no longer
+// overlaps, a store costs its full latency).  global_view marks such a pointer
+// as global memory (the round trip through an integer keeps the compiler from
+// folding the cast away) and its accesses become global loads and stores.
+template <typename T>
+__device__ __forceinline__ T* global_view(T* p) {
+  return (T*)(__attribute__((address_space(1))) T*)(reinterpret_cast<unsigned long long>(p));
+}
+
 // ---- a1: B = M + G and per-block sum of B^2 -------------------------------
 // Every block covers FORM_CHUNK consecutive elements of one layer; one launch
 // covers up to MAXS layers of any shapes (the passes are elementwise), layer
@@ -167,6 +179,19 @@ struct CholTab {
 hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s,
                            const int* run_if = nullptr);
 
+// The fixed pseudo-random direction that completes column j of P1 past the
+// numerical rank (row i; scale sqrt(3/m) gives unit expected norm): an
+// integer hash of (row, column), uniform in [-scale, scale).
+__device__ __forceinline__ float fill_value(unsigned i, unsigned j, float scale) {
+  // integer hash of (row, column): xorshift-multiply rounds
+  unsigned h = i * 0x9E3779B1u + j * 0x85EBCA77u + 0x27D4EB2Fu;
+  h ^= h >> 16; h *= 0x7FEB352Du;
+  h ^= h >> 15; h *= 0x846CA68Bu;
+  h ^= h >> 16;
+  return scale * (static_cast<float>(h >> 8) * (2.0f / 16777216.0f) - 1.0f);   // uniform in [-1, 1)
+}
+
+
 // P = P~ T^{-1} by block columns.  In place (Pin == Pout, same type) is
 // allowed: the workgroup of a row tile reads its block column of P~ before it
 // writes that block column of P, and reads only finished columns of P
@@ -205,6 +230,41 @@ struct ColnormArgs {
   const int* run_if;
 };
 hipError_t launch_colnorm(const ColnormArgs& a, int nl, hipStream_t s);
+
+// ---- the sync branch of small layers (k_small.hip) ----------------------------
+// Layers with r <= SMALL_R and m r, n r <= SMALL_MR: P~ = B Q and R = B^T P
+// on the fp64 GEMM kernels, then the two kernels below.
+constexpr int SMALL_R = 64;
+constexpr int SMALL_MR = 8192;
+constexpr int SMALL_ROWS = 16;    // rows of M and X per workgroup of the update
+bool small_sync_fits(int m, int n, int r);
+struct SmallQrArgs {               // CholQR twice, one workgroup per layer
+  int m, r;
+  const double* Pt[MAXB];          // P~ (m x r fp64)
+  double* P64[MAXB];               // out: P in fp64 (may be Pt)
+  float* P32[MAXB];                // out: P in fp32
+  int* rankdef[MAXB];              // out: 1 if a pivot was floored
+  int* rankdef_host[MAXB];         // NULL, or its mirror in pinned host memory
+  const int* run_if;
+};
+hipError_t launch_small_cholqr(const SmallQrArgs& a, int nl, hipStream_t s);
+struct SmallUpdArgs {              // column norms, Q and the M / X update
+  int m, n, r;
+  float one_minus_mu;
+  float c;                         // eta sqrt(m / n)
+  float* M[MAXB];
+  float* X[MAXB];
+  const float* P[MAXB];            // m x r fp32
+  const float* R[MAXB];            // n x r fp32
+  float* Q[MAXB];                  // out: n x r
+  const void* G[MAXB];             // reversal of a speculative skip update, as UpdateVecArgs
+  float gc[MAXB];
+  int g_bf16;
+  int spec;                        // 0, 1, or 2 = ctl->spec_cur
+  float xdecay[MAXB];
+  const StepCtl* ctl;              // NULL: run; else only on a sync step
+};
+hipError_t launch_small_update(const SmallUpdArgs& a, int nl, hipStream_t s);
 
 // ---- error-feedback momentum and weight update ------------------------------
 // M = M - (1-mu) P R^T (M holds B on entry); X = X - c P Q^T, c = eta sqrt(m/n)

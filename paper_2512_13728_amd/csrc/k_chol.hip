@@ -15,9 +15,7 @@
 //   chol_trail W[k+1:, k+1:] -= X^T X, upper tiles only            (fp64 MFMA)
 // and the triangular solve, one launch per block column c:
 //   P[:, c] = (P~[:, c] - P[:, :c] T[:c, c]) D_c                   (fp64 MFMA)
-#include <type_traits>
-#include <utility>
-
+#include "chol_wave.hpp"
 #include "common.hpp"
 #include "mfma_tile.hpp"
 
@@ -25,166 +23,49 @@ namespace cd {
 namespace {
 
 constexpr int CB = CHOL_BLOCK;
+using Wave64 = WaveChol<CB>;
 
-// One wave per layer: lane j holds column j of the 64 x 64 diagonal block
-// (upper triangle; rows past the matrix padded with the identity) in
-// registers.  Right-looking Cholesky: at pivot p the lanes publish row p of
-// the updated block in LDS and every lane reads it back with uniform-address
-// loads (a broadcast), then updates its own column.  The register array is
-// shifted by one row per pivot inside the update (a[i] holds row p + i), so
-// the pivot row is always a[0] and every index is a constant while the pivot
-// loop itself stays rolled: the kernel is a few KB of code instead of a
-// fully unrolled 100 KB that the instruction cache cannot hold.
-//
-// A pivot at or below the floor is raised to it and the rest of its row of T
-// is set to zero (as is the row of the block row that k_chol_panel forms,
-// through rowok): the numerically dependent direction then adds nothing to
-// the trailing matrix.  Dividing its rounding-level residuals by the floor's
-// square root instead would subtract their squares from the next pivots,
-// which fall under the floor in turn, and the entries grow without bound.
-//
-// D = T^{-1} follows by back substitution, lane c solving T d = e_c from the
-// last row up, with T read from LDS and the unknowns shifted the same way;
-// the columns of floored pivots are stored as zero, so that P~ T^{-1} is
-// zero in those columns (k_fill_dead then gives them new directions).
-constexpr int TLD = CB + 1;   // padded row of T in LDS (column stores hit distinct banks)
-constexpr int TPAD = CB;      // leading doubles: back-substitution reads above row 0 stay in the array
-constexpr int SEG = 8;        // pivots per segment of the diagonal-block loops
-
-// f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>), in order
-template <class F, int... I>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
-  (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-  static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
-
+// One wave per layer: the factorisation of the diagonal block (chol_wave.hpp)
+// and its inverse D_k; T_kk goes back over W_kk.
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
                                                   int pass, const int* run_if) {
-  __shared__ __attribute__((aligned(16))) double rowb[2 * CB];   // row p, then zeros
-  __shared__ double Tsb[TPAD + CB * TLD];
-  __shared__ double pinv[CB];                                     // 1 / T[p][p]
-  __shared__ int okb[CB];                                         // pivot p not floored
-  double* const Ts = Tsb + TPAD;   // Ts[j * TLD + i] = T[i][j]
+  __shared__ __attribute__((aligned(16))) Wave64::Lds lds;
   if (skip_launch(run_if)) return;
   const CholTab t = tab[blockIdx.x];
+  double* const W = global_view(t.W);
+  double* const floor_ = global_view(t.floor_);
+  int* const rankdef = global_view(t.rankdef);
   const int j = threadIdx.x;
   const long long ld = r;
   const int k0 = kb * CB, nb = min(CB, r - k0);
   double fl;
   if (kb == 0) {
     double md = 0.0;
-    for (int k = j; k < r; k += 64) md = fmax(md, t.W[k * ld + k]);
+    for (int k = j; k < r; k += 64) md = fmax(md, W[k * ld + k]);
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) md = fmax(md, __shfl_xor(md, o, 64));
     fl = fmax(1e-13 * md, 1e-60);
     if (j == 0) {
-      *t.floor_ = fl;
+      *floor_ = fl;
       if (pass == 0) {
-        *t.rankdef = 0;
+        *rankdef = 0;
         if (t.rankdef_host) *t.rankdef_host = 0;
       }
     }
   } else {
-    fl = *t.floor_;
+    fl = *floor_;
   }
-  double a[CB];   // a[i] = A[p + i][j] at pivot p
-#pragma unroll
-  for (int i = 0; i < CB; ++i) {
-    if (i < nb && j < nb) a[i] = i <= j ? t.W[(k0 + i) * ld + k0 + j] : 0.0;
-    else a[i] = i == j ? 1.0 : 0.0;
-  }
-  rowb[CB + j] = 0.0;
-  Tsb[j] = 0.0;
-  bool def = false;
-  // Only the block's nb pivots run: the identity padding of a last, partial
-  // block would factor to itself, and its rows are never stored.  At pivot p
-  // only rows p .. 63 remain, so the pivots run in segments of SEG whose
-  // register arrays carry 64, 64 - SEG, ... rows (rows past the live range
-  // stay untouched and unused).
-  auto pivot = [&](auto na, int p) {
-    constexpr int NA = decltype(na)::value;
-    // the pivot A[p][p] is lane p's a[0]: read across the wave (no LDS trip)
-    const double a0 = a[0];
-    double d = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(a0), p),
-                                __builtin_amdgcn_readlane(__double2loint(a0), p));
-    const bool floored = !(d > fl);   // uniform over the wave
-    if (floored) { d = fl; def = true; }
-    // 1/sqrt(d): the hardware estimate refined by two Newton steps (error
-    // squared each step), then sqrt(d) = d / sqrt(d); both within about an
-    // ulp, with no divide in the pivot's dependency chain
-    double inv = __builtin_amdgcn_rsq(d);
-#pragma unroll
-    for (int it = 0; it < 2; ++it) inv = fma(inv, fma(-0.5 * d * inv, inv, 0.5), inv);
-    const double piv = d * inv;
-    // row p of T (zero left of the diagonal, and right of a floored pivot)
-    const double tp = j == p ? piv : (j > p && !floored ? a[0] * inv : 0.0);
-    Ts[j * TLD + p] = tp;
-    if (j == p) {
-      pinv[p] = inv;
-      okb[p] = floored ? 0 : 1;
-      t.rowok[k0 + p] = floored ? 0 : 1;
-    }
-    __syncthreads();
-    rowb[j] = tp;
-    __syncthreads();
-    // rows below p: A[p + i][j] -= T[p][p + i] T[p][j], shifted up one row;
-    // lanes j < p + i only touch the (unused) lower triangle.  The row is read
-    // whole before the update (one LDS round trip, not one per pair).
-    double rv[NA];
-#pragma unroll
-    for (int i = 1; i < NA; ++i) rv[i] = rowb[p + i];
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = 1; i < NA; ++i) a[i - 1] = fma(-rv[i], tp, a[i]);
-    a[NA - 1] = 0.0;
-    __syncthreads();
-  };
-  // segment s: pivots [s SEG, (s + 1) SEG) with CB - s SEG live rows
-  static_for<CB / SEG>([&](auto sc) {
-    constexpr int S = decltype(sc)::value;
-#pragma unroll 1
-    for (int p = S * SEG; p < min(nb, (S + 1) * SEG); ++p) pivot(std::integral_constant<int, CB - S * SEG>{}, p);
-  });
-
-  // f[k] = d[p - k] at step p, from p = nb - 1 down; entries with k > p lie
-  // above row 0 and are never stored, so the steps of pivots below
-  // 64 - SEG s carry only 64 - SEG s entries
-  double f[CB];
-#pragma unroll
-  for (int k = 0; k < CB; ++k) f[k] = k == nb - 1 - j ? 1.0 : 0.0;
-  double* D = t.Dinv + static_cast<long long>(kb) * CB * CB;
-  // the column of a floored pivot is stored as zero: P~ T^{-1} then has a
-  // zero column there and the other columns are unchanged (with row p of T
-  // zero right of the diagonal, column j != p of T^{-1} is zero in row p)
-  const bool cin = j < nb && okb[j];
+  const bool def = Wave64::factor(lds, j, nb, fl, [&](int i) { return W[(k0 + i) * ld + k0 + j]; });
+  if (j < nb) global_view(t.rowok)[k0 + j] = lds.okb[j];
+  double* D = global_view(t.Dinv) + static_cast<long long>(kb) * CB * CB;
   for (int p = nb; p < CB; ++p) D[p * CB + j] = 0.0;   // rows past a partial block
-  auto back = [&](auto nf, int p) {
-    constexpr int NF = decltype(nf)::value;
-    const double x = f[0] * pinv[p];
-    D[p * CB + j] = cin ? x : 0.0;
-    const double* col = Ts + p * TLD + p;   // col[-k] = T[p - k][p]
-    double cv[NF];
-#pragma unroll
-    for (int k = 1; k < NF; ++k) cv[k] = col[-k];
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int k = 1; k < NF; ++k) f[k - 1] = fma(-cv[k], x, f[k]);
-    f[NF - 1] = 0.0;
-  };
-  // segments from the last down: segment s carries (s + 1) SEG entries
-  static_for<CB / SEG>([&](auto ic) {
-    constexpr int S = CB / SEG - 1 - decltype(ic)::value;
-#pragma unroll 1
-    for (int p = min(nb, (S + 1) * SEG) - 1; p >= S * SEG; --p) back(std::integral_constant<int, (S + 1) * SEG>{}, p);
-  });
+  Wave64::inverse(lds, j, nb, [&](int p, double x) { D[p * CB + j] = x; });
+  const double* Ts = Wave64::Ts(lds);
 #pragma unroll 4
   for (int i = 0; i < nb; ++i)
-    if (j < nb && i <= j) t.W[(k0 + i) * ld + k0 + j] = Ts[j * TLD + i];
+    if (j < nb && i <= j) W[(k0 + i) * ld + k0 + j] = Ts[j * Wave64::TLD + i];
   if (j == 0 && def) {
-    *t.rankdef = 1;
+    *rankdef = 1;
     if (t.rankdef_host) *t.rankdef_host = 1;
   }
 }
@@ -230,8 +111,10 @@ __global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ 
   const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
   const int k0 = kb * CB, nb = min(CB, r - k0), k1 = k0 + nb;
   const int j0 = k1 + blockIdx.x * CB;
-  const double* D = t.Dinv + static_cast<long long>(kb) * CB * CB;
-  const double* Wp = t.W + static_cast<long long>(k0) * r;  // block row k
+  const double* D = global_view(t.Dinv) + static_cast<long long>(kb) * CB * CB;
+  double* const W = global_view(t.W);
+  const int* const rowok = global_view(t.rowok);
+  const double* Wp = W + static_cast<long long>(k0) * r;  // block row k
   Tile64 T;
   T.zero();
   for (int kk0 = 0; kk0 < nb; kk0 += GBK) {
@@ -251,7 +134,7 @@ __global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ 
         const int row = wm0 + i * 16 + Mfma<double>::out_row(lane, v);
         const int col = j0 + wn0 + j * 16 + (lane & 15);
         if (row < nb && col < r)
-          t.W[static_cast<long long>(k0 + row) * r + col] = t.rowok[k0 + row] ? T.acc[i][j][v] : 0.0;
+          W[static_cast<long long>(k0 + row) * r + col] = rowok[k0 + row] ? T.acc[i][j][v] : 0.0;
       }
 }
 
@@ -269,7 +152,8 @@ __global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ 
   while (u >= nt - ti) { u -= nt - ti; ++ti; }
   const int tj = ti + u;
   const int i0 = k1 + ti * CB, j0 = k1 + tj * CB;
-  const double* X = t.W + static_cast<long long>(k0) * r;   // rows k0..k1 of T
+  double* const W = global_view(t.W);
+  const double* X = W + static_cast<long long>(k0) * r;   // rows k0..k1 of T
   Tile64 T;
   T.zero();
   for (int kk0 = 0; kk0 < nb; kk0 += GBK) {
@@ -288,7 +172,7 @@ __global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ 
       for (int v = 0; v < 4; ++v) {
         const int row = i0 + wm0 + i * 16 + Mfma<double>::out_row(lane, v);
         const int col = j0 + wn0 + j * 16 + (lane & 15);
-        if (row < r && col < r) t.W[static_cast<long long>(row) * r + col] -= T.acc[i][j][v];
+        if (row < r && col < r) W[static_cast<long long>(row) * r + col] -= T.acc[i][j][v];
       }
 }
 
@@ -302,30 +186,22 @@ __global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ 
 // at once.
 constexpr int FILL_ROWS = 64;
 
-__device__ __forceinline__ float fill_value(unsigned i, unsigned j, float scale) {
-  // integer hash of (row, column): xorshift-multiply rounds
-  unsigned h = i * 0x9E3779B1u + j * 0x85EBCA77u + 0x27D4EB2Fu;
-  h ^= h >> 16; h *= 0x7FEB352Du;
-  h ^= h >> 15; h *= 0x846CA68Bu;
-  h ^= h >> 16;
-  return scale * (static_cast<float>(h >> 8) * (2.0f / 16777216.0f) - 1.0f);   // uniform in [-1, 1)
-}
-
 template <typename T>
 __global__ __launch_bounds__(256) void k_fill_dead(const CholTab* __restrict__ ct,
                                                    const TrsmTab* __restrict__ tt, int r, const int* run_if) {
   if (skip_launch(run_if)) return;
   const CholTab c = ct[blockIdx.y];
-  if (*c.rankdef == 0) return;
+  if (*global_view(c.rankdef) == 0) return;
+  const int* const rowok = global_view(c.rowok);
   const TrsmTab t = tt[blockIdx.y];
-  T* P1 = static_cast<T*>(t.Pout);
+  T* P1 = global_view(static_cast<T*>(t.Pout));
   const int i0 = blockIdx.x * FILL_ROWS;
   const int rows = min(FILL_ROWS, t.m - i0);
   if (rows <= 0) return;
   const float scale = sqrtf(3.0f / static_cast<float>(t.m));
   for (int e = threadIdx.x; e < rows * r; e += 256) {
     const int i = i0 + e / r, j = e % r;
-    if (!c.rowok[j]) P1[static_cast<long long>(i) * r + j] = static_cast<T>(fill_value(i, j, scale));
+    if (!rowok[j]) P1[static_cast<long long>(i) * r + j] = static_cast<T>(fill_value(i, j, scale));
   }
 }
 
@@ -348,8 +224,9 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
   const int c0 = cb * CB, nbc = min(CB, r - c0);
-  const TIn* Pin = static_cast<const TIn*>(t.Pin);
-  TOut* Pout = static_cast<TOut*>(t.Pout);
+  const TIn* Pin = global_view(static_cast<const TIn*>(t.Pin));
+  TOut* Pout = global_view(static_cast<TOut*>(t.Pout));
+  const double* const W = global_view(t.W);
   if constexpr (IDENT) {
     // T^{-1} is upper triangular: a row tile below the diagonal block is zero
     if (lt.y > cb) {
@@ -371,7 +248,7 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
   Prefetch<double, CB, 256, false> pb;
   if (kbeg < c0) {
     pa.load(Prow, r, 0, m - i0, kbeg, c0, tid);
-    pb.load(t.W + c0, r, 0, nbc, kbeg, c0, tid);
+    pb.load(W + c0, r, 0, nbc, kbeg, c0, tid);
   }
   for (int k0 = kbeg; k0 < c0; k0 += GBK) {
     pa.template store<double>(As, tid);
@@ -379,7 +256,7 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
     __syncthreads();
     if (k0 + GBK < c0) {
       pa.load(Prow, r, 0, m - i0, k0 + GBK, c0, tid);
-      pb.load(t.W + c0, r, 0, nbc, k0 + GBK, c0, tid);
+      pb.load(W + c0, r, 0, nbc, k0 + GBK, c0, tid);
     }
     T.mma_stage<true>(As, Bs, wm0, wn0, lane);
     __syncthreads();
@@ -402,7 +279,7 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
         }
         Ys[row * YLD + col] = y;
       }
-  const double* D = t.Dinv + static_cast<long long>(cb) * CB * CB;
+  const double* D = global_view(t.Dinv) + static_cast<long long>(cb) * CB * CB;
   T.zero();
   for (int k0 = 0; k0 < nbc; k0 += GBK) {
     stage_tile<double, double, CB, 256, false>(Bs, D, CB, 0, nbc, k0, nbc, tid);

@@ -1,0 +1,331 @@
+// The sync branch of small layers (r <= SMALL_R, m r and n r <= SMALL_MR) in
+// four launches instead of the blocked pipeline's seventeen or so: the power
+// products P~ = B Q and R = B^T P run on the fp64 GEMM kernels (no split-K),
+// and the two kernels here do the rest.
+//
+//   k_small_cholqr   Orthogonalize (Algorithm 1 / 2): the thin-QR factor of
+//                    P~ with positive diagonal by CholQR twice, one workgroup
+//                    per layer with the whole m x r panel in LDS, fp64
+//                    throughout (Gram matrix on the fp64 MFMA, the one-wave
+//                    Cholesky factorisation and inverse of the blocked
+//                    kernels' diagonal blocks, P T^-1), the same pivot floor
+//                    and completion past the numerical rank as the blocked
+//                    kernels.  Writes P in fp64 (for R = B^T P) and fp32.
+//   k_small_update   ColumnNormalize and the error-feedback / weight updates:
+//                    every workgroup forms the column norms of R (fixed order,
+//                    fp64), Q = R / norm (the first workgroup stores Q), and
+//                    updates its rows of M = B - (1 - mu) P R^T and
+//                    X -= eta sqrt(m/n) P Q^T with fp32 products, k in order.
+//
+// At these sizes every launch is a few microseconds of latency and the work a
+// fraction of it, so fewer launches is what the step needs.
+#include "chol_wave.hpp"
+#include "common.hpp"
+#include "mfma_tile.hpp"
+
+namespace cd {
+namespace {
+
+constexpr int SQR_THREADS = 256;
+constexpr int BATCH = 8;   // global loads issued before their LDS stores
+
+// dst[e] = f(src[e]) for e < count, BATCH loads per thread in flight (a copy
+// loop that stores each value before loading the next would wait out the
+// memory latency once per element)
+template <int NT, typename TD, typename TS, typename F>
+__device__ __forceinline__ void copy_batched(TD* dst, const TS* src, int count, int tid, F&& f) {
+  for (int e0 = 0; e0 < count; e0 += NT * BATCH) {
+    TS v[BATCH];
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const int e = e0 + u * NT + tid;
+      v[u] = e < count ? src[e] : TS(0);
+    }
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const int e = e0 + u * NT + tid;
+      if (e < count) f(dst, e, v[u]);
+    }
+  }
+}
+
+// One workgroup per layer, the whole m x r panel in LDS (fp64, row-major).
+// Each CholQR pass:
+//   W = P^T P        fp64 MFMA, 16 x 16 upper tiles; wave w takes the 16-row
+//                    groups w, w + 4, ..., and the four partial sums are added
+//                    into W in wave order
+//   W = T^T T, T^-1  wave 0 (chol_wave.hpp), the same pivot floor as the
+//                    blocked kernels; T^-1 is written over W
+//   P <- P T^-1      fp64 MFMA, 16 x 16 tiles (the columns of floored pivots
+//                    come out zero)
+// then, after pass 0, the completion past the numerical rank.
+// LDS at NB = 64: panel 64 KB, W 32 KB, factorisation 35 KB.
+template <int NB>
+__global__ __launch_bounds__(SQR_THREADS) void k_small_cholqr(SmallQrArgs a) {
+  using WC = WaveChol<NB>;
+  constexpr int NT = NB / 16;                  // 16-column blocks
+  constexpr int NTILE = NT * (NT + 1) / 2;     // upper 16 x 16 tiles of W
+  __shared__ double Pl[SMALL_MR];
+  __shared__ double Wl[NB * NB];               // W (upper triangle), then T^-1; row stride NB
+  __shared__ __attribute__((aligned(16))) typename WC::Lds wc;
+  __shared__ int floored;
+  if (skip_launch(a.run_if)) return;
+  const int l = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int m = a.m, r = a.r, mr = m * r;
+  copy_batched<SQR_THREADS>(Pl, a.Pt[l], mr, tid, [](double* d, int e, double v) { d[e] = v; });
+  __syncthreads();
+  // MFMA operands: lane owns column (lane % 16) of a 16-column block and rows
+  // (k indices) 4 (lane / 16) + q of a group of 16, q = 0..3 (one per MFMA)
+  const int col = lane & 15, kq = 4 * (lane >> 4);
+  bool any_dead = false;   // uniform: every thread reads the same flags
+  for (int pass = 0; pass < 2; ++pass) {
+    {
+      f64x4 acc[NTILE];
+#pragma unroll
+      for (int t = 0; t < NTILE; ++t) acc[t] = f64x4{};
+      for (int k0 = wave * 16; k0 < m; k0 += 4 * 16) {
+        double x[NT][4];
+#pragma unroll
+        for (int b = 0; b < NT; ++b)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = k0 + kq + q, c = b * 16 + col;
+            x[b][q] = (row < m && c < r) ? Pl[row * r + c] : 0.0;
+          }
+        int t = 0;
+#pragma unroll
+        for (int bi = 0; bi < NT; ++bi)
+#pragma unroll
+          for (int bj = bi; bj < NT; ++bj, ++t)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(x[bi][q], x[bj][q], acc[t], 0, 0, 0);
+      }
+#pragma unroll 1
+      for (int w = 0; w < 4; ++w) {
+        if (wave == w) {
+          int t = 0;
+#pragma unroll
+          for (int bi = 0; bi < NT; ++bi)
+#pragma unroll
+            for (int bj = bi; bj < NT; ++bj, ++t)
+#pragma unroll
+              for (int v = 0; v < 4; ++v) {
+                const int row = bi * 16 + Mfma<double>::out_row(lane, v), c = bj * 16 + col;
+                if (row < r && c < r) {
+                  double* const wp = Wl + row * NB + c;
+                  *wp = (w == 0 ? 0.0 : *wp) + acc[t][v];
+                }
+              }
+        }
+        __syncthreads();
+      }
+    }
+    if (wave == 0) {
+      // j made opaque here: otherwise the compiler keeps the register
+      // arrays' initial values (functions of j and r only) live across the
+      // pass loop, and spills
+      int j = lane;
+      __asm__ volatile("" : "+v"(j));
+      // pivot floor: 1e-13 of the largest diagonal (at least 1e-60)
+      double md = j < r ? Wl[j * NB + j] : 0.0;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) md = fmax(md, __shfl_xor(md, o, 64));
+      const double fl = fmax(1e-13 * md, 1e-60);
+      // factor() holds W in registers once it starts, so T^-1 may go over it
+      const bool def = WC::factor(wc, j, r, fl, [&](int i) { return Wl[i * NB + j]; });
+      WC::inverse(wc, j, r, [&](int p, double x) {
+        if (j < r) Wl[p * NB + j] = x;
+      });
+      if (j == 0) floored = def ? 1 : 0;
+    }
+    __syncthreads();
+    const bool dead = floored != 0;
+    any_dead = any_dead || dead;
+    // P T^-1 on the fp64 MFMA in 16 x 16 output tiles (row block ib, column
+    // block jb), K over the column blocks kb <= jb (T^-1 is upper
+    // triangular).  A tile reads only its own row block of P, so the tiles go
+    // in rounds of whole row blocks: every wave forms its tiles of the round
+    // (at most 4), then, after a barrier, the pass-0 result goes over the
+    // panel (pass 1: straight to P64 / P32).
+    {
+      const int nbk = (r + 15) / 16, mb = (m + 15) / 16;
+      const int rows_per_round = 16 / nbk;   // nbk <= 4
+      const float scale = sqrtf(3.0f / static_cast<float>(m));
+      double* __restrict__ P64 = a.P64[l];
+      float* __restrict__ P32 = a.P32[l];
+      for (int ib0 = 0; ib0 < mb; ib0 += rows_per_round) {
+        const int ntile = min(rows_per_round, mb - ib0) * nbk;
+        f64x4 o[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          o[u] = f64x4{};
+          const int t = wave + 4 * u;
+          if (t < ntile) {
+            const int ib = ib0 + t / nbk, jb = t - (t / nbk) * nbk;
+            const int row = ib * 16 + col, cj = jb * 16 + col;
+            for (int kb = 0; kb <= jb; ++kb)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int k = kb * 16 + kq + q;
+                const double x = (row < m && k < r) ? Pl[row * r + k] : 0.0;
+                const double y = (k < r && cj < r) ? Wl[k * NB + cj] : 0.0;
+                o[u] = __builtin_amdgcn_mfma_f64_16x16x4f64(x, y, o[u], 0, 0, 0);
+              }
+          }
+        }
+        if (pass == 0) __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int t = wave + 4 * u;
+          if (t < ntile) {
+            const int ib = ib0 + t / nbk, jb = t - (t / nbk) * nbk;
+            const int j = jb * 16 + col;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int i = ib * 16 + Mfma<double>::out_row(lane, v);
+              if (i < m && j < r) {
+                const int e = i * r + j;
+                if (pass == 0) {
+                  // completion past the numerical rank: the fixed pseudo-random
+                  // direction of each column whose pass-0 pivot was floored,
+                  // orthonormalised by the second pass
+                  Pl[e] = (dead && !wc.okb[j]) ? static_cast<double>(fill_value(i, j, scale)) : o[u][v];
+                } else {
+                  P64[e] = o[u][v];
+                  P32[e] = static_cast<float>(o[u][v]);
+                }
+              }
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  if (tid == 0) {
+    *a.rankdef[l] = any_dead ? 1 : 0;
+    if (a.rankdef_host[l]) *a.rankdef_host[l] = any_dead ? 1 : 0;
+  }
+}
+
+constexpr int SUP_THREADS = 256;
+
+// One workgroup per (row band, layer).  R and Q are held transposed in LDS
+// (k-major), so that the lanes of a wave, which own consecutive columns c,
+// read consecutive words.
+__global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
+  __shared__ float Rt[SMALL_MR];
+  __shared__ float Qt[SMALL_MR];
+  __shared__ float Pb[SMALL_ROWS * SMALL_R];
+  __shared__ double part[SUP_THREADS];
+  __shared__ float nrm[SMALL_R];
+  if (a.ctl != nullptr && a.ctl->flag == 0) return;   // not a sync step
+  const int l = blockIdx.y, tid = threadIdx.x;
+  const int m = a.m, n = a.n, r = a.r;
+  const float* __restrict__ R = a.R[l];
+  // R (n x r, row-major) into Rt (k-major); the loads in batches, row-major
+  // order, then the transposed stores
+  copy_batched<SUP_THREADS>(Rt, R, n * r, tid, [n, r](float* d, int e, float v) {
+    const int c = e / r, k = e - c * r;
+    d[k * n + c] = v;
+  });
+  __syncthreads();
+  // column norms: tpc consecutive threads per column k, thread q summing
+  // rows q, q + tpc, ... in order, then the tpc partial sums in order (the
+  // order depends on n and r only)
+  const int tpc = SUP_THREADS / r;
+  {
+    double s = 0.0;
+    const int k = tid / tpc, q = tid - k * tpc;
+    if (k < r)
+      for (int c = q; c < n; c += tpc) {
+        const double v = Rt[k * n + c];
+        s = fma(v, v, s);
+      }
+    part[tid] = s;
+  }
+  __syncthreads();
+  if (tid < r) {
+    double s = 0.0;
+    for (int q = 0; q < tpc; ++q) s += part[tid * tpc + q];
+    nrm[tid] = static_cast<float>(fmax(sqrt(s), 1e-30));
+  }
+  __syncthreads();
+  float* __restrict__ Qo = a.Q[l];
+  for (int e = tid; e < n * r; e += SUP_THREADS) {
+    const int k = e / n, c = e - k * n;
+    const float q = Rt[e] / nrm[k];
+    Qt[e] = q;
+    if (blockIdx.x == 0) Qo[c * r + k] = q;
+  }
+  // this band's rows of P
+  const int i0 = blockIdx.x * SMALL_ROWS, rows = min(SMALL_ROWS, m - i0);
+  const float* __restrict__ P = a.P[l];
+  copy_batched<SUP_THREADS>(Pb, P + static_cast<long long>(i0) * r, rows * r, tid,
+                            [](float* d, int e, float v) { d[e] = v; });
+  __syncthreads();
+  float* __restrict__ Mo = a.M[l];
+  float* __restrict__ Xo = a.X[l];
+  const void* G = a.G[l];
+  const bool spec = (a.spec == 2 ? a.ctl->spec_cur : a.spec) != 0;
+  const float gc = spec ? a.gc[l] : 0.0f, xd = spec ? 1.0f : a.xdecay[l];
+  const float cm = -a.one_minus_mu, cx = -a.c;
+  // each thread owns one column c of every row of the band: the band's
+  // M, X (and G) values of that column are all requested before any
+  // arithmetic, so that their latency overlaps
+  for (int c = tid; c < n; c += SUP_THREADS) {
+    float mv[SMALL_ROWS], xv[SMALL_ROWS], gv[SMALL_ROWS];
+#pragma unroll
+    for (int t = 0; t < SMALL_ROWS; ++t) {
+      if (t < rows) {
+        const long long off = static_cast<long long>(i0 + t) * n + c;
+        mv[t] = Mo[off];
+        xv[t] = Xo[off];
+        gv[t] = gc == 0.0f ? 0.0f
+                           : (a.g_bf16 ? __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(G)[off]) << 16)
+                                       : static_cast<const float*>(G)[off]);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < SMALL_ROWS; ++t) {
+      if (t >= rows) break;
+      const float* prow = Pb + t * r;
+      float sm = 0.0f, sx = 0.0f;
+      for (int k = 0; k < r; ++k) {
+        const float pk = prow[k];
+        sm = fmaf(pk, Rt[k * n + c], sm);
+        sx = fmaf(pk, Qt[k * n + c], sx);
+      }
+      const long long off = static_cast<long long>(i0 + t) * n + c;
+      const float x = gc != 0.0f ? fmaf(gc, gv[t], xv[t]) : xv[t] * xd;
+      Mo[off] = fmaf(cm, sm, mv[t]);
+      Xo[off] = fmaf(cx, sx, x);
+    }
+  }
+}
+
+}  // namespace
+
+bool small_sync_fits(int m, int n, int r) {
+  return r >= 1 && r <= SMALL_R && 1LL * m * r <= SMALL_MR && 1LL * n * r <= SMALL_MR;
+}
+
+hipError_t launch_small_cholqr(const SmallQrArgs& a, int nl, hipStream_t s) {
+  if (nl <= 0) return hipSuccess;
+  if (!small_sync_fits(a.m, 1, a.r)) return hipErrorInvalidValue;
+  if (a.r <= 16) hipLaunchKernelGGL(k_small_cholqr<16>, dim3(nl), dim3(SQR_THREADS), 0, s, a);
+  else if (a.r <= 32) hipLaunchKernelGGL(k_small_cholqr<32>, dim3(nl), dim3(SQR_THREADS), 0, s, a);
+  else hipLaunchKernelGGL(k_small_cholqr<64>, dim3(nl), dim3(SQR_THREADS), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_small_update(const SmallUpdArgs& a, int nl, hipStream_t s) {
+  if (nl <= 0) return hipSuccess;
+  if (!small_sync_fits(a.m, a.n, a.r) || (a.spec == 2 && !a.ctl)) return hipErrorInvalidValue;
+  const dim3 grid((a.m + SMALL_ROWS - 1) / SMALL_ROWS, nl);
+  hipLaunchKernelGGL(k_small_update, grid, dim3(SUP_THREADS), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace cd

@@ -33,7 +33,7 @@ def test_every_timed_kind_has_a_bound():
     for k in kinds:
         assert k in bench.KIND_BOUND, k
         bound, dtype, mult = bench.KIND_BOUND[k]
-        assert bound in ("hbm", "mfma")
+        assert bound in ("hbm", "mfma", "alu")
         assert (dtype is None) == (bound == "hbm")
         if dtype is not None:
             assert dtype in bench.PEAK_TFLOPS

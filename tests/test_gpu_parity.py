@@ -146,7 +146,10 @@ def test_rmmc_exactly_zero_and_deterministic():
                                    # fp32 vector update (r <= 32): ragged column strips of
                                    # four and of two columns per lane, a tall narrow matrix
                                    (97, 515, 5), (130, 259, 20), (8197, 6, 3), (300, 1000, 32),
-                                   (257, 333, 48)])
+                                   (257, 333, 48),
+                                   # the four-launch path of small layers at its limits:
+                                   # m r = 8192, n r = 8192, r = 64 and r = 1
+                                   (128, 128, 64), (8192, 7, 1), (2047, 2048, 4), (33, 8192, 1)])
 def test_sync_step_teacher_forced(m, n, r):
     w = S.small_workload(m, n, r, k=max(2, r // 2))
     M, X, Q = _state(w, 0)
@@ -191,10 +194,13 @@ def test_zero_buffer_sync_is_defined():
 
 
 @pytest.mark.parametrize("gd", ["f32", "bf16"])
-def test_rank_deficient_buffer_is_completed(gd):
+@pytest.mark.parametrize("m,n,r,k", [(192, 160, 96, 5), (96, 80, 48, 5)])
+def test_rank_deficient_buffer_is_completed(gd, m, n, r, k):
     """B of exact rank k < r (only its first k rows are nonzero, in either
     gradient dtype) on a sync step: P~ = B Q has rank k, so r - k pass-0
-    Cholesky pivots fall under the floor, in both 64-column blocks of r = 96.
+    Cholesky pivots fall under the floor: in both 64-column blocks of r = 96
+    (the blocked factorisation), and in the one-workgroup factorisation of a
+    small layer (r = 48).
     Like a Householder QR factor, P still has orthonormal columns: the first k
     are unique and match the oracle (as do those of R and Q, and M = mu B),
     the others complete the basis orthogonally to B's column space (so the
@@ -208,7 +214,6 @@ def test_rank_deficient_buffer_is_completed(gd):
     step, and the step after it is a plain full-rank step that matches the
     oracle: no column of Q is lost for good."""
     from gpu_util import device_to_numpy
-    m, n, r, k = 192, 160, 96, 5
     gen = torch.Generator().manual_seed(77)
     G = torch.zeros(m, n)
     G[:k] = torch.randn(k, n, generator=gen) * 0.01
@@ -383,7 +388,7 @@ def test_more_shape_batches_than_streams(gd):
 
 
 @pytest.mark.parametrize("policy", [O.POLICY_RMMC, O.POLICY_ALWAYS_SYNC])
-@pytest.mark.parametrize("m,n,r", [(512, 1536, 64), (2048, 512, 256), (300, 700, 37)])
+@pytest.mark.parametrize("m,n,r", [(512, 1536, 64), (2048, 512, 256), (300, 700, 37), (128, 256, 32)])
 def test_bf16_gradient_steps(m, n, r, policy):
     gd = "bf16"
     w = S.small_workload(m, n, r, grad_dtype=gd, k=16)
@@ -571,7 +576,7 @@ def test_kernel_timing_brackets_only_the_named_kinds():
         M, X, Q = _state(w, 0)
         stream = S.GradientStream(w, 0, device="cpu")
         if kinds == "pick":
-            upd = [k for k in runs[0][0] if k.startswith("update")]
+            upd = [k for k in runs[0][0] if k in ("update_f32", "update_bf16", "small_update")]
             assert len(upd) == 1
             kinds = ["gate", upd[0]]
         Gp.set_timing(True, kinds)
@@ -585,7 +590,7 @@ def test_kernel_timing_brackets_only_the_named_kinds():
                 Gp.set_timing(True, ["no_such_kind"])
     (k_all, f_all, s_all), (k_sel, f_sel, s_sel) = runs
     assert f_all == f_sel and f_all[0]
-    assert set(k_sel) == {"gate", [k for k in k_all if k.startswith("update")][0]}
+    assert set(k_sel) == {"gate", [k for k in k_all if k in ("update_f32", "update_bf16", "small_update")][0]}
     for k, v in k_sel.items():
         assert v["launches"] == k_all[k]["launches"] and v["total_ms"] > 0
     assert len(k_all) > 5 and k_all["gate"]["launches"] == 3
@@ -620,8 +625,10 @@ def test_full_timing_runs_batches_serially_with_identical_results():
         assert np.array_equal(a, b)
     kt = outs[1][2]
     n_sync = sum(f for _, f in outs[0][0])
-    # one update launch per shape batch and sync step
-    assert kt["update_f32"]["launches"] == len(shapes) * n_sync
+    # one update launch per shape batch and sync step (these small layers
+    # take the four-launch path: P~ = BQ, CholQR2, R = B^T P, update)
+    assert kt["small_update"]["launches"] == len(shapes) * n_sync
+    assert kt["small_cholqr"]["launches"] == len(shapes) * n_sync
 
 
 def test_wrong_operands_are_refused_before_any_work():
