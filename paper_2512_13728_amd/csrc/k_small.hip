@@ -211,24 +211,51 @@ __global__ __launch_bounds__(SQR_THREADS) void k_small_cholqr(SmallQrArgs a) {
 
 constexpr int SUP_THREADS = 256;
 
-// One workgroup per (row band, layer).  R and Q are held transposed in LDS
-// (k-major), so that the lanes of a wave, which own consecutive columns c,
-// read consecutive words.
+// One workgroup per (row band, layer).  Every global read is requested at
+// the start, so that their latencies overlap: this thread's column of the
+// band's M, X (and G) rows, the band's rows of P, and R.  R and Q are held
+// transposed in LDS (k-major, row stride n + 1), so that the lanes of a wave,
+// which own consecutive columns c, read consecutive words, and the
+// transposing stores of consecutive k fall into different banks.
 __global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
-  __shared__ float Rt[SMALL_MR];
-  __shared__ float Qt[SMALL_MR];
+  __shared__ float Rt[SMALL_MR + SMALL_R];
+  __shared__ float Qt[SMALL_MR + SMALL_R];
   __shared__ float Pb[SMALL_ROWS * SMALL_R];
   __shared__ double part[SUP_THREADS];
   __shared__ float nrm[SMALL_R];
   if (a.ctl != nullptr && a.ctl->flag == 0) return;   // not a sync step
   const int l = blockIdx.y, tid = threadIdx.x;
-  const int m = a.m, n = a.n, r = a.r;
-  const float* __restrict__ R = a.R[l];
-  // R (n x r, row-major) into Rt (k-major); the loads in batches, row-major
-  // order, then the transposed stores
-  copy_batched<SUP_THREADS>(Rt, R, n * r, tid, [n, r](float* d, int e, float v) {
+  const int m = a.m, n = a.n, r = a.r, ldt = n + 1;
+  const int i0 = blockIdx.x * SMALL_ROWS, rows = min(SMALL_ROWS, m - i0);
+  float* __restrict__ Mo = a.M[l];
+  float* __restrict__ Xo = a.X[l];
+  const void* G = a.G[l];
+  const bool spec = (a.spec == 2 ? a.ctl->spec_cur : a.spec) != 0;
+  const float gc = spec ? a.gc[l] : 0.0f, xd = spec ? 1.0f : a.xdecay[l];
+  const float cm = -a.one_minus_mu, cx = -a.c;
+  // each thread owns one column c of every row of the band
+  float mv[SMALL_ROWS], xv[SMALL_ROWS], gv[SMALL_ROWS];
+  auto load_column = [&](int c) {
+#pragma unroll
+    for (int t = 0; t < SMALL_ROWS; ++t) {
+      if (t < rows) {
+        const long long off = static_cast<long long>(i0 + t) * n + c;
+        mv[t] = Mo[off];
+        xv[t] = Xo[off];
+        gv[t] = gc == 0.0f ? 0.0f
+                           : (a.g_bf16 ? __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(G)[off]) << 16)
+                                       : static_cast<const float*>(G)[off]);
+      }
+    }
+  };
+  if (tid < n) load_column(tid);
+  // this band's rows of P, and R (n x r, row-major) into Rt (k-major); the
+  // loads in batches, row-major order, then the stores
+  copy_batched<SUP_THREADS>(Pb, a.P[l] + static_cast<long long>(i0) * r, rows * r, tid,
+                            [](float* d, int e, float v) { d[e] = v; });
+  copy_batched<SUP_THREADS>(Rt, a.R[l], n * r, tid, [ldt, r](float* d, int e, float v) {
     const int c = e / r, k = e - c * r;
-    d[k * n + c] = v;
+    d[k * ldt + c] = v;
   });
   __syncthreads();
   // column norms: tpc consecutive threads per column k, thread q summing
@@ -240,7 +267,7 @@ __global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
     const int k = tid / tpc, q = tid - k * tpc;
     if (k < r)
       for (int c = q; c < n; c += tpc) {
-        const double v = Rt[k * n + c];
+        const double v = Rt[k * ldt + c];
         s = fma(v, v, s);
       }
     part[tid] = s;
@@ -255,38 +282,13 @@ __global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
   float* __restrict__ Qo = a.Q[l];
   for (int e = tid; e < n * r; e += SUP_THREADS) {
     const int k = e / n, c = e - k * n;
-    const float q = Rt[e] / nrm[k];
-    Qt[e] = q;
+    const float q = Rt[k * ldt + c] / nrm[k];
+    Qt[k * ldt + c] = q;
     if (blockIdx.x == 0) Qo[c * r + k] = q;
   }
-  // this band's rows of P
-  const int i0 = blockIdx.x * SMALL_ROWS, rows = min(SMALL_ROWS, m - i0);
-  const float* __restrict__ P = a.P[l];
-  copy_batched<SUP_THREADS>(Pb, P + static_cast<long long>(i0) * r, rows * r, tid,
-                            [](float* d, int e, float v) { d[e] = v; });
   __syncthreads();
-  float* __restrict__ Mo = a.M[l];
-  float* __restrict__ Xo = a.X[l];
-  const void* G = a.G[l];
-  const bool spec = (a.spec == 2 ? a.ctl->spec_cur : a.spec) != 0;
-  const float gc = spec ? a.gc[l] : 0.0f, xd = spec ? 1.0f : a.xdecay[l];
-  const float cm = -a.one_minus_mu, cx = -a.c;
-  // each thread owns one column c of every row of the band: the band's
-  // M, X (and G) values of that column are all requested before any
-  // arithmetic, so that their latency overlaps
   for (int c = tid; c < n; c += SUP_THREADS) {
-    float mv[SMALL_ROWS], xv[SMALL_ROWS], gv[SMALL_ROWS];
-#pragma unroll
-    for (int t = 0; t < SMALL_ROWS; ++t) {
-      if (t < rows) {
-        const long long off = static_cast<long long>(i0 + t) * n + c;
-        mv[t] = Mo[off];
-        xv[t] = Xo[off];
-        gv[t] = gc == 0.0f ? 0.0f
-                           : (a.g_bf16 ? __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(G)[off]) << 16)
-                                       : static_cast<const float*>(G)[off]);
-      }
-    }
+    if (c != tid) load_column(c);
 #pragma unroll
     for (int t = 0; t < SMALL_ROWS; ++t) {
       if (t >= rows) break;
@@ -294,8 +296,8 @@ __global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
       float sm = 0.0f, sx = 0.0f;
       for (int k = 0; k < r; ++k) {
         const float pk = prow[k];
-        sm = fmaf(pk, Rt[k * n + c], sm);
-        sx = fmaf(pk, Qt[k * n + c], sx);
+        sm = fmaf(pk, Rt[k * ldt + c], sm);
+        sx = fmaf(pk, Qt[k * ldt + c], sx);
       }
       const long long off = static_cast<long long>(i0 + t) * n + c;
       const float x = gc != 0.0f ? fmaf(gc, gv[t], xv[t]) : xv[t] * xd;
