@@ -41,6 +41,7 @@ import glob
 import hashlib
 import json
 import math
+import shlex
 import os
 import re
 import sys
@@ -74,8 +75,8 @@ POLICIES = {"rmmc": 0, "always": 1, "never": 2, "every_h": 3}
 # kernel kind -> (kernel-name pattern in the profiler's output, source files);
 # kinds whose kernel template is shared with other kinds have no pattern
 CSRC = os.path.join(ROOT, "paper_2512_13728_amd", "csrc")
-_STREAM = ["k_stream.hip", "common.hpp"]
-_BF = ["k_gemm_bf.hip", "bf16_split.hpp", "mfma_tile.hpp", "common.hpp"]
+_STREAM = ["k_stream.hip", "common.hpp", "plan.hpp"]
+_BF = ["k_gemm_bf.hip", "bf16_split.hpp", "mfma_tile.hpp", "common.hpp", "plan.hpp"]
 KIND_KERNEL = {
     "form_buffer": (r"k_form_buffer<\w+, 0>", _STREAM),
     "form_buffer_local": (r"k_form_buffer<\w+, 1>", _STREAM),
@@ -83,8 +84,8 @@ KIND_KERNEL = {
     "gate": (r"k_gate\b", _STREAM),
     "update_bf16": (r"k_update_pl<1,", _BF),
     "update_bf16x6": (r"k_update_pl<3,", _BF),
-    "update_f32": (r"k_update_vec<", ["k_update_vec.hip", "common.hpp"]),
-    "cholesky_f64": (None, ["k_chol.hip", "mfma_tile.hpp", "common.hpp"]),
+    "update_f32": (r"k_update_vec<", ["k_update_vec.hip", "common.hpp", "plan.hpp"]),
+    "cholesky_f64": (None, ["k_chol.hip", "chol_wave.hpp", "mfma_tile.hpp", "common.hpp", "plan.hpp"]),
 }
 COPY_PATTERN = r"neg_kernel"          # the calibration copy: b = -a, fp32, elementwise
 PMC_PROFILE = os.path.join(ROOT, "profiles", "{workload}_hbm_traffic_pmc.txt")
@@ -152,8 +153,8 @@ def summarize_trace(d: str, bench_json: str, out: str):
     wl = b["config"].get("workload_name", "gpt1p3b")
     lines = [f"# rocprofv3 kernel statistics: {b['config']['workload']}",
              "# commands (from the repository root):",
-             f"#   rocprofv3 --kernel-trace --stats -f csv -d {d} -o bench -- python3 bench.py "
-             f"{WORKLOAD_ARGS.get(wl, '')}> {bench_json}",
+             f"#   rocprofv3 --kernel-trace --stats -f csv -d {d} -o bench -- "
+             f"{b.get('command', 'python3 bench.py ' + WORKLOAD_ARGS.get(wl, '')).strip()} > {bench_json}",
              f"#   python3 bench.py --summarize-trace {d} {bench_json} {out}",
              "# calls include the warmup steps and the untimed profiling pass (the same",
              "# trajectory once more); torch kernels (input generation, state reset)",
@@ -413,7 +414,7 @@ def cpu_baseline(w, n_sync: int, n_local: int, steps: int):
     reps = 0
     t_start = time.perf_counter()
     try:
-        while reps == 0 or (time.perf_counter() - t_start < 10.0 and reps < 5):
+        while reps == 0 or (time.perf_counter() - t_start < 10.0 and reps < 20):
             Ls = [O.OracleLayer.from_arrays(M, X, Q) for (M, X, Q, _, _) in data]
             t0 = time.perf_counter()
             O.group_step(Ls, [d[3] for d in data], w.mu, w.eta, w.tau, policy=O.POLICY_ALWAYS_SYNC)
@@ -729,6 +730,8 @@ def main():
                                    for k, v in kt.items()},
         "rmmc_trace": [None if (isinstance(x, float) and math.isnan(x)) else x for x in rmmcs],
         "cpu_baseline": cpu,
+        # the command line of this run (the profile summaries quote it)
+        "command": " ".join(["python3", "bench.py"] + [shlex.quote(a) for a in sys.argv[1:]]),
     }
     print(json.dumps(out), flush=True)
 

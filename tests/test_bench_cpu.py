@@ -164,3 +164,20 @@ def test_counted_bytes_per_step_by_branch(tmp_path, monkeypatch):
     assert bench.counted_step_bytes("gpt160m") == {}
     monkeypatch.setattr(bench, "source_digest", lambda files: "0000000000000000")
     assert bench.counted_step_bytes("gpt1p3b") == {}
+
+
+def test_kernel_digests_cover_their_includes():
+    """A kind's counted traffic is trusted only while the digest of its
+    source files matches: the list must hold every header its kernel file
+    includes, directly or through other headers."""
+    import re
+    for kind, (_, files) in bench.KIND_KERNEL.items():
+        closure, todo = set(), [files[0]]
+        while todo:
+            f = todo.pop()
+            if f in closure:
+                continue
+            closure.add(f)
+            text = open(os.path.join(bench.CSRC, f)).read()
+            todo += re.findall(r'#include "([^"]+)"', text)
+        assert closure <= set(files), (kind, sorted(closure - set(files)))
