@@ -172,7 +172,7 @@ __device__ __forceinline__ float load_g1(const void* G, bool bf, long long i) {
 }
 
 template <int S, int BN>
-__global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
+__global__ __launch_bounds__(256, 4) void k_update_pl(UpdatePlArgs u) {
   constexpr int TM = 4, TN = BN / 32;   // wave tile 64 x BN/2
   constexpr int PLANE_BYTES = S * (UBM + 2 * BN) * BLD * 2;
   constexpr int SLD = BN + 4;           // padded row of the fp32 accumulator staging tile
@@ -285,16 +285,89 @@ __global__ __launch_bounds__(256) void k_update_pl(UpdatePlArgs u) {
   // 16-byte row segments: M += -(1 - mu) (P R^T), then X += -c (P Q^T).
   float* st = reinterpret_cast<float*>(smem);
   const bool vec = (u.n & 3) == 0;
-#pragma unroll
-  for (int which = 0; which < 2; ++which) {
+  auto dump = [&](const f32x4 (&acc)[TM][TN]) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int v = 0; v < 4; ++v)
-          st[(wm0 + i * 16 + 4 * (lane >> 4) + v) * SLD + wn0 + j * 16 + (lane & 15)] =
-              which == 0 ? am[i][j][v] : ax[i][j][v];
+          st[(wm0 + i * 16 + 4 * (lane >> 4) + v) * SLD + wn0 + j * 16 + (lane & 15)] = acc[i][j][v];
+  };
+  if (vec && m0 + UBM <= u.m && n0 + BN <= u.n && u.n < (1 << 23)) {
+    // Interior tile.  Every load a thread makes (its 8 row segments of M, then
+    // of X) is issued before the first store: a store to M may alias a later
+    // load as far as the compiler knows, so a load-modify-store loop would
+    // keep one 16-byte request per thread in flight and leave the epilogue
+    // bound by memory latency.
+    constexpr int SEGS = BN / 4;                  // 16-byte segments per tile row
+    constexpr int PER = UBM * SEGS / 256;         // per thread and matrix
+    constexpr int RSTEP = 256 / SEGS;             // tile rows between a thread's segments
+    const int row0 = tid / SEGS, c4 = (tid % SEGS) * 4;
+    // tile base (uniform) plus a 32-bit element offset per segment: 128 rows
+    // of any layer this library accepts stay far below 2^31 elements
+    const long long tile0 = static_cast<long long>(__builtin_amdgcn_readfirstlane(m0)) * u.n +
+                            __builtin_amdgcn_readfirstlane(n0);
+    char* const Mt = reinterpret_cast<char*>(u.M[l] + tile0);
+    char* const Xt = reinterpret_cast<char*>(u.X[l] + tile0);
+    unsigned o[PER];   // byte offsets (under 2^32: 128 rows of at most 2^23 columns)
+#pragma unroll
+    for (int i = 0; i < PER; ++i) o[i] = static_cast<unsigned>((row0 + i * RSTEP) * u.n + c4) * 4u;
+    const float* const sr = st + row0 * SLD + c4;
+    nt4 w[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) w[i] = __builtin_nontemporal_load(reinterpret_cast<const nt4*>(Mt + o[i]));
+    dump(am);
+    __syncthreads();
+    nt4 x[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) x[i] = __builtin_nontemporal_load(reinterpret_cast<const nt4*>(Xt + o[i]));
+    const float cm = -u.one_minus_mu;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const float4 a = *reinterpret_cast<const float4*>(sr + i * RSTEP * SLD);
+      nt4 v = w[i];
+      v.x = fmaf(cm, a.x, v.x); v.y = fmaf(cm, a.y, v.y);
+      v.z = fmaf(cm, a.z, v.z); v.w = fmaf(cm, a.w, v.w);
+      __builtin_nontemporal_store(v, reinterpret_cast<nt4*>(Mt + o[i]));
+    }
+    // X: first undo a speculative skip-branch update (X += gc G; that update
+    // already applied the weight decay), else apply the decay
+    const bool spec = (u.spec == 2 ? u.ctl->spec_cur : u.spec) != 0;
+    const float gc = spec ? u.gc[l] : 0.f;
+    if (gc != 0.f) {
+      const void* const G = u.G[l];
+      const bool gbf = u.g_bf16 != 0;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const float4 g = load_g4(G, gbf, tile0 + o[i] / 4);
+        x[i].x = fmaf(gc, g.x, x[i].x); x[i].y = fmaf(gc, g.y, x[i].y);
+        x[i].z = fmaf(gc, g.z, x[i].z); x[i].w = fmaf(gc, g.w, x[i].w);
+      }
+    } else if (!spec) {
+      const float xd = u.xdecay[l];
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        x[i].x *= xd; x[i].y *= xd; x[i].z *= xd; x[i].w *= xd;
+      }
+    }
+    __syncthreads();
+    dump(ax);
+    __syncthreads();
+    const float cx = -u.c;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const float4 a = *reinterpret_cast<const float4*>(sr + i * RSTEP * SLD);
+      nt4 v = x[i];
+      v.x = fmaf(cx, a.x, v.x); v.y = fmaf(cx, a.y, v.y);
+      v.z = fmaf(cx, a.z, v.z); v.w = fmaf(cx, a.w, v.w);
+      __builtin_nontemporal_store(v, reinterpret_cast<nt4*>(Xt + o[i]));
+    }
+    return;
+  }
+#pragma unroll
+  for (int which = 0; which < 2; ++which) {
+    dump(which == 0 ? am : ax);
     __syncthreads();
     float* Y = which == 0 ? u.M[l] : u.X[l];
     const float coef = which == 0 ? -u.one_minus_mu : -u.c;
