@@ -99,12 +99,30 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       }
 }
 
+// Sum of the split-K partials in split order.  16-byte vectors of V
+// elements when the sizes and bases allow (count and stride multiples of V),
+// so that every thread has `splits` vector loads in flight.
 template <typename TP, typename TO>
 __global__ __launch_bounds__(256) void k_reduce(ReduceArgs a) {
   if (skip_launch(a.run_if)) return;
+  constexpr int V = 16 / sizeof(TP);
+  typedef TP vec_t __attribute__((ext_vector_type(V)));
   const int l = blockIdx.y;
   const TP* p = static_cast<const TP*>(a.part[l]);
   TO* o = static_cast<TO*>(a.out[l]);
+  const bool vec = a.count % V == 0 && a.stride % V == 0 &&
+                   (reinterpret_cast<unsigned long long>(p) & 15) == 0 &&
+                   (reinterpret_cast<unsigned long long>(o) & (sizeof(TO) * V - 1)) == 0;
+  if (vec) {
+    const long long nv = a.count / V;
+    for (long long i = blockIdx.x * 256LL + threadIdx.x; i < nv; i += 256LL * gridDim.x) {
+      vec_t s = *reinterpret_cast<const vec_t*>(p + i * V);
+      for (int k = 1; k < a.splits; ++k) s += *reinterpret_cast<const vec_t*>(p + k * a.stride + i * V);
+#pragma unroll
+      for (int c = 0; c < V; ++c) o[i * V + c] = static_cast<TO>(s[c]);
+    }
+    return;
+  }
   for (long long i = blockIdx.x * 256LL + threadIdx.x; i < a.count; i += 256LL * gridDim.x) {
     TP s = p[i];
     for (int k = 1; k < a.splits; ++k) s += p[k * a.stride + i];
@@ -158,7 +176,7 @@ hipError_t launch_gemm(const GemmArgs& g, int nl, GemmKind kind, hipStream_t s) 
 
 hipError_t launch_reduce_splits(const ReduceArgs& a, int nl, bool part64, bool out64, hipStream_t s) {
   if (nl <= 0 || a.count <= 0) return hipSuccess;
-  long long blocks = (a.count + 255) / 256;
+  long long blocks = (a.count / 2 + 255) / 256;   // two or four elements per thread
   if (blocks > 4096) blocks = 4096;
   const dim3 grid(static_cast<unsigned>(blocks), nl);
   if (part64 && out64) hipLaunchKernelGGL((k_reduce<double, double>), grid, dim3(256), 0, s, a);
