@@ -54,7 +54,8 @@ METRIC = "Dion+RMMC optimizer step: params updated/sec/GPU + achieved HBM GB/s"
 PEAK_HBM_GBPS = 8000.0
 PEAK_TFLOPS = {"f64": 78.6, "f32": 157.3, "bf16": 2500.0}
 # bound, MFMA dtype and executed MFMA flops per algorithmic flop, per kernel kind
-# (bf16x6: each fp32 product is formed from six bf16 piece products)
+# (bf16x6: each fp32 product is formed from six bf16 piece products; bf16x9:
+# nine slice products of the exact Gram matrix)
 KIND_BOUND = {
     "form_buffer": ("hbm", None, 1), "form_buffer_local": ("hbm", None, 1),
     "local_update": ("hbm", None, 1), "gate": ("hbm", None, 1),
@@ -66,6 +67,8 @@ KIND_BOUND = {
     "power_bq_bf16x3": ("mfma", "bf16", 3), "power_btp_bf16x3": ("mfma", "bf16", 3),
     "update_bf16": ("hbm", None, 1), "gram_bf16x6": ("mfma", "bf16", 6),
     "apply_bf16x6": ("mfma", "bf16", 6), "trtri_f64": ("mfma", "f64", 1),
+    # exact Gram matrix: nine slice products per fp64-accurate product
+    "gram_bf16x9": ("mfma", "bf16", 9),
     "update_f32": ("hbm", None, 1),
     # small layers: one workgroup per layer, latency-bound; priced against the fp64 peak
     "small_cholqr": ("alu", "f64", 1), "small_update": ("hbm", None, 1),

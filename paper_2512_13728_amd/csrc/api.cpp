@@ -95,12 +95,12 @@ int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk, int pieces 
 // ---- optional per-kernel timing (HIP events on the launch stream) ----------
 enum Kind { K_FORM, K_FORM_X, K_GATE, K_LOCAL, K_PBQ, K_PBQ_BF, K_GRAM, K_GRAM_BF, K_CHOL, K_TRSM, K_TRTRI,
             K_APPLY_BF, K_PBTP, K_PBTP3, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_UPDATE_F32,
-            K_SMALL_QR, K_SMALL_UPD, K_NKINDS };
+            K_SMALL_QR, K_SMALL_UPD, K_GRAM_X, K_NKINDS };
 const char* const kKindName[K_NKINDS] = {
     "form_buffer", "form_buffer_local", "gate", "local_update", "power_bq_f64", "power_bq_bf16x3", "gram_f64",
     "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_f64",
     "power_btp_bf16x3", "reduce_splits", "colnorm", "update_bf16x6", "update_bf16", "update_f32",
-    "small_cholqr", "small_update"};
+    "small_cholqr", "small_update", "gram_bf16x9"};
 static_assert(K_NKINDS <= 32, "the timing mask holds one bit per kind");
 
 // Timing events only measure: recording them without the system-scope fence
@@ -150,7 +150,8 @@ struct cd_layer {
   double* prev = nullptr;       // device, 1 double
   int* rankdef = nullptr;       // device, 1 int
   int* rowok = nullptr;         // device, r_max ints: rows of T whose pivot was not floored
-  double* pa = nullptr;         // m x r_max fp64: P~
+  double* pa = nullptr;         // m x r_max fp64: P~ (bf16-gradient layers: the slice planes
+                                // and exponents of the exact pass-0 Gram matrix)
   float* pb = nullptr;          // m x r_max: P~ after the first CholQR pass
   float* Uf = nullptr;          // r_max^2: inverse Cholesky factor (fp32) for the bf16 apply
   float* P = nullptr;           // m x r_max fp32: the orthonormal P
@@ -331,7 +332,7 @@ LayerLayout layer_layout(int m, int n, int rm) {
   lo.prev = c.put(sizeof(double));
   lo.rankdef = c.put(sizeof(int));
   lo.rowok = c.put(sizeof(int) * R);
-  lo.pa = c.put(sizeof(double) * M * R);
+  lo.pa = c.put(std::max(sizeof(double) * M * R, cd::gram_x_bytes(m, rm)));
   lo.pb = c.put(sizeof(float) * M * R);
   lo.Uf = c.put(sizeof(float) * R * R);
   lo.P = c.put(sizeof(float) * M * R);
@@ -735,13 +736,39 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
                 [&](int j) { return static_cast<void*>(lay(j)->pa); }, part);
   }
   if (stage == 1) {
-    // the pass-0 Gram matrix in fp64: kappa(P~) reaches 1e5-1e6 in these streams
-    if (fast)
-      return gemm(K_GRAM, mr * (r + 1), 4.0 * mr + 8.0 * rr, cd::GemmKind::F64_FROM_F32, r, r, m, false,
-                  r, false, r, true, [&](int j) { return static_cast<const void*>(lay(j)->P); },
-                  [&](int j) { return static_cast<const void*>(lay(j)->P); },
-                  [&](int j) { return static_cast<void*>(lay(j)->W); },
-                  [&](int j) { return static_cast<void*>(lay(j)->gram_part); });
+    // the pass-0 Gram matrix to fp64 accuracy: kappa(P~) reaches 1e5-1e6 in
+    // these streams.  bf16-gradient layers (fp32 P~): exact slice products on
+    // the bf16 MFMA (k_gram.hip), 64 x 64 upper tiles split over K as the fp64
+    // kernel's
+    if (fast) {
+      cd::GramXArgs xa{};
+      xa.m = m; xa.r = r; xa.run_if = run_if;
+      xa.mp = (m + cd::GX_CHUNK - 1) / cd::GX_CHUNK * cd::GX_CHUNK;
+      plan_splits(r, r, m, nl, true, &xa.kchunk, 0, true);
+      xa.kchunk = (xa.kchunk + cd::GX_CHUNK - 1) / cd::GX_CHUNK * cd::GX_CHUNK;
+      xa.splits = (xa.mp + xa.kchunk - 1) / xa.kchunk;
+      xa.split_stride = 1LL * r * r;
+      if (xa.splits > 1) {
+        const size_t need = static_cast<size_t>(xa.splits) * r * r;
+        for (int j = 0; j < nl; ++j)
+          if (need > lay(j)->gram_cap)
+            return fail(CD_ENOMEM, "Gram workspace too small (%zu > %zu doubles)", need, lay(j)->gram_cap);
+      }
+      for (int j = 0; j < nl; ++j) {
+        xa.P[j] = lay(j)->P;
+        xa.S[j] = reinterpret_cast<__bf16*>(lay(j)->pa);
+        xa.E[j] = reinterpret_cast<int*>(reinterpret_cast<char*>(lay(j)->pa) + 6LL * r * xa.mp);
+        xa.C[j] = xa.splits > 1 ? static_cast<void*>(lay(j)->gram_part) : static_cast<void*>(lay(j)->W);
+      }
+      cd_status st = run(g, K_GRAM_X, (10.0 * mr + 8.0 * rr * xa.splits) * nl, mr * (r + 1) * nl, s,
+                         [&] { return cd::launch_gram_x(xa, nl, s); });
+      if (st != CD_OK || xa.splits == 1) return st;
+      cd::ReduceArgs ra{};
+      ra.count = 1LL * r * r; ra.stride = xa.split_stride; ra.splits = xa.splits; ra.run_if = run_if;
+      for (int j = 0; j < nl; ++j) { ra.part[j] = lay(j)->gram_part; ra.out[j] = lay(j)->W; }
+      return run(g, K_REDUCE, static_cast<double>(ra.count) * nl * 8.0 * (xa.splits + 1), 0.0, s,
+                 [&] { return cd::launch_reduce_splits(ra, nl, true, true, s); });
+    }
     return gemm(K_GRAM, mr * (r + 1), 8.0 * mr + 8.0 * rr, cd::GemmKind::F64, r, r, m, false, r, false,
                 r, true, [&](int j) { return static_cast<const void*>(lay(j)->pa); },
                 [&](int j) { return static_cast<const void*>(lay(j)->pa); },

@@ -162,6 +162,30 @@ struct ReduceArgs {
 };
 hipError_t launch_reduce_splits(const ReduceArgs& a, int nl, bool part64, bool out64, hipStream_t s);
 
+// ---- exact Gram matrix of an fp32 panel on the bf16 MFMA (k_gram.hip) -------
+// W = P^T P (r x r, upper 64 x 64 tiles) of P (m x r, row-major): per chunk
+// of GX_CHUNK rows, column exponents E and three bf16 slice planes S
+// (column-major, mp = m rounded up to GX_CHUNK rows per column), then the
+// product, split over K like the GEMMs (fp64 partials, or W itself when
+// splits == 1).
+constexpr int GX_CHUNK = 128;
+struct GramXArgs {
+  int m, mp, r;
+  int splits, kchunk;              // K split (kchunk a multiple of GX_CHUNK)
+  long long split_stride;          // doubles between partials (r * r)
+  const float* P[MAXB];
+  __bf16* S[MAXB];                 // 3 planes of r x mp
+  int* E[MAXB];                    // (mp / GX_CHUNK) x r exponents
+  void* C[MAXB];                   // fp64 W (splits == 1) or partials
+  const int* run_if;
+};
+// bytes of the slice planes and exponents for m x r (16-byte aligned pieces)
+inline size_t gram_x_bytes(long long m, long long r) {
+  const long long mp = (m + GX_CHUNK - 1) / GX_CHUNK * GX_CHUNK;
+  return static_cast<size_t>(6 * r * mp + (4 * r * (mp / GX_CHUNK) + 15) / 16 * 16 + 16);
+}
+hipError_t launch_gram_x(const GramXArgs& a, int nl, hipStream_t s);
+
 // ---- Cholesky of the Gram matrix and triangular solve ------------------------
 // Per-layer workspace pointers (static for the life of a group) for the
 // blocked fp64 Cholesky W = T^T T (T overwrites the upper triangle of W, r x r,
