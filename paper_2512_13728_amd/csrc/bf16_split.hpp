@@ -45,6 +45,15 @@ __device__ __forceinline__ void split_bf16(float v, __bf16 (&p)[S]) {
   }
 }
 
+// A second layout for tiles staged only as whole 16-byte k granules (a
+// quarter-wave storing four consecutive rows): rows of 64 bytes, the four
+// granules XOR-permuted by bits 2-3 of the row.  Such a store, and a fragment
+// read (16 consecutive rows, one granule), each cover all 64 banks once.
+constexpr int BLD64 = BK16;
+__device__ __forceinline__ int lds_off64(int row, int k) {
+  return row * BLD64 + ((((k >> 3) ^ (row >> 2)) & 3) << 3) + (k & 7);
+}
+
 // Store 4 consecutive-k values of one row into the S planes.
 template <int S, int ROWS>
 __device__ __forceinline__ void put4(__bf16* planes, int row, int kq, float v0, float v1, float v2,
@@ -190,6 +199,9 @@ struct Stage {
 // bf16 fragment: lane l owns row (l % 16) and k = 8 (l / 16) .. + 7.
 __device__ __forceinline__ bf16x8 bfrag(const __bf16* plane, int row0, int lane) {
   return *reinterpret_cast<const bf16x8*>(plane + lds_off(row0 + (lane & 15), 8 * (lane >> 4)));
+}
+__device__ __forceinline__ bf16x8 bfrag64(const __bf16* plane, int row0, int lane) {
+  return *reinterpret_cast<const bf16x8*>(plane + lds_off64(row0 + (lane & 15), 8 * (lane >> 4)));
 }
 
 __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {

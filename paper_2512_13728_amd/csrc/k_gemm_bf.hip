@@ -174,19 +174,20 @@ __device__ __forceinline__ float load_g1(const void* G, bool bf, long long i) {
 template <int S, int BN>
 __global__ __launch_bounds__(256, 4) void k_update_pl(UpdatePlArgs u) {
   constexpr int TM = 4, TN = BN / 32;   // wave tile 64 x BN/2
-  constexpr int PLANE_BYTES = S * (UBM + 2 * BN) * BLD * 2;
+  constexpr int PLANE_BYTES = S * (UBM + 2 * BN) * BLD64 * 2;
   constexpr int SLD = BN + 4;           // padded row of the fp32 accumulator staging tile
   constexpr int STAGE_BYTES = UBM * SLD * 4;
   constexpr int SMEM = PLANE_BYTES > STAGE_BYTES ? PLANE_BYTES : STAGE_BYTES;
   constexpr int ROWS = UBM + 2 * BN;    // LDS rows per plane: P, then R, then Q
-  // the R and Q regions start at multiples of 64 rows, so the swizzle of
-  // lds_off agrees between plane rows (stores) and region rows (bfrag)
-  static_assert(UBM % 64 == 0 && BN % 64 == 0, "region offsets must be multiples of 64 rows");
+  // the R and Q regions start at multiples of 4 rows, so the swizzle of
+  // lds_off64 agrees between plane rows (stores) and region rows (bfrag64)
+  static_assert(UBM % 4 == 0 && BN % 4 == 0, "region offsets must be multiples of 4 rows");
   constexpr int CHUNKS = S * ROWS * (BK16 / 8);   // 16-byte chunks per stage
-  constexpr int CPT = (CHUNKS + 255) / 256;
+  constexpr int CPT = CHUNKS / 256;
+  static_assert(CHUNKS % 256 == 0, "whole chunks per thread");
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   if (u.ctl != nullptr && u.ctl->flag == 0) return;   // not a sync step
-  __bf16* Ls = reinterpret_cast<__bf16*>(smem);   // [S][ROWS][BLD]
+  __bf16* Ls = reinterpret_cast<__bf16*>(smem);   // [S][ROWS][BLD64]
   const int l = blockIdx.z;
   const int tiles_n = (u.n + BN - 1) / BN;
   const int tiles_m = (u.m + UBM - 1) / UBM;
@@ -202,75 +203,64 @@ __global__ __launch_bounds__(256, 4) void k_update_pl(UpdatePlArgs u) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 64, wn0 = (wave & 1) * (BN / 2);
   const long long pP = static_cast<long long>(u.m) * u.rp, pN = static_cast<long long>(u.n) * u.rp;
-  // copy what the lambdas need out of the argument struct (taking the address
-  // of the by-value kernel argument would force it into scratch memory)
-  const __bf16* const gP = u.P[l];
-  const __bf16* const gR = u.R[l];
-  const __bf16* const gQ = u.Q[l];
-  const int um = u.m, un = u.n, urp = u.rp;
 
-  // chunk c -> (plane s, LDS row, 8-element k group)
-  auto chunk_src = [&](int c, int k0, bool& ok) -> const uint4* {
-    const int s = c / (ROWS * 4), rem = c - s * ROWS * 4;
-    const int row = rem >> 2, kg = (rem & 3) * 8;
+  // The thread's chunks: chunk i is row (tid / 4) + 64 (i % 4) of the stage's
+  // rows [P | R | Q] in plane i / 4, 8 k values from 8 (tid % 4).  Its source
+  // is a base that is uniform over the workgroup plus a 32-bit byte offset
+  // (rows past m (P) or n (R, Q) read the last row instead: they only reach
+  // outputs past the matrix, which are not written); its LDS slot is one
+  // per-thread offset plus a constant.
+  static_assert(ROWS == 256, "four 64-row groups per plane");
+  const int crow = tid >> 2, kg = (tid & 3) * 8;
+  const char* bp[CPT];
+  unsigned off[CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int s = i / 4, row = crow + 64 * (i % 4);
     const __bf16* base;
-    int grow, lim;
-    if (row < UBM) { base = gP + s * pP; grow = m0 + row; lim = um; }
-    else if (row < UBM + BN) { base = gR + s * pN; grow = n0 + row - UBM; lim = un; }
-    else { base = gQ + s * pN; grow = n0 + row - UBM - BN; lim = un; }
-    ok = grow < lim;
-    return reinterpret_cast<const uint4*>(base + static_cast<long long>(ok ? grow : 0) * urp + k0 + kg);
-  };
-  uint4 pre[CPT];
-  auto load = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + i * 256;
-      uint4 v = {0u, 0u, 0u, 0u};
-      if (c < CHUNKS) {
-        bool ok;
-        const uint4* p = chunk_src(c, k0, ok);
-        if (ok) v = *p;
-      }
-      pre[i] = v;
-    }
-  };
-  auto store = [&]() {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + i * 256;
-      if (c < CHUNKS) {
-        const int s = c / (ROWS * 4), rem = c - s * ROWS * 4;
-        *reinterpret_cast<uint4*>(Ls + s * ROWS * BLD + lds_off(rem >> 2, (rem & 3) * 8)) = pre[i];
-      }
-    }
-  };
-
+    int grow;
+    if (row < UBM) { base = u.P[l] + s * pP; grow = min(m0 + row, u.m - 1); }
+    else if (row < UBM + BN) { base = u.R[l] + s * pN; grow = min(n0 + row - UBM, u.n - 1); }
+    else { base = u.Q[l] + s * pN; grow = min(n0 + row - UBM - BN, u.n - 1); }
+    bp[i] = reinterpret_cast<const char*>(base);
+    off[i] = static_cast<unsigned>((grow * u.rp + kg) * 2);
+  }
+  const int slot0 = lds_off64(crow, kg);   // + (s * ROWS + 64 (i % 4)) * BLD64 for chunk i
+  // native vectors (the HIP uint4 struct would keep the array in scratch memory)
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 pre[CPT];
   f32x4 am[TM][TN], ax[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) { am[i][j] = f32x4{}; ax[i][j] = f32x4{}; }
 
-  load(0);
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) pre[i] = *reinterpret_cast<const u32x4*>(bp[i] + off[i]);
   for (int k0 = 0; k0 < u.rp; k0 += BK16) {
-    store();
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+      *reinterpret_cast<u32x4*>(Ls + slot0 + ((i / 4) * ROWS + 64 * (i % 4)) * BLD64) = pre[i];
     __syncthreads();
-    if (k0 + BK16 < u.rp) load(k0 + BK16);
+    if (k0 + BK16 < u.rp) {
+      const unsigned kb = static_cast<unsigned>((k0 + BK16) * 2);
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) pre[i] = *reinterpret_cast<const u32x4*>(bp[i] + off[i] + kb);
+    }
 #pragma unroll
     for (int sum = S - 1; sum >= 0; --sum)
 #pragma unroll
       for (int p = 0; p <= sum; ++p) {
-        const __bf16* Pp = Ls + p * ROWS * BLD;
-        const __bf16* Rq = Ls + ((sum - p) * ROWS + UBM) * BLD;
-        const __bf16* Qq = Rq + BN * BLD;
+        const __bf16* Pp = Ls + p * ROWS * BLD64;
+        const __bf16* Rq = Ls + ((sum - p) * ROWS + UBM) * BLD64;
+        const __bf16* Qq = Rq + BN * BLD64;
         bf16x8 a[TM];
 #pragma unroll
-        for (int i = 0; i < TM; ++i) a[i] = bfrag(Pp, wm0 + i * 16, lane);
+        for (int i = 0; i < TM; ++i) a[i] = bfrag64(Pp, wm0 + i * 16, lane);
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          const bf16x8 rb = bfrag(Rq, wn0 + j * 16, lane);
-          const bf16x8 qb = bfrag(Qq, wn0 + j * 16, lane);
+          const bf16x8 rb = bfrag64(Rq, wn0 + j * 16, lane);
+          const bf16x8 qb = bfrag64(Qq, wn0 + j * 16, lane);
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             am[i][j] = mfma_bf16(a[i], rb, am[i][j]);

@@ -123,23 +123,15 @@ __global__ __launch_bounds__(256) void k_slice(GramXArgs a) {
   }
 }
 
-// LDS layout of a staged 64 x 32 slice tile: rows (columns of P~) of 64
-// bytes, the four 16-byte k granules XOR-permuted by bits 2-3 of the row.
-// A fragment read (16 lanes: 16 consecutive rows, one granule) and a staging
-// store (16 lanes: 4 consecutive rows, all four granules) then each cover all
-// 64 banks once.
-__device__ __forceinline__ int gx_off(int row, int k) {
-  return row * BK16 + ((((k >> 3) ^ (row >> 2)) & 3) << 3) + (k & 7);
-}
-
 // 32-row fragment of a 32x32x16 MFMA: lane l owns row (l % 32) and
 // k = 16 h + 8 (l / 32) .. + 7.
 __device__ __forceinline__ bf16x8 frag32(const __bf16* plane, int row0, int h, int lane) {
-  return *reinterpret_cast<const bf16x8*>(plane + gx_off(row0 + (lane & 31), 16 * h + 8 * (lane >> 5)));
+  return *reinterpret_cast<const bf16x8*>(plane + lds_off64(row0 + (lane & 31), 16 * h + 8 * (lane >> 5)));
 }
 
 __global__ __launch_bounds__(256, 2) void k_gram_x(GramXArgs a) {
-  // LDS: [operand A|B][slice][64 rows][32 k]
+  // LDS: [operand A|B][slice][64 rows][32 k], rows as lds_off64 lays them out
+  // (a staging store and a fragment read each cover the 64 banks once)
   __shared__ __attribute__((aligned(16))) __bf16 Ls[2 * 3 * 64 * BK16];
   __shared__ int es[2][64];
   if (skip_launch(a.run_if)) return;
@@ -173,7 +165,7 @@ __global__ __launch_bounds__(256, 2) void k_gram_x(GramXArgs a) {
   }
 #pragma unroll
   for (int u = 0; u < 6; ++u) base[u] = reinterpret_cast<const char*>(a.S[l] + (u % 3) * plane);
-  const int soff = gx_off(c, pc * 8);
+  const int soff = lds_off64(c, pc * 8);
   uint4 p0, p1, p2, p3, p4, p5;   // the next stage's pieces
 #define GX_LOAD(step)                                                                                     \
   do {                                                                                                    \
