@@ -216,7 +216,11 @@ constexpr int SUP_THREADS = 256;
 // band's M, X (and G) rows, the band's rows of P, and R.  R and Q are held
 // transposed in LDS (k-major, row stride n + 1), so that the lanes of a wave,
 // which own consecutive columns c, read consecutive words, and the
-// transposing stores of consecutive k fall into different banks.
+// transposing stores of consecutive k fall into different banks.  The
+// products: a thread takes its column of R and Q into registers once, then
+// forms the band's rows together (k outer, rows inner, each sum in k order),
+// reading P as broadcasts from LDS.
+template <int NR>
 __global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
   __shared__ float Rt[SMALL_MR + SMALL_R];
   __shared__ float Qt[SMALL_MR + SMALL_R];
@@ -289,20 +293,37 @@ __global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
   __syncthreads();
   for (int c = tid; c < n; c += SUP_THREADS) {
     if (c != tid) load_column(c);
+    constexpr int KB = NR < 32 ? NR : 32;   // k values of R and Q held at a time
+    float sm[SMALL_ROWS], sx[SMALL_ROWS];
+#pragma unroll
+    for (int t = 0; t < SMALL_ROWS; ++t) { sm[t] = 0.0f; sx[t] = 0.0f; }
+#pragma unroll
+    for (int k0 = 0; k0 < NR; k0 += KB) {
+      if (k0 >= r) break;
+      float rc[KB], qc[KB];
+#pragma unroll
+      for (int k = 0; k < KB; ++k) {
+        rc[k] = k0 + k < r ? Rt[(k0 + k) * ldt + c] : 0.0f;
+        qc[k] = k0 + k < r ? Qt[(k0 + k) * ldt + c] : 0.0f;
+      }
+#pragma unroll
+      for (int k = 0; k < KB; ++k) {
+        if (k0 + k >= r) break;
+#pragma unroll
+        for (int t = 0; t < SMALL_ROWS; ++t) {
+          const float pk = t < rows ? Pb[t * r + k0 + k] : 0.0f;
+          sm[t] = fmaf(pk, rc[k], sm[t]);
+          sx[t] = fmaf(pk, qc[k], sx[t]);
+        }
+      }
+    }
 #pragma unroll
     for (int t = 0; t < SMALL_ROWS; ++t) {
       if (t >= rows) break;
-      const float* prow = Pb + t * r;
-      float sm = 0.0f, sx = 0.0f;
-      for (int k = 0; k < r; ++k) {
-        const float pk = prow[k];
-        sm = fmaf(pk, Rt[k * ldt + c], sm);
-        sx = fmaf(pk, Qt[k * ldt + c], sx);
-      }
       const long long off = static_cast<long long>(i0 + t) * n + c;
       const float x = gc != 0.0f ? fmaf(gc, gv[t], xv[t]) : xv[t] * xd;
-      Mo[off] = fmaf(cm, sm, mv[t]);
-      Xo[off] = fmaf(cx, sx, x);
+      Mo[off] = fmaf(cm, sm[t], mv[t]);
+      Xo[off] = fmaf(cx, sx[t], x);
     }
   }
 }
@@ -326,7 +347,9 @@ hipError_t launch_small_update(const SmallUpdArgs& a, int nl, hipStream_t s) {
   if (nl <= 0) return hipSuccess;
   if (!small_sync_fits(a.m, a.n, a.r) || (a.spec == 2 && !a.ctl)) return hipErrorInvalidValue;
   const dim3 grid((a.m + SMALL_ROWS - 1) / SMALL_ROWS, nl);
-  hipLaunchKernelGGL(k_small_update, grid, dim3(SUP_THREADS), 0, s, a);
+  if (a.r <= 16) hipLaunchKernelGGL(k_small_update<16>, grid, dim3(SUP_THREADS), 0, s, a);
+  else if (a.r <= 32) hipLaunchKernelGGL(k_small_update<32>, grid, dim3(SUP_THREADS), 0, s, a);
+  else hipLaunchKernelGGL(k_small_update<64>, grid, dim3(SUP_THREADS), 0, s, a);
   return hipGetLastError();
 }
 
