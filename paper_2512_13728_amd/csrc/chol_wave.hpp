@@ -52,6 +52,31 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// use(i, load(i)) for i = 0 .. N - 1, the loads in chunks of up to CHUNK:
+// chunk c + 1 is requested before chunk c is used (the compiler may not move
+// loads or uses across the scheduling barriers), so the values in flight
+// never exceed two chunks' registers.
+template <int N, int CHUNK = 16, class Load, class Use>
+__device__ __forceinline__ void chunked(Load&& load, Use&& use) {
+  constexpr int NC = (N + CHUNK - 1) / CHUNK;
+  if constexpr (N > 0) {
+    double buf[2][CHUNK];
+    static_for<NC + 1>([&](auto cc) {
+      constexpr int C = decltype(cc)::value;
+      if constexpr (C < NC) {
+#pragma unroll
+        for (int i = 0; i < CHUNK && C * CHUNK + i < N; ++i) buf[C & 1][i] = load(C * CHUNK + i);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (C > 0) {
+#pragma unroll
+        for (int i = 0; i < CHUNK && (C - 1) * CHUNK + i < N; ++i) use((C - 1) * CHUNK + i, buf[(C - 1) & 1][i]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  }
+}
+
 template <int NB>
 struct WaveChol {
   static_assert(NB == 16 || NB == 32 || NB == 64, "block of 16, 32 or 64 columns");
@@ -118,13 +143,11 @@ struct WaveChol {
       wave_sync();
       // rows below p: A[p + i][j] -= T[p][p + i] T[p][j], shifted up one row;
       // lanes j < p + i only touch the (unused) lower triangle.  The row is
-      // read whole before the update (one LDS round trip, not one per pair).
-      double rv[NA];
-#pragma unroll
-      for (int i = 1; i < NA; ++i) rv[i] = s.rowb[p + i];
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 1; i < NA; ++i) a[i - 1] = fma(-rv[i], tp, a[i]);
+      // read in chunks, each requested before the previous one is used, so
+      // that one LDS round trip is exposed per pivot and at most two chunks
+      // are held.
+      chunked<NA - 1>([&](int i) { return s.rowb[p + 1 + i]; },
+                      [&](int i, double v) { a[i] = fma(-v, tp, a[i + 1]); });
       a[NA - 1] = 0.0;
       wave_sync();
     };
@@ -156,12 +179,8 @@ struct WaveChol {
       const double x = f[0] * s.pinv[p];
       put(p, cin ? x : 0.0);
       const double* col = T + p * TLD + p;   // col[-k] = T[p - k][p]
-      double cv[NF];
-#pragma unroll
-      for (int k = 1; k < NF; ++k) cv[k] = col[-k];
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int k = 1; k < NF; ++k) f[k - 1] = fma(-cv[k], x, f[k]);
+      chunked<NF - 1>([&](int k) { return col[-1 - k]; },
+                      [&](int k, double v) { f[k] = fma(-v, x, f[k + 1]); });
       f[NF - 1] = 0.0;
     };
     // segments from the last down: segment g carries (g + 1) SEG entries

@@ -27,7 +27,7 @@ using Wave64 = WaveChol<CB>;
 
 // One wave per layer: the factorisation of the diagonal block (chol_wave.hpp)
 // and its inverse D_k; T_kk goes back over W_kk.
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
+__global__ __launch_bounds__(64) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
                                                   int pass, const int* run_if) {
   __shared__ __attribute__((aligned(16))) Wave64::Lds lds;
   if (skip_launch(run_if)) return;
@@ -212,9 +212,14 @@ template <typename TIn, typename TOut, bool IDENT>
 __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, const int2* __restrict__ tiles,
                                               int r, int cb, int mlimit, const int* run_if) {
   constexpr int YLD = CB + 4;
-  __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
+  // Y takes the A tile's place once the first product is done (52 KB in all
+  // instead of 70: the workgroup then fits where one workgroup of the
+  // concurrently running update or product kernels left)
+  constexpr int AY = tile_elems<CB>() > CB * YLD ? tile_elems<CB>() : CB * YLD;
+  __shared__ __attribute__((aligned(16))) double AYs[AY];
   __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
-  __shared__ __attribute__((aligned(16))) double Ys[CB * YLD];
+  double* const As = AYs;
+  double* const Ys = AYs;
   if (skip_launch(run_if)) return;
   const int2 lt = tiles[blockIdx.x];
   const TrsmTab t = tab[lt.x];
