@@ -284,7 +284,7 @@ def summarize_pmc(fdir: str, wdir: str, out: str, workload: str, cal_mib: int):
              f"-- python3 bench.py {WORKLOAD_ARGS.get(workload, '')}--no-cpu-baseline --copy-calibration {cal_mib}",
              f"#   rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'cd::|neg_kernel' -f csv -d {wdir} -o pmc "
              f"-- python3 bench.py {WORKLOAD_ARGS.get(workload, '')}--no-cpu-baseline --copy-calibration {cal_mib}",
-             f"#   python3 bench.py --summarize-pmc {fdir} {wdir} {out} --copy-calibration {cal_mib}",
+             f"#   python3 bench.py {_wl_flag(workload)}--summarize-pmc {fdir} {wdir} {out} --copy-calibration {cal_mib}",
              f"# calibration: a streaming copy (b = -a, fp32) of {cal_bytes} B read + {cal_bytes} B written;",
              f"#   FETCH_SIZE x {factor['FETCH_SIZE']:.4f} and WRITE_SIZE x {factor['WRITE_SIZE']:.4f} give bytes",
              "# all dispatches of the run (warmup steps, profiling pass, timed pass); bytes are scaled, per dispatch", "",
@@ -337,6 +337,11 @@ def counted_step_bytes(workload: str):
 
 N_CU, N_XCD, SIMD_PER_CU = 256, 8, 4
 # the bench arguments that select each profiled workload (default: the 1.3B set)
+def _wl_flag(workload: str) -> str:
+    """The --workload option a summarising command needs (none for the default)."""
+    return "" if workload == "gpt1p3b" else f"--workload {workload} "
+
+
 WORKLOAD_ARGS = {"gpt1p3b": "", "gpt160m": "--workload gpt160m --steps 50 ",
                  "mixed1p3b": "--workload mixed1p3b --steps 200 ", "single256": "--workload single256 "}
 
@@ -362,7 +367,7 @@ def summarize_mfma(d: str, out: str, workload: str):
              f"#   rocprofv3 --pmc {' '.join(counters)} --kernel-include-regex 'cd::' -f csv -d {d} -o pmc "
              f"-- python3 bench.py {WORKLOAD_ARGS.get(workload, '')}--no-cpu-baseline --steps 2 --warmup 1 "
              "--policy always",
-             f"#   python3 bench.py --summarize-mfma {d} {out}",
+             f"#   python3 bench.py {_wl_flag(workload)}--summarize-mfma {d} {out}",
              f"# mfma_busy = SQ_VALU_MFMA_BUSY_CYCLES / ({N_CU * SIMD_PER_CU} SIMDs x GRBM_GUI_ACTIVE / {N_XCD} XCDs):",
              "# the fraction of the kernel's cycles in which an average SIMD's matrix unit was busy", "",
              f"{'kernel':64s} {'disp':>5s} {'cycles/disp':>12s} {'mfma_busy':>10s}"]
