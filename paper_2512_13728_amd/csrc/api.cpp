@@ -646,7 +646,11 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
       ga.C[j] = ga.splits > 1 ? Pof(j) : Cof(j);
     }
     cd_status st2 = run(g, tkind, bytes * nl, flops * nl, s, [&] {
-      return pieces > 0 ? cd::launch_gemm_bf(ga, nl, pieces, s) : cd::launch_gemm(ga, nl, kind, s);
+      if (pieces > 0) return cd::launch_gemm_bf(ga, nl, pieces, s);
+      // P~ = B Q of small layers: every operand straight into registers
+      if (small && kind == cd::GemmKind::F64_FROM_F32 && a_kc && cd::small_gemm_fits(Nr, K))
+        return cd::launch_small_gemm(ga, nl, kind, s);
+      return cd::launch_gemm(ga, nl, kind, s);
     });
     if (st2 != CD_OK) return st2;
     if (ga.splits > 1) {

@@ -160,6 +160,73 @@ struct WaveChol {
     return def;
   }
 
+  // factor() with T^{-1} formed in the same pivot loop (NB <= 32): lanes NB ..
+  // 2 NB - 1 hold the columns of the identity and undergo the same row
+  // operations.  With W = T^T T, the elimination that turns W into T turns I
+  // into E = T^{-T}: at pivot p, row p of E is final once scaled by
+  // 1 / sqrt(d), and every row i > p takes E[i][c] -= T[p][i] E[p][c] /
+  // sqrt(d), the update the W columns take.  Row p of E, i.e. column p of
+  // T^{-1}, is zero for a floored pivot, as inverse() returns it.
+  // put_inv(c, p, x): x = (T^{-1})[c][p] for c < NB, p < nb.  Replaces
+  // inverse() and its nb back-substitution steps.
+  template <class Load, class PutInv>
+  __device__ static bool factor_inv(Lds& s, int j, int nb, double fl, Load&& load, PutInv&& put_inv) {
+    static_assert(NB <= 32, "two columns per lane pair: the block and the identity");
+    const bool lane_in = j < NB;
+    const bool lane_e = j >= NB && j < 2 * NB;
+    const int c = j - NB;                 // identity column of an E lane
+    double* const T = Ts(s);
+    double a[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      if (lane_in) {
+        if (i < nb && j < nb) a[i] = i <= j ? load(i) : 0.0;
+        else a[i] = i == j ? 1.0 : 0.0;
+      } else {
+        a[i] = (lane_e && i == c && c < nb) ? 1.0 : 0.0;
+      }
+    }
+    if (lane_in) {
+      s.rowb[NB + j] = 0.0;
+      s.Tsb[j] = 0.0;
+    }
+    bool def = false;
+    auto pivot = [&](auto na, int p) {
+      constexpr int NA = decltype(na)::value;
+      const double a0 = a[0];
+      double d = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(a0), p),
+                                  __builtin_amdgcn_readlane(__double2loint(a0), p));
+      const bool floored = !(d > fl);
+      if (floored) { d = fl; def = true; }
+      double inv = __builtin_amdgcn_rsq(d);
+#pragma unroll
+      for (int it = 0; it < 2; ++it) inv = fma(inv, fma(-0.5 * d * inv, inv, 0.5), inv);
+      const double piv = d * inv;
+      // row p of T (block lanes) or of E (identity lanes)
+      const double tp = lane_in ? (j == p ? piv : (j > p && !floored ? a[0] * inv : 0.0))
+                                : (floored ? 0.0 : a[0] * inv);
+      if (lane_in) T[j * TLD + p] = tp;
+      if (lane_e) put_inv(c, p, tp);
+      if (j == p) {
+        s.pinv[p] = inv;
+        s.okb[p] = floored ? 0 : 1;
+      }
+      wave_sync();
+      if (lane_in) s.rowb[j] = tp;
+      wave_sync();
+      chunked<NA - 1>([&](int i) { return s.rowb[p + 1 + i]; },
+                      [&](int i, double v) { a[i] = fma(-v, tp, a[i + 1]); });
+      a[NA - 1] = 0.0;
+      wave_sync();
+    };
+    static_for<NB / SEG>([&](auto gc) {
+      constexpr int G = decltype(gc)::value;
+#pragma unroll 1
+      for (int p = G * SEG; p < min(nb, (G + 1) * SEG); ++p) pivot(std::integral_constant<int, NB - G * SEG>{}, p);
+    });
+    return def;
+  }
+
   // Lane j (< nb) computes column j of T^{-1} after factor(): put(p, x) with
   // x = (T^{-1})[p][j] for p = nb - 1 down to 0, x = 0 in the column of a
   // floored pivot (with row p of T zero right of the diagonal, column j != p

@@ -272,6 +272,10 @@ struct SmallQrArgs {               // CholQR twice, one workgroup per layer
   const int* run_if;
 };
 hipError_t launch_small_cholqr(const SmallQrArgs& a, int nl, hipStream_t s);
+// C = A B for P~ = B Q of small layers (no split-K): kind F64_FROM_F32, A
+// k-contiguous, B row-major (b_kc false), N <= SMALL_R, K <= 1024.
+bool small_gemm_fits(int N, int K);
+hipError_t launch_small_gemm(const GemmArgs& g, int nl, GemmKind kind, hipStream_t s);
 struct SmallUpdArgs {              // column norms, Q and the M / X update
   int m, n, r;
   float one_minus_mu;

@@ -132,11 +132,18 @@ __global__ __launch_bounds__(SQR_THREADS) void k_small_cholqr(SmallQrArgs a) {
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) md = fmax(md, __shfl_xor(md, o, 64));
       const double fl = fmax(1e-13 * md, 1e-60);
-      // factor() holds W in registers once it starts, so T^-1 may go over it
-      const bool def = WC::factor(wc, j, r, fl, [&](int i) { return Wl[i * NB + j]; });
-      WC::inverse(wc, j, r, [&](int p, double x) {
-        if (j < r) Wl[p * NB + j] = x;
-      });
+      // the factorisation holds W in registers once it starts, so T^-1 may
+      // go over it (NB <= 32: formed in the factorisation's own pivot loop)
+      bool def;
+      if constexpr (NB <= 32) {
+        def = WC::factor_inv(wc, j, r, fl, [&](int i) { return Wl[i * NB + j]; },
+                             [&](int c, int p, double x) { Wl[c * NB + p] = x; });
+      } else {
+        def = WC::factor(wc, j, r, fl, [&](int i) { return Wl[i * NB + j]; });
+        WC::inverse(wc, j, r, [&](int p, double x) {
+          if (j < r) Wl[p * NB + j] = x;
+        });
+      }
       if (j == 0) floored = def ? 1 : 0;
     }
     __syncthreads();
@@ -206,6 +213,90 @@ __global__ __launch_bounds__(SQR_THREADS) void k_small_cholqr(SmallQrArgs a) {
   if (tid == 0) {
     *a.rankdef[l] = any_dead ? 1 : 0;
     if (a.rankdef_host[l]) *a.rankdef_host[l] = any_dead ? 1 : 0;
+  }
+}
+
+// P~ = B Q of small layers (N = r <= 64, K = n <= 1024; A = B fp32
+// row-major, B = Q fp32, C fp64) on the fp64 MFMA: one workgroup per 16 rows
+// of C, the four waves taking a quarter of K each, every operand loaded
+// straight into registers (a wave's whole K range in at most two rounds of
+// loads, the second requested before the first is used), and the four
+// partial tiles added in wave order through LDS.  At these sizes the blocked
+// kernel's K loop is a chain of memory latencies, one per stage: 256 x 256,
+// r = 16 took 10.2 us there and takes 7.6 here.  (For R = B^T P, whose A
+// operand is not k-contiguous, the same scheme measured 10.6 us against the
+// blocked kernel's 9.3, which therefore stays.)
+constexpr int SG_KMAX = 1024;
+template <typename TB, typename TC, bool A_KC, int NT>
+__global__ __launch_bounds__(256) void k_small_gemm(GemmArgs g) {
+  constexpr int D = 4 / NT;              // 16-k chunks per round of loads
+  constexpr int NC = NT * 16;
+  __shared__ double red[4][16][NC + 1];
+  if (skip_launch(g.run_if)) return;
+  const int l = blockIdx.y, row0 = blockIdx.x * 16;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* __restrict__ A = static_cast<const float*>(g.A[l]);
+  const TB* __restrict__ B = static_cast<const TB*>(g.B[l]);
+  // the wave's K range: a quarter of K, rounded up to 16
+  const int kw = (g.K + 63) / 64 * 16;
+  const int kw0 = wave * kw, kw1 = min(g.K, kw0 + kw);
+  // MFMA operand of lane l for the q-th product of a 16-k chunk at k0: row
+  // (or column) l % 16, k = k0 + 4 (l / 16) + q
+  const int ri = lane & 15, kl = 4 * (lane >> 4);
+  const int row = row0 + ri;
+  f64x4 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = f64x4{};
+  double a[2][D][4], b[2][D][NT][4];
+  auto load = [&](int buf, int kb) {
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int k = kb + 16 * d + kl + q;
+        const bool kin = k < kw1;
+        a[buf][d][q] = (kin && row < g.M)
+                           ? static_cast<double>(A_KC ? A[static_cast<long long>(row) * g.lda + k]
+                                                      : A[static_cast<long long>(k) * g.lda + row])
+                           : 0.0;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const int c = t * 16 + ri;
+          b[buf][d][t][q] = (kin && c < g.N) ? static_cast<double>(B[static_cast<long long>(k) * g.ldb + c]) : 0.0;
+        }
+      }
+  };
+  auto mult = [&](int buf) {
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[buf][d][q], b[buf][d][t][q], acc[t], 0, 0, 0);
+  };
+  constexpr int KR = 16 * D;             // k per round
+  if (kw0 < kw1) load(0, kw0);
+  if (kw0 + KR < kw1) load(1, kw0 + KR);
+  for (int kb = kw0; kb < kw1; kb += 2 * KR) {
+    mult(0);
+    if (kb + 2 * KR < kw1) load(0, kb + 2 * KR);
+    if (kb + KR < kw1) {
+      mult(1);
+      if (kb + 3 * KR < kw1) load(1, kb + 3 * KR);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) red[wave][Mfma<double>::out_row(lane, v)][t * 16 + ri] = acc[t][v];
+  __syncthreads();
+  TC* __restrict__ C = static_cast<TC*>(g.C[l]);
+  for (int e = tid; e < 16 * NC; e += 256) {
+    const int i = e / NC, c = e - i * NC;
+    if (row0 + i < g.M && c < g.N)
+      C[static_cast<long long>(row0 + i) * g.ldc + c] =
+          static_cast<TC>(((red[0][i][c] + red[1][i][c]) + red[2][i][c]) + red[3][i][c]);
   }
 }
 
@@ -332,6 +423,24 @@ __global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
 
 bool small_sync_fits(int m, int n, int r) {
   return r >= 1 && r <= SMALL_R && 1LL * m * r <= SMALL_MR && 1LL * n * r <= SMALL_MR;
+}
+
+template <typename TB, typename TC, bool A_KC>
+hipError_t launch_sg(const GemmArgs& g, int nl, hipStream_t s) {
+  const dim3 grid((g.M + 15) / 16, nl);
+  if (g.N <= 16) hipLaunchKernelGGL((k_small_gemm<TB, TC, A_KC, 1>), grid, dim3(256), 0, s, g);
+  else if (g.N <= 32) hipLaunchKernelGGL((k_small_gemm<TB, TC, A_KC, 2>), grid, dim3(256), 0, s, g);
+  else hipLaunchKernelGGL((k_small_gemm<TB, TC, A_KC, 4>), grid, dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+bool small_gemm_fits(int N, int K) { return N >= 1 && N <= SMALL_R && K >= 1 && K <= SG_KMAX; }
+
+hipError_t launch_small_gemm(const GemmArgs& g, int nl, GemmKind kind, hipStream_t s) {
+  if (nl <= 0) return hipSuccess;
+  if (!small_gemm_fits(g.N, g.K) || g.splits != 1 || g.b_kc) return hipErrorInvalidValue;
+  if (kind == GemmKind::F64_FROM_F32 && g.a_kc) return launch_sg<float, double, true>(g, nl, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_small_cholqr(const SmallQrArgs& a, int nl, hipStream_t s) {
