@@ -714,11 +714,12 @@ def main():
             "workload_name": w.name,
             "params": w.params, "rank": w.r, "grad_dtype": w.grad_dtype, "state_dtype": "f32",
             "power_iteration_dtype": ("P~ = BQ and R = B^T P on bf16 MFMA with 2-piece fp32 splits "
-                                      "(3 products, ~2^-16 relative); CholQR2 pass 0 Gram + Cholesky in fp64, pass 1 "
-                                      "fp32-accurate (bf16 x 6); M/X update bf16 products, fp32 "
-                                      "accumulation" if w.grad_dtype == "bf16" else
-                                      "P~ = BQ, Gram and CholQR in fp64; R and the M/X update on bf16 "
-                                      "MFMA with 3-piece fp32 splits"),
+                                      "(3 products, ~2^-16 relative); CholQR2 pass 0: Gram exact to fp64 "
+                                      "accumulation (3 bf16 slices per value, 9 products on bf16 MFMA) and "
+                                      "Cholesky in fp64, pass 1 fp32-accurate (bf16 x 6); M/X update bf16 "
+                                      "products, fp32 accumulation" if w.grad_dtype == "bf16" else
+                                      "P~ = BQ, R = B^T P, Gram and CholQR in fp64; the M/X update on bf16 "
+                                      "MFMA with 3-piece fp32 splits (fp32 vector units at r <= 32)"),
             "policy": args.policy + (f" (H = {args.H})" if args.policy == "every_h" else ""),
             "steps_mode": "asynchronous (no host read per step)" if asyn else "blocking (gate read per step)",
             "tau": w.tau, "trajectory_steps": K,
