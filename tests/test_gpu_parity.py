@@ -194,13 +194,14 @@ def test_zero_buffer_sync_is_defined():
 
 
 @pytest.mark.parametrize("gd", ["f32", "bf16"])
-@pytest.mark.parametrize("m,n,r,k", [(192, 160, 96, 5), (96, 80, 48, 5)])
+@pytest.mark.parametrize("m,n,r,k", [(192, 160, 96, 5), (96, 80, 48, 5), (64, 80, 24, 5), (48, 40, 12, 3)])
 def test_rank_deficient_buffer_is_completed(gd, m, n, r, k):
     """B of exact rank k < r (only its first k rows are nonzero, in either
     gradient dtype) on a sync step: P~ = B Q has rank k, so r - k pass-0
     Cholesky pivots fall under the floor: in both 64-column blocks of r = 96
     (the blocked factorisation), and in the one-workgroup factorisation of a
-    small layer (r = 48).
+    small layer (r = 48: T^-1 by back substitution; r = 24 and 12: T^-1 formed
+    in the pivot loop by the identity's columns).
     Like a Householder QR factor, P still has orthonormal columns: the first k
     are unique and match the oracle (as do those of R and Q, and M = mu B),
     the others complete the basis orthogonally to B's column space (so the
