@@ -346,8 +346,23 @@ __global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
   if (tid < n) load_column(tid);
   // this band's rows of P, and R (n x r, row-major) into Rt (k-major); the
   // loads in batches, row-major order, then the stores
-  copy_batched<SUP_THREADS>(Pb, a.P[l] + static_cast<long long>(i0) * r, rows * r, tid,
-                            [](float* d, int e, float v) { d[e] = v; });
+  // P's band in rows of NR values (zero past r and past the band), so the
+  // products below need no bounds: a zero adds nothing to a sum
+  {
+    const float* __restrict__ Pg = a.P[l] + static_cast<long long>(i0) * r;
+    constexpr int PE = SMALL_ROWS * NR, PPER = (PE + SUP_THREADS - 1) / SUP_THREADS;
+    float v[PPER];
+#pragma unroll
+    for (int u = 0; u < PPER; ++u) {
+      const int e = u * SUP_THREADS + tid, t = e / NR, k = e - t * NR;
+      v[u] = (e < PE && t < rows && k < r) ? Pg[t * r + k] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < PPER; ++u) {
+      const int e = u * SUP_THREADS + tid;
+      if (e < PE) Pb[e] = v[u];
+    }
+  }
   copy_batched<SUP_THREADS>(Rt, a.R[l], n * r, tid, [ldt, r](float* d, int e, float v) {
     const int c = e / r, k = e - c * r;
     d[k * ldt + c] = v;
@@ -388,33 +403,41 @@ __global__ __launch_bounds__(SUP_THREADS) void k_small_update(SmallUpdArgs a) {
     float sm[SMALL_ROWS], sx[SMALL_ROWS];
 #pragma unroll
     for (int t = 0; t < SMALL_ROWS; ++t) { sm[t] = 0.0f; sx[t] = 0.0f; }
+    // (no early exits, so that the loops unroll: past r the R and Q values
+    // and P's entries are zero, and a sum that starts at +0 is unchanged by
+    // adding 0 x 0).  P is read through an offset the compiler cannot see
+    // through, so that it does not hoist the whole band into registers
+    // across the column loop.
+    int pofs = 0;
+    __asm__ volatile("" : "+v"(pofs));
+    const float* const Pr = Pb + pofs;
 #pragma unroll
     for (int k0 = 0; k0 < NR; k0 += KB) {
-      if (k0 >= r) break;
-      float rc[KB], qc[KB];
+      if (k0 < r) {
+        float rc[KB], qc[KB];
 #pragma unroll
-      for (int k = 0; k < KB; ++k) {
-        rc[k] = k0 + k < r ? Rt[(k0 + k) * ldt + c] : 0.0f;
-        qc[k] = k0 + k < r ? Qt[(k0 + k) * ldt + c] : 0.0f;
-      }
-#pragma unroll
-      for (int k = 0; k < KB; ++k) {
-        if (k0 + k >= r) break;
-#pragma unroll
-        for (int t = 0; t < SMALL_ROWS; ++t) {
-          const float pk = t < rows ? Pb[t * r + k0 + k] : 0.0f;
-          sm[t] = fmaf(pk, rc[k], sm[t]);
-          sx[t] = fmaf(pk, qc[k], sx[t]);
+        for (int k = 0; k < KB; ++k) {
+          rc[k] = k0 + k < r ? Rt[(k0 + k) * ldt + c] : 0.0f;
+          qc[k] = k0 + k < r ? Qt[(k0 + k) * ldt + c] : 0.0f;
         }
+#pragma unroll
+        for (int k = 0; k < KB; ++k)
+#pragma unroll
+          for (int t = 0; t < SMALL_ROWS; ++t) {
+            const float pk = Pr[t * NR + k0 + k];
+            sm[t] = fmaf(pk, rc[k], sm[t]);
+            sx[t] = fmaf(pk, qc[k], sx[t]);
+          }
       }
     }
 #pragma unroll
     for (int t = 0; t < SMALL_ROWS; ++t) {
-      if (t >= rows) break;
-      const long long off = static_cast<long long>(i0 + t) * n + c;
-      const float x = gc != 0.0f ? fmaf(gc, gv[t], xv[t]) : xv[t] * xd;
-      Mo[off] = fmaf(cm, sm[t], mv[t]);
-      Xo[off] = fmaf(cx, sx[t], x);
+      if (t < rows) {
+        const long long off = static_cast<long long>(i0 + t) * n + c;
+        const float x = gc != 0.0f ? fmaf(gc, gv[t], xv[t]) : xv[t] * xd;
+        Mo[off] = fmaf(cm, sm[t], mv[t]);
+        Xo[off] = fmaf(cx, sx[t], x);
+      }
     }
   }
 }
@@ -456,7 +479,11 @@ hipError_t launch_small_update(const SmallUpdArgs& a, int nl, hipStream_t s) {
   if (nl <= 0) return hipSuccess;
   if (!small_sync_fits(a.m, a.n, a.r) || (a.spec == 2 && !a.ctl)) return hipErrorInvalidValue;
   const dim3 grid((a.m + SMALL_ROWS - 1) / SMALL_ROWS, nl);
-  if (a.r <= 16) hipLaunchKernelGGL(k_small_update<16>, grid, dim3(SUP_THREADS), 0, s, a);
+  // the products run over NR k values whatever r is (zeros past r): NR the
+  // smallest of 4, 8, 16, 32, 64 that holds r
+  if (a.r <= 4) hipLaunchKernelGGL(k_small_update<4>, grid, dim3(SUP_THREADS), 0, s, a);
+  else if (a.r <= 8) hipLaunchKernelGGL(k_small_update<8>, grid, dim3(SUP_THREADS), 0, s, a);
+  else if (a.r <= 16) hipLaunchKernelGGL(k_small_update<16>, grid, dim3(SUP_THREADS), 0, s, a);
   else if (a.r <= 32) hipLaunchKernelGGL(k_small_update<32>, grid, dim3(SUP_THREADS), 0, s, a);
   else hipLaunchKernelGGL(k_small_update<64>, grid, dim3(SUP_THREADS), 0, s, a);
   return hipGetLastError();
