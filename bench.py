@@ -69,6 +69,8 @@ KIND_BOUND = {
     "apply_bf16x6": ("mfma", "bf16", 6), "trtri_f64": ("mfma", "f64", 1),
     # exact Gram matrix: nine slice products per fp64-accurate product
     "gram_bf16x9": ("mfma", "bf16", 9),
+    # the buffer pass fused into P~ = B Q (predicted sync steps, bf16 gradients)
+    "form_power_bq_bf16x3": ("mfma", "bf16", 3),
     "update_f32": ("hbm", None, 1),
     # small layers: one workgroup per layer, latency-bound; priced against the fp64 peak
     "small_cholqr": ("alu", "f64", 1), "small_update": ("hbm", None, 1),

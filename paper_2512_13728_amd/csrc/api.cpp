@@ -30,6 +30,7 @@
 
 #include "../../include/curvadion.h"
 #include "common.hpp"
+#include "form_bq.hpp"
 #include "plan.hpp"
 
 namespace {
@@ -95,12 +96,12 @@ int plan_splits(int M, int N, int K, int nl, bool fp64, int* kchunk, int pieces 
 // ---- optional per-kernel timing (HIP events on the launch stream) ----------
 enum Kind { K_FORM, K_FORM_X, K_GATE, K_LOCAL, K_PBQ, K_PBQ_BF, K_GRAM, K_GRAM_BF, K_CHOL, K_TRSM, K_TRTRI,
             K_APPLY_BF, K_PBTP, K_PBTP3, K_REDUCE, K_COLNORM, K_UPDATE, K_UPDATE_BF1, K_UPDATE_F32,
-            K_SMALL_QR, K_SMALL_UPD, K_GRAM_X, K_NKINDS };
+            K_SMALL_QR, K_SMALL_UPD, K_GRAM_X, K_FORM_BQ, K_NKINDS };
 const char* const kKindName[K_NKINDS] = {
     "form_buffer", "form_buffer_local", "gate", "local_update", "power_bq_f64", "power_bq_bf16x3", "gram_f64",
     "gram_bf16x6", "cholesky_f64", "trsm_f64", "trtri_f64", "apply_bf16x6", "power_btp_f64",
     "power_btp_bf16x3", "reduce_splits", "colnorm", "update_bf16x6", "update_bf16", "update_f32",
-    "small_cholqr", "small_update", "gram_bf16x9"};
+    "small_cholqr", "small_update", "gram_bf16x9", "form_power_bq_bf16x3"};
 static_assert(K_NKINDS <= 32, "the timing mask holds one bit per kind");
 
 // Timing events only measure: recording them without the system-scope fence
@@ -189,6 +190,7 @@ struct ShapeClass {
 struct Unit {
   int sc;                // shape class
   std::vector<int> sel;  // positions in the group
+  int fbq_splits = 1, fbq_kchunk = 0;   // K slices of the fused buffer pass + P~ = B Q
   int off;               // first factor-table entry
   int toff, nt;          // its (layer, 64-row tile of m) pairs in trsm_tiles
   int rtoff, nrt;        // its (layer, 64-row tile of r_max) pairs in trtri_tiles
@@ -206,7 +208,9 @@ struct cd_group {
   int H = 1;
   int nparts_stride = 0;
   double* parts = nullptr;      // [L][nparts_stride]
-  int* nparts = nullptr;        // [L]
+  int* nparts = nullptr;        // [L]: partials of the buffer pass
+  int* nparts_fx = nullptr;     // [L]: partials of the fused buffer pass + P~ = B Q
+  std::vector<int> np_fx;       // the same on the host; empty: no fused pass planned
   double** prev = nullptr;      // [L] device pointers to each layer's prev_norm
   double* norms = nullptr;      // [L] gate workspace
   unsigned* counter = nullptr;  // gate completion counter (returns to zero)
@@ -374,7 +378,7 @@ void carve_layer(cd_layer* L, char* base, const LayerLayout& lo) {
 
 // The device tables of a group of L layers, as byte offsets into one block.
 struct GroupLayout {
-  size_t parts, nparts, prev, norms, counter, ctl, out_dev, chol_tab, trsm_tab[3], trsm_tiles, trtri_tiles;
+  size_t parts, nparts, nparts_fx, prev, norms, counter, ctl, out_dev, chol_tab, trsm_tab[3], trsm_tiles, trtri_tiles;
   size_t total;
 };
 
@@ -383,6 +387,7 @@ GroupLayout group_layout(int L, int nparts_stride, size_t ntiles, size_t nrtiles
   Carver c;
   lo.parts = c.put(sizeof(double) * L * nparts_stride);
   lo.nparts = c.put(sizeof(int) * L);
+  lo.nparts_fx = c.put(sizeof(int) * L);
   lo.prev = c.put(sizeof(double*) * L);
   lo.norms = c.put(sizeof(double) * L);
   lo.counter = c.put(sizeof(unsigned));
@@ -399,6 +404,7 @@ GroupLayout group_layout(int L, int nparts_stride, size_t ntiles, size_t nrtiles
 void carve_group(cd_group* g, char* base, const GroupLayout& lo) {
   g->parts = reinterpret_cast<double*>(base + lo.parts);
   g->nparts = reinterpret_cast<int*>(base + lo.nparts);
+  g->nparts_fx = reinterpret_cast<int*>(base + lo.nparts_fx);
   g->prev = reinterpret_cast<double**>(base + lo.prev);
   g->norms = reinterpret_cast<double*>(base + lo.norms);
   g->counter = reinterpret_cast<unsigned*>(base + lo.counter);
@@ -493,6 +499,27 @@ void plan_group(cd_group* g, cd_layer* const* layers, int n, std::vector<int>& n
       g->units.push_back(std::move(u));
     }
   }
+  // the fused buffer pass + P~ = B Q of bf16-gradient layers: K slices per
+  // unit, so that a launch has about three workgroups per CU (one fits) and
+  // a slice keeps at least 512 k
+  g->np_fx.clear();
+  if (g->g_bf16) {
+    g->np_fx.assign(n, 0);
+    for (Unit& u : g->units) {
+      const int m = g->shapes[u.sc].m, nn = g->shapes[u.sc].n;
+      const long long tiles = 1LL * ((m + cd::FBQ_BM - 1) / cd::FBQ_BM) * static_cast<long long>(u.sel.size());
+      int sp = 1;
+      while (tiles * sp < 768 && nn / (2 * sp) >= 512 && sp < 16) sp *= 2;
+      int kc = (nn + sp - 1) / sp;
+      kc = (kc + cd::GBK - 1) / cd::GBK * cd::GBK;
+      u.fbq_kchunk = kc;
+      u.fbq_splits = (nn + kc - 1) / kc;
+      for (int li : u.sel) {
+        g->np_fx[li] = cd::form_bq_nparts(m, u.fbq_splits);
+        g->nparts_stride = std::max(g->nparts_stride, g->np_fx[li]);
+      }
+    }
+  }
   std::vector<long long> numel(n);
   for (int i = 0; i < n; ++i) numel[i] = 1LL * layers[i]->d.m * layers[i]->d.n;
   g->sbatches = cd::plan_stream_batches(numel, cd::MAXS, cd::MAX_STREAM_BLOCKS, cd::FORM_CHUNK);
@@ -528,6 +555,8 @@ cd_status build_group(cd_layer* const* layers, int n, cd_group** out) {
   if (e == hipSuccess) e = hipEventCreateWithFlags(&g->ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&g->done_ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipMemcpy(g->nparts, np.data(), sizeof(int) * n, hipMemcpyHostToDevice);
+  if (e == hipSuccess && !g->np_fx.empty())
+    e = hipMemcpy(g->nparts_fx, g->np_fx.data(), sizeof(int) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->prev, pv.data(), sizeof(double*) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->chol_tab, ct.data(), sizeof(cd::CholTab) * n, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(g->trsm_tab[0], t0.data(), sizeof(cd::TrsmTab) * n, hipMemcpyHostToDevice);
@@ -983,13 +1012,83 @@ cd_status enqueue_form(cd_group* g, const void* const* G, float* const* M, float
   return CD_OK;
 }
 
+// Whether a step at rank r can take the fused buffer pass + P~ = B Q:
+// bf16-gradient layers with r in (256, 512] whose split partials fit.
+bool fused_fits(const cd_group* g, int r) {
+  if (g->np_fx.empty() || r < cd::FBQ_RMIN || r > cd::FBQ_RMAX) return false;
+  for (const Unit& u : g->units) {
+    const int m = g->shapes[u.sc].m;
+    if (u.fbq_splits > 1)
+      for (int li : u.sel)
+        if (static_cast<size_t>(u.fbq_splits) * m * r * sizeof(float) > g->layers[li]->split_cap) return false;
+  }
+  return true;
+}
+
+// 1'. B = M + G fused into P~ = B Q (k_form_bq.hip), per unit on the unit's
+// stream of the sync branch (forked from s and joined back to it here), then
+// the split partials of P~ added in split order into P.
+cd_status enqueue_form_bq(cd_group* g, const void* const* G, float* const* M, float* const* Q, int r,
+                          hipStream_t s) {
+  const int nu = static_cast<int>(g->units.size());
+  const int nside = (g->timer.on && g->timer.mask == ~0u) ? 0 : g->nside;
+  auto stream_of = [&](int u) -> hipStream_t {
+    const int k = u % (nside + 1);
+    return k == 0 ? s : g->side[k - 1];
+  };
+  if (nside > 0) {
+    CD_HIP(hipEventRecord(g->fork_ev, s));
+    for (int i = 0; i < nside; ++i) CD_HIP(hipStreamWaitEvent(g->side[i], g->fork_ev, 0));
+  }
+  for (int ui = 0; ui < nu; ++ui) {
+    const Unit& u = g->units[ui];
+    const hipStream_t su = stream_of(ui);
+    const int m = g->shapes[u.sc].m, n = g->shapes[u.sc].n, nl = static_cast<int>(u.sel.size());
+    cd::FormBqArgs fa{};
+    fa.m = m; fa.n = n; fa.r = r;
+    fa.splits = u.fbq_splits; fa.kchunk = u.fbq_kchunk;
+    fa.split_stride = 1LL * m * r;
+    for (int j = 0; j < nl; ++j) {
+      cd_layer* Ly = g->layers[u.sel[j]];
+      fa.M[j] = M[u.sel[j]];
+      fa.G[j] = static_cast<const __bf16*>(G[u.sel[j]]);
+      fa.Q[j] = Q[u.sel[j]];
+      fa.C[j] = fa.splits > 1 ? static_cast<float*>(Ly->split_part) : Ly->P;
+      fa.part[j] = g->parts + 1LL * u.sel[j] * g->nparts_stride;
+    }
+    const double mn = 1.0 * m * n, mr = 1.0 * m * r, nr = 1.0 * n * r;
+    cd_status st = run(g, K_FORM_BQ, (10.0 * mn + 4.0 * nr + 4.0 * mr) * nl, 2.0 * mn * r * nl, su,
+                       [&] { return cd::launch_form_bq(fa, nl, su); });
+    if (st != CD_OK) return st;
+    if (fa.splits > 1) {
+      cd::ReduceArgs ra{};
+      ra.count = 1LL * m * r; ra.stride = fa.split_stride; ra.splits = fa.splits; ra.run_if = nullptr;
+      for (int j = 0; j < nl; ++j) {
+        ra.part[j] = g->layers[u.sel[j]]->split_part;
+        ra.out[j] = g->layers[u.sel[j]]->P;
+      }
+      st = run(g, K_REDUCE, static_cast<double>(ra.count) * nl * 4.0 * (fa.splits + 1), 0.0, su,
+               [&] { return cd::launch_reduce_splits(ra, nl, false, false, su); });
+      if (st != CD_OK) return st;
+    }
+  }
+  for (int i = 0; i < nside; ++i) {
+    CD_HIP(hipEventRecord(g->join_ev[i], g->side[i]));
+    CD_HIP(hipStreamWaitEvent(s, g->join_ev[i], 0));
+  }
+  return CD_OK;
+}
+
 // 2. the gate: norms, RMMC, prev_norm, max, the branch (g > tau, or
 // fixed_flag >= 0 for a fixed policy) into g->out_dev and the control word;
 // with to_host also into the pinned block, followed by the step's sequence
 // number.
-cd_status enqueue_gate(cd_group* g, hipStream_t s, bool to_host, int spec_mode, int fixed_flag) {
+// fused: the partials come from the fused buffer pass + P~ = B Q.
+cd_status enqueue_gate(cd_group* g, hipStream_t s, bool to_host, int spec_mode, int fixed_flag,
+                       bool fused = false) {
   cd::GateArgs ga{};
-  ga.L = g->L; ga.nparts_stride = g->nparts_stride; ga.parts = g->parts; ga.nparts = g->nparts;
+  ga.L = g->L; ga.nparts_stride = g->nparts_stride; ga.parts = g->parts;
+  ga.nparts = fused ? g->nparts_fx : g->nparts;
   ga.prev = g->prev; ga.eps = g->eps; ga.tau = g->tau; ga.out = g->out_dev;
   ga.norms = g->norms; ga.counter = g->counter;
   ga.ctl = g->ctl; ga.spec_mode = spec_mode; ga.fixed_flag = fixed_flag;
@@ -1008,8 +1107,10 @@ cd_status enqueue_gate(cd_group* g, hipStream_t s, bool to_host, int spec_mode, 
 // predicated on the control word, spec taken from it.
 enum Branch { BR_LOCAL = 0, BR_SYNC = 1, BR_BOTH = 2 };
 
+// fused: P~ = B Q of every unit already came out of the fused buffer pass.
 cd_status enqueue_branch(cd_group* g, int branch, int spec, const void* const* G, float* const* M,
-                         float* const* X, float* const* Q, float mu, float eta, int r, hipStream_t s) {
+                         float* const* X, float* const* Q, float mu, float eta, int r, hipStream_t s,
+                         bool fused = false) {
   if (branch == BR_LOCAL || branch == BR_BOTH) {
     for (const std::vector<int>& batch : g->sbatches) {
       if (branch == BR_LOCAL && spec != 0) break;
@@ -1058,7 +1159,7 @@ cd_status enqueue_branch(cd_group* g, int branch, int spec, const void* const* G
       CD_HIP(hipEventRecord(g->fork_ev, s));
       for (int i = 0; i < nside; ++i) CD_HIP(hipStreamWaitEvent(g->side[i], g->fork_ev, 0));
     }
-    for (int stage = 0; stage < 6; ++stage) {
+    for (int stage = fused ? 1 : 0; stage < 6; ++stage) {
       for (int ui = 0; ui < nu; ++ui) {
         const Unit& u = g->units[ui];
         const hipStream_t su = stream_of(ui);
@@ -1149,9 +1250,18 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   else if (g->pred_known) spec_mode = g->predict_skip ? 1 : 0;
   else spec_mode = 2;
 
-  st = enqueue_form(g, G, M, X, eta, spec_mode, s);
+  // A step that syncs for certain -- a fixed policy's sync step, or a layer's
+  // first step (prev_norm = 0: RMMC = ||B|| / eps) -- forms B inside
+  // P~ = B Q when the layers allow it (bf16 gradients, 256 < r <= 512): M and
+  // G are streamed once, and P~ is ready when the gate decides.  A sync that
+  // is only predicted (the previous step synced) takes the plain buffer pass:
+  // the step after a sync usually skips, and a misprediction would waste the
+  // whole product.  (Should a first step skip after all, B = 0, P~ is unused
+  // workspace and the local branch finds M = B as after a plain buffer pass.)
+  const bool fused = spec_mode == 0 && (fixed ? fsync : (blocking && any_prev_zero)) && fused_fits(g, r);
+  st = fused ? enqueue_form_bq(g, G, M, Q, r, s) : enqueue_form(g, G, M, X, eta, spec_mode, s);
   if (st != CD_OK) return st;
-  st = enqueue_gate(g, s, true, spec_mode, fixed ? (fsync ? 1 : 0) : -1);
+  st = enqueue_gate(g, s, true, spec_mode, fixed ? (fsync ? 1 : 0) : -1, fused);
   if (st != CD_OK) return st;
   CD_HIP(hipEventRecord(g->ev, s));
   for (int i = 0; i < g->L; ++i) {
@@ -1170,7 +1280,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
   // the output (3. the decision point, standing in for the max all-reduce).
   bool sync = fsync;
   if (fixed) {
-    st = enqueue_branch(g, fsync ? BR_SYNC : BR_LOCAL, spec_mode, G, M, X, Q, mu, eta, r, s);
+    st = enqueue_branch(g, fsync ? BR_SYNC : BR_LOCAL, spec_mode, G, M, X, Q, mu, eta, r, s, fused);
     if (st != CD_OK) return st;
   } else if (!blocking) {
     st = enqueue_branch(g, BR_BOTH, 2, G, M, X, Q, mu, eta, r, s);
@@ -1182,7 +1292,7 @@ cd_status group_step_impl(cd_group* g, const void* const* G, float* const* M, fl
     const cd::GateOut* go = gate_out(g);
     if (!fixed) {
       sync = go->flag != 0;
-      st = enqueue_branch(g, sync ? BR_SYNC : BR_LOCAL, go->spec, G, M, X, Q, mu, eta, r, s);
+      st = enqueue_branch(g, sync ? BR_SYNC : BR_LOCAL, go->spec, G, M, X, Q, mu, eta, r, s, fused);
       if (st != CD_OK) return st;
     }
     if (rmmc_per_layer) std::memcpy(rmmc_per_layer, go + 1, sizeof(double) * g->L);

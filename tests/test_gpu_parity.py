@@ -389,8 +389,56 @@ def test_more_shape_batches_than_streams(gd):
 
 
 @pytest.mark.parametrize("policy", [O.POLICY_RMMC, O.POLICY_ALWAYS_SYNC])
-@pytest.mark.parametrize("m,n,r", [(512, 1536, 64), (2048, 512, 256), (300, 700, 37), (128, 256, 32)])
+def test_bf16_fused_buffer_pass_group(policy):
+    """Five shapes of two bf16-gradient layers at r = 288.  On a step that
+    syncs for certain (every step of the fixed policy; under the RMMC gate the
+    first one, where every layer starts from prev_norm = 0) each shape batch
+    forms its B inside P~ = B Q on its own stream and the gate adds those
+    passes' partial sums; the RMMC gate's later steps take the plain buffer
+    pass, so the RMMC statistic mixes both kinds of partial sums.  Every
+    layer's RMMC and the decision against the oracle at every step, all
+    layers' outputs teacher-forced, and a rerun bit-identical."""
+    shapes = [(300, 400), (400, 300), (288, 1030), (700, 320), (320, 320)]
+    shapes = [s for s in shapes for _ in range(2)]
+    r = 288
+    w = S.Workload("fused", tuple(shapes), r=r, grad_dtype="bf16", steps=4, k=8, tau=0.3, stream_id=41)
+    pol = cdl.POLICY_RMMC if policy == O.POLICY_RMMC else cdl.POLICY_ALWAYS_SYNC
+    runs = []
+    for rep in range(2):
+        Ls = [cdl.Layer(m, n, r, grad_dtype="bf16", policy=pol, tau=0.3) for m, n in shapes]
+        Gp = cdl.Group(Ls)
+        st = [_state(w, i) for i in range(len(shapes))]
+        streams = [S.GradientStream(w, i, device="cpu") for i in range(len(shapes))]
+        flags = []
+        for t in range(w.steps):
+            Gs = [s.next().to(DEV) for s in streams]
+            args = (Gp, Ls, Gs, [s[0] for s in st], [s[1] for s in st], [s[2] for s in st], w.mu, w.eta, r)
+            if rep == 0:
+                info, errs = group_step_and_compare(*args, 0.3, policy)
+                _check_group(info, errs, 0.3, policy, bf16=True, tag=f"fused step {t + 1}")
+                flags.append(info["flag_gpu"])
+            else:
+                _, flag, _, _ = Gp.step(*args[2:])
+                torch.cuda.synchronize()
+                flags.append(flag)
+        runs.append((flags, [f64(t) for s in st for t in s]))
+        print(f"run {rep + 1}: decisions {flags}", flush=True)
+    assert runs[0][0] == runs[1][0] and runs[0][0][0]
+    for a, b in zip(runs[0][1], runs[1][1]):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("policy", [O.POLICY_RMMC, O.POLICY_ALWAYS_SYNC])
+@pytest.mark.parametrize("m,n,r", [(512, 1536, 64), (2048, 512, 256), (300, 700, 37), (128, 256, 32),
+                                   # 256 < r <= 512: a predicted or fixed sync forms B inside
+                                   # P~ = B Q (one workgroup per 128-row band and K slice), with
+                                   # ragged bands, an odd rank (scalar loads of Q), a row length
+                                   # that is not a multiple of four (scalar loads of M and G), and
+                                   # the full 512-wide tile over two K slices
+                                   (300, 1000, 300), (257, 700, 257), (1030, 2051, 500), (2048, 2048, 512)])
 def test_bf16_gradient_steps(m, n, r, policy):
+    """Three steps of one bf16-gradient layer against the oracle (teacher-forced);
+    under the RMMC policy step 1 syncs and the later ones follow the gate."""
     gd = "bf16"
     w = S.small_workload(m, n, r, grad_dtype=gd, k=16)
     M, X, Q = _state(w, 0)
