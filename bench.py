@@ -207,17 +207,20 @@ STEP_COMMON = (r"k_form_buffer<", r"k_gate\b", r"k_local_update<")
 
 def steps_of(dispatches):
     """Library dispatches (in order) cut into steps: a step starts at its
-    first buffer-pass launch (k_form_buffer) and runs until the next step's.
-    Returns [(kind, [indices])], kind "sync" when a sync-branch kernel ran."""
-    steps, cur, prev_form = [], None, False
+    first buffer-pass launch (k_form_buffer, or k_form_bq where the pass is
+    fused into P~ = B Q) after the previous step's gate and runs until the
+    next step's.  Returns [(kind, [indices])], kind "sync" when a sync-branch
+    kernel ran."""
+    steps, cur, gated = [], None, True
     for i, (_, name, _) in enumerate(dispatches):
         if "cd::" not in name:
             continue
-        form = re.search(r"k_form_buffer<", name) is not None
-        if form and not prev_form:
+        if re.search(r"k_form_buffer<|k_form_bq<", name) and gated:
             cur = []
             steps.append(cur)
-        prev_form = form
+            gated = False
+        if re.search(r"k_gate\b", name):
+            gated = True
         if cur is not None:
             cur.append(i)
     out = []
