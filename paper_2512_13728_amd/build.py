@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libcurvadion.so")
 OBJDIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["k_stream.hip", "k_gemm.hip", "k_gemm_bf.hip", "k_chol.hip", "k_colnorm.hip", "k_update_vec.hip", "k_small.hip", "k_gram.hip", "k_form_bq.hip", "api.cpp"]
+SOURCES = ["k_stream.hip", "k_gemm.hip", "k_gemm_bf.hip", "k_chol.hip", "k_colnorm.hip", "k_update_vec.hip", "k_small.hip", "k_gram.hip", "k_form_bq.hip", "k_nearid.hip", "api.cpp"]
 
 # -packed-fp32-ops: keep the compiler from emitting packed fp32 arithmetic
 # (v_pk_*_f32); scalar and vector fp32 code is compiled as plain VALU ops.

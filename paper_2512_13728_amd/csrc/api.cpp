@@ -150,6 +150,7 @@ struct cd_layer {
   void* ws = nullptr;           // the one device allocation the pointers below are carved from
   double* prev = nullptr;       // device, 1 double
   int* rankdef = nullptr;       // device, 1 int
+  int* nid_ok = nullptr;        // device, 1 int: the second CholQR pass took the near-identity path
   int* rowok = nullptr;         // device, r_max ints: rows of T whose pivot was not floored
   double* pa = nullptr;         // m x r_max fp64: P~ (bf16-gradient layers: the slice planes
                                 // and exponents of the exact pass-0 Gram matrix)
@@ -160,7 +161,8 @@ struct cd_layer {
   double* W = nullptr;          // r_max^2 Gram matrix, then its Cholesky factor
   double* Dinv = nullptr;       // inverses of the 64 x 64 diagonal blocks of the factor
   double* floor_ = nullptr;     // pivot floor of the current factorisation
-  double* gram_part = nullptr;  // split-K partials of the Gram matrix
+  double* gram_part = nullptr;  // split-K partials of the Gram matrix; between the second Gram
+                                // matrix and the step's end, the near-identity factor's buffers
   void* split_part = nullptr;   // split-K partials of the skinny GEMMs (fp32 or fp64)
   size_t split_cap = 0;         // bytes of split_part
   size_t gram_cap = 0;          // doubles of gram_part
@@ -294,7 +296,7 @@ long long blocks_for(long long numel) { return (numel + cd::FORM_CHUNK - 1) / cd
 // (every piece 256-byte aligned).  cd_layer_create allocates the block; the
 // allocation-free step carves it from the static scratch array.
 struct LayerLayout {
-  size_t prev, rankdef, rowok, pa, pb, Uf, P, R, W, Dinv, floor_, gram_part, split_part, colsq, planes, colnrm;
+  size_t prev, rankdef, nid_ok, rowok, pa, pb, Uf, P, R, W, Dinv, floor_, gram_part, split_part, colsq, planes, colnrm;
   size_t split_cap;   // bytes of split_part
   size_t gram_cap;    // doubles of gram_part
   size_t total;
@@ -327,6 +329,8 @@ LayerLayout layer_layout(int m, int n, int rm) {
     }
     gram_cap = std::max(gram_cap, static_cast<size_t>(plan_splits(r, r, m, 1, true, &kc, 0, true)) * r * r);
   }
+  // the second pass's near-identity factor (fp32-gradient layers) borrows it
+  gram_cap = std::max(gram_cap, 2 * static_cast<size_t>(rm) * rm + cd::nearid_parts(rm));
   const size_t M = m, N = n, R = rm;
   const size_t nchunks = (N + cd::COLNORM_ROWS - 1) / cd::COLNORM_ROWS;
   const size_t nblk = (R + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK;
@@ -335,6 +339,7 @@ LayerLayout layer_layout(int m, int n, int rm) {
   Carver c;
   lo.prev = c.put(sizeof(double));
   lo.rankdef = c.put(sizeof(int));
+  lo.nid_ok = c.put(sizeof(int));
   lo.rowok = c.put(sizeof(int) * R);
   lo.pa = c.put(std::max(sizeof(double) * M * R, cd::gram_x_bytes(m, rm)));
   lo.pb = c.put(sizeof(float) * M * R);
@@ -358,6 +363,7 @@ LayerLayout layer_layout(int m, int n, int rm) {
 void carve_layer(cd_layer* L, char* base, const LayerLayout& lo) {
   L->prev = reinterpret_cast<double*>(base + lo.prev);
   L->rankdef = reinterpret_cast<int*>(base + lo.rankdef);
+  L->nid_ok = reinterpret_cast<int*>(base + lo.nid_ok);
   L->rowok = reinterpret_cast<int*>(base + lo.rowok);
   L->pa = reinterpret_cast<double*>(base + lo.pa);
   L->pb = reinterpret_cast<float*>(base + lo.pb);
@@ -487,7 +493,7 @@ void plan_group(cd_group* g, cd_layer* const* layers, int n, std::vector<int>& n
         cd_layer* L = layers[u.sel[j]];
         const int k = off + j;
         ct[k] = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok,
-                            rankdef_host ? rankdef_host + u.sel[j] : nullptr};
+                            rankdef_host ? rankdef_host + u.sel[j] : nullptr, L->gram_part, L->nid_ok};
         factor_tabs(L, t0[k], t1[k], t2[k]);
         for (int rt = 0; rt < (L->d.m + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt) tiles.push_back(int2{j, rt});
         for (int rt = 0; rt < (L->d.r_max + cd::CHOL_BLOCK - 1) / cd::CHOL_BLOCK; ++rt)
@@ -923,13 +929,22 @@ cd_status enqueue_sync(cd_group* g, const ShapeClass& sc, const std::vector<int>
 
 // Between the stages of CholQR pass `pass`, over every layer: Cholesky of each
 // W, then either the fp64 triangular solve (fp32 layers: P1 = P~ T^-1, then
-// P = P1 T^-1) or the inverse U = T^-1 in fp32 for the bf16 x 6 apply.
+// P = P1 T^-1) or the inverse U = T^-1 in fp32 for the bf16 x 6 apply.  The
+// second pass of fp32 layers, whose W = P1^T P1 is the identity to about
+// kappa^2 u_fp64, factors W by the near-identity iteration; the blocked
+// factorisation then runs only for layers where W is too far from I.
 cd_status enqueue_factor(cd_group* g, const Unit& u, int r, int pass, hipStream_t s, const int* run_if) {
   const int nl = static_cast<int>(u.sel.size());
   const double L = nl, rr = 1.0 * r * r;
   const cd::CholTab* ct = g->chol_tab + u.off;
-  cd_status st = run(g, K_CHOL, 16.0 * rr * L, (1.0 / 3.0) * rr * r * L, s,
-                     [&] { return cd::launch_cholesky(ct, nl, r, pass, s, run_if); });
+  const bool nearid = pass == 1 && !g->g_bf16;
+  cd_status st = run(g, K_CHOL, 16.0 * rr * L, (1.0 / 3.0) * rr * r * L, s, [&] {
+    if (nearid) {
+      const hipError_t e = cd::launch_nearid(ct, nl, r, s, run_if);
+      if (e != hipSuccess) return e;
+    }
+    return cd::launch_cholesky(ct, nl, r, pass, s, run_if, nearid);
+  });
   if (st != CD_OK) return st;
   if (!g->g_bf16) {
     // in place in the fp64 panel: P1 = P~ T^-1 (pass 0), P = P1 T1^-1 (pass 1)
@@ -1480,7 +1495,7 @@ cd_status static_step_impl(const cd_layer_desc* desc, double* prev_norm, long lo
   su.prev = prev_norm;
   su.counter = g->counter;
   su.ct = g->chol_tab;
-  su.ctv = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok, nullptr};
+  su.ctv = cd::CholTab{L->W, L->Dinv, L->floor_, L->rankdef, L->rowok, nullptr, L->gram_part, L->nid_ok};
   su.tt[0] = g->trsm_tab[0];
   su.tt[1] = g->trsm_tab[1];
   su.tt[2] = g->trsm_tab[2];

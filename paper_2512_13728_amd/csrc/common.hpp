@@ -198,10 +198,19 @@ struct CholTab {
   int* rankdef;                    // set to 1 when a pivot was raised to the floor
   int* rowok;                      // r: 0 for the rows of floored pivots, else 1
   int* rankdef_host;               // NULL, or a mirror of rankdef in pinned host memory
+  double* nid;                     // second pass without pivots: two r x r buffers, then
+                                   // nearid_parts(r) partial sums
+  int* nid_ok;                     // 1: the second pass's factor came from launch_nearid
 };
 // All CHOL_BLOCK steps for `nlayers` layers of rank r; `pass` 0 clears rankdef.
+// gated: layers whose nid_ok is set are skipped (their factor is formed).
 hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s,
-                           const int* run_if = nullptr);
+                           const int* run_if = nullptr, bool gated = false);
+// The factor T1 of a Gram matrix W1 = I + E with ||E||_F <= 2^-10 and the
+// inverses of its diagonal blocks, by a fixed-point iteration (k_nearid.hip);
+// sets nid_ok per layer.  W1 in, T1 out over its upper triangle.
+hipError_t launch_nearid(const CholTab* tab, int nlayers, int r, hipStream_t s, const int* run_if = nullptr);
+int nearid_parts(int r);           // partial sums launch_nearid keeps per layer
 
 // The fixed pseudo-random direction that completes column j of P1 past the
 // numerical rank (row i; scale sqrt(3/m) gives unit expected norm): an

@@ -28,10 +28,11 @@ using Wave64 = WaveChol<CB>;
 // One wave per layer: the factorisation of the diagonal block (chol_wave.hpp)
 // and its inverse D_k; T_kk goes back over W_kk.
 __global__ __launch_bounds__(64) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
-                                                  int pass, const int* run_if) {
+                                                  int pass, const int* run_if, int gated) {
   __shared__ __attribute__((aligned(16))) Wave64::Lds lds;
   if (skip_launch(run_if)) return;
   const CholTab t = tab[blockIdx.x];
+  if (gated && *global_view(t.nid_ok)) return;
   double* const W = global_view(t.W);
   double* const floor_ = global_view(t.floor_);
   int* const rankdef = global_view(t.rankdef);
@@ -70,43 +71,13 @@ __global__ __launch_bounds__(64) void k_chol_diag(const CholTab* __restrict__ ta
   }
 }
 
-// 64 x 64 fp64 MFMA tile: acc += A(64 x K) B(K x 64) with both operands staged
-// through LDS.  4 waves as 2 x 2, each 32 x 32.
-struct Tile64 {
-  f64x4 acc[2][2];
-  __device__ void zero() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{};
-  }
-  // B is always staged k-major; A as A_KC says
-  template <bool A_KC>
-  __device__ void mma_stage(const double* As, const double* Bs, int wm0, int wn0, int lane) {
-#pragma unroll
-    for (int kk = 0; kk < GBK; kk += 16) {
-      f64x4 a[2], b[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = frag<double, CB, A_KC>(As, wm0 + i * 16, kk, lane);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = frag<double, CB, false>(Bs, wn0 + j * 16, kk, lane);
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
-    }
-  }
-};
-
 __global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ tab, int r, int kb,
-                                                    const int* run_if) {
+                                                    const int* run_if, int gated) {
   __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
   __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
   if (skip_launch(run_if)) return;
   const CholTab t = tab[blockIdx.y];
+  if (gated && *global_view(t.nid_ok)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
   const int k0 = kb * CB, nb = min(CB, r - k0), k1 = k0 + nb;
@@ -139,11 +110,12 @@ __global__ __launch_bounds__(256) void k_chol_panel(const CholTab* __restrict__ 
 }
 
 __global__ __launch_bounds__(256) void k_chol_trail(const CholTab* __restrict__ tab, int r, int kb,
-                                                    const int* run_if) {
+                                                    const int* run_if, int gated) {
   __shared__ __attribute__((aligned(16))) double As[tile_elems<CB>()];
   __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
   if (skip_launch(run_if)) return;
   const CholTab t = tab[blockIdx.y];
+  if (gated && *global_view(t.nid_ok)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
   const int k0 = kb * CB, nb = min(CB, r - k0), k1 = k0 + nb;
@@ -323,17 +295,18 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
 
 }  // namespace
 
-hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s, const int* run_if) {
+hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s, const int* run_if,
+                           bool gated) {
   if (nlayers <= 0) return hipSuccess;
   if (r < 1) return hipErrorInvalidValue;
-  const int nblk = (r + CB - 1) / CB;
+  const int nblk = (r + CB - 1) / CB, g = gated ? 1 : 0;
   for (int kb = 0; kb < nblk; ++kb) {
-    hipLaunchKernelGGL(k_chol_diag, dim3(nlayers), dim3(64), 0, s, tab, r, kb, pass, run_if);
+    hipLaunchKernelGGL(k_chol_diag, dim3(nlayers), dim3(64), 0, s, tab, r, kb, pass, run_if, g);
     const int k1 = min(r, (kb + 1) * CB);
     if (k1 >= r) break;
     const int nt = (r - k1 + CB - 1) / CB;
-    hipLaunchKernelGGL(k_chol_panel, dim3(nt, nlayers), dim3(256), 0, s, tab, r, kb, run_if);
-    hipLaunchKernelGGL(k_chol_trail, dim3(nt * (nt + 1) / 2, nlayers), dim3(256), 0, s, tab, r, kb, run_if);
+    hipLaunchKernelGGL(k_chol_panel, dim3(nt, nlayers), dim3(256), 0, s, tab, r, kb, run_if, g);
+    hipLaunchKernelGGL(k_chol_trail, dim3(nt * (nt + 1) / 2, nlayers), dim3(256), 0, s, tab, r, kb, run_if, g);
   }
   return hipGetLastError();
 }

@@ -202,6 +202,37 @@ __device__ __forceinline__ typename Mfma<T>::vec4_t frag(const T* S, int row0, i
   }
 }
 
+// 64 x 64 fp64 MFMA tile: acc += A(64 x K) B(K x 64) with both operands staged
+// through LDS.  4 waves as 2 x 2, each 32 x 32.
+struct Tile64 {
+  f64x4 acc[2][2];
+  __device__ void zero() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{};
+  }
+  // B is always staged k-major; A as A_KC says
+  template <bool A_KC>
+  __device__ void mma_stage(const double* As, const double* Bs, int wm0, int wn0, int lane) {
+#pragma unroll
+    for (int kk = 0; kk < GBK; kk += 16) {
+      f64x4 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = frag<double, 64, A_KC>(As, wm0 + i * 16, kk, lane);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = frag<double, 64, false>(Bs, wn0 + j * 16, kk, lane);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+    }
+  }
+};
+
 // Block index -> tile index so that consecutive tiles land on the same XCD
 // (workgroups are dispatched round-robin over the 8 XCDs).  The grid must be
 // padded to 8 * per; indices >= ntiles are idle.
