@@ -955,8 +955,8 @@ cd_status enqueue_factor(cd_group* g, const Unit& u, int r, int pass, hipStream_
       bytes += 16.0 * mr + 8.0 * rr;
     }
     st = run(g, K_TRSM, bytes, flops, s, [&] {
-      return cd::launch_trsm(g->trsm_tab[pass == 0 ? 0 : 2] + u.off, g->trsm_tiles + u.toff, u.nt, r, true,
-                             true, s, false, 0, run_if);
+      return cd::launch_trsm_rl(g->trsm_tab[pass == 0 ? 0 : 2] + u.off, g->trsm_tiles + u.toff, u.nt, r, s,
+                                run_if);
     });
     if (st != CD_OK || pass == 0) return st;
     // P rounded to fp32 (the update's operand planes and cd_layer_last_factors)

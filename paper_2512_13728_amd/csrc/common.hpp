@@ -246,6 +246,9 @@ hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, i
                             hipStream_t s, const int* run_if = nullptr);
 hipError_t launch_trsm(const TrsmTab* tab, const int2* tiles, int ntiles, int r, bool in64, bool out64,
                        hipStream_t s, bool ident = false, int mlimit = 0, const int* run_if = nullptr);
+// The same solve, right-looking, for fp64 panels in place (Pin == Pout).
+hipError_t launch_trsm_rl(const TrsmTab* tab, const int2* tiles, int ntiles, int r, hipStream_t s,
+                          const int* run_if = nullptr);
 
 // ---- ColumnNormalize --------------------------------------------------------
 constexpr int COLNORM_ROWS = 64;   // rows per partial

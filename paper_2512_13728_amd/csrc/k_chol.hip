@@ -293,6 +293,110 @@ __global__ __launch_bounds__(256) void k_trsm(const TrsmTab* __restrict__ tab, c
       }
 }
 
+// The same solve for fp64 panels in place (fp32-gradient layers), right-
+// looking: launch c (-1 <= c <= nblk - 2) reads the finished block column c
+// and takes every block column j > c of one 64-row tile per workgroup,
+//   j = c + 1:  P[:, j] = (P~[:, j] - P[:, c] T[c, j]) D_j   (c = -1: P~[:, 0] D_0)
+//   j > c + 1:  P~[:, j] -= P[:, c] T[c, j]
+// Every block of the panel is written by one workgroup and column c by none,
+// so a launch has no races.  It spans nblk - c - 1 column blocks of each row
+// tile, each with one or two 64 x 64 x 64 products, where the left-looking
+// form keeps m / 64 workgroups busy for the whole K = 64 c of every column.
+__global__ __launch_bounds__(256) void k_trsm_rl(const TrsmTab* __restrict__ tab, const int2* __restrict__ tiles,
+                                                 int r, int c, const int* run_if) {
+  constexpr int YLD = CB + 4;
+  constexpr int AY = tile_elems<CB>() > CB * YLD ? tile_elems<CB>() : CB * YLD;
+  __shared__ __attribute__((aligned(16))) double AYs[AY];
+  __shared__ __attribute__((aligned(16))) double Bs[tile_elems<CB>()];
+  double* const As = AYs;
+  double* const Ys = AYs;
+  if (skip_launch(run_if)) return;
+  const int2 lt = tiles[blockIdx.x];
+  const TrsmTab t = tab[lt.x];
+  const int m = t.m, i0 = lt.y * CB;
+  if (i0 >= m) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
+  const int j = c + 1 + blockIdx.y, j0 = j * CB, nbj = min(CB, r - j0);
+  double* const P = global_view(static_cast<double*>(t.Pout));
+  const double* const W = global_view(t.W);
+  Tile64 T;
+  T.zero();
+  if (c >= 0) {
+    // acc = P[i-tile, c-block] T[c-block, j-block]; block c is whole (c < nblk - 1)
+    const int c0 = c * CB;
+    for (int k0 = 0; k0 < CB; k0 += GBK) {
+      stage_tile<double, double, CB, 256, true>(As, P + static_cast<long long>(i0) * r + c0, r, 0, m - i0, k0, CB,
+                                                tid);
+      stage_tile<double, double, CB, 256, false>(Bs, W + static_cast<long long>(c0) * r + j0, r, 0, nbj, k0, CB,
+                                                 tid);
+      __syncthreads();
+      T.mma_stage<true>(As, Bs, wm0, wn0, lane);
+      __syncthreads();
+    }
+  }
+  if (j > c + 1) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = wm0 + i * 16 + Mfma<double>::out_row(lane, v);
+          const int col = wn0 + jj * 16 + (lane & 15);
+          if (i0 + row < m && col < nbj) P[static_cast<long long>(i0 + row) * r + j0 + col] -= T.acc[i][jj][v];
+        }
+    return;
+  }
+  // Y = P~[:, j] - acc, into LDS as the A operand of Y D_j ([row][k], k = column)
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = wm0 + i * 16 + Mfma<double>::out_row(lane, v);
+        const int col = wn0 + jj * 16 + (lane & 15);
+        double y = 0.0;
+        if (i0 + row < m && col < nbj) y = P[static_cast<long long>(i0 + row) * r + j0 + col] - T.acc[i][jj][v];
+        Ys[row * YLD + col] = y;
+      }
+  const double* D = global_view(t.Dinv) + static_cast<long long>(j) * CB * CB;
+  T.zero();
+  for (int k0 = 0; k0 < nbj; k0 += GBK) {
+    stage_tile<double, double, CB, 256, false>(Bs, D, CB, 0, nbj, k0, nbj, tid);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < GBK; kk += 16) {
+      f64x4 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        a[i] = *reinterpret_cast<const f64x4*>(Ys + (wm0 + i * 16 + (lane & 15)) * YLD + k0 + kk +
+                                               4 * (lane >> 4));
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) b[jj] = frag<double, CB, false>(Bs, wn0 + jj * 16, kk, lane);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj)
+            T.acc[i][jj] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i][q], b[jj][q], T.acc[i][jj], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = wm0 + i * 16 + Mfma<double>::out_row(lane, v);
+        const int col = wn0 + jj * 16 + (lane & 15);
+        if (i0 + row < m && col < nbj) P[static_cast<long long>(i0 + row) * r + j0 + col] = T.acc[i][jj][v];
+      }
+}
+
 }  // namespace
 
 hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hipStream_t s, const int* run_if,
@@ -317,6 +421,18 @@ hipError_t launch_fill_dead(const CholTab* ct, const TrsmTab* tt, int nlayers, i
   const dim3 grid((mmax + FILL_ROWS - 1) / FILL_ROWS, nlayers);
   if (p64) hipLaunchKernelGGL(k_fill_dead<double>, grid, dim3(256), 0, s, ct, tt, r, run_if);
   else hipLaunchKernelGGL(k_fill_dead<float>, grid, dim3(256), 0, s, ct, tt, r, run_if);
+  return hipGetLastError();
+}
+
+hipError_t launch_trsm_rl(const TrsmTab* tab, const int2* tiles, int ntiles, int r, hipStream_t s,
+                          const int* run_if) {
+  if (ntiles <= 0) return hipSuccess;
+  if (r < 1) return hipErrorInvalidValue;
+  const int nblk = (r + CB - 1) / CB;
+  // c = -1 only finishes block column 0 (there is nothing to subtract yet)
+  for (int c = -1; c <= nblk - 2; ++c)
+    hipLaunchKernelGGL(k_trsm_rl, dim3(ntiles, c < 0 ? 1 : nblk - c - 1), dim3(256), 0, s, tab, tiles, r, c,
+                       run_if);
   return hipGetLastError();
 }
 
