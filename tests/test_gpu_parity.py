@@ -272,6 +272,55 @@ def test_rank_deficient_buffer_is_completed(gd, m, n, r, k):
             _check_step(d, 0.5, O.POLICY_ALWAYS_SYNC, bf16=gd == "bf16")
 
 
+@pytest.mark.parametrize("m,n,r", [(700, 640, 96), (520, 900, 160)])
+def test_second_pass_paths_mixed_in_one_launch(m, n, r):
+    """Three fp32 layers of one shape step together (one batch, one launch
+    per kernel); the middle one's buffer has exact rank 5.  Its pass-0 pivots
+    fall under the floor and the completed columns leave P1^T P1 far from the
+    identity, so its second CholQR pass takes the blocked factorisation, while
+    the other two layers' second pass takes the near-identity factor (their
+    Gram matrices are within 2^-10 of I): both paths in the same launches,
+    gated per layer, at r = 96 (two whole blocks) and r = 160 (a partial third
+    block).  The full-rank layers match the oracle to the fp32 bounds; the
+    deficient one has orthonormal P whose unique columns (and those of R and
+    Q, and M = mu B) match the oracle, as test_rank_deficient_buffer_is_completed
+    checks for one layer alone."""
+    from gpu_util import device_to_numpy
+    k = 5
+    w = S.small_workload(m, n, r, layers=3, stream_id=131)
+    Ls = [cdl.Layer(m, n, r, policy=cdl.POLICY_ALWAYS_SYNC) for _ in range(3)]
+    Gp = cdl.Group(Ls)
+    st = [list(_state(w, i)) for i in range(3)]
+    gen = torch.Generator().manual_seed(131)
+    Gd = torch.zeros(m, n)
+    Gd[:k] = torch.randn(k, n, generator=gen) * 0.01
+    st[1][0] = torch.zeros(m, n, device=DEV)
+    st[1][2] = torch.linalg.qr(torch.randn(n, r, generator=gen, dtype=torch.float64))[0].float().contiguous().to(DEV)
+    streams = [S.GradientStream(w, i, device="cpu") for i in range(3)]
+    Gs = [streams[0].next().to(DEV), Gd.to(DEV), streams[2].next().to(DEV)]
+    Q1 = f64(st[1][2])
+    info, errs = group_step_and_compare(Gp, Ls, Gs, [s[0] for s in st], [s[1] for s in st],
+                                        [s[2] for s in st], w.mu, w.eta, r, w.tau, O.POLICY_ALWAYS_SYNC,
+                                        check=[0, 2])
+    _check_group(info, errs, w.tau, O.POLICY_ALWAYS_SYNC, tag=f"mixed paths {m}x{n} r={r}")
+    assert info["flag_gpu"] and Ls[1].rank_deficient()
+    assert not Ls[0].rank_deficient() and not Ls[2].rank_deficient()
+    Pa, Ra = Ls[1].last_factors()
+    Pg = device_to_numpy(Pa, (m, r)).astype(np.float64)
+    Rg = device_to_numpy(Ra, (n, r)).astype(np.float64)
+    B = f64(Gd)
+    _, Po, Ro = O.power_iteration(B, Q1)
+    Qo = O.column_normalize(Ro)
+    orth = np.abs(Pg.T @ Pg - np.eye(r)).max()
+    print(f"deficient layer: P {rel(Pg[:, :k], Po[:, :k]):.3g} R {rel(Rg[:, :k], Ro[:, :k]):.3g} "
+          f"|P^T P - I| {orth:.3g}", flush=True)
+    assert rel(Pg[:, :k], Po[:, :k]) <= 1e-5
+    assert rel(Rg[:, :k], Ro[:, :k]) <= 1e-5
+    assert rel(f64(st[1][2])[:, :k], Qo[:, :k]) <= 1e-5
+    assert rel(f64(st[1][0]), w.mu * B) <= 1e-5
+    assert orth <= 1e-5
+
+
 @pytest.mark.parametrize("tau,policy", [(0.5, O.POLICY_RMMC), (0.1, O.POLICY_RMMC),
                                         (0.5, O.POLICY_ALWAYS_SYNC)])
 def test_single256_trajectory(tau, policy):
