@@ -12,10 +12,10 @@
 // ||E||_F <= 2^-10, NID_ITERS = 4 products leave it below 1e-18.  The
 // inverses of the diagonal 64 x 64 blocks, which the triangular solve needs,
 // follow from the series (I + U_kk)^{-1} = sum_j (-U_kk)^j, cut after the
-// fifth power (remainder below ||U_kk||^6, about 1e-19).  Every
-// product runs in parallel over 64 x 64 tiles on the fp64 MFMA, where the
-// blocked factorisation makes r / 64 dependent steps of a few microseconds
-// each.
+// fifth power (remainder below ||U_kk||^6, about 1e-19).  Every product
+// runs in parallel over 32 x 32 quadrants of the upper 64 x 64 tiles on the
+// fp64 MFMA, where the blocked factorisation makes r / 64 dependent steps of
+// a few microseconds each.
 //
 // Layers whose ||E||_F exceeds the bound (a floored first-pass pivot, whose
 // column was replaced by a pseudo-random direction, or kappa past about
@@ -88,56 +88,98 @@ __global__ __launch_bounds__(256) void k_nid_start(const CholTab* __restrict__ t
   if (tid == 0) global_view(t.nid)[2LL * r * r + blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-// U_dst = Phi(E - U_src^T U_src) on upper tile blockIdx.x (src, dst: 0 or 1,
-// the two r x r buffers); dst < 0: the last step, T1 = I + U goes over W.
+// U_dst = Phi(E - U_src^T U_src) on one 32 x 32 quadrant of an upper 64 x 64
+// tile (src, dst: 0 or 1, the two r x r buffers; dst < 0: the last step,
+// T1 = I + U goes over W).  Four workgroups per tile, so that the tiles of
+// the last block rows, whose K runs to r, take a quarter of the time one
+// workgroup would; the four waves take every fourth 32-wide k slice and their
+// partial products are added in wave order.
+constexpr int NQ = 32;
 __global__ __launch_bounds__(256) void k_nid_iter(const CholTab* __restrict__ tab, int r, int src, int dst,
                                                   const int* run_if) {
-  __shared__ __attribute__((aligned(16))) double As[tile_elems<NB>()];
-  __shared__ __attribute__((aligned(16))) double Bs[tile_elems<NB>()];
+  constexpr int SL = GBK * (NQ + KPAD);   // one staged k slice of 32 columns
+  constexpr int RLD = NQ + 1;
+  static_assert(4 * NQ * RLD <= 4 * SL, "the wave partials fit in the A staging");
+  __shared__ __attribute__((aligned(16))) double As[4 * SL];
+  __shared__ __attribute__((aligned(16))) double Bs[4 * SL];
   __shared__ double sh;
   if (skip_launch(run_if)) return;
   const CholTab t = tab[blockIdx.y];
   const int nblk = (r + NB - 1) / NB;
   if (!(e_norm2(t, r, nblk * (nblk + 1) / 2, &sh) <= NID_BOUND2)) return;
   int ti, tj;
-  upper_tile(blockIdx.x, nblk, ti, tj);
-  const int i0 = ti * NB, j0 = tj * NB;
+  upper_tile(blockIdx.x >> 2, nblk, ti, tj);
+  const int qi = (blockIdx.x >> 1) & 1, qj = blockIdx.x & 1;
+  const int i0 = ti * NB + qi * NQ, j0 = tj * NB + qj * NQ;
+  if (i0 >= r || j0 >= r) return;         // a quadrant past a partial last block
   double* const W = global_view(t.W);
-  const double* const Us = global_view(t.nid) + static_cast<long long>(src) * r * r;
+  double* const Ud = dst >= 0 ? global_view(t.nid) + static_cast<long long>(dst) * r * r : nullptr;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 1) * 32, wn0 = (wave & 1) * 32;
-  // (U^T U)[i][j] = sum_k U[k][i] U[k][j]; U is upper triangular, so k < i0 + 64
-  const int kend = min(i0 + NB, r);
-  Tile64 T;
-  T.zero();
-  for (int k0 = 0; k0 < kend; k0 += GBK) {
-    // A(i, k) = U[k][i0 + i];  B(k, j) = U[k][j0 + j]
-    stage_tile<double, double, NB, 256, false>(As, Us + i0, r, 0, r - i0, k0, kend, tid);
-    stage_tile<double, double, NB, 256, false>(Bs, Us + j0, r, 0, r - j0, k0, kend, tid);
+  if (ti == tj && qi > qj) {              // below the diagonal: U is zero there
+    if (Ud)
+      for (int e = tid; e < NQ * NQ; e += 256) {
+        const int row = i0 + e / NQ, col = j0 + e % NQ;
+        if (row < r && col < r) Ud[static_cast<long long>(row) * r + col] = 0.0;
+      }
+    return;
+  }
+  const double* const Us = global_view(t.nid) + static_cast<long long>(src) * r * r;
+  // (U^T U)[i][j] = sum_k U[k][i] U[k][j]; U is upper triangular, so k < i0 + 32
+  const int kend = min(i0 + NQ, r);
+  f64x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{};
+  for (int k0 = 0; k0 < kend; k0 += 4 * GBK) {
+    // slice w: A(i, k) = U[k][i0 + i], B(k, j) = U[k][j0 + j], k in k0 + 32 w ..
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      stage_tile<double, double, NQ, 256, false>(As + w * SL, Us + i0, r, 0, r - i0, k0 + w * GBK, kend, tid);
+      stage_tile<double, double, NQ, 256, false>(Bs + w * SL, Us + j0, r, 0, r - j0, k0 + w * GBK, kend, tid);
+    }
     __syncthreads();
-    T.mma_stage<false>(As, Bs, wm0, wn0, lane);
+#pragma unroll
+    for (int kk = 0; kk < GBK; kk += 16) {
+      f64x4 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = frag<double, NQ, false>(As + wave * SL, i * 16, kk, lane);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = frag<double, NQ, false>(Bs + wave * SL, j * 16, kk, lane);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+    }
     __syncthreads();
   }
-  double* const Ud = dst >= 0 ? global_view(t.nid) + static_cast<long long>(dst) * r * r : nullptr;
+  double* const red = As;                 // [wave][row][RLD]
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = i0 + wm0 + i * 16 + Mfma<double>::out_row(lane, v);
-        const int col = j0 + wn0 + j * 16 + (lane & 15);
-        if (row >= r || col >= r) continue;
-        const long long o = static_cast<long long>(row) * r + col;
-        if (row > col) {                     // below the diagonal of a diagonal tile
-          if (Ud) Ud[o] = 0.0;
-          continue;
-        }
-        const double s = (W[o] - (row == col ? 1.0 : 0.0)) - T.acc[i][j][v];
-        const double u = row == col ? 0.5 * s : s;
-        if (Ud) Ud[o] = u;
-        else W[o] = row == col ? 1.0 + u : u;
-      }
+      for (int v = 0; v < 4; ++v)
+        red[(wave * NQ + i * 16 + Mfma<double>::out_row(lane, v)) * RLD + j * 16 + (lane & 15)] = acc[i][j][v];
+  __syncthreads();
+  for (int e = tid; e < NQ * NQ; e += 256) {
+    const int lr = e / NQ, lc = e % NQ, row = i0 + lr, col = j0 + lc;
+    if (row >= r || col >= r) continue;
+    const long long o = static_cast<long long>(row) * r + col;
+    if (row > col) {                      // below the diagonal of a diagonal tile
+      if (Ud) Ud[o] = 0.0;
+      continue;
+    }
+    const double* const p = red + lr * RLD + lc;
+    const double sum = ((p[0] + p[NQ * RLD]) + p[2 * NQ * RLD]) + p[3 * NQ * RLD];
+    const double sv = (W[o] - (row == col ? 1.0 : 0.0)) - sum;
+    const double u = row == col ? 0.5 * sv : sv;
+    if (Ud) Ud[o] = u;
+    else W[o] = row == col ? 1.0 + u : u;
+  }
 }
 
 // D_k = (T1_kk)^{-1} = sum_{j <= NID_SERIES} (-U_kk)^j by Horner's rule
@@ -206,7 +248,7 @@ hipError_t launch_nearid(const CholTab* tab, int nlayers, int r, hipStream_t s, 
   hipLaunchKernelGGL(k_nid_start, dim3(nt, nlayers), dim3(256), 0, s, tab, r, run_if);
   for (int it = 0; it < NID_ITERS; ++it) {
     const int src = it & 1, dst = it + 1 < NID_ITERS ? (src ^ 1) : -1;
-    hipLaunchKernelGGL(k_nid_iter, dim3(nt, nlayers), dim3(256), 0, s, tab, r, src, dst, run_if);
+    hipLaunchKernelGGL(k_nid_iter, dim3(4 * nt, nlayers), dim3(256), 0, s, tab, r, src, dst, run_if);
   }
   hipLaunchKernelGGL(k_nid_dinv, dim3(nblk, nlayers), dim3(256), 0, s, tab, r, run_if);
   return hipGetLastError();
