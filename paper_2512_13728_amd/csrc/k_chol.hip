@@ -25,47 +25,122 @@ namespace {
 constexpr int CB = CHOL_BLOCK;
 using Wave64 = WaveChol<CB>;
 
-// One wave per layer: the factorisation of the diagonal block (chol_wave.hpp)
-// and its inverse D_k; T_kk goes back over W_kk.
-__global__ __launch_bounds__(64) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
-                                                  int pass, const int* run_if, int gated) {
-  __shared__ __attribute__((aligned(16))) Wave64::Lds lds;
+// Orders the LDS accesses of the workgroup's waves across a barrier without
+// waiting for their global stores (a plain __syncthreads would also wait for
+// every store of T and D in flight, once per pivot).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Two waves per layer: the factorisation of the diagonal block and its
+// inverse D_k in one pivot loop.  Wave 0 holds the block, one column per lane
+// (rows shifted by one per pivot, as in chol_wave.hpp), and stores each row
+// of T_kk over W_kk as soon as it is known; wave 1 holds the identity's
+// columns and applies the same row operations, which turn I into
+// E = T_kk^{-T} (the two-wave form of factor_inv, whose one-wave form carries
+// both halves for blocks of up to 32 columns): row p of E is final once
+// scaled by 1 / T[p][p], zero for a floored pivot, and D_k[c][p] = E[p][c].
+// Per pivot, wave 0 publishes row p of T and the pivot's reciprocal in LDS
+// (double-buffered by pivot parity), one barrier, then both waves update
+// their rows below p.  Where the one-wave kernel ran the 64-step back
+// substitution after the factorisation, wave 1 works beside wave 0.
+__global__ __launch_bounds__(128) void k_chol_diag(const CholTab* __restrict__ tab, int r, int kb,
+                                                   int pass, const int* run_if, int gated) {
+  constexpr int ELD = CB + 1;
+  constexpr int SEG = Wave64::SEG;
+  __shared__ __attribute__((aligned(16))) double rowb[2][2 * CB];   // row p of T, then zeros
+  __shared__ double pinv[2];                                         // 1 / T[p][p]; 0: floored
+  __shared__ double Es[CB * ELD];                                    // E[p][c] at p * ELD + c
+  __shared__ int okb[CB];
   if (skip_launch(run_if)) return;
   const CholTab t = tab[blockIdx.x];
   if (gated && *global_view(t.nid_ok)) return;
   double* const W = global_view(t.W);
   double* const floor_ = global_view(t.floor_);
   int* const rankdef = global_view(t.rankdef);
-  const int j = threadIdx.x;
+  const int tid = threadIdx.x, j = tid & 63;
+  const bool ewave = tid >= 64;                 // uniform per wave
   const long long ld = r;
   const int k0 = kb * CB, nb = min(CB, r - k0);
-  double fl;
-  if (kb == 0) {
-    double md = 0.0;
-    for (int k = j; k < r; k += 64) md = fmax(md, W[k * ld + k]);
+  double fl = 0.0;
+  if (!ewave) {
+    if (kb == 0) {
+      double md = 0.0;
+      for (int k = j; k < r; k += 64) md = fmax(md, W[k * ld + k]);
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) md = fmax(md, __shfl_xor(md, o, 64));
-    fl = fmax(1e-13 * md, 1e-60);
-    if (j == 0) {
-      *floor_ = fl;
-      if (pass == 0) {
-        *rankdef = 0;
-        if (t.rankdef_host) *t.rankdef_host = 0;
+      for (int o = 32; o > 0; o >>= 1) md = fmax(md, __shfl_xor(md, o, 64));
+      fl = fmax(1e-13 * md, 1e-60);
+      if (j == 0) {
+        *floor_ = fl;
+        if (pass == 0) {
+          *rankdef = 0;
+          if (t.rankdef_host) *t.rankdef_host = 0;
+        }
+      }
+    } else {
+      fl = *floor_;
+    }
+  }
+  double a[CB];   // a[i] = row p + i of this lane's column at pivot p
+#pragma unroll
+  for (int i = 0; i < CB; ++i) {
+    if (ewave) a[i] = (i == j && j < nb) ? 1.0 : 0.0;
+    else if (i < nb && j < nb) a[i] = i <= j ? W[(k0 + i) * ld + k0 + j] : 0.0;
+    else a[i] = i == j ? 1.0 : 0.0;
+  }
+  if (!ewave) {
+    rowb[0][CB + j] = 0.0;
+    rowb[1][CB + j] = 0.0;
+  }
+  bool def = false;                             // wave 0: a pivot was floored
+  auto pivot = [&](auto na, int p) {
+    constexpr int NA = decltype(na)::value;
+    const int b = p & 1;
+    double tp;
+    if (!ewave) {
+      const double a0 = a[0];
+      double d = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(a0), p),
+                                  __builtin_amdgcn_readlane(__double2loint(a0), p));
+      const bool floored = !(d > fl);
+      if (floored) { d = fl; def = true; }
+      double inv = __builtin_amdgcn_rsq(d);
+#pragma unroll
+      for (int it = 0; it < 2; ++it) inv = fma(inv, fma(-0.5 * d * inv, inv, 0.5), inv);
+      const double piv = d * inv;
+      tp = j == p ? piv : (j > p && !floored ? a0 * inv : 0.0);
+      if (j >= p && j < nb) W[(k0 + p) * ld + k0 + j] = tp;
+      rowb[b][j] = tp;
+      if (j == p) {
+        pinv[b] = floored ? 0.0 : inv;
+        okb[p] = floored ? 0 : 1;
       }
     }
-  } else {
-    fl = *floor_;
+    lds_barrier();
+    if (ewave) {
+      tp = a[0] * pinv[b];
+      Es[p * ELD + j] = tp;
+    }
+    chunked<NA - 1>([&](int i) { return rowb[b][p + 1 + i]; },
+                    [&](int i, double v) { a[i] = fma(-v, tp, a[i + 1]); });
+    a[NA - 1] = 0.0;
+  };
+  // segment g: pivots [g SEG, (g + 1) SEG) with CB - g SEG live rows (both
+  // waves run the same pivots, hence the same barriers)
+  static_for<CB / SEG>([&](auto gc) {
+    constexpr int G = decltype(gc)::value;
+#pragma unroll 1
+    for (int p = G * SEG; p < min(nb, (G + 1) * SEG); ++p) pivot(std::integral_constant<int, CB - G * SEG>{}, p);
+  });
+  __syncthreads();
+  if (!ewave && j < nb) global_view(t.rowok)[k0 + j] = okb[j];
+  double* const D = global_view(t.Dinv) + static_cast<long long>(kb) * CB * CB;
+  for (int idx = tid; idx < CB * CB; idx += 128) {
+    const int p = idx / CB, q = idx % CB;
+    D[idx] = (p < nb && q < nb) ? Es[q * ELD + p] : 0.0;   // (T^{-1})[p][q] = E[q][p]
   }
-  const bool def = Wave64::factor(lds, j, nb, fl, [&](int i) { return W[(k0 + i) * ld + k0 + j]; });
-  if (j < nb) global_view(t.rowok)[k0 + j] = lds.okb[j];
-  double* D = global_view(t.Dinv) + static_cast<long long>(kb) * CB * CB;
-  for (int p = nb; p < CB; ++p) D[p * CB + j] = 0.0;   // rows past a partial block
-  Wave64::inverse(lds, j, nb, [&](int p, double x) { D[p * CB + j] = x; });
-  const double* Ts = Wave64::Ts(lds);
-#pragma unroll 4
-  for (int i = 0; i < nb; ++i)
-    if (j < nb && i <= j) W[(k0 + i) * ld + k0 + j] = Ts[j * Wave64::TLD + i];
-  if (j == 0 && def) {
+  if (tid == 0 && def) {
     *rankdef = 1;
     if (t.rankdef_host) *t.rankdef_host = 1;
   }
@@ -405,7 +480,7 @@ hipError_t launch_cholesky(const CholTab* tab, int nlayers, int r, int pass, hip
   if (r < 1) return hipErrorInvalidValue;
   const int nblk = (r + CB - 1) / CB, g = gated ? 1 : 0;
   for (int kb = 0; kb < nblk; ++kb) {
-    hipLaunchKernelGGL(k_chol_diag, dim3(nlayers), dim3(64), 0, s, tab, r, kb, pass, run_if, g);
+    hipLaunchKernelGGL(k_chol_diag, dim3(nlayers), dim3(128), 0, s, tab, r, kb, pass, run_if, g);
     const int k1 = min(r, (kb + 1) * CB);
     if (k1 >= r) break;
     const int nt = (r - k1 + CB - 1) / CB;
